@@ -1,0 +1,172 @@
+/*
+ * dtst.h -- C ABI of the DTST spectral-layer library for AMD MI355X (gfx950).
+ *
+ * The library computes, on one GPU's shard of a spatially decomposed
+ * (x, y, z, t) grid, the hot path of one Fourier-neural-operator spectral
+ * layer as defined in "DRIFT: Direct Reduced Fourier Transforms for
+ * Distributed Spectral Neural Operators" (arXiv 2607.14394):
+ *
+ *   forward partial DFT   Sec. IV-B Eq. (dtst_decompose), basis of Sec. V-B
+ *                         Eq. (basis_matrix), summed over shards as in
+ *                         Eq. (dtst_reduce) through the `accumulate` flag
+ *   mode-wise channel mix Sec. V-A Eq. (partitioned_conv) on a mode range S_p
+ *   inverse partial DFT   Sec. V-A Eq. (dtst_inverse)
+ *   adjoints              Sec. V-C (backward pass)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Dimensions are ordered (x, y, z, t); t is innermost in memory.
+ * Retained modes: x, y, z keep the stored indices {0..k-1} U {N-k..N-1}
+ * (Sec. III, Fig. 5), t keeps {0..kt-1} (the half spectrum of a real
+ * signal).  Within a dimension modes are stored in ascending stored index.
+ * M = (2kx)(2ky)(2kz)kt and the flattened mode index is
+ * m = ((ix*Ky + iy)*Kz + iz)*Kt + it.
+ *
+ * Basis (Sec. V-B): B_i[k, j] = exp(-2 pi i ((k * (offset_i + j)) mod N_i) / N_i);
+ * the exponent is reduced in exact integer arithmetic, the trigonometric
+ * value is taken in fp64 and rounded once to fp32.
+ *
+ * Inverse of the half spectrum: y[n] = (1/prod N) Re sum_k w(k_t) Yhat[k]
+ * conj(phi_k(n)) with w(0) = 1, w(N_t/2) = 1 for even N_t, w = 2 otherwise.
+ *
+ * Memory: every array argument is a contiguous, row-major DEVICE pointer
+ * owned by the caller, aligned to 16 bytes.  Complex arrays are interleaved
+ * (re, im) fp32 pairs, the layout of torch.complex64.
+ *
+ *   x, y, g_x, g_y           (B, C, Nx_loc, Ny_loc, Nz_loc, Nt_loc) fp32
+ *   xhat, yhat, g_xhat, ...  (B, C, 2kx, 2ky, 2kz, kt) complex64
+ *   w_shard, g_w_shard       (m1 - m0, C_in, C_out) complex64
+ *
+ * C is C_in for forward / forward_adj / the mix input and C_out for the
+ * mix output / inverse / inverse_adj.
+ *
+ * Execution: every execute call is asynchronous on `stream` (a hipStream_t
+ * passed as void*, NULL = the default stream), allocates nothing and never
+ * synchronises the host.  All validation happens on the host before any
+ * launch; on an error nothing is launched, outputs are untouched and the
+ * status says why (dtst_last_error() gives the detail for the calling
+ * thread).  Nothing throws across the ABI and nothing aborts.  Plans are
+ * immutable after creation and may be used concurrently from several
+ * streams as long as each concurrent call has its own workspace.
+ */
+#ifndef DTST_H
+#define DTST_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DTST_VERSION_MAJOR 0
+#define DTST_VERSION_MINOR 1
+
+typedef struct dtst_plan_st* dtst_plan_t; /* opaque; created and owned by the library */
+
+typedef enum {
+  DTST_OK = 0,
+  DTST_ERR_INVALID_ARG = 1,   /* bad descriptor, pointer, size, range or plan */
+  DTST_ERR_UNSUPPORTED = 2,   /* valid geometry outside what the kernels cover */
+  DTST_ERR_OUT_OF_MEMORY = 3, /* device allocation at plan creation failed */
+  DTST_ERR_DEVICE = 4         /* a HIP call or kernel launch failed */
+} dtst_status;
+
+/* Geometry of one shard (Sec. IV-A problem setting; offsets of Sec. V-B). */
+typedef struct {
+  int64_t n_global[4]; /* N_x, N_y, N_z, N_t of the global grid, each >= 1          */
+  int64_t n_local[4];  /* local extents N_i^loc of this shard, each >= 1            */
+  int64_t offset[4];   /* global index of the shard's first element, p_i N_i^loc;   */
+                       /* 0 <= offset, offset + n_local <= n_global                 */
+  int32_t kmax[3];     /* x, y, z keep 2k indices; need 1 <= 2k <= N (Sec. III)     */
+  int32_t kt;          /* t keeps 0..kt-1; need 1 <= kt <= N_t/2 + 1                */
+  int64_t batch;       /* B >= 0 (0 makes every execute call a no-op)              */
+  int64_t c_in;        /* input channels  >= 1                                     */
+  int64_t c_out;       /* output channels >= 1                                     */
+} dtst_desc;
+
+/* ---- host-only helpers (no GPU needed) --------------------------------- */
+
+/* Check a descriptor.  DTST_OK, DTST_ERR_INVALID_ARG for a geometry the
+ * method does not define, DTST_ERR_UNSUPPORTED for one the kernels do not
+ * cover (currently: kt <= 16, N_t^loc <= 64, and per-kernel LDS limits). */
+dtst_status dtst_desc_validate(const dtst_desc* d);
+
+/* Workspace bytes the execute calls of this geometry need (>= 0). */
+dtst_status dtst_desc_workspace_bytes(const dtst_desc* d, size_t* bytes);
+
+/* Write the fp32 basis matrix of dimension `dim` (0..3 = x, y, z, t) that
+ * the plan uploads, as an interleaved complex (K_dim x N_dim^loc) host array
+ * of `count` floats (count must equal 2*K_dim*N_dim^loc).  kind 0: the
+ * forward basis B_dim of Eq. (basis_matrix); kind 1: conj(B_dim), the
+ * inverse basis before the 1/prod N and half-spectrum weights.  Sec. V-B. */
+dtst_status dtst_basis_host(const dtst_desc* d, int dim, int kind, float* out, size_t count);
+
+/* ---- plans ------------------------------------------------------------- */
+
+/* Validate `d`, build every basis table on the host in fp64, round to fp32
+ * and upload them to the current HIP device (synchronously).  The plan is
+ * bound to that device.  On success *out receives the plan. */
+dtst_status dtst_plan(const dtst_desc* d, dtst_plan_t* out);
+
+/* Free the plan's device tables.  Using a destroyed plan afterwards returns
+ * DTST_ERR_INVALID_ARG. */
+dtst_status dtst_plan_destroy(dtst_plan_t p);
+
+/* Number of retained modes M and the workspace size for every execute call
+ * of this plan.  Either output pointer may be NULL. */
+dtst_status dtst_plan_info(dtst_plan_t p, int64_t* n_modes, size_t* workspace_bytes);
+
+/* ---- execute calls ------------------------------------------------------ */
+
+/* Forward partial spectrum of the shard (Sec. IV-B Eq. dtst_decompose):
+ *   xhat[b,c,k] (+)= sum_{n in shard} x[b,c,n] prod_i B_i[k_i, n_i]
+ * for the C_in channels.  accumulate = 0 overwrites xhat; 1 adds to it, so
+ * calling it for every shard in turn forms the sum of Eq. (dtst_reduce).
+ * The contraction order is t, z, y, x (Algorithm 1). */
+dtst_status dtst_forward(dtst_plan_t p, const float* x, void* xhat, int accumulate,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* Mode-wise channel mix on the flattened mode range [m0, m1) (Sec. V-A,
+ * Eq. partitioned_conv), with w_shard the local weights R_theta^(p):
+ *   op 0:  yhat[b,o,m]  = sum_i xhat[b,i,m] * w[m-m0,i,o]         (xhat: C_in,  yhat: C_out)
+ *   op 1:  yhat[b,i,m]  = sum_o xhat[b,o,m] * conj(w[m-m0,i,o])   (xhat: C_out, yhat: C_in)
+ * op 1 is the data gradient of op 0.  Only columns m0..m1-1 of yhat are
+ * written; the rest is untouched, so running the disjoint ranges one after
+ * another assembles the whole spectrum.  0 <= m0 <= m1 <= M. */
+dtst_status dtst_mix(dtst_plan_t p, const void* xhat, const void* w_shard, void* yhat,
+                     int64_t m0, int64_t m1, int op, void* stream);
+
+/* Inverse partial DFT onto the shard (Sec. V-A Eq. dtst_inverse, half
+ * spectrum in t) for the C_out channels:
+ *   y[b,c,n] = (1/prod N) Re sum_k w(k_t) yhat[b,c,k] conj(prod_i B_i[k_i, n_i]).
+ * Expansion order x, y, z, t. */
+dtst_status dtst_inverse(dtst_plan_t p, const void* yhat, float* y,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* Adjoint of dtst_forward (Sec. V-C), C_in channels:
+ *   g_x[b,c,n] = Re sum_k g_xhat[b,c,k] conj(prod_i B_i[k_i, n_i]). */
+dtst_status dtst_forward_adj(dtst_plan_t p, const void* g_xhat, float* g_x,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* Adjoint of dtst_inverse (Sec. V-C), C_out channels:
+ *   g_yhat[b,c,k] (+)= (w(k_t)/prod N) sum_n g_y[b,c,n] prod_i B_i[k_i, n_i]. */
+dtst_status dtst_inverse_adj(dtst_plan_t p, const float* g_y, void* g_yhat, int accumulate,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* Gradient of the local weights on [m0, m1) (Sec. V-A, Sec. V-C; local, no
+ * synchronisation needed):
+ *   g_w[m-m0,i,o] (+)= sum_b conj(xhat[b,i,m]) * g_yhat[b,o,m]. */
+dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, void* g_w_shard,
+                           int64_t m0, int64_t m1, int accumulate, void* stream);
+
+/* ---- diagnostics -------------------------------------------------------- */
+const char* dtst_status_string(dtst_status s);
+/* Detail of the last error on the calling thread ("" if none). */
+const char* dtst_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DTST_H */

@@ -1,0 +1,343 @@
+// C ABI of the DTST library: plans, validation and the execute calls.
+//
+// Every execute call validates its arguments on the host first; on any
+// error it launches nothing, leaves the outputs untouched and records a
+// message retrievable with dtst_last_error() on the calling thread.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "dtst_internal.h"
+
+struct dtst_plan_st {
+  dtst::Derived dv;
+  int device = 0;
+  float* blob = nullptr;  // device copy of every basis image
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+std::mutex g_plans_mu;
+std::unordered_set<const dtst_plan_st*>& live_plans() {
+  static std::unordered_set<const dtst_plan_st*> s;
+  return s;
+}
+
+dtst_status fail(dtst_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+dtst_status ok() {
+  g_last_error.clear();
+  return DTST_OK;
+}
+
+bool is_live(const dtst_plan_st* p) {
+  std::lock_guard<std::mutex> lk(g_plans_mu);
+  return p != nullptr && live_plans().count(p) != 0;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Makes the plan's device current for the duration of a call.
+struct DeviceGuard {
+  int prev = -1;
+  bool switched = false;
+  hipError_t err = hipSuccess;
+  explicit DeviceGuard(int dev) {
+    err = hipGetDevice(&prev);
+    if (err == hipSuccess && prev != dev) {
+      err = hipSetDevice(dev);
+      switched = err == hipSuccess;
+    }
+  }
+  ~DeviceGuard() {
+    if (switched) (void)hipSetDevice(prev);
+  }
+};
+
+dtst_status device_status(int e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(DTST_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(static_cast<hipError_t>(e)));
+}
+
+dtst_status check_plan(const dtst_plan_st* p) {
+  if (!is_live(p)) return fail(DTST_ERR_INVALID_ARG, "plan is null or was destroyed");
+  return DTST_OK;
+}
+
+dtst_status check_ptr(const void* ptr, const char* name) {
+  if (ptr == nullptr) return fail(DTST_ERR_INVALID_ARG, std::string(name) + " is null");
+  if (!aligned16(ptr)) return fail(DTST_ERR_INVALID_ARG, std::string(name) + " is not 16-byte aligned");
+  return DTST_OK;
+}
+
+dtst_status check_ws(const dtst_plan_st* p, const void* ws, size_t ws_bytes) {
+  if (ws_bytes < p->dv.ws_bytes)
+    return fail(DTST_ERR_INVALID_ARG, "workspace too small: need " + std::to_string(p->dv.ws_bytes) +
+                                          " bytes, got " + std::to_string(ws_bytes));
+  if (p->dv.ws_bytes > 0) return check_ptr(ws, "workspace");
+  return DTST_OK;
+}
+
+size_t w1_bytes(const dtst::Derived& dv) {
+  const int64_t cmax = dv.d.c_in > dv.d.c_out ? dv.d.c_in : dv.d.c_out;
+  size_t b = size_t(dv.d.batch) * cmax * dv.d.n_local[0] * dv.d.n_local[1] * dv.K[2] * dv.K[3] * 8;
+  return (b + 255) / 256 * 256;
+}
+
+#define DTST_TRY(expr)                 \
+  do {                                 \
+    dtst_status s_ = (expr);           \
+    if (s_ != DTST_OK) return s_;      \
+  } while (0)
+
+// Forward-direction chain: streaming t+z, then y, then x (with accumulate).
+dtst_status run_forward_chain(const dtst_plan_st* p, int64_t channels, const float* x, void* xhat,
+                              int accumulate, void* ws, const float* timg, void* stream) {
+  const dtst::Derived& dv = p->dv;
+  const int64_t B = dv.d.batch;
+  if (B == 0) return ok();
+  char* w1 = static_cast<char*>(ws);
+  char* w2 = w1 + w1_bytes(dv);
+  const int64_t rows = B * channels * dv.d.n_local[0] * dv.d.n_local[1];
+  int e = dtst::launch_fwd_tz(dv.sc, x, w1, rows, timg, p->blob + dv.img.z_fwd, stream);
+  if (e != hipSuccess) return device_status(e, "t+z contraction launch");
+  e = dtst::launch_axis(dv.ay_f, B * channels * dv.d.n_local[0], w1, w2, p->blob + dv.img.y_fwd, 0, stream);
+  if (e != hipSuccess) return device_status(e, "y contraction launch");
+  e = dtst::launch_axis(dv.ax_f, B * channels, w2, xhat, p->blob + dv.img.x_fwd, accumulate, stream);
+  if (e != hipSuccess) return device_status(e, "x contraction launch");
+  return ok();
+}
+
+// Inverse-direction chain: x, then y, then streaming z+t with Re.
+dtst_status run_inverse_chain(const dtst_plan_st* p, int64_t channels, const void* yhat, float* y, void* ws,
+                              const float* timg, void* stream) {
+  const dtst::Derived& dv = p->dv;
+  const int64_t B = dv.d.batch;
+  if (B == 0) return ok();
+  char* v2 = static_cast<char*>(ws);    // (.., Nx, Ny, Kz, Kt)
+  char* v1 = v2 + w1_bytes(dv);         // (.., Nx, Ky, Kz, Kt)
+  int e = dtst::launch_axis(dv.ax_i, B * channels, yhat, v1, p->blob + dv.img.x_inv, 0, stream);
+  if (e != hipSuccess) return device_status(e, "x expansion launch");
+  e = dtst::launch_axis(dv.ay_i, B * channels * dv.d.n_local[0], v1, v2, p->blob + dv.img.y_inv, 0, stream);
+  if (e != hipSuccess) return device_status(e, "y expansion launch");
+  const int64_t rows = B * channels * dv.d.n_local[0] * dv.d.n_local[1];
+  e = dtst::launch_inv_zt(dv.sc, v2, y, rows, timg, p->blob + dv.img.z_inv, stream);
+  if (e != hipSuccess) return device_status(e, "z+t expansion launch");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dtst_status_string(dtst_status s) {
+  switch (s) {
+    case DTST_OK: return "DTST_OK";
+    case DTST_ERR_INVALID_ARG: return "DTST_ERR_INVALID_ARG";
+    case DTST_ERR_UNSUPPORTED: return "DTST_ERR_UNSUPPORTED";
+    case DTST_ERR_OUT_OF_MEMORY: return "DTST_ERR_OUT_OF_MEMORY";
+    case DTST_ERR_DEVICE: return "DTST_ERR_DEVICE";
+  }
+  return "DTST_ERR_UNKNOWN";
+}
+
+const char* dtst_last_error(void) { return g_last_error.c_str(); }
+
+dtst_status dtst_desc_validate(const dtst_desc* d) {
+  dtst::Derived dv;
+  std::string err;
+  const dtst_status s = dtst::derive(d, &dv, &err);
+  if (s != DTST_OK) return fail(s, err);
+  const size_t mix_max = dtst::mix_lds_bytes(1, dv.d.batch, dv.d.c_in, dv.d.c_out);
+  if (mix_max > 160 * 1024)
+    return fail(DTST_ERR_UNSUPPORTED, "batch * channels too large for one mode of the mix kernels");
+  return ok();
+}
+
+dtst_status dtst_desc_workspace_bytes(const dtst_desc* d, size_t* bytes) {
+  if (!bytes) return fail(DTST_ERR_INVALID_ARG, "bytes is null");
+  dtst::Derived dv;
+  std::string err;
+  const dtst_status s = dtst::derive(d, &dv, &err);
+  if (s != DTST_OK) return fail(s, err);
+  *bytes = dv.ws_bytes;
+  return ok();
+}
+
+dtst_status dtst_basis_host(const dtst_desc* d, int dim, int kind, float* out, size_t count) {
+  dtst::Derived dv;
+  std::string err;
+  const dtst_status s = dtst::derive(d, &dv, &err);
+  if (s != DTST_OK) return fail(s, err);
+  if (dim < 0 || dim > 3 || (kind != 0 && kind != 1) || out == nullptr)
+    return fail(DTST_ERR_INVALID_ARG, "dim must be 0..3, kind 0 or 1, out non-null");
+  const size_t need = size_t(2) * dv.K[dim] * d->n_local[dim];
+  if (count != need) return fail(DTST_ERR_INVALID_ARG, "count must be 2*K*N_loc = " + std::to_string(need));
+  dtst::plain_basis(*d, dim, kind, out);
+  return ok();
+}
+
+dtst_status dtst_plan(const dtst_desc* d, dtst_plan_t* out) {
+  if (!out) return fail(DTST_ERR_INVALID_ARG, "out is null");
+  const dtst_status vs = dtst_desc_validate(d);
+  if (vs != DTST_OK) return vs;
+  dtst_plan_st* p = new (std::nothrow) dtst_plan_st();
+  if (!p) return fail(DTST_ERR_OUT_OF_MEMORY, "host allocation failed");
+  std::string err;
+  dtst::derive(d, &p->dv, &err);
+  std::vector<float> host;
+  try {
+    dtst::build_images(p->dv, &host);
+  } catch (...) {
+    delete p;
+    return fail(DTST_ERR_OUT_OF_MEMORY, "host allocation of the basis tables failed");
+  }
+  hipError_t e = hipGetDevice(&p->device);
+  if (e != hipSuccess) {
+    delete p;
+    return fail(DTST_ERR_DEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  }
+  e = hipMalloc(&p->blob, host.size() * sizeof(float));
+  if (e != hipSuccess) {
+    delete p;
+    (void)hipGetLastError();
+    return fail(e == hipErrorOutOfMemory ? DTST_ERR_OUT_OF_MEMORY : DTST_ERR_DEVICE,
+                std::string("hipMalloc of the basis tables: ") + hipGetErrorString(e));
+  }
+  e = hipMemcpy(p->blob, host.data(), host.size() * sizeof(float), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(p->blob);
+    delete p;
+    return fail(DTST_ERR_DEVICE, std::string("hipMemcpy of the basis tables: ") + hipGetErrorString(e));
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    live_plans().insert(p);
+  }
+  *out = p;
+  return ok();
+}
+
+dtst_status dtst_plan_destroy(dtst_plan_t p) {
+  {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    if (p == nullptr || live_plans().erase(p) == 0)
+      return fail(DTST_ERR_INVALID_ARG, "plan is null or was destroyed");
+  }
+  DeviceGuard guard(p->device);
+  const hipError_t e = hipFree(p->blob);
+  delete p;
+  if (e != hipSuccess) return fail(DTST_ERR_DEVICE, std::string("hipFree: ") + hipGetErrorString(e));
+  return ok();
+}
+
+dtst_status dtst_plan_info(dtst_plan_t p, int64_t* n_modes, size_t* workspace_bytes) {
+  DTST_TRY(check_plan(p));
+  if (n_modes) *n_modes = p->dv.M;
+  if (workspace_bytes) *workspace_bytes = p->dv.ws_bytes;
+  return ok();
+}
+
+dtst_status dtst_forward(dtst_plan_t p, const float* x, void* xhat, int accumulate, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  DTST_TRY(check_plan(p));
+  if (p->dv.d.batch == 0) return ok();
+  DTST_TRY(check_ptr(x, "x"));
+  DTST_TRY(check_ptr(xhat, "xhat"));
+  DTST_TRY(check_ws(p, workspace, workspace_bytes));
+  if (accumulate != 0 && accumulate != 1) return fail(DTST_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  return run_forward_chain(p, p->dv.d.c_in, x, xhat, accumulate, workspace, p->blob + p->dv.img.t_fwd, stream);
+}
+
+dtst_status dtst_inverse_adj(dtst_plan_t p, const float* g_y, void* g_yhat, int accumulate, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  DTST_TRY(check_plan(p));
+  if (p->dv.d.batch == 0) return ok();
+  DTST_TRY(check_ptr(g_y, "g_y"));
+  DTST_TRY(check_ptr(g_yhat, "g_yhat"));
+  DTST_TRY(check_ws(p, workspace, workspace_bytes));
+  if (accumulate != 0 && accumulate != 1) return fail(DTST_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  return run_forward_chain(p, p->dv.d.c_out, g_y, g_yhat, accumulate, workspace,
+                           p->blob + p->dv.img.t_fwd_adjoint_of_inverse, stream);
+}
+
+dtst_status dtst_inverse(dtst_plan_t p, const void* yhat, float* y, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  DTST_TRY(check_plan(p));
+  if (p->dv.d.batch == 0) return ok();
+  DTST_TRY(check_ptr(yhat, "yhat"));
+  DTST_TRY(check_ptr(y, "y"));
+  DTST_TRY(check_ws(p, workspace, workspace_bytes));
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  return run_inverse_chain(p, p->dv.d.c_out, yhat, y, workspace, p->blob + p->dv.img.t_inv, stream);
+}
+
+dtst_status dtst_forward_adj(dtst_plan_t p, const void* g_xhat, float* g_x, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  DTST_TRY(check_plan(p));
+  if (p->dv.d.batch == 0) return ok();
+  DTST_TRY(check_ptr(g_xhat, "g_xhat"));
+  DTST_TRY(check_ptr(g_x, "g_x"));
+  DTST_TRY(check_ws(p, workspace, workspace_bytes));
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  return run_inverse_chain(p, p->dv.d.c_in, g_xhat, g_x, workspace,
+                           p->blob + p->dv.img.t_inv_adjoint_of_forward, stream);
+}
+
+dtst_status dtst_mix(dtst_plan_t p, const void* xhat, const void* w_shard, void* yhat, int64_t m0, int64_t m1,
+                     int op, void* stream) {
+  DTST_TRY(check_plan(p));
+  const dtst::Derived& dv = p->dv;
+  if (op != 0 && op != 1) return fail(DTST_ERR_INVALID_ARG, "op must be 0 (W) or 1 (W^H)");
+  if (m0 < 0 || m1 < m0 || m1 > dv.M)
+    return fail(DTST_ERR_INVALID_ARG, "mode range must satisfy 0 <= m0 <= m1 <= M = " + std::to_string(dv.M));
+  if (dv.d.batch == 0 || m1 == m0) return ok();
+  DTST_TRY(check_ptr(xhat, "xhat"));
+  DTST_TRY(check_ptr(w_shard, "w_shard"));
+  DTST_TRY(check_ptr(yhat, "yhat"));
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  const int e = op == 0 ? dtst::launch_mix(xhat, w_shard, yhat, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0, m1,
+                                           stream)
+                        : dtst::launch_mix_h(xhat, w_shard, yhat, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0,
+                                             m1, stream);
+  return device_status(e, "mix launch");
+}
+
+dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, void* g_w_shard, int64_t m0,
+                           int64_t m1, int accumulate, void* stream) {
+  DTST_TRY(check_plan(p));
+  const dtst::Derived& dv = p->dv;
+  if (m0 < 0 || m1 < m0 || m1 > dv.M)
+    return fail(DTST_ERR_INVALID_ARG, "mode range must satisfy 0 <= m0 <= m1 <= M = " + std::to_string(dv.M));
+  if (accumulate != 0 && accumulate != 1) return fail(DTST_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  if (dv.d.batch == 0 || m1 == m0) return ok();
+  DTST_TRY(check_ptr(xhat, "xhat"));
+  DTST_TRY(check_ptr(g_yhat, "g_yhat"));
+  DTST_TRY(check_ptr(g_w_shard, "g_w_shard"));
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  const int e = dtst::launch_wgrad(xhat, g_yhat, g_w_shard, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0, m1,
+                                   accumulate, stream);
+  return device_status(e, "wgrad launch");
+}
+
+}  // extern "C"

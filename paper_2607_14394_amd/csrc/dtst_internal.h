@@ -1,0 +1,97 @@
+// Internal declarations shared by the host tables, the C ABI and the HIP
+// kernels of the DTST library.  Not part of the public interface.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "dtst.h"
+
+namespace dtst {
+
+// ---------------------------------------------------------------------------
+// Streaming t+z kernels (forward: real rows -> (Kz x Kt) complex rows;
+// inverse: the mirror).  One "row" is the contiguous (N_z x N_t) block of a
+// fixed (b, c, x, y).
+//
+//   CT   number of 16-wide column tiles holding (Re kt | Im kt): 1 if kt <= 8
+//        (columns 0..7 = Re, 8..15 = Im), 2 if kt <= 16 (tile 0 Re, tile 1 Im)
+//   TH   number of 16-wide t groups: N_t padded to 16*TH, t = 16h + 4g + j
+//   MT   16-row tiles per z class: rows [0, KCP) = Re, [KCP, 2 KCP) = Im,
+//        KCP = 8*MT slots per class
+//   NCLS 1, or 2 when z is folded: with N_z^loc = N_z even,
+//        B[k, z + N/2] = (-1)^k B[k, z], so even k see x[z] + x[z+N/2] and
+//        odd k see x[z] - x[z+N/2]; class c holds the modes p = 2s + c.
+// ---------------------------------------------------------------------------
+struct StreamCfg {
+  int ct = 1, th = 1, mt = 2, ncls = 1;
+  int nt = 0, nz = 0, kt = 0, kz = 0;
+  int zh = 0;   // z extent per class pass (N_z/2 folded, N_z otherwise)
+  int zt = 0;   // ceil(zh / 16)
+  int kcp = 0;  // padded slots per class = 8*mt
+  int vec = 0;  // 1 when N_t % 4 == 0 (16-byte row chunks)
+  size_t lds_bytes = 0;
+};
+
+// Generic complex contraction along a middle axis:
+//   out[b][k][n] (+)= sum_j basis[k][j] in[b][j][n],
+// b < nb, j < J, k < KO, n < NN (complex elements).
+struct AxisCfg {
+  int64_t nb = 0;
+  int J = 0, KO = 0, NN = 0;
+  int JQ = 0;      // ceil(J / 16)
+  int ktiles = 0;  // ceil(KO / 16)
+};
+
+// Float offsets of each kernel-ready image inside the plan's device blob.
+struct Images {
+  size_t t_fwd = 0, t_fwd_adjoint_of_inverse = 0;  // streaming forward, B operand
+  size_t z_fwd = 0;                                // streaming forward, LDS image
+  size_t t_inv = 0, t_inv_adjoint_of_forward = 0;  // streaming inverse, A operand
+  size_t z_inv = 0;                                // streaming inverse, LDS image
+  size_t y_fwd = 0, x_fwd = 0, y_inv = 0, x_inv = 0;  // axis images
+  size_t total = 0;
+};
+
+struct Derived {
+  dtst_desc d{};
+  int64_t K[4] = {0, 0, 0, 0};
+  int64_t M = 0;
+  StreamCfg sc;
+  AxisCfg ay_f, ax_f, ax_i, ay_i;  // per-channel shapes; nb is per (b, c) below
+  size_t ws_bytes = 0;
+  Images img;
+};
+
+// Host-side validation and derivation (pure C++; no HIP).
+dtst_status derive(const dtst_desc* d, Derived* out, std::string* err);
+// Build every image of the blob (fp64 maths, rounded to fp32 once).
+void build_images(const Derived& dv, std::vector<float>* blob);
+// Plain (K x N_loc) complex fp32 basis of one dimension (kind 0: B, 1: conj B).
+void plain_basis(const dtst_desc& d, int dim, int kind, float* out);
+
+// Retained stored index of position p along dimension dim (0..3).
+int64_t retained_index(const dtst_desc& d, int dim, int64_t p);
+
+// ---------------------------------------------------------------------------
+// Kernel launchers (defined in the .hip sources).  All return hipSuccess or
+// the launch error as an int (hipError_t).
+// ---------------------------------------------------------------------------
+int launch_fwd_tz(const StreamCfg& c, const float* x, void* out, int64_t rows,
+                  const float* timg, const float* zimg, void* stream);
+int launch_inv_zt(const StreamCfg& c, const void* in, float* y, int64_t rows,
+                  const float* timg, const float* zimg, void* stream);
+int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const float* img,
+                int accumulate, void* stream);
+// LDS bytes per staged mode of a mix launch (op 0: mix / wgrad, 1: mix_h).
+size_t mix_lds_bytes(int op, int64_t B, int64_t ci, int64_t co);
+int launch_mix(const void* xhat, const void* w, void* yhat, int64_t B, int64_t ci, int64_t co,
+               int64_t M, int64_t m0, int64_t m1, void* stream);
+int launch_mix_h(const void* gy, const void* w, void* gx, int64_t B, int64_t ci, int64_t co,
+                 int64_t M, int64_t m0, int64_t m1, void* stream);
+int launch_wgrad(const void* xhat, const void* gy, void* gw, int64_t B, int64_t ci, int64_t co,
+                 int64_t M, int64_t m0, int64_t m1, int accumulate, void* stream);
+
+}  // namespace dtst

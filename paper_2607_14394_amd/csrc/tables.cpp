@@ -1,0 +1,385 @@
+// Host-side geometry validation and basis tables of the DTST library.
+//
+// Everything here is plain C++ (no HIP): it derives the kernel
+// configuration from a descriptor and builds, in fp64, the kernel-ready
+// images of the per-dimension basis matrices of Sec. V-B Eq. (basis_matrix),
+//   B_i[k, j] = exp(-2 pi i ((k * (offset_i + j)) mod N_i) / N_i),
+// each value rounded once to fp32.  The exponent is reduced in exact
+// integer arithmetic before the angle is formed, so no precision is lost to
+// large k*n products (k*n reaches 2.6e5 at N = 512).
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <limits>
+
+#include "dtst_internal.h"
+
+namespace dtst {
+
+namespace {
+
+constexpr double kTwoPi = 6.283185307179586476925286766559;
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
+
+// exp(-2 pi i r / N) with r = (k * n) mod N, k, n >= 0.
+inline void twiddle(int64_t N, int64_t k, int64_t n, double* re, double* im) {
+  const int64_t r = ((k % N) * (n % N)) % N;
+  const double ang = kTwoPi * static_cast<double>(r) / static_cast<double>(N);
+  *re = std::cos(ang);
+  *im = -std::sin(ang);
+}
+
+// Real-inverse weight of stored t index kt (Sec. V-A inverse, half spectrum).
+inline double half_weight(int64_t nt, int64_t kt) {
+  if (kt == 0) return 1.0;
+  if (nt % 2 == 0 && kt == nt / 2) return 1.0;
+  return 2.0;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > std::numeric_limits<int64_t>::max() / a) return false;
+  *out = a * b;
+  return true;
+}
+
+}  // namespace
+
+int64_t retained_index(const dtst_desc& d, int dim, int64_t p) {
+  if (dim == 3) return p;
+  const int64_t k = d.kmax[dim];
+  return p < k ? p : d.n_global[dim] - 2 * k + p;
+}
+
+dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
+  if (!d || !out) {
+    *err = "null descriptor";
+    return DTST_ERR_INVALID_ARG;
+  }
+  static const char* names[4] = {"x", "y", "z", "t"};
+  for (int i = 0; i < 4; ++i) {
+    if (d->n_global[i] < 1 || d->n_local[i] < 1 || d->offset[i] < 0 ||
+        d->n_local[i] > d->n_global[i] || d->offset[i] > d->n_global[i] - d->n_local[i]) {
+      *err = std::string("dimension ") + names[i] +
+             ": need n_global >= 1, n_local >= 1, 0 <= offset, offset + n_local <= n_global";
+      return DTST_ERR_INVALID_ARG;
+    }
+    if (d->n_global[i] > (int64_t(1) << 30)) {
+      *err = std::string("dimension ") + names[i] + ": n_global above 2^30";
+      return DTST_ERR_INVALID_ARG;
+    }
+  }
+  for (int i = 0; i < 3; ++i) {
+    if (d->kmax[i] < 1 || 2 * int64_t(d->kmax[i]) > d->n_global[i]) {
+      *err = std::string("dimension ") + names[i] + ": need 1 <= 2*kmax <= n_global";
+      return DTST_ERR_INVALID_ARG;
+    }
+  }
+  if (d->kt < 1 || d->kt > d->n_global[3] / 2 + 1) {
+    *err = "t: need 1 <= kt <= n_global_t/2 + 1";
+    return DTST_ERR_INVALID_ARG;
+  }
+  if (d->batch < 0 || d->c_in < 1 || d->c_out < 1) {
+    *err = "need batch >= 0, c_in >= 1, c_out >= 1";
+    return DTST_ERR_INVALID_ARG;
+  }
+
+  Derived dv;
+  dv.d = *d;
+  for (int i = 0; i < 3; ++i) dv.K[i] = 2 * int64_t(d->kmax[i]);
+  dv.K[3] = d->kt;
+  dv.M = dv.K[0] * dv.K[1] * dv.K[2] * dv.K[3];
+
+  // Element counts must stay far inside int64.
+  const int64_t cmax = std::max(d->c_in, d->c_out);
+  int64_t t = 1;
+  bool ok = mul_ok(std::max<int64_t>(d->batch, 1), cmax, &t);
+  for (int i = 0; i < 4 && ok; ++i) ok = mul_ok(t, d->n_local[i], &t);
+  int64_t tm = 1;
+  ok = ok && mul_ok(std::max<int64_t>(d->batch, 1), cmax, &tm) && mul_ok(tm, dv.M, &tm);
+  int64_t tw = 1;
+  ok = ok && mul_ok(dv.M, d->c_in, &tw) && mul_ok(tw, d->c_out, &tw);
+  if (!ok || t > (int64_t(1) << 50) || tm > (int64_t(1) << 50) || tw > (int64_t(1) << 50)) {
+    *err = "problem size overflows the supported element counts";
+    return DTST_ERR_INVALID_ARG;
+  }
+
+  // ---- streaming t+z configuration ----
+  StreamCfg& sc = dv.sc;
+  sc.nt = static_cast<int>(d->n_local[3]);
+  sc.nz = static_cast<int>(d->n_local[2]);
+  sc.kt = d->kt;
+  sc.kz = static_cast<int>(dv.K[2]);
+  if (sc.kt <= 8) {
+    sc.ct = 1;
+  } else if (sc.kt <= 16) {
+    sc.ct = 2;
+  } else {
+    *err = "kt > 16 is not covered by the streaming kernels";
+    return DTST_ERR_UNSUPPORTED;
+  }
+  if (sc.nt <= 16) {
+    sc.th = 1;
+  } else if (sc.nt <= 32) {
+    sc.th = 2;
+  } else if (sc.nt <= 64) {
+    sc.th = 4;
+  } else {
+    *err = "local N_t > 64 is not covered by the streaming kernels";
+    return DTST_ERR_UNSUPPORTED;
+  }
+  const bool fold = d->n_local[2] == d->n_global[2] && d->n_global[2] % 2 == 0;
+  sc.ncls = fold ? 2 : 1;
+  const int slots = static_cast<int>(ceil_div(sc.kz, sc.ncls));
+  int kcp = static_cast<int>(round_up(slots, 16));
+  if (kcp == 48) kcp = 64;
+  if (kcp > 64) {
+    *err = "more than 64 retained z modes per parity class is not covered";
+    return DTST_ERR_UNSUPPORTED;
+  }
+  sc.kcp = kcp;
+  sc.mt = kcp / 8;
+  sc.zh = fold ? sc.nz / 2 : sc.nz;
+  sc.zt = static_cast<int>(ceil_div(sc.zh, 16));
+  sc.vec = (sc.nt % 4 == 0) ? 1 : 0;
+  sc.lds_bytes = size_t(sc.ncls) * sc.zt * sc.mt * 64 * 16;
+  if (sc.lds_bytes > 160 * 1024) {
+    *err = "z basis image exceeds the 160 KiB LDS of a workgroup";
+    return DTST_ERR_UNSUPPORTED;
+  }
+
+  // ---- axis contractions ----
+  auto axis = [](int J, int KO, int64_t NN) {
+    AxisCfg a;
+    a.J = J;
+    a.KO = KO;
+    a.NN = static_cast<int>(NN);
+    a.JQ = static_cast<int>(ceil_div(J, 16));
+    a.ktiles = static_cast<int>(ceil_div(KO, 16));
+    return a;
+  };
+  const int64_t nn_y = dv.K[2] * dv.K[3];
+  const int64_t nn_x = dv.K[1] * nn_y;
+  if (nn_x > (int64_t(1) << 30)) {
+    *err = "retained mode count too large";
+    return DTST_ERR_UNSUPPORTED;
+  }
+  dv.ay_f = axis(static_cast<int>(d->n_local[1]), static_cast<int>(dv.K[1]), nn_y);
+  dv.ax_f = axis(static_cast<int>(d->n_local[0]), static_cast<int>(dv.K[0]), nn_x);
+  dv.ax_i = axis(static_cast<int>(dv.K[0]), static_cast<int>(d->n_local[0]), nn_x);
+  dv.ay_i = axis(static_cast<int>(dv.K[1]), static_cast<int>(d->n_local[1]), nn_y);
+
+  // ---- workspace: two complex intermediates of the largest channel count ----
+  const int64_t bc = d->batch * cmax;
+  const size_t w1 = round_up(size_t(bc) * d->n_local[0] * d->n_local[1] * nn_y * 8, 256);
+  const size_t w2 = round_up(size_t(bc) * d->n_local[0] * dv.K[1] * nn_y * 8, 256);
+  dv.ws_bytes = w1 + w2;
+
+  // ---- image offsets (floats, 256-byte aligned) ----
+  Images& im = dv.img;
+  size_t off = 0;
+  auto take = [&off](size_t n) {
+    size_t o = off;
+    off = round_up(off + n, 64);
+    return o;
+  };
+  const size_t t_img = size_t(sc.th) * 4 * sc.ct * 64;
+  const size_t z_img = size_t(sc.ncls) * sc.zt * sc.mt * 64 * 4;
+  im.t_fwd = take(t_img);
+  im.t_fwd_adjoint_of_inverse = take(t_img);
+  im.z_fwd = take(z_img);
+  im.t_inv = take(t_img);
+  im.t_inv_adjoint_of_forward = take(t_img);
+  im.z_inv = take(z_img);
+  auto axis_img = [](const AxisCfg& a) { return size_t(a.ktiles) * a.JQ * 3 * 64 * 4; };
+  im.y_fwd = take(axis_img(dv.ay_f));
+  im.x_fwd = take(axis_img(dv.ax_f));
+  im.y_inv = take(axis_img(dv.ay_i));
+  im.x_inv = take(axis_img(dv.ax_i));
+  im.total = off;
+
+  *out = dv;
+  return DTST_OK;
+}
+
+namespace {
+
+// Complex basis value of dimension dim at (mode position p, local index j).
+inline void bval(const dtst_desc& d, int dim, int64_t p, int64_t j, double* re, double* im) {
+  twiddle(d.n_global[dim], retained_index(d, dim, p), d.offset[dim] + j, re, im);
+}
+
+// t image of the forward streaming kernel (B operand of the first MFMA):
+// entry ((h*4 + j)*CT + ct)*64 + lane holds Bt'[t][c] with t = 16h + 4g + j,
+// c = 16ct + m (m = lane & 15, g = lane >> 4); c < 8CT is Re B_t[kt=c][t],
+// otherwise Im B_t[kt = c - 8CT][t]; times scale(kt).
+void t_forward_image(const Derived& dv, bool adjoint_of_inverse, float* dst) {
+  const StreamCfg& sc = dv.sc;
+  const dtst_desc& d = dv.d;
+  const int ktp = 8 * sc.ct;
+  const double ntot = double(d.n_global[0]) * d.n_global[1] * d.n_global[2] * d.n_global[3];
+  for (int h = 0; h < sc.th; ++h)
+    for (int j = 0; j < 4; ++j)
+      for (int ct = 0; ct < sc.ct; ++ct)
+        for (int lane = 0; lane < 64; ++lane) {
+          const int m = lane & 15, g = lane >> 4;
+          const int t = 16 * h + 4 * g + j;
+          const int c = 16 * ct + m;
+          const bool is_re = c < ktp;
+          const int kt = is_re ? c : c - ktp;
+          double v = 0.0;
+          if (t < sc.nt && kt < sc.kt) {
+            double re, im;
+            bval(d, 3, kt, t, &re, &im);
+            double s = adjoint_of_inverse ? half_weight(d.n_global[3], kt) / ntot : 1.0;
+            v = s * (is_re ? re : im);
+          }
+          dst[((h * 4 + j) * sc.ct + ct) * 64 + lane] = static_cast<float>(v);
+        }
+}
+
+// z image of the forward streaming kernel (A operand of the second MFMA,
+// staged in LDS): float4 entry ((cl*ZT + zt)*MT + mt)*64 + lane, component
+// i, holds row r = 16mt + m at z = 16zt + 4g + i of class cl; rows [0, KCP)
+// are Re B_z[p][z], rows [KCP, 2KCP) are Im B_z[p][z], p = s*NCLS + cl.
+void z_forward_image(const Derived& dv, float* dst) {
+  const StreamCfg& sc = dv.sc;
+  const dtst_desc& d = dv.d;
+  for (int cl = 0; cl < sc.ncls; ++cl)
+    for (int zt = 0; zt < sc.zt; ++zt)
+      for (int mt = 0; mt < sc.mt; ++mt)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int i = 0; i < 4; ++i) {
+            const int m = lane & 15, g = lane >> 4;
+            const int row = 16 * mt + m;
+            const int z = 16 * zt + 4 * g + i;
+            const bool is_re = row < sc.kcp;
+            const int s = is_re ? row : row - sc.kcp;
+            const int p = s * sc.ncls + cl;
+            double v = 0.0;
+            if (p < sc.kz && z < sc.zh) {
+              double re, im;
+              bval(d, 2, p, z, &re, &im);
+              v = is_re ? re : im;
+            }
+            dst[((((size_t)cl * sc.zt + zt) * sc.mt + mt) * 64 + lane) * 4 + i] = static_cast<float>(v);
+          }
+}
+
+// t image of the inverse streaming kernel (A operand of its second MFMA):
+// entry ((mt*CT + ct)*4 + i)*64 + lane holds A[t][c] with t = 16mt + m,
+// c = 16ct + 4g + i: Re C_t[t][kt] for c < 8CT, -Im C_t[t][kt] otherwise,
+// where C_t[t][kt] = scale(kt) conj(B_t[kt][t]).
+void t_inverse_image(const Derived& dv, bool is_inverse, float* dst) {
+  const StreamCfg& sc = dv.sc;
+  const dtst_desc& d = dv.d;
+  const int ktp = 8 * sc.ct;
+  const double ntot = double(d.n_global[0]) * d.n_global[1] * d.n_global[2] * d.n_global[3];
+  for (int mt = 0; mt < sc.th; ++mt)
+    for (int ct = 0; ct < sc.ct; ++ct)
+      for (int i = 0; i < 4; ++i)
+        for (int lane = 0; lane < 64; ++lane) {
+          const int m = lane & 15, g = lane >> 4;
+          const int t = 16 * mt + m;
+          const int c = 16 * ct + 4 * g + i;
+          const bool is_re = c < ktp;
+          const int kt = is_re ? c : c - ktp;
+          double v = 0.0;
+          if (t < sc.nt && kt < sc.kt) {
+            double re, im;
+            bval(d, 3, kt, t, &re, &im);  // B_t = re + i im; conj(B_t) = re - i im
+            const double s = is_inverse ? half_weight(d.n_global[3], kt) / ntot : 1.0;
+            v = is_re ? s * re : s * im;  // -Im(s conj B_t) = s * im
+          }
+          dst[((mt * sc.ct + ct) * 4 + i) * 64 + lane] = static_cast<float>(v);
+        }
+}
+
+// z image of the inverse streaming kernel (B operand of its first MFMA,
+// staged in LDS): float4 entry ((cl*ZT + zt)*MT + q)*64 + lane, component
+// i, holds row kz' = 16q + 4g + i at z = 16zt + m: Re C_z[z][p] for
+// kz' < KCP and Im C_z[z][p] otherwise, C_z[z][p] = conj(B_z[p][z]).
+void z_inverse_image(const Derived& dv, float* dst) {
+  const StreamCfg& sc = dv.sc;
+  const dtst_desc& d = dv.d;
+  for (int cl = 0; cl < sc.ncls; ++cl)
+    for (int zt = 0; zt < sc.zt; ++zt)
+      for (int q = 0; q < sc.mt; ++q)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int i = 0; i < 4; ++i) {
+            const int m = lane & 15, g = lane >> 4;
+            const int kzp = 16 * q + 4 * g + i;
+            const int z = 16 * zt + m;
+            const bool is_re = kzp < sc.kcp;
+            const int s = is_re ? kzp : kzp - sc.kcp;
+            const int p = s * sc.ncls + cl;
+            double v = 0.0;
+            if (p < sc.kz && z < sc.zh) {
+              double re, im;
+              bval(d, 2, p, z, &re, &im);
+              v = is_re ? re : -im;
+            }
+            dst[((((size_t)cl * sc.zt + zt) * sc.mt + q) * 64 + lane) * 4 + i] = static_cast<float>(v);
+          }
+}
+
+// Axis image: float4 entry ((kt*JQ + q)*3 + part)*64 + lane, component i,
+// holds part (Re, Im, -Im) of basis[k][j], k = 16kt + m, j = 16q + 4g + i.
+// forward: basis[k][j] = B_dim[k][j]; inverse: basis[k][j] = conj(B_dim[j][k]).
+void axis_image(const Derived& dv, const AxisCfg& a, int dim, bool inverse, float* dst) {
+  const dtst_desc& d = dv.d;
+  for (int kt = 0; kt < a.ktiles; ++kt)
+    for (int q = 0; q < a.JQ; ++q)
+      for (int part = 0; part < 3; ++part)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int i = 0; i < 4; ++i) {
+            const int m = lane & 15, g = lane >> 4;
+            const int k = 16 * kt + m;
+            const int j = 16 * q + 4 * g + i;
+            double v = 0.0;
+            if (k < a.KO && j < a.J) {
+              double re, im;
+              if (inverse) {
+                bval(d, dim, j, k, &re, &im);
+                im = -im;
+              } else {
+                bval(d, dim, k, j, &re, &im);
+              }
+              v = part == 0 ? re : (part == 1 ? im : -im);
+            }
+            dst[((((size_t)kt * a.JQ + q) * 3 + part) * 64 + lane) * 4 + i] = static_cast<float>(v);
+          }
+}
+
+}  // namespace
+
+void build_images(const Derived& dv, std::vector<float>* blob) {
+  blob->assign(dv.img.total, 0.0f);
+  float* b = blob->data();
+  t_forward_image(dv, false, b + dv.img.t_fwd);
+  t_forward_image(dv, true, b + dv.img.t_fwd_adjoint_of_inverse);
+  z_forward_image(dv, b + dv.img.z_fwd);
+  t_inverse_image(dv, true, b + dv.img.t_inv);
+  t_inverse_image(dv, false, b + dv.img.t_inv_adjoint_of_forward);
+  z_inverse_image(dv, b + dv.img.z_inv);
+  axis_image(dv, dv.ay_f, 1, false, b + dv.img.y_fwd);
+  axis_image(dv, dv.ax_f, 0, false, b + dv.img.x_fwd);
+  axis_image(dv, dv.ay_i, 1, true, b + dv.img.y_inv);
+  axis_image(dv, dv.ax_i, 0, true, b + dv.img.x_inv);
+}
+
+void plain_basis(const dtst_desc& d, int dim, int kind, float* out) {
+  const int64_t K = dim < 3 ? 2 * int64_t(d.kmax[dim]) : d.kt;
+  const int64_t n = d.n_local[dim];
+  for (int64_t p = 0; p < K; ++p)
+    for (int64_t j = 0; j < n; ++j) {
+      double re, im;
+      bval(d, dim, p, j, &re, &im);
+      out[(p * n + j) * 2 + 0] = static_cast<float>(re);
+      out[(p * n + j) * 2 + 1] = static_cast<float>(kind == 1 ? -im : im);
+    }
+}
+
+}  // namespace dtst

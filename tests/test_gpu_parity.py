@@ -1,0 +1,242 @@
+"""GPU parity of every C-ABI call against the fp64 oracle, element by element,
+on the same fp32 inputs, at sizes the oracle handles in seconds.  The cases
+cover several MFMA tiles plus ragged tails in every dimension, odd extents,
+the folded and unfolded z paths, both k_t column layouts, shards with
+offsets (slab, pencil, t-shard), retained counts above the local extent,
+full retention, and empty calls."""
+
+import numpy as np
+import pytest
+
+import oracle as O
+from gpu_common import (Guarded, check, desc_of, dev, geometry, np_of, rand_cplx, rand_real, say,
+                        torch_gpu)
+
+pytestmark = pytest.mark.gpu
+
+# name: (n_global, n_local, offset, kmax, kt, B, C_in, C_out)
+CASES = {
+    "tiny_baseline": ((12, 10, 8, 8), (12, 10, 8, 8), (0, 0, 0, 0), (3, 2, 2), 3, 1, 2, 2),
+    "tiny_slab": ((12, 10, 8, 8), (4, 10, 8, 8), (4, 0, 0, 0), (3, 2, 2), 3, 1, 2, 2),
+    "tiny_pencil": ((12, 10, 8, 8), (4, 5, 8, 8), (8, 5, 0, 0), (3, 2, 2), 3, 2, 1, 3),
+    "odd_extents": ((9, 7, 5, 6), (9, 7, 5, 6), (0, 0, 0, 0), (2, 3, 1), 3, 1, 1, 1),
+    "odd_shard": ((9, 7, 5, 6), (3, 7, 5, 6), (6, 0, 0, 0), (2, 3, 1), 4, 1, 1, 1),
+    "nyquist_t": ((6, 6, 4, 6), (6, 6, 4, 6), (0, 0, 0, 0), (2, 2, 1), 4, 1, 1, 1),
+    "k_above_nloc": ((12, 6, 4, 4), (2, 6, 4, 4), (6, 0, 0, 0), (3, 1, 1), 2, 1, 1, 1),
+    "all_modes": ((6, 4, 4, 6), (6, 4, 4, 6), (0, 0, 0, 0), (3, 2, 2), 4, 1, 1, 1),
+    "t_shard_odd": ((8, 6, 4, 10), (8, 6, 4, 5), (0, 0, 0, 5), (2, 2, 1), 4, 1, 2, 1),
+    "fold_ragged": ((24, 40, 48, 32), (24, 40, 48, 32), (0, 0, 0, 0), (5, 9, 11), 7, 2, 3, 5),
+    "slab_like_cfg2": ((64, 64, 64, 32), (16, 64, 64, 32), (32, 0, 0, 0), (16, 16, 16), 8, 1, 3, 2),
+    "z_shard_unfolded": ((16, 20, 64, 16), (16, 20, 30, 16), (0, 0, 17, 0), (4, 5, 9), 5, 1, 2, 2),
+    "kt16_two_col_tiles": ((16, 16, 32, 32), (16, 16, 32, 32), (0, 0, 0, 0), (4, 4, 8), 16, 1, 2, 2),
+    "kz64_unfolded_odd_nz": ((8, 8, 129, 8), (8, 8, 129, 8), (0, 0, 0, 0), (2, 2, 32), 5, 1, 1, 2),
+    "nt64_kt12": ((8, 12, 20, 64), (8, 12, 20, 64), (0, 0, 0, 0), (2, 3, 5), 12, 1, 2, 1),
+    "nt21_pdebench_like": ((16, 16, 16, 21), (16, 16, 16, 21), (0, 0, 0, 0), (4, 4, 4), 8, 1, 2, 2),
+    "cfg1_full": ((32, 32, 32, 8), (32, 32, 32, 8), (0, 0, 0, 0), (8, 8, 8), 4, 1, 8, 8),
+}
+
+
+def _setup(name):
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry(*CASES[name])
+    g.validate()
+    say(f"[case {name}] n_global={g.n_global} n_local={g.n_local} offset={g.offset} "
+        f"kmax={g.kmax} kt={g.kt} B={g.batch} Cin={g.c_in} Cout={g.c_out}")
+    plan = D.Plan(desc_of(g))
+    return torch, D, g, plan
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_forward_and_accumulate(name):
+    torch, D, g, plan = _setup(name)
+    x = rand_real((g.batch, g.c_in) + g.n_local, 101)
+    ref = O.forward(x, g)
+    out = Guarded(torch, plan.spectral_shape(g.c_in), torch.complex64)
+    plan.forward(dev(torch, x), out.t)
+    torch.cuda.synchronize()
+    check(np_of(out.t), ref, "forward")
+    assert out.guards_intact()
+    plan.forward(dev(torch, x), out.t, accumulate=True)
+    torch.cuda.synchronize()
+    check(np_of(out.t), 2 * ref, "forward accumulate")
+    assert out.guards_intact()
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_inverse(name):
+    torch, D, g, plan = _setup(name)
+    yh = rand_cplx((g.batch, g.c_out) + g.K, 102)
+    ref = O.inverse(yh, g)
+    out = Guarded(torch, plan.spatial_shape(g.c_out), torch.float32)
+    plan.inverse(dev(torch, yh), out.t)
+    torch.cuda.synchronize()
+    check(np_of(out.t), ref, "inverse")
+    assert out.guards_intact()
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_adjoints(name):
+    torch, D, g, plan = _setup(name)
+    G = rand_cplx((g.batch, g.c_in) + g.K, 103)
+    out = Guarded(torch, plan.spatial_shape(g.c_in), torch.float32)
+    plan.forward_adj(dev(torch, G), out.t)
+    torch.cuda.synchronize()
+    check(np_of(out.t), O.forward_adj(G, g), "forward_adj")
+    assert out.guards_intact()
+    gy = rand_real((g.batch, g.c_out) + g.n_local, 104)
+    ref = O.inverse_adj(gy, g)
+    out2 = Guarded(torch, plan.spectral_shape(g.c_out), torch.complex64)
+    plan.inverse_adj(dev(torch, gy), out2.t)
+    torch.cuda.synchronize()
+    check(np_of(out2.t), ref, "inverse_adj")
+    plan.inverse_adj(dev(torch, gy), out2.t, accumulate=True)
+    torch.cuda.synchronize()
+    check(np_of(out2.t), 2 * ref, "inverse_adj accumulate")
+    assert out2.guards_intact()
+
+
+@pytest.mark.parametrize("name", ["tiny_pencil", "fold_ragged", "cfg1_full", "kt16_two_col_tiles"])
+def test_mix_ranges_and_wgrad(name):
+    torch, D, g, plan = _setup(name)
+    M = plan.n_modes
+    X = rand_cplx((g.batch, g.c_in) + g.K, 105)
+    W = rand_cplx((M, g.c_in, g.c_out), 106, var=1.0 / (g.c_in * g.c_out))
+    Xd, Wd = dev(torch, X), dev(torch, W)
+    # full range
+    Y = Guarded(torch, plan.spectral_shape(g.c_out), torch.complex64)
+    plan.mix(Xd, Wd, Y.t, 0, M, op=0)
+    torch.cuda.synchronize()
+    check(np_of(Y.t).reshape(g.batch, g.c_out, M), O.mix(X, W, 0, M), "mix full")
+    assert Y.guards_intact()
+    # a middle range leaves every other column untouched
+    m0, m1 = M // 3, (2 * M) // 3 + 1
+    sentinel = rand_cplx((g.batch, g.c_out) + g.K, 107)
+    Y2 = Guarded(torch, plan.spectral_shape(g.c_out), torch.complex64, fill=dev(torch, sentinel))
+    plan.mix(Xd, Wd[m0:m1].contiguous(), Y2.t, m0, m1, op=0)
+    torch.cuda.synchronize()
+    ref = O.mix(X, W[m0:m1], m0, m1, yhat_in=sentinel)
+    got = np_of(Y2.t).reshape(g.batch, g.c_out, M)
+    check(got[:, :, m0:m1], ref[:, :, m0:m1], "mix range")
+    assert np.array_equal(got[:, :, :m0], sentinel.reshape(g.batch, g.c_out, M)[:, :, :m0])
+    assert np.array_equal(got[:, :, m1:], sentinel.reshape(g.batch, g.c_out, M)[:, :, m1:])
+    assert Y2.guards_intact()
+    # ranges run one after another assemble the full mix (replaces the AllGather)
+    Y3 = torch.zeros(plan.spectral_shape(g.c_out), dtype=torch.complex64, device="cuda")
+    bounds = np.linspace(0, M, 5).astype(int)
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        plan.mix(Xd, Wd[a:b].contiguous(), Y3, int(a), int(b), op=0)
+    torch.cuda.synchronize()
+    check(np_of(Y3).reshape(g.batch, g.c_out, M), O.mix(X, W, 0, M), "mix pieced")
+    # data gradient (op = 1)
+    GY = rand_cplx((g.batch, g.c_out) + g.K, 108)
+    GX = Guarded(torch, plan.spectral_shape(g.c_in), torch.complex64)
+    plan.mix(dev(torch, GY), Wd, GX.t, 0, M, op=1)
+    torch.cuda.synchronize()
+    check(np_of(GX.t).reshape(g.batch, g.c_in, M), O.mix_data_grad(GY, W, 0, M), "mix data grad")
+    assert GX.guards_intact()
+    # weight gradient on a range, with accumulate
+    GW = Guarded(torch, (m1 - m0, g.c_in, g.c_out), torch.complex64)
+    plan.wgrad(Xd, dev(torch, GY), GW.t, m0, m1)
+    torch.cuda.synchronize()
+    refw = O.mix_wgrad(X, GY, m0, m1)
+    check(np_of(GW.t), refw, "wgrad")
+    plan.wgrad(Xd, dev(torch, GY), GW.t, m0, m1, accumulate=True)
+    torch.cuda.synchronize()
+    check(np_of(GW.t), 2 * refw, "wgrad accumulate")
+    assert GW.guards_intact()
+
+
+def test_slab_sum_equals_full_domain():
+    """Eq. (dtst_reduce) on one GPU: per-slab forwards accumulated into one
+    output equal the full-domain coefficients (and the oracle)."""
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    ng, k, kt, B, C = (32, 24, 16, 8), (6, 5, 4), 5, 1, 3
+    x = rand_real((B, C) + ng, 109)
+    full = geometry(ng, ng, (0, 0, 0, 0), k, kt, B, C, C)
+    ref = O.forward(x, full)
+    acc = torch.zeros((B, C) + full.K, dtype=torch.complex64, device="cuda")
+    for p in range(4):
+        g = geometry(ng, (8,) + ng[1:], (8 * p, 0, 0, 0), k, kt, B, C, C)
+        plan = D.Plan(desc_of(g))
+        plan.forward(dev(torch, x[:, :, 8 * p:8 * p + 8]), acc, accumulate=(p > 0))
+    torch.cuda.synchronize()
+    check(np_of(acc), ref, "sum over x-slabs")
+    # pencil split over x and y, accumulated
+    acc2 = torch.zeros_like(acc)
+    first = True
+    for px in range(2):
+        for py in range(2):
+            g = geometry(ng, (16, 12, 16, 8), (16 * px, 12 * py, 0, 0), k, kt, B, C, C)
+            plan = D.Plan(desc_of(g))
+            plan.forward(dev(torch, x[:, :, 16 * px:16 * px + 16, 12 * py:12 * py + 12]), acc2, accumulate=not first)
+            first = False
+    torch.cuda.synchronize()
+    check(np_of(acc2), ref, "sum over pencils")
+
+
+def test_gpu_adjoint_dot_products():
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry(*CASES["fold_ragged"])
+    plan = D.Plan(desc_of(g))
+    x = dev(torch, rand_real((g.batch, g.c_in) + g.n_local, 110)).double()
+    G = dev(torch, rand_cplx((g.batch, g.c_in) + g.K, 111))
+    Fx = torch.empty(plan.spectral_shape(g.c_in), dtype=torch.complex64, device="cuda")
+    plan.forward(x.float(), Fx)
+    FtG = torch.empty(plan.spatial_shape(g.c_in), dtype=torch.float32, device="cuda")
+    plan.forward_adj(G, FtG)
+    lhs = torch.real(torch.vdot(G.flatten().to(torch.complex128), Fx.flatten().to(torch.complex128))).item()
+    rhs = torch.dot(FtG.double().flatten(), x.flatten()).item()
+    assert abs(lhs - rhs) <= 1e-5 * abs(lhs)
+
+
+def test_empty_batch_and_empty_range_are_noops():
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry((8, 8, 8, 8), (8, 8, 8, 8), (0, 0, 0, 0), (2, 2, 2), 3, 0, 2, 2)
+    plan = D.Plan(desc_of(g))
+    assert plan.ws_bytes == 0
+    x = torch.empty((0, 2, 8, 8, 8, 8), dtype=torch.float32, device="cuda")
+    xh = torch.empty((0, 2) + g.K, dtype=torch.complex64, device="cuda")
+    plan.forward(x, xh)
+    plan.inverse(xh, x)
+    g1 = geometry((8, 8, 8, 8), (8, 8, 8, 8), (0, 0, 0, 0), (2, 2, 2), 3, 1, 2, 2)
+    plan1 = D.Plan(desc_of(g1))
+    X = torch.ones((1, 2) + g1.K, dtype=torch.complex64, device="cuda")
+    Y = torch.full((1, 2) + g1.K, 3.0, dtype=torch.complex64, device="cuda")
+    W = torch.empty((0, 2, 2), dtype=torch.complex64, device="cuda")
+    D.dtst_mix(plan1.handle, X, W, Y, 5, 5, 0)
+    torch.cuda.synchronize()
+    assert bool((Y == 3.0).all().item())
+
+
+def test_errors_launch_nothing():
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry(*CASES["tiny_slab"])
+    plan = D.Plan(desc_of(g))
+    x = dev(torch, rand_real((g.batch, g.c_in) + g.n_local, 112))
+    out = torch.full(plan.spectral_shape(g.c_in), 5.0, dtype=torch.complex64, device="cuda")
+    small_ws = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(D.DtstError) as e:
+        D.dtst_forward(plan.handle, x, out, 0, small_ws)
+    assert e.value.status == 1 and "workspace" in str(e.value)
+    with pytest.raises(D.DtstError):
+        D.dtst_mix(plan.handle, out, out, out, 0, plan.n_modes + 1, 0)
+    with pytest.raises(D.DtstError):
+        D.dtst_mix(plan.handle, out, out, out, 0, 1, 2)
+    with pytest.raises(D.DtstError):
+        D.dtst_forward(plan.handle, x, out, 2, plan.ws)
+    mis = torch.empty(plan.spectral_shape(g.c_in)[0] * 1000 + 8, dtype=torch.uint8, device="cuda")[4:]
+    with pytest.raises(D.DtstError) as e:
+        D.dtst_forward(plan.handle, x, mis, 0, plan.ws)
+    assert "aligned" in str(e.value)
+    torch.cuda.synchronize()
+    assert bool((out == 5.0).all().item())
+    h = plan.handle
+    plan.close()
+    with pytest.raises(D.DtstError) as e:
+        D.dtst_forward(h, x, out, 0, small_ws)
+    assert "destroyed" in str(e.value)
