@@ -1,0 +1,297 @@
+#!/usr/bin/env python3
+"""Benchmark of one DTST spectral layer (forward partial DFT + mode-wise
+channel mix + inverse partial DFT) on one MI355X.
+
+A step is one pass of the whole layer over one batch of synthetic input
+already resident in HBM.  The default workload is the 128^3 x 32 global grid
+split into 8 x-slabs of 16 (B = 1, C = 16, modes 32/32/32/8), run the way the
+method runs on 8 GPUs but one shard after another on this GPU: the slab
+forwards accumulate into one spectrum (the sum that replaces the AllReduce),
+the mix runs over the 8 mode ranges S_p in turn (which assembles the full
+spectrum the AllGather would), and every slab is then expanded back.
+
+Prints one JSON line with the step time, the layer's GB/s and TFLOP/s, a
+roofline entry for the kernel that takes the most time (its average launch
+time measured here with HIP events on the launch stream), and the fp64 CPU
+oracle timed on a bounded sample of the same workload on this host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+FP32_MFMA_PEAK_TFS = 157.3   # MI355X dense fp32 matrix
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "hbm_counters.json")
+STREAM_SRC = os.path.join(ROOT, "paper_2607_14394_amd", "csrc", "k_stream.hip")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4],
+                    help="workload table entry (default 2: 128^3x32 in 8 x-slabs)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-times", action="store_true",
+                    help="skip the per-kernel event pass (used under rocprofv3)")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+# Algorithmic work of each kernel role (direct-definition counts: a real x
+# complex multiply-add is 4 flops, complex x complex 8; bytes are the
+# tensors each kernel must read and write once).
+# ---------------------------------------------------------------------------
+def work(g, channels, m_count=None):
+    B = g["batch"]
+    Nx, Ny, Nz, Nt = g["n_local"]
+    k = g["kmax"]
+    Kx, Ky, Kz, Kt = 2 * k[0], 2 * k[1], 2 * k[2], g["kt"]
+    C = channels
+    M = Kx * Ky * Kz * Kt
+    rows = B * C * Nx * Ny
+    w = {}
+    w["stream_fwd_tz"] = dict(
+        bytes=rows * (Nz * Nt * 4 + Kz * Kt * 8),
+        flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz,
+        mfma_flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz * (0.5 if _folded(g) else 1.0))
+    w["axis_fwd_y"] = dict(bytes=B * C * Nx * (Ny + Ky) * Kz * Kt * 8, flops=B * C * Nx * Kz * Kt * 8 * Ky * Ny)
+    w["axis_fwd_x"] = dict(bytes=B * C * (Nx + Kx) * Ky * Kz * Kt * 8, flops=B * C * Ky * Kz * Kt * 8 * Kx * Nx)
+    w["axis_inv_x"] = dict(bytes=w["axis_fwd_x"]["bytes"], flops=w["axis_fwd_x"]["flops"])
+    w["axis_inv_y"] = dict(bytes=w["axis_fwd_y"]["bytes"], flops=w["axis_fwd_y"]["flops"])
+    w["stream_inv_zt"] = dict(bytes=w["stream_fwd_tz"]["bytes"], flops=w["stream_fwd_tz"]["flops"],
+                              mfma_flops=w["stream_fwd_tz"]["mfma_flops"])
+    mc = M if m_count is None else m_count
+    ci, co = g["c_in"], g["c_out"]
+    w["mix"] = dict(bytes=mc * ci * co * 8 + B * (ci + co) * mc * 8, flops=8 * B * mc * ci * co)
+    for v in w.values():
+        v.setdefault("mfma_flops", v["flops"])
+    return w
+
+
+def _folded(g):
+    return g["n_local"][2] == g["n_global"][2] and g["n_global"][2] % 2 == 0
+
+
+def _sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+# ---------------------------------------------------------------------------
+def build_workload(torch, D, synth, cfg, device):
+    c = synth.CONFIGS[cfg]
+    shards = []
+    if cfg == 2:
+        full = synth.full_domain(2)
+        x_full = synth.torch_input(2, full, device)
+        P = c["shards"]
+        lx = c["n_local"][0]
+        for p in range(P):
+            g = synth.geometry(2, p)
+            shards.append((g, x_full[:, :, p * lx:(p + 1) * lx].contiguous()))
+        del x_full
+        torch.cuda.empty_cache()
+    else:
+        g = synth.geometry(cfg)
+        shards.append((g, synth.torch_input(cfg, g, device)))
+    g0 = shards[0][0]
+    plans = [D.Plan(g, device) for g, _ in shards]
+    M = plans[0].n_modes
+    W = synth.torch_weights(M, g0["c_in"], g0["c_out"], synth.seed_of(cfg, "weights"), device)
+    xhat = torch.empty(plans[0].spectral_shape(g0["c_in"]), dtype=torch.complex64, device=device)
+    yhat = torch.empty(plans[0].spectral_shape(g0["c_out"]), dtype=torch.complex64, device=device)
+    ys = [torch.empty(p.spatial_shape(g0["c_out"]), dtype=torch.float32, device=device) for p in plans]
+    P = len(plans) if cfg == 2 else 1
+    bounds = [(M * r) // P for r in range(P + 1)]
+    ranges = [(bounds[r], bounds[r + 1]) for r in range(P)]
+    return shards, plans, W, xhat, yhat, ys, ranges
+
+
+def layer_step(plans, shards, W, xhat, yhat, ys, ranges):
+    for p, (plan, (_, x)) in enumerate(zip(plans, shards)):
+        plan.forward(x, xhat, accumulate=p > 0)
+    for m0, m1 in ranges:
+        plans[0].mix(xhat, W[m0:m1], yhat, m0, m1)
+    for plan, y in zip(plans, ys):
+        plan.inverse(yhat, y)
+
+
+def cpu_baseline(torch, synth, cfg, shards, W, layer_bytes):
+    """The fp64 oracle on a bounded sample: shard 0's forward, the mix over
+    one mode range, shard 0's inverse (1/P of the layer for P shards)."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+    except Exception:  # pragma: no cover
+        threadpool_limits = None
+    cores = len(os.sched_getaffinity(0))
+    g, x = shards[0]
+    P = len(shards)
+    M = W.shape[0]
+    m1 = M // P
+    geo = O.Geometry(g["n_global"], g["n_local"], g["offset"], g["kmax"], g["kt"], g["batch"], g["c_in"], g["c_out"])
+    xs = x.cpu().numpy()
+    Ws = W[:m1].cpu().numpy()
+    ctx = threadpool_limits(limits=cores) if threadpool_limits else None
+    try:
+        t0 = time.perf_counter()
+        X = O.forward(xs, geo)
+        Y = O.mix(X, Ws, 0, m1, c_out=g["c_out"])
+        O.inverse(Y.reshape((g["batch"], g["c_out"]) + geo.K), geo)
+        dt = time.perf_counter() - t0
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1) if threadpool_limits else cores
+    finally:
+        if ctx is not None:
+            ctx.__exit__(None, None, None)
+    frac = 1.0 / P
+    return {"value": round(layer_bytes * frac / dt / 1e9, 3), "unit": "GB/s", "cores": int(threads),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"fp64 oracle: forward of shard 0 ({g['c_in']} channels), mix over modes [0, {m1}), "
+                      f"inverse of shard 0 = 1/{P} of the layer; GB/s scaled by that fraction"}
+
+
+def traffic_entry(kernel, launches_per_step):
+    """HBM bytes per launch from committed FETCH_SIZE / WRITE_SIZE counters,
+    scaled by the copy-kernel calibration; None when the kernel source
+    changed since the counters were taken."""
+    try:
+        with open(COUNTERS_FILE) as f:
+            c = json.load(f)
+    except Exception:
+        return None
+    ent = c.get("kernels", {}).get(kernel)
+    if not ent or ent.get("source_sha") != _sha(STREAM_SRC):
+        return None
+    return ent["fetch_kib"] * 1024 * c["fetch_scale"] + ent["write_kib"] * 1024 * c["write_scale"]
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs every shard of the decomposition one after "
+              "another on a single MI355X (no collectives); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_14394_amd as D
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    device = "cuda"
+    cfg = args.workload
+    log(f"building workload {cfg}")
+    shards, plans, W, xhat, yhat, ys, ranges = build_workload(torch, D, synth, cfg, device)
+    g0 = shards[0][0]
+    log(f"warmup {args.warmup} steps")
+
+    # ---- warmup ----
+    for _ in range(args.warmup):
+        layer_step(plans, shards, W, xhat, yhat, ys, ranges)
+    torch.cuda.synchronize()
+
+    log(f"timing {args.steps} steps")
+    # ---- timed region: K steps bracketed by events on the launch stream ----
+    stream = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        layer_step(plans, shards, W, xhat, yhat, ys, ranges)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+
+    # ---- per-kernel pass: every launch bracketed by HIP events ----
+    kernel_ms = {}
+    if not args.no_kernel_times:
+        D.dtst_profile_enable(True)
+        D.dtst_profile_collect()
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            layer_step(plans, shards, W, xhat, yhat, ys, ranges)
+        torch.cuda.synchronize()
+        prof = D.dtst_profile_collect()
+        D.dtst_profile_enable(False)
+        kernel_ms = {k: (n, tot / n) for k, (n, tot) in prof.items()}
+
+    # ---- accounting ----
+    P = len(shards)
+    per = work(g0, g0["c_in"])
+    per_mix = work(g0, g0["c_in"], m_count=plans[0].n_modes // P)
+    launches = {"stream_fwd_tz": P, "axis_fwd_y": P, "axis_fwd_x": P, "mix": P, "axis_inv_x": P,
+                "axis_inv_y": P, "stream_inv_zt": P}
+    layer_flops = sum(per[k]["flops"] * n for k, n in launches.items() if k != "mix") + P * per_mix["mix"]["flops"]
+    layer_mfma = sum(per[k]["mfma_flops"] * n for k, n in launches.items() if k != "mix") + P * per_mix["mix"]["flops"]
+    B, ci, co = g0["batch"], g0["c_in"], g0["c_out"]
+    vol = 1
+    for v in g0["n_local"]:
+        vol *= v
+    M = plans[0].n_modes
+    layer_bytes = P * B * (ci + co) * vol * 4 + M * ci * co * 8   # read x, write y, read W
+    sec = ms_per_step / 1e3
+    gbs = layer_bytes / sec / 1e9
+
+    roof = None
+    stages = {}
+    if kernel_ms:
+        for k, (n, avg) in kernel_ms.items():
+            wk = per_mix["mix"] if k == "mix" else per.get(k)
+            if wk is None:
+                continue
+            stages[k] = {"launches_per_step": n // args.steps, "avg_ms": round(avg, 4),
+                         "GB_s": round(wk["bytes"] / (avg / 1e3) / 1e9, 1),
+                         "TFLOP_s": round(wk["flops"] / (avg / 1e3) / 1e12, 2),
+                         "mfma_TFLOP_s": round(wk["mfma_flops"] / (avg / 1e3) / 1e12, 2)}
+        dom = max(kernel_ms, key=lambda k: kernel_ms[k][0] * kernel_ms[k][1])
+        n, avg = kernel_ms[dom]
+        wk = per_mix["mix"] if dom == "mix" else per[dom]
+        ach = wk["bytes"] / (avg / 1e3) / 1e9
+        tr = traffic_entry(dom, n // args.steps)
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None if tr is None else int(tr),
+                "algorithmic_bytes_per_launch": int(wk["bytes"]), "avg_launch_ms": round(avg, 4)}
+
+    out = {
+        "metric": "spectral-layer ms and GB/s + TFLOP/s per MI355X (fwd partial DFT+mix+inverse)",
+        "value": round(gbs, 2), "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "layer_ms": round(ms_per_step, 4),
+        "layer_TFLOP_s": round(layer_flops / sec / 1e12, 3),
+        "layer_mfma_TFLOP_s": round(layer_mfma / sec / 1e12, 3),
+        "layer_bytes": int(layer_bytes), "layer_flops": int(layer_flops),
+        "config": {"workload": synth.CONFIGS[cfg]["name"], "global_grid": list(g0["n_global"]),
+                   "local_shard": list(g0["n_local"]), "shards_run_in_sequence": P, "batch": B,
+                   "c_in": ci, "c_out": co, "modes": [2 * g0["kmax"][0], 2 * g0["kmax"][1], 2 * g0["kmax"][2],
+                                                      g0["kt"]]},
+        "roofline": roof, "stages": stages,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(torch, synth, cfg, shards, W, layer_bytes)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -160,6 +160,25 @@ dtst_status dtst_inverse_adj(dtst_plan_t p, const float* g_y, void* g_yhat, int 
 dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, void* g_w_shard,
                            int64_t m0, int64_t m1, int accumulate, void* stream);
 
+/* ---- instrumentation ----------------------------------------------------- */
+
+/* Per-kernel device time, for callers that time the path (benchmarks,
+ * tuning).  While enabled, every kernel the execute calls launch is
+ * bracketed by a pair of HIP events recorded on the call's stream; nothing
+ * else changes.  Process-wide; off by default. */
+typedef struct {
+  char name[40];     /* kernel role, e.g. "stream_fwd_tz", "axis_fwd_y", "mix" */
+  int64_t launches;  /* launches collected */
+  double total_ms;   /* summed event-to-event device time */
+} dtst_kernel_time;
+
+dtst_status dtst_profile_enable(int on);
+
+/* Wait for every recorded launch, write up to `capacity` per-kernel totals
+ * (only kernels with launches > 0) to `out`, set *count, and reset the
+ * totals.  Synchronises the host with the recorded events. */
+dtst_status dtst_profile_collect(dtst_kernel_time* out, int capacity, int* count);
+
 /* ---- diagnostics -------------------------------------------------------- */
 const char* dtst_status_string(dtst_status s);
 /* Detail of the last error on the calling thread ("" if none). */

@@ -4,7 +4,7 @@ Argument marshalling only: every function here forwards to the C ABI of the
 same name declared in ``include/dtst.h``.  Device arrays are torch tensors
 (PyTorch provides device memory and streams); their data pointers and the
 current HIP stream are passed straight through.  The library must be built
-(``python -m paper_2607_14394_amd.build``); importing this module fails
+(``python paper_2607_14394_amd/build.py``); importing this module fails
 loudly when it is missing -- there is no fallback implementation.
 """
 
@@ -16,7 +16,8 @@ import os
 __all__ = [
     "DtstError", "Desc", "lib", "make_desc", "dtst_desc_validate", "dtst_desc_workspace_bytes",
     "dtst_basis_host", "dtst_plan", "dtst_plan_destroy", "dtst_plan_info", "dtst_forward", "dtst_mix",
-    "dtst_inverse", "dtst_forward_adj", "dtst_inverse_adj", "dtst_mix_wgrad", "Plan", "LIB_PATH",
+    "dtst_inverse", "dtst_forward_adj", "dtst_inverse_adj", "dtst_mix_wgrad", "dtst_profile_enable",
+    "dtst_profile_collect", "Plan", "LIB_PATH",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdtst.so")
@@ -30,6 +31,10 @@ class DtstError(RuntimeError):
     def __init__(self, status, msg):
         super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
         self.status = status
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 40), ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
 
 
 class Desc(ctypes.Structure):
@@ -48,7 +53,7 @@ class Desc(ctypes.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"libdtst.so not found at {LIB_PATH}; build it with "
-                          "`python -m paper_2607_14394_amd.build` (no fallback path exists)")
+                          "`python paper_2607_14394_amd/build.py` (no fallback path exists)")
     L = ctypes.CDLL(LIB_PATH)
     P, I64, SZ, I, VP = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p
     sig = {
@@ -69,6 +74,10 @@ def _load():
         fn = getattr(L, name)
         fn.argtypes = args
         fn.restype = ctypes.c_int
+    L.dtst_profile_enable.argtypes = [I]
+    L.dtst_profile_enable.restype = ctypes.c_int
+    L.dtst_profile_collect.argtypes = [ctypes.POINTER(KernelTime), I, ctypes.POINTER(I)]
+    L.dtst_profile_collect.restype = ctypes.c_int
     L.dtst_status_string.argtypes = [ctypes.c_int]
     L.dtst_status_string.restype = ctypes.c_char_p
     L.dtst_last_error.argtypes = []
@@ -191,6 +200,19 @@ def dtst_inverse_adj(plan, g_y, g_yhat, accumulate, ws, stream=None):
 def dtst_mix_wgrad(plan, xhat, g_yhat, g_w_shard, m0, m1, accumulate, stream=None):
     _check(lib.dtst_mix_wgrad(plan, _ptr(xhat), _ptr(g_yhat), _ptr(g_w_shard), int(m0), int(m1), int(accumulate),
                               _stream(stream)))
+
+
+def dtst_profile_enable(on=True):
+    _check(lib.dtst_profile_enable(1 if on else 0))
+
+
+def dtst_profile_collect():
+    """{kernel role: (launches, total_ms)} since the last collect."""
+    cap = 32
+    arr = (KernelTime * cap)()
+    n = ctypes.c_int(0)
+    _check(lib.dtst_profile_collect(arr, cap, ctypes.byref(n)))
+    return {arr[i].name.decode(): (arr[i].launches, arr[i].total_ms) for i in range(n.value)}
 
 
 class Plan:

@@ -1,7 +1,7 @@
 """Build step of the DTST library: compiles the HIP/C++ sources under
 ``csrc/`` for gfx950 with hipcc and links ``libdtst.so`` next to this file.
 
-Run ``python -m paper_2607_14394_amd.build`` (or call ``build()``).  Every
+Run ``python paper_2607_14394_amd/build.py`` (or call ``build()``).  Every
 call recompiles.
 """
 

@@ -102,6 +102,65 @@ size_t w1_bytes(const dtst::Derived& dv) {
     if (s_ != DTST_OK) return s_;      \
   } while (0)
 
+// ---- per-kernel event timing (dtst_profile_enable / dtst_profile_collect) ----
+enum KernelRole { K_FWD_TZ, K_AXIS_FWD_Y, K_AXIS_FWD_X, K_AXIS_INV_X, K_AXIS_INV_Y, K_INV_ZT, K_MIX, K_MIX_H,
+                  K_WGRAD, K_COUNT };
+const char* const kRoleNames[K_COUNT] = {"stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "axis_inv_x", "axis_inv_y",
+                                         "stream_inv_zt", "mix", "mix_h", "wgrad"};
+
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  struct Rec {
+    int role;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  double total_ms[K_COUNT] = {};
+  int64_t launches[K_COUNT] = {};
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Profiler& prof() {
+  static Profiler p;
+  return p;
+}
+
+// Runs one launcher; when profiling is on, brackets it with events on `stream`.
+template <class F>
+int timed(int role, void* stream, F&& launch) {
+  Profiler& P = prof();
+  bool on;
+  {
+    std::lock_guard<std::mutex> lk(P.mu);
+    on = P.on;
+  }
+  if (!on) return launch();
+  hipEvent_t a, b;
+  {
+    std::lock_guard<std::mutex> lk(P.mu);
+    a = P.get();
+    b = P.get();
+  }
+  if (a == nullptr || b == nullptr) return launch();
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipEventRecord(a, s);
+  const int e = launch();
+  (void)hipEventRecord(b, s);
+  std::lock_guard<std::mutex> lk(P.mu);
+  P.pending.push_back({role, a, b});
+  return e;
+}
+
 // Forward-direction chain: streaming t+z, then y, then x (with accumulate).
 dtst_status run_forward_chain(const dtst_plan_st* p, int64_t channels, const float* x, void* xhat,
                               int accumulate, void* ws, const float* timg, void* stream) {
@@ -111,11 +170,16 @@ dtst_status run_forward_chain(const dtst_plan_st* p, int64_t channels, const flo
   char* w1 = static_cast<char*>(ws);
   char* w2 = w1 + w1_bytes(dv);
   const int64_t rows = B * channels * dv.d.n_local[0] * dv.d.n_local[1];
-  int e = dtst::launch_fwd_tz(dv.sc, x, w1, rows, timg, p->blob + dv.img.z_fwd, stream);
+  int e = timed(K_FWD_TZ, stream,
+                [&] { return dtst::launch_fwd_tz(dv.sc, x, w1, rows, timg, p->blob + dv.img.z_fwd, stream); });
   if (e != hipSuccess) return device_status(e, "t+z contraction launch");
-  e = dtst::launch_axis(dv.ay_f, B * channels * dv.d.n_local[0], w1, w2, p->blob + dv.img.y_fwd, 0, stream);
+  e = timed(K_AXIS_FWD_Y, stream, [&] {
+    return dtst::launch_axis(dv.ay_f, B * channels * dv.d.n_local[0], w1, w2, p->blob + dv.img.y_fwd, 0, stream);
+  });
   if (e != hipSuccess) return device_status(e, "y contraction launch");
-  e = dtst::launch_axis(dv.ax_f, B * channels, w2, xhat, p->blob + dv.img.x_fwd, accumulate, stream);
+  e = timed(K_AXIS_FWD_X, stream, [&] {
+    return dtst::launch_axis(dv.ax_f, B * channels, w2, xhat, p->blob + dv.img.x_fwd, accumulate, stream);
+  });
   if (e != hipSuccess) return device_status(e, "x contraction launch");
   return ok();
 }
@@ -128,12 +192,17 @@ dtst_status run_inverse_chain(const dtst_plan_st* p, int64_t channels, const voi
   if (B == 0) return ok();
   char* v2 = static_cast<char*>(ws);    // (.., Nx, Ny, Kz, Kt)
   char* v1 = v2 + w1_bytes(dv);         // (.., Nx, Ky, Kz, Kt)
-  int e = dtst::launch_axis(dv.ax_i, B * channels, yhat, v1, p->blob + dv.img.x_inv, 0, stream);
+  int e = timed(K_AXIS_INV_X, stream, [&] {
+    return dtst::launch_axis(dv.ax_i, B * channels, yhat, v1, p->blob + dv.img.x_inv, 0, stream);
+  });
   if (e != hipSuccess) return device_status(e, "x expansion launch");
-  e = dtst::launch_axis(dv.ay_i, B * channels * dv.d.n_local[0], v1, v2, p->blob + dv.img.y_inv, 0, stream);
+  e = timed(K_AXIS_INV_Y, stream, [&] {
+    return dtst::launch_axis(dv.ay_i, B * channels * dv.d.n_local[0], v1, v2, p->blob + dv.img.y_inv, 0, stream);
+  });
   if (e != hipSuccess) return device_status(e, "y expansion launch");
   const int64_t rows = B * channels * dv.d.n_local[0] * dv.d.n_local[1];
-  e = dtst::launch_inv_zt(dv.sc, v2, y, rows, timg, p->blob + dv.img.z_inv, stream);
+  e = timed(K_INV_ZT, stream,
+            [&] { return dtst::launch_inv_zt(dv.sc, v2, y, rows, timg, p->blob + dv.img.z_inv, stream); });
   if (e != hipSuccess) return device_status(e, "z+t expansion launch");
   return ok();
 }
@@ -221,6 +290,12 @@ dtst_status dtst_plan(const dtst_desc* d, dtst_plan_t* out) {
     (void)hipFree(p->blob);
     delete p;
     return fail(DTST_ERR_DEVICE, std::string("hipMemcpy of the basis tables: ") + hipGetErrorString(e));
+  }
+  const int pe = dtst::prepare_stream(&p->dv.sc);
+  if (pe != hipSuccess) {
+    (void)hipFree(p->blob);
+    delete p;
+    return fail(DTST_ERR_DEVICE, std::string("kernel setup: ") + hipGetErrorString(static_cast<hipError_t>(pe)));
   }
   {
     std::lock_guard<std::mutex> lk(g_plans_mu);
@@ -315,10 +390,11 @@ dtst_status dtst_mix(dtst_plan_t p, const void* xhat, const void* w_shard, void*
   DTST_TRY(check_ptr(yhat, "yhat"));
   DeviceGuard guard(p->device);
   if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
-  const int e = op == 0 ? dtst::launch_mix(xhat, w_shard, yhat, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0, m1,
-                                           stream)
-                        : dtst::launch_mix_h(xhat, w_shard, yhat, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0,
-                                             m1, stream);
+  const int e = timed(op == 0 ? K_MIX : K_MIX_H, stream, [&] {
+    return op == 0 ? dtst::launch_mix(xhat, w_shard, yhat, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0, m1, stream)
+                   : dtst::launch_mix_h(xhat, w_shard, yhat, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0, m1,
+                                        stream);
+  });
   return device_status(e, "mix launch");
 }
 
@@ -335,9 +411,55 @@ dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, 
   DTST_TRY(check_ptr(g_w_shard, "g_w_shard"));
   DeviceGuard guard(p->device);
   if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
-  const int e = dtst::launch_wgrad(xhat, g_yhat, g_w_shard, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0, m1,
-                                   accumulate, stream);
+  const int e = timed(K_WGRAD, stream, [&] {
+    return dtst::launch_wgrad(xhat, g_yhat, g_w_shard, dv.d.batch, dv.d.c_in, dv.d.c_out, dv.M, m0, m1,
+                              accumulate, stream);
+  });
   return device_status(e, "wgrad launch");
+}
+
+dtst_status dtst_profile_enable(int on) {
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> lk(P.mu);
+  P.on = on != 0;
+  return ok();
+}
+
+dtst_status dtst_profile_collect(dtst_kernel_time* out, int capacity, int* count) {
+  if (count == nullptr || (capacity > 0 && out == nullptr) || capacity < 0)
+    return fail(DTST_ERR_INVALID_ARG, "need count, and out when capacity > 0");
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> lk(P.mu);
+  hipError_t err = hipSuccess;
+  for (const Profiler::Rec& r : P.pending) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e == hipSuccess) {
+      P.total_ms[r.role] += ms;
+      P.launches[r.role] += 1;
+    } else if (err == hipSuccess) {
+      err = e;
+    }
+    P.pool.push_back(r.a);
+    P.pool.push_back(r.b);
+  }
+  P.pending.clear();
+  int n = 0;
+  for (int k = 0; k < K_COUNT; ++k) {
+    if (P.launches[k] == 0) continue;
+    if (n < capacity) {
+      std::snprintf(out[n].name, sizeof(out[n].name), "%s", kRoleNames[k]);
+      out[n].launches = P.launches[k];
+      out[n].total_ms = P.total_ms[k];
+    }
+    ++n;
+    P.launches[k] = 0;
+    P.total_ms[k] = 0.0;
+  }
+  *count = n < capacity ? n : capacity;
+  if (err != hipSuccess) return fail(DTST_ERR_DEVICE, std::string("event timing: ") + hipGetErrorString(err));
+  return ok();
 }
 
 }  // extern "C"

@@ -33,6 +33,8 @@ struct StreamCfg {
   int kcp = 0;  // padded slots per class = 8*mt
   int vec = 0;  // 1 when N_t % 4 == 0 (16-byte row chunks)
   size_t lds_bytes = 0;
+  // filled at plan creation on the plan's device (prepare_stream)
+  int grid_fwd = 0, grid_inv = 0;  // resident workgroups of each kernel
 };
 
 // Generic complex contraction along a middle axis:
@@ -79,6 +81,8 @@ int64_t retained_index(const dtst_desc& d, int dim, int64_t p);
 // Kernel launchers (defined in the .hip sources).  All return hipSuccess or
 // the launch error as an int (hipError_t).
 // ---------------------------------------------------------------------------
+// Sets kernel attributes and resident-grid sizes for the current device.
+int prepare_stream(StreamCfg* c);
 int launch_fwd_tz(const StreamCfg& c, const float* x, void* out, int64_t rows,
                   const float* timg, const float* zimg, void* stream);
 int launch_inv_zt(const StreamCfg& c, const void* in, float* y, int64_t rows,

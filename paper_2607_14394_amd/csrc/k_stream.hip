@@ -321,19 +321,36 @@ StreamArgs args_of(const StreamCfg& c, int64_t rows) {
   return a;
 }
 
-int grid_for(const void* fn, size_t lds, int64_t rows) {
-  int dev = 0;
-  (void)hipGetDevice(&dev);
-  int cus = 256;
-  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, lds) != hipSuccess || per_cu < 1) per_cu = 1;
+int resident_grid(const void* fn, size_t lds) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, lds) != hipSuccess) return 0;
+  return cus * (per_cu > 0 ? per_cu : 1);
+}
+
+int grid_for(int resident, int64_t rows) {
   const int64_t want = (rows + 3) / 4;
-  const int64_t cap = int64_t(cus) * per_cu;
-  return static_cast<int>(want < cap ? want : cap);
+  return static_cast<int>(want < resident ? want : resident);
 }
 
 }  // namespace
+
+int prepare_stream(StreamCfg* c) {
+  fwd_fn f;
+  inv_fn v;
+  pick(*c, &f, &v);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(c->lds_bytes));
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(v), hipFuncAttributeMaxDynamicSharedMemorySize,
+                          int(c->lds_bytes));
+  if (e != hipSuccess) return e;
+  c->grid_fwd = resident_grid(reinterpret_cast<const void*>(f), c->lds_bytes);
+  c->grid_inv = resident_grid(reinterpret_cast<const void*>(v), c->lds_bytes);
+  if (c->grid_fwd <= 0 || c->grid_inv <= 0) return hipErrorInvalidConfiguration;
+  return hipSuccess;
+}
 
 int launch_fwd_tz(const StreamCfg& c, const float* x, void* out, int64_t rows, const float* timg,
                   const float* zimg, void* stream) {
@@ -341,12 +358,8 @@ int launch_fwd_tz(const StreamCfg& c, const float* x, void* out, int64_t rows, c
   fwd_fn f;
   inv_fn v;
   pick(c, &f, &v);
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(c.lds_bytes));
-  if (e != hipSuccess) return e;
-  const int grid = grid_for(reinterpret_cast<const void*>(f), c.lds_bytes, rows);
-  hipLaunchKernelGGL(f, dim3(grid), dim3(256), c.lds_bytes, static_cast<hipStream_t>(stream), x,
-                     static_cast<float2*>(out), timg, reinterpret_cast<const float4*>(zimg), args_of(c, rows));
+  hipLaunchKernelGGL(f, dim3(grid_for(c.grid_fwd, rows)), dim3(256), c.lds_bytes, static_cast<hipStream_t>(stream),
+                     x, static_cast<float2*>(out), timg, reinterpret_cast<const float4*>(zimg), args_of(c, rows));
   return hipGetLastError();
 }
 
@@ -356,11 +369,7 @@ int launch_inv_zt(const StreamCfg& c, const void* in, float* y, int64_t rows, co
   fwd_fn f;
   inv_fn v;
   pick(c, &f, &v);
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(v),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(c.lds_bytes));
-  if (e != hipSuccess) return e;
-  const int grid = grid_for(reinterpret_cast<const void*>(v), c.lds_bytes, rows);
-  hipLaunchKernelGGL(v, dim3(grid), dim3(256), c.lds_bytes, static_cast<hipStream_t>(stream),
+  hipLaunchKernelGGL(v, dim3(grid_for(c.grid_inv, rows)), dim3(256), c.lds_bytes, static_cast<hipStream_t>(stream),
                      static_cast<const float2*>(in), y, timg, reinterpret_cast<const float4*>(zimg),
                      args_of(c, rows));
   return hipGetLastError();
