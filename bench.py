@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-times", action="store_true",
                     help="skip the per-kernel event pass (used under rocprofv3)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy three times (the known-size "
+                         "reference for the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
@@ -70,11 +73,17 @@ def work(g, channels, m_count=None):
     w["stream_fwd_tz"] = dict(
         bytes=rows * (Nz * Nt * 4 + Kz * Kt * 8),
         flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz,
-        mfma_flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz * (0.5 if _folded(g) else 1.0))
+        mfma_flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz * (0.5 if _folded(g, 2) else 1.0))
+    fy = 0.5 if _folded(g, 1) else 1.0
+    fx = 0.5 if _folded(g, 0) else 1.0
     w["axis_fwd_y"] = dict(bytes=B * C * Nx * (Ny + Ky) * Kz * Kt * 8, flops=B * C * Nx * Kz * Kt * 8 * Ky * Ny)
     w["axis_fwd_x"] = dict(bytes=B * C * (Nx + Kx) * Ky * Kz * Kt * 8, flops=B * C * Ky * Kz * Kt * 8 * Kx * Nx)
-    w["axis_inv_x"] = dict(bytes=w["axis_fwd_x"]["bytes"], flops=w["axis_fwd_x"]["flops"])
-    w["axis_inv_y"] = dict(bytes=w["axis_fwd_y"]["bytes"], flops=w["axis_fwd_y"]["flops"])
+    w["axis_fwd_y"]["mfma_flops"] = w["axis_fwd_y"]["flops"] * fy
+    w["axis_fwd_x"]["mfma_flops"] = w["axis_fwd_x"]["flops"] * fx
+    w["axis_inv_x"] = dict(bytes=w["axis_fwd_x"]["bytes"], flops=w["axis_fwd_x"]["flops"],
+                           mfma_flops=w["axis_fwd_x"]["mfma_flops"])
+    w["axis_inv_y"] = dict(bytes=w["axis_fwd_y"]["bytes"], flops=w["axis_fwd_y"]["flops"],
+                           mfma_flops=w["axis_fwd_y"]["mfma_flops"])
     w["stream_inv_zt"] = dict(bytes=w["stream_fwd_tz"]["bytes"], flops=w["stream_fwd_tz"]["flops"],
                               mfma_flops=w["stream_fwd_tz"]["mfma_flops"])
     mc = M if m_count is None else m_count
@@ -85,8 +94,9 @@ def work(g, channels, m_count=None):
     return w
 
 
-def _folded(g):
-    return g["n_local"][2] == g["n_global"][2] and g["n_global"][2] % 2 == 0
+def _folded(g, dim):
+    """The library folds a dimension whose whole even extent is local."""
+    return g["n_local"][dim] == g["n_global"][dim] and g["n_global"][dim] % 2 == 0
 
 
 def _sha(path):
@@ -192,10 +202,21 @@ def main():
         sys.exit(2)
 
     import torch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.calibrate_copy:
+        n = 1 << 28                      # 2^28 floats = 1 GiB
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_each_way": n * 4, "copies": 3}), flush=True)
+        return
+
     import paper_2607_14394_amd as D
     import synth
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
     device = "cuda"
     cfg = args.workload
     log(f"building workload {cfg}")

@@ -40,11 +40,20 @@ struct StreamCfg {
 // Generic complex contraction along a middle axis:
 //   out[b][k][n] (+)= sum_j basis[k][j] in[b][j][n],
 // b < nb, j < J, k < KO, n < NN (complex elements).
+//
+// fold 1 (forward, the contracted spatial axis is the whole even extent):
+//   the K loop runs over j < J/2 with in[j] +- in[j + J/2]; k tiles
+//   [0, kth) hold the even modes p = 2s, tiles [kth, 2 kth) the odd ones.
+// fold 2 (inverse, the output spatial axis is the whole even extent): the K
+//   loop runs over the J/2 even and J/2 odd modes; k tiles cover rows
+//   y < KO/2 and write E + O at y and E - O at y + KO/2.
 struct AxisCfg {
   int64_t nb = 0;
   int J = 0, KO = 0, NN = 0;
-  int JQ = 0;      // ceil(J / 16)
-  int ktiles = 0;  // ceil(KO / 16)
+  int fold = 0;
+  int JQ = 0;      // 16-wide K steps
+  int ktiles = 0;  // 16-row k tiles
+  int kth = 0;     // fold 1: k tiles per parity class
 };
 
 // Float offsets of each kernel-ready image inside the plan's device blob.

@@ -7,12 +7,25 @@
 // (dtst_reduce) (j = x, k = k_x), and the inverse expansions over x and y
 // with conj(B)^T (Sec. V-A Eq. dtst_inverse, reverse order).  The complex
 // product is done as four real MFMA products with the basis split into
-// (Re, Im, -Im) parts, so the epilogue is lane-local.
+// (Re, Im) parts and the imaginary input negated once per load, so the
+// epilogue is lane-local.
 //
-// Work split: a 256-thread workgroup owns one b, 64 consecutive n (16 per
-// wave) and a block of up to KT*16 rows k.  Every lane streams in[b][j][n]
-// for its n with 8-byte loads (16 lanes cover 128 contiguous bytes); the
-// basis image is read with 16-byte loads that hit in L1/L2.
+// Folding (FOLD != 0): when the spatial side of the contraction covers the
+// whole even global extent N, exp(-2 pi i k (n + N/2) / N) = (-1)^k
+// exp(-2 pi i k n / N).  A forward contraction (FOLD = 1) then feeds the even
+// retained modes with in[j] + in[j + N/2] and the odd ones with
+// in[j] - in[j + N/2] over j < N/2; an inverse expansion (FOLD = 2) forms the
+// even-mode sum E and odd-mode sum O once and writes E + O at n and E - O at
+// n + N/2.  Either way the MFMA work halves.  The parity of a retained mode
+// equals the parity of its position p, because N is even.
+//
+// Work split: a 256-thread workgroup owns one b, 64*NT consecutive n (16*NT
+// per wave) and a block of up to KT 16-row tiles of k.  Every lane streams
+// in[b][j][n] for its n with 8-byte loads (16 lanes cover 128 contiguous
+// bytes), one 16-row step ahead of the MFMAs that consume it; the basis image
+// is read with 16-byte loads that hit in L1/L2.  The epilogue trades values
+// between neighbouring lanes so that every store writes two complex values
+// (16 bytes) and each store instruction covers whole 128-byte lines.
 #include <hip/hip_runtime.h>
 
 #include "dtst_internal.h"
@@ -26,9 +39,16 @@ __device__ __forceinline__ v4f mfma(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// Value of the neighbouring lane (lane ^ 1) via DPP quad_perm [1, 0, 3, 2].
+__device__ __forceinline__ float swap_adjacent(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xf, 0xf, false));
+}
+
 struct AxisArgs {
   int64_t nb, total;
-  int J, KO, NN, JQ, ktiles, kblocks, nblocks, acc;
+  int J, KO, NN, JQ, ktiles, kth, kblocks, nblocks, acc;
+  int jh;  // FOLD 1: J/2 (contracted half); FOLD 2: J/2 (modes per class)
+  int oh;  // FOLD 2: KO/2 (output half)
 };
 
 // Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
@@ -40,59 +60,152 @@ __device__ __forceinline__ int64_t xcd_logical(int64_t bid, int64_t grid) {
   return (bid % 8) * per + bid / 8;
 }
 
-template <int KT>
+// Stores the four rows k0 + i (i = 0..3) of one 16-column tile held by this
+// lane (row i: value (re[i], im[i]) at column n) with 16-byte stores: even
+// lanes write rows 0 and 2, odd lanes rows 1 and 3, each as the pair of
+// columns (n & ~1, (n & ~1) + 1).  NN is even, so pairs never straddle the
+// end of a row.  rowok(i) says whether row k0 + i exists.
+template <class RowPtr, class RowOk>
+__device__ __forceinline__ void store_tile(const float (&re)[4], const float (&im)[4], int n, bool nok, int acc,
+                                           RowPtr rowptr, RowOk rowok) {
+  const bool odd = n & 1;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    // even lanes need their neighbour's rows 2h, odd lanes their neighbour's rows 2h + 1
+    const int give = odd ? 2 * h : 2 * h + 1;
+    const float rr = swap_adjacent(re[give]);
+    const float ri = swap_adjacent(im[give]);
+    const int row = odd ? 2 * h + 1 : 2 * h;
+    const float4 v = odd ? make_float4(rr, ri, re[row], im[row]) : make_float4(re[row], im[row], rr, ri);
+    if (nok && rowok(row)) {
+      float4* o = reinterpret_cast<float4*>(rowptr(row) + (n & ~1));
+      float4 w = v;
+      if (acc) {
+        const float4 old = *o;
+        w.x += old.x;
+        w.y += old.y;
+        w.z += old.z;
+        w.w += old.w;
+      }
+      *o = w;
+    }
+  }
+}
+
+template <int KT, int NT, int FOLD>
 __global__ void __launch_bounds__(256)
 axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float4* __restrict__ img,
             AxisArgs a) {
+  constexpr int NC = FOLD == 2 ? 2 : 1;  // input classes loaded per K step
+  constexpr int NS = FOLD == 1 ? 2 : 1;  // input rows combined per K index
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
   const int wave = threadIdx.x >> 6;
   for (int64_t hw = blockIdx.x; hw < a.total; hw += gridDim.x) {
-    const int64_t grid_round = (hw / gridDim.x == (a.total - 1) / gridDim.x)
-                                   ? a.total - (hw / gridDim.x) * gridDim.x
-                                   : int64_t(gridDim.x);
     const int64_t base = (hw / gridDim.x) * gridDim.x;
+    const int64_t grid_round = (a.total - base < int64_t(gridDim.x)) ? a.total - base : int64_t(gridDim.x);
     const int64_t L = base + xcd_logical(hw - base, grid_round);
     const int nbk = static_cast<int>(L % a.nblocks);
     const int64_t rest = L / a.nblocks;
     const int kb = static_cast<int>(rest % a.kblocks);
     const int64_t b = rest / a.kblocks;
 
-    const int n = nbk * 64 + wave * 16 + m;
-    const bool nok = n < a.NN;
-    const float2* inb = in + b * int64_t(a.J) * a.NN + n;
+    const int nw = nbk * (64 * NT) + wave * (16 * NT);  // first column of this wave
+    const float2* inb = in + b * int64_t(a.J) * a.NN;
 
-    v4f accr[KT], acci[KT];
+    // K index jj = 16q + 4g + i.  FOLD 0: row jj.  FOLD 1: rows jj and
+    // jj + J/2.  FOLD 2: rows 2jj (even modes) and 2jj + 1 (odd modes).
+    auto load = [&](int q, float2 (&dst)[NC][NS][NT][4], bool (&ok)[NT][4]) {
 #pragma unroll
-    for (int kk = 0; kk < KT; ++kk) {
-      accr[kk] = v4f{0.f, 0.f, 0.f, 0.f};
-      acci[kk] = v4f{0.f, 0.f, 0.f, 0.f};
-    }
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int jj = 16 * q + 4 * g + i;
+          const int n = nw + 16 * nt + m;
+          const int lim = FOLD == 0 ? a.J : a.jh;
+          const bool v_ok = jj < lim && n < a.NN;
+          ok[nt][i] = v_ok;
+#pragma unroll
+          for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+              const int row = FOLD == 0 ? jj : (FOLD == 1 ? jj + s * a.jh : 2 * jj + c);
+              dst[c][s][nt][i] = inb[v_ok ? int64_t(row) * a.NN + n : 0];
+            }
+        }
+    };
 
+    // FOLD 2 keeps separate even / odd accumulators (index e).
+    constexpr int NE = FOLD == 2 ? 2 : 1;
+    v4f accr[NE][KT][NT], acci[NE][KT][NT];
+#pragma unroll
+    for (int e = 0; e < NE; ++e)
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          accr[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+          acci[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+        }
+
+    float2 vn[NC][NS][NT][4];
+    bool okn[NT][4];
+    load(0, vn, okn);
     for (int q = 0; q < a.JQ; ++q) {
-      float2 v[4];
+      // B operands: V[c or fold class][nt][i] as (re, im, -im)
+      constexpr int NV = FOLD == 0 ? 1 : 2;
+      float vr[NV][NT][4], vi[NV][NT][4], nvi[NV][NT][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int j = 16 * q + 4 * g + i;
-        v[i] = (nok && j < a.J) ? inb[int64_t(j) * a.NN] : make_float2(0.f, 0.f);
-      }
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool o = okn[nt][i];
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            float2 x;
+            if (FOLD == 1) {
+              const float2 p0 = vn[0][0][nt][i], p1 = vn[0][NS - 1][nt][i];
+              x = v == 0 ? make_float2(p0.x + p1.x, p0.y + p1.y) : make_float2(p0.x - p1.x, p0.y - p1.y);
+            } else {
+              x = vn[FOLD == 2 ? v : 0][0][nt][i];
+            }
+            if (!o) x = make_float2(0.f, 0.f);
+            vr[v][nt][i] = x.x;
+            vi[v][nt][i] = x.y;
+            nvi[v][nt][i] = -x.y;
+          }
+        }
+      if (q + 1 < a.JQ) load(q + 1, vn, okn);
+
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk) {
-        const int kt = kb * KT + kk;
-        if (kt < a.ktiles) {
-          const float4* ip = img + (int64_t(kt) * a.JQ + q) * 3 * 64 + lane;
-          const float4 br = ip[0], bi = ip[64], nbi = ip[128];
-          v4f r = accr[kk], s = acci[kk];
-          r = mfma(br.x, v[0].x, r); r = mfma(nbi.x, v[0].y, r);
-          s = mfma(br.x, v[0].y, s); s = mfma(bi.x, v[0].x, s);
-          r = mfma(br.y, v[1].x, r); r = mfma(nbi.y, v[1].y, r);
-          s = mfma(br.y, v[1].y, s); s = mfma(bi.y, v[1].x, s);
-          r = mfma(br.z, v[2].x, r); r = mfma(nbi.z, v[2].y, r);
-          s = mfma(br.z, v[2].y, s); s = mfma(bi.z, v[2].x, s);
-          r = mfma(br.w, v[3].x, r); r = mfma(nbi.w, v[3].y, r);
-          s = mfma(br.w, v[3].y, s); s = mfma(bi.w, v[3].x, s);
-          accr[kk] = r;
-          acci[kk] = s;
+        const int kt = min(kb * KT + kk, a.ktiles - 1);
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+          // image: FOLD 2 -> [kt][q][class][part], else [kt][q][part]
+          const float4* ip = img + ((int64_t(kt) * a.JQ + q) * NE + e) * 2 * 64 + lane;
+          const float4 br = ip[0], bi = ip[64];
+          const int v = FOLD == 1 ? (kt >= a.kth ? 1 : 0) : (FOLD == 2 ? e : 0);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+              const float r = br[i], im = bi[i];
+              float xr, xi, xni;
+              if (FOLD == 1) {  // uniform select of the fold class of this tile
+                xr = v ? vr[NV - 1][nt][i] : vr[0][nt][i];
+                xi = v ? vi[NV - 1][nt][i] : vi[0][nt][i];
+                xni = v ? nvi[NV - 1][nt][i] : nvi[0][nt][i];
+              } else {
+                xr = vr[FOLD == 2 ? e : 0][nt][i];
+                xi = vi[FOLD == 2 ? e : 0][nt][i];
+                xni = nvi[FOLD == 2 ? e : 0][nt][i];
+              }
+              accr[e][kk][nt] = mfma(r, xr, accr[e][kk][nt]);
+              acci[e][kk][nt] = mfma(r, xi, acci[e][kk][nt]);
+              accr[e][kk][nt] = mfma(im, xni, accr[e][kk][nt]);
+              acci[e][kk][nt] = mfma(im, xr, acci[e][kk][nt]);
+            }
         }
       }
     }
@@ -100,24 +213,70 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
 #pragma unroll
     for (int kk = 0; kk < KT; ++kk) {
       const int kt = kb * KT + kk;
-      if (kt < a.ktiles && nok) {
+      if (kt >= a.ktiles) continue;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int k = 16 * kt + 4 * g + i;
-          if (k < a.KO) {
-            float2* o = out + (b * a.KO + k) * int64_t(a.NN) + n;
-            float2 val = make_float2(accr[kk][i], acci[kk][i]);
-            if (a.acc) {
-              const float2 old = *o;
-              val.x += old.x;
-              val.y += old.y;
+      for (int nt = 0; nt < NT; ++nt) {
+        const int n = nw + 16 * nt + m;
+        const bool nok = n < a.NN;
+        float2* ob = out + b * int64_t(a.KO) * a.NN;
+        if (FOLD == 0) {
+          float re[4], im[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            re[i] = accr[0][kk][nt][i];
+            im[i] = acci[0][kk][nt][i];
+          }
+          const int k0 = 16 * kt + 4 * g;
+          store_tile(re, im, n, nok, a.acc, [&](int i) { return ob + int64_t(k0 + i) * a.NN; },
+                     [&](int i) { return k0 + i < a.KO; });
+        } else if (FOLD == 1) {
+          // tile kt holds class c = kt >= kth, slots s = 16 (kt - c kth) + 4g + i, mode p = 2s + c
+          float re[4], im[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            re[i] = accr[0][kk][nt][i];
+            im[i] = acci[0][kk][nt][i];
+          }
+          const int c = kt >= a.kth ? 1 : 0;
+          const int s0 = 16 * (kt - c * a.kth) + 4 * g;
+          store_tile(re, im, n, nok, a.acc, [&](int i) { return ob + int64_t(2 * (s0 + i) + c) * a.NN; },
+                     [&](int i) { return 2 * (s0 + i) + c < a.KO; });
+        } else {
+          // rows y = 16kt + 4g + i < KO/2: E + O at y, E - O at y + KO/2
+          const int y0 = 16 * kt + 4 * g;
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            float re[4], im[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float er = accr[0][kk][nt][i], ei = acci[0][kk][nt][i];
+              const float odr = accr[NE - 1][kk][nt][i], odi = acci[NE - 1][kk][nt][i];
+              re[i] = hf == 0 ? er + odr : er - odr;
+              im[i] = hf == 0 ? ei + odi : ei - odi;
             }
-            *o = val;
+            store_tile(re, im, n, nok, a.acc,
+                       [&](int i) { return ob + int64_t(y0 + i + hf * a.oh) * a.NN; },
+                       [&](int i) { return y0 + i < a.oh; });
           }
         }
       }
     }
   }
+}
+
+template <int KT, int FOLD>
+void launch_kt(int nt, int grid, hipStream_t s, const float2* pin, float2* pout, const float4* pimg,
+               const AxisArgs& a) {
+  if (nt == 2) hipLaunchKernelGGL((axis_kernel<KT, 2, FOLD>), dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
+  else hipLaunchKernelGGL((axis_kernel<KT, 1, FOLD>), dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
+}
+
+template <int FOLD>
+void launch_fold(int kt, int nt, int grid, hipStream_t s, const float2* pin, float2* pout, const float4* pimg,
+                 const AxisArgs& a) {
+  if (kt == 1) launch_kt<1, FOLD>(nt, grid, s, pin, pout, pimg, a);
+  else if (kt == 2) launch_kt<2, FOLD>(nt, grid, s, pin, pout, pimg, a);
+  else launch_kt<4, FOLD>(nt, grid, s, pin, pout, pimg, a);
 }
 
 }  // namespace
@@ -132,10 +291,18 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
   a.NN = c.NN;
   a.JQ = c.JQ;
   a.ktiles = c.ktiles;
+  a.kth = c.kth;
+  a.jh = c.J / 2;
+  a.oh = c.KO / 2;
   a.acc = accumulate ? 1 : 0;
-  a.nblocks = (c.NN + 63) / 64;
-  int kt = c.ktiles <= 1 ? 1 : (c.ktiles <= 2 ? 2 : 4);
+  // FOLD 2 keeps two accumulator sets; cap its k block at 2 tiles.
+  const int kmax = c.fold == 2 ? 2 : 4;
+  int kt = c.ktiles <= 1 ? 1 : (c.ktiles <= 2 || kmax == 2 ? 2 : 4);
   a.kblocks = (c.ktiles + kt - 1) / kt;
+  // Two 16-column tiles per wave when that still leaves several workgroups per CU.
+  int nt = 2;
+  if (nb * a.kblocks * ((c.NN + 127) / 128) < 2048) nt = 1;
+  a.nblocks = (c.NN + 64 * nt - 1) / (64 * nt);
   a.total = nb * a.kblocks * a.nblocks;
   const int64_t cap = int64_t(1) << 22;
   const int grid = static_cast<int>(a.total < cap ? a.total : cap);
@@ -143,9 +310,9 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
   const float2* pin = static_cast<const float2*>(in);
   float2* pout = static_cast<float2*>(out);
   const float4* pimg = reinterpret_cast<const float4*>(img);
-  if (kt == 1) hipLaunchKernelGGL(axis_kernel<1>, dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
-  else if (kt == 2) hipLaunchKernelGGL(axis_kernel<2>, dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
-  else hipLaunchKernelGGL(axis_kernel<4>, dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
+  if (c.fold == 1) launch_fold<1>(kt, nt, grid, s, pin, pout, pimg, a);
+  else if (c.fold == 2) launch_fold<2>(kt, nt, grid, s, pin, pout, pimg, a);
+  else launch_fold<0>(kt, nt, grid, s, pin, pout, pimg, a);
   return hipGetLastError();
 }
 

@@ -38,104 +38,134 @@ struct StreamArgs {
 
 // ---------------------------------------------------------------------------
 // Forward: x (rows x N_z x N_t) fp32 -> out (rows x K_z x K_t) complex.
+//
+// Every wave walks its (row, z-tile) pairs in order and keeps the next
+// pair's loads in flight while it computes the current one.  Loads are
+// unconditional (out-of-range lanes read the row start) and masked when the
+// values are used, so nothing between the loads and the MFMAs forces an
+// early wait.  Within a tile the independent accumulator chains are
+// interleaved step by step.
 // ---------------------------------------------------------------------------
-template <int CT, int TH, int MT, int NCLS>
-__global__ void __launch_bounds__(256)
-fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
-              const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
-  extern __shared__ float4 lds[];
-  const int nimg = NCLS * a.zt * MT * 64;
-  for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
-  __syncthreads();
-
+template <int CT, int TH, int MT, int NCLS, bool VEC>
+__device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2* __restrict__ out,
+                                            const float (&bt)[TH * 4][CT], const float4* lds,
+                                            const StreamArgs& a, int64_t wave, int64_t wstride) {
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
   constexpr int KTP = 8 * CT;
-
-  // B operand of the t contraction, step s = 4h + j covers t = 16h + 4g + j.
-  float bt[TH * 4][CT];
-#pragma unroll
-  for (int s = 0; s < TH * 4; ++s)
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) bt[s][ct] = timg[(s * CT + ct) * 64 + lane];
-
-  const int wpb = blockDim.x >> 6;
-  const int64_t wstride = int64_t(gridDim.x) * wpb;
   const int64_t row_len = int64_t(a.nz) * a.nt;
+  const int64_t n_iter = ((a.rows - 1 - wave) / wstride + 1) * a.zt;
 
-  for (int64_t r = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6); r < a.rows; r += wstride) {
+  // Load the tile of (row r, z-tile zt) into dst; ok[hf][h] (VEC) or
+  // ok[hf][4h + j] (scalar) records which values are inside the row.
+  auto load_tile = [&](int64_t r, int zt, float (&dst)[NCLS][TH][4], bool (&ok)[NCLS][TH * 4]) {
     const float* xr = x + r * row_len;
-    v4f P[NCLS][MT][CT];
+    const int zl = zt * 16 + m;
+    const bool zok = zl < a.zh;
+#pragma unroll
+    for (int hf = 0; hf < NCLS; ++hf) {
+      const int64_t zoff = int64_t(zl + hf * a.zh) * a.nt;
+#pragma unroll
+      for (int h = 0; h < TH; ++h) {
+        if (VEC) {
+          const int t0 = 16 * h + 4 * g;
+          const bool v_ok = zok && t0 < a.nt;
+          const float4 v = *reinterpret_cast<const float4*>(xr + (v_ok ? zoff + t0 : 0));
+          dst[hf][h][0] = v.x; dst[hf][h][1] = v.y; dst[hf][h][2] = v.z; dst[hf][h][3] = v.w;
+          ok[hf][4 * h] = v_ok;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int t = 16 * h + 4 * g + j;
+            const bool v_ok = zok && t < a.nt;
+            dst[hf][h][j] = xr[v_ok ? zoff + t : 0];
+            ok[hf][4 * h + j] = v_ok;
+          }
+        }
+      }
+    }
+  };
+
+  float xn[NCLS][TH][4];
+  bool okn[NCLS][TH * 4];
+  load_tile(wave, 0, xn, okn);
+  int64_t rn = wave;
+  int ztn = 0;
+  v4f P[NCLS][MT][CT];
+
+  for (int64_t it = 0; it < n_iter; ++it) {
+    float xv[NCLS][TH][4];
+    bool ok[NCLS][TH * 4];
+#pragma unroll
+    for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+      for (int h = 0; h < TH; ++h)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          xv[hf][h][j] = xn[hf][h][j];
+          ok[hf][4 * h + j] = okn[hf][4 * h + j];
+        }
+    const int64_t r = rn;
+    const int zt = ztn;
+    if (++ztn == a.zt) {
+      ztn = 0;
+      rn += wstride;
+    }
+    if (it + 1 < n_iter) load_tile(rn, ztn, xn, okn);
+
+    // z basis of this tile (independent of the loads).
+    float4 A[NCLS][MT];
 #pragma unroll
     for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int mt = 0; mt < MT; ++mt) A[cl][mt] = lds[((cl * a.zt + zt) * MT + mt) * 64 + lane];
 
-    for (int zt = 0; zt < a.zt; ++zt) {
-      const int zl = zt * 16 + m;
-      const bool zok = zl < a.zh;
-      // Contract t for z = zl (and z = zl + N_z/2 when folded).
-      v4f V[NCLS][CT];
-#pragma unroll
-      for (int hf = 0; hf < NCLS; ++hf) {
-        const float* src = xr + int64_t(zl + hf * a.zh) * a.nt;
-        float xv[TH][4];
-        if (a.vec) {
-#pragma unroll
-          for (int h = 0; h < TH; ++h) {
-            const int t0 = 16 * h + 4 * g;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (zok && t0 < a.nt) v = *reinterpret_cast<const float4*>(src + t0);
-            xv[h][0] = v.x; xv[h][1] = v.y; xv[h][2] = v.z; xv[h][3] = v.w;
-          }
-        } else {
-#pragma unroll
-          for (int h = 0; h < TH; ++h)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int t = 16 * h + 4 * g + j;
-              xv[h][j] = (zok && t < a.nt) ? src[t] : 0.f;
-            }
-        }
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int h = 0; h < TH; ++h)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc = mfma(xv[h][j], bt[h * 4 + j][ct], acc);
-          V[hf][ct] = acc;
-        }
-      }
-      if (NCLS == 2) {
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          const v4f s = V[0][ct] + V[1][ct];
-          const v4f d = V[0][ct] - V[1][ct];
-          V[0][ct] = s;
-          V[NCLS - 1][ct] = d;
-        }
-      }
-      // Contract z: accumulator register i of V is the B operand of the
-      // step whose K index is z = 16zt + 4g + i.
+    if (zt == 0) {
 #pragma unroll
       for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const float4 A = lds[((cl * a.zt + zt) * MT + mt) * 64 + lane];
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            v4f p = P[cl][mt][ct];
-            p = mfma(A.x, V[cl][ct][0], p);
-            p = mfma(A.y, V[cl][ct][1], p);
-            p = mfma(A.z, V[cl][ct][2], p);
-            p = mfma(A.w, V[cl][ct][3], p);
-            P[cl][mt][ct] = p;
-          }
-        }
+          for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = v4f{0.f, 0.f, 0.f, 0.f};
     }
+
+    // Contract t for z = 16zt + m (and z + N_z/2 when folded).
+    v4f V[NCLS][CT];
+#pragma unroll
+    for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) V[hf][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int h = 0; h < TH; ++h)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int hf = 0; hf < NCLS; ++hf) {
+          const float xa = ok[hf][VEC ? 4 * h : 4 * h + j] ? xv[hf][h][j] : 0.f;
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) V[hf][ct] = mfma(xa, bt[h * 4 + j][ct], V[hf][ct]);
+        }
+    if (NCLS == 2) {
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        const v4f s = V[0][ct] + V[NCLS - 1][ct];
+        const v4f d = V[0][ct] - V[NCLS - 1][ct];
+        V[0][ct] = s;
+        V[NCLS - 1][ct] = d;
+      }
+    }
+    // Contract z: accumulator register i of V is the B operand of the
+    // step whose K index is z = 16zt + 4g + i.
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = mfma(A[cl][mt][i], V[cl][ct][i], P[cl][mt][ct]);
+
+    if (zt != a.zt - 1) continue;
 
     // Combine the real-stacked products into complex coefficients:
     // (Re B) V and (Im B) V sit in row tiles mt and mt + MT/2 of the same lane;
@@ -165,12 +195,14 @@ fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
   }
 }
 
-// ---------------------------------------------------------------------------
-// Inverse: in (rows x K_z x K_t) complex -> y (rows x N_z x N_t) fp32.
-// ---------------------------------------------------------------------------
+// Register budget: the common shapes fit 4 waves per SIMD (128 registers);
+// the widest ones (many z classes / k_t tiles) are left to the compiler.
+#define DTST_STREAM_WAVES(CT, MT, NCLS, TH) \
+  __attribute__((amdgpu_waves_per_eu(((CT) * (MT) * (NCLS) <= 4 && (TH) <= 2) ? 4 : 1)))
+
 template <int CT, int TH, int MT, int NCLS>
-__global__ void __launch_bounds__(256)
-inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
+__global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH)
+fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
               const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
   extern __shared__ float4 lds[];
   const int nimg = NCLS * a.zt * MT * 64;
@@ -178,27 +210,42 @@ inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
-  const int m = lane & 15, g = lane >> 4;
-  constexpr int KTP = 8 * CT;
-
-  // A operand of the t expansion: rows t = 16mt + m, K index c = 16ct + 4g + i.
-  float ta[TH][CT][4];
+  // B operand of the t contraction, step s = 4h + j covers t = 16h + 4g + j.
+  float bt[TH * 4][CT];
 #pragma unroll
-  for (int mt = 0; mt < TH; ++mt)
+  for (int s = 0; s < TH * 4; ++s)
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) ta[mt][ct][i] = timg[((mt * CT + ct) * 4 + i) * 64 + lane];
+    for (int ct = 0; ct < CT; ++ct) bt[s][ct] = timg[(s * CT + ct) * 64 + lane];
 
   const int wpb = blockDim.x >> 6;
   const int64_t wstride = int64_t(gridDim.x) * wpb;
+  const int64_t wave = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  if (wave >= a.rows) return;
+  if (a.vec) fwd_tz_body<CT, TH, MT, NCLS, true>(x, out, bt, lds, a, wave, wstride);
+  else fwd_tz_body<CT, TH, MT, NCLS, false>(x, out, bt, lds, a, wave, wstride);
+}
+
+// ---------------------------------------------------------------------------
+// Inverse: in (rows x K_z x K_t) complex -> y (rows x N_z x N_t) fp32.
+//
+// Each row's spectrum is loaded one row ahead.  Per z-tile the z expansion
+// (one accumulator chain per class and column tile), the unfold, and the t
+// expansion (one chain per output tile) run as interleaved MFMA phases; all
+// stores of the tile follow them.
+// ---------------------------------------------------------------------------
+template <int CT, int TH, int MT, int NCLS, bool VEC>
+__device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float* __restrict__ y,
+                                            const float (&ta)[TH][CT][4], const float4* lds,
+                                            const StreamArgs& a, int64_t wave, int64_t wstride) {
+  const int lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  constexpr int KTP = 8 * CT;
   const int64_t row_len = int64_t(a.nz) * a.nt;
 
-  for (int64_t r = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6); r < a.rows; r += wstride) {
+  // Spectrum values this lane needs from one row: slot s = 16qh + 4g + i of
+  // class cl at k_t column c = 16ct + m (Re and Im columns read the same value).
+  auto load_u = [&](int64_t r, float2 (&dst)[NCLS][CT][MT / 2][4], bool (&ok)[NCLS][CT][MT / 2][4]) {
     const float2* urow = in + r * int64_t(a.kz) * a.kt;
-    // A operand of the z expansion (rows c, K index kz' = 16q + 4g + i):
-    // kz' < KCP pairs with Re C_z, kz' >= KCP with Im C_z.
-    float A[NCLS][CT][MT][4];
 #pragma unroll
     for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
@@ -210,32 +257,56 @@ inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
             const int s = 16 * qh + 4 * g + i;
             const int p = s * NCLS + cl;
             const int c = 16 * ct + m;
-            const bool is_re = c < KTP;
-            const int kt = is_re ? c : c - KTP;
-            float2 u = make_float2(0.f, 0.f);
-            if (p < a.kz && kt < a.kt) u = urow[p * a.kt + kt];
+            const int kt = c < KTP ? c : c - KTP;
+            const bool v_ok = p < a.kz && kt < a.kt;
+            dst[cl][ct][qh][i] = urow[v_ok ? p * a.kt + kt : 0];
+            ok[cl][ct][qh][i] = v_ok;
+          }
+  };
+
+  float2 un[NCLS][CT][MT / 2][4];
+  bool okn[NCLS][CT][MT / 2][4];
+  load_u(wave, un, okn);
+  for (int64_t r = wave; r < a.rows; r += wstride) {
+    // A operand of the z expansion (rows c, K index kz' = 16q + 4g + i):
+    // kz' < KCP pairs with Re C_z, kz' >= KCP with Im C_z.
+    float A[NCLS][CT][MT][4];
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int qh = 0; qh < MT / 2; ++qh)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const bool is_re = 16 * ct + m < KTP;
+            const float2 u = okn[cl][ct][qh][i] ? un[cl][ct][qh][i] : make_float2(0.f, 0.f);
             A[cl][ct][qh][i] = is_re ? u.x : u.y;
             A[cl][ct][qh + MT / 2][i] = is_re ? -u.y : u.x;
           }
+    if (r + wstride < a.rows) load_u(r + wstride, un, okn);
 
     float* yrow = y + r * row_len;
     for (int zt = 0; zt < a.zt; ++zt) {
+      float4 B[NCLS][MT];
+#pragma unroll
+      for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+        for (int q = 0; q < MT; ++q) B[cl][q] = lds[((cl * a.zt + zt) * MT + q) * 64 + lane];
+
       v4f W[NCLS][CT];
 #pragma unroll
       for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
+        for (int ct = 0; ct < CT; ++ct) W[cl][ct] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int q = 0; q < MT; ++q) {
-            const float4 B = lds[((cl * a.zt + zt) * MT + q) * 64 + lane];
-            acc = mfma(A[cl][ct][q][0], B.x, acc);
-            acc = mfma(A[cl][ct][q][1], B.y, acc);
-            acc = mfma(A[cl][ct][q][2], B.z, acc);
-            acc = mfma(A[cl][ct][q][3], B.w, acc);
-          }
-          W[cl][ct] = acc;
-        }
+      for (int q = 0; q < MT; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) W[cl][ct] = mfma(A[cl][ct][q][i], B[cl][q][i], W[cl][ct]);
       if (NCLS == 2) {
         // even modes + odd modes at z, even - odd at z + N_z/2
 #pragma unroll
@@ -246,33 +317,91 @@ inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
           W[NCLS - 1][ct] = d;
         }
       }
+      v4f Y[NCLS][TH];
+#pragma unroll
+      for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+        for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+            for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = mfma(ta[mt][ct][i], W[hf][ct][i], Y[hf][mt]);
+
       const int zl = zt * 16 + m;
       const bool zok = zl < a.zh;
+      if (VEC && TH == 2 && a.nt == 32) {
+        // Rows of exactly 32 floats: lanes m and m^8 trade one 16-byte
+        // chunk (DPP row rotate by 8) so that each store instruction writes
+        // 8 whole 128-byte rows instead of 16 half rows.
+        const bool lo = m < 8;
+        const int za = zt * 16 + (m & 7), zb = za + 8;
+        const int tch = (lo ? 0 : 16) + 4 * g;
+#pragma unroll
+        for (int hf = 0; hf < NCLS; ++hf) {
+          float va[4], vb[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float send = lo ? Y[hf][TH - 1][i] : Y[hf][0][i];
+            const float recv = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(send), 0x128, 0xf, 0xf, false));
+            va[i] = lo ? Y[hf][0][i] : recv;
+            vb[i] = lo ? recv : Y[hf][TH - 1][i];
+          }
+          if (za < a.zh)
+            *reinterpret_cast<float4*>(yrow + int64_t(za + hf * a.zh) * a.nt + tch) = make_float4(va[0], va[1], va[2], va[3]);
+          if (zb < a.zh)
+            *reinterpret_cast<float4*>(yrow + int64_t(zb + hf * a.zh) * a.nt + tch) = make_float4(vb[0], vb[1], vb[2], vb[3]);
+        }
+        continue;
+      }
 #pragma unroll
       for (int hf = 0; hf < NCLS; ++hf) {
         float* dst = yrow + int64_t(zl + hf * a.zh) * a.nt;
 #pragma unroll
         for (int mt = 0; mt < TH; ++mt) {
-          v4f Y = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            Y = mfma(ta[mt][ct][0], W[hf][ct][0], Y);
-            Y = mfma(ta[mt][ct][1], W[hf][ct][1], Y);
-            Y = mfma(ta[mt][ct][2], W[hf][ct][2], Y);
-            Y = mfma(ta[mt][ct][3], W[hf][ct][3], Y);
-          }
           const int t0 = 16 * mt + 4 * g;
-          if (a.vec) {
-            if (zok && t0 < a.nt) *reinterpret_cast<float4*>(dst + t0) = make_float4(Y[0], Y[1], Y[2], Y[3]);
-          } else if (zok) {
+          if (VEC) {
+            if (zok && t0 < a.nt)
+              *reinterpret_cast<float4*>(dst + t0) = make_float4(Y[hf][mt][0], Y[hf][mt][1], Y[hf][mt][2], Y[hf][mt][3]);
+          } else {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              if (t0 + i < a.nt) dst[t0 + i] = Y[i];
+              if (zok && t0 + i < a.nt) dst[t0 + i] = Y[hf][mt][i];
           }
         }
       }
     }
   }
+}
+
+template <int CT, int TH, int MT, int NCLS>
+__global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH)
+inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
+              const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
+  extern __shared__ float4 lds[];
+  const int nimg = NCLS * a.zt * MT * 64;
+  for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63;
+  // A operand of the t expansion: rows t = 16mt + m, K index c = 16ct + 4g + i.
+  float ta[TH][CT][4];
+#pragma unroll
+  for (int mt = 0; mt < TH; ++mt)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ta[mt][ct][i] = timg[((mt * CT + ct) * 4 + i) * 64 + lane];
+
+  const int wpb = blockDim.x >> 6;
+  const int64_t wstride = int64_t(gridDim.x) * wpb;
+  const int64_t wave = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  if (wave >= a.rows) return;
+  if (a.vec) inv_zt_body<CT, TH, MT, NCLS, true>(in, y, ta, lds, a, wave, wstride);
+  else inv_zt_body<CT, TH, MT, NCLS, false>(in, y, ta, lds, a, wave, wstride);
 }
 
 typedef void (*fwd_fn)(const float*, float2*, const float*, const float4*, StreamArgs);

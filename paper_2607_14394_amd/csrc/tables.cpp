@@ -151,13 +151,23 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
   }
 
   // ---- axis contractions ----
-  auto axis = [](int J, int KO, int64_t NN) {
+  auto axis = [](int J, int KO, int64_t NN, int fold) {
     AxisCfg a;
     a.J = J;
     a.KO = KO;
     a.NN = static_cast<int>(NN);
-    a.JQ = static_cast<int>(ceil_div(J, 16));
-    a.ktiles = static_cast<int>(ceil_div(KO, 16));
+    a.fold = fold;
+    if (fold == 1) {
+      a.JQ = static_cast<int>(ceil_div(J / 2, 16));
+      a.kth = static_cast<int>(ceil_div(KO / 2, 16));
+      a.ktiles = 2 * a.kth;
+    } else if (fold == 2) {
+      a.JQ = static_cast<int>(ceil_div(J / 2, 16));
+      a.ktiles = static_cast<int>(ceil_div(KO / 2, 16));
+    } else {
+      a.JQ = static_cast<int>(ceil_div(J, 16));
+      a.ktiles = static_cast<int>(ceil_div(KO, 16));
+    }
     return a;
   };
   const int64_t nn_y = dv.K[2] * dv.K[3];
@@ -166,10 +176,13 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
     *err = "retained mode count too large";
     return DTST_ERR_UNSUPPORTED;
   }
-  dv.ay_f = axis(static_cast<int>(d->n_local[1]), static_cast<int>(dv.K[1]), nn_y);
-  dv.ax_f = axis(static_cast<int>(d->n_local[0]), static_cast<int>(dv.K[0]), nn_x);
-  dv.ax_i = axis(static_cast<int>(dv.K[0]), static_cast<int>(d->n_local[0]), nn_x);
-  dv.ay_i = axis(static_cast<int>(dv.K[1]), static_cast<int>(d->n_local[1]), nn_y);
+  // A dimension folds when this shard holds its whole even global extent.
+  const bool fold_x = d->n_local[0] == d->n_global[0] && d->n_global[0] % 2 == 0;
+  const bool fold_y = d->n_local[1] == d->n_global[1] && d->n_global[1] % 2 == 0;
+  dv.ay_f = axis(static_cast<int>(d->n_local[1]), static_cast<int>(dv.K[1]), nn_y, fold_y ? 1 : 0);
+  dv.ax_f = axis(static_cast<int>(d->n_local[0]), static_cast<int>(dv.K[0]), nn_x, fold_x ? 1 : 0);
+  dv.ax_i = axis(static_cast<int>(dv.K[0]), static_cast<int>(d->n_local[0]), nn_x, fold_x ? 2 : 0);
+  dv.ay_i = axis(static_cast<int>(dv.K[1]), static_cast<int>(d->n_local[1]), nn_y, fold_y ? 2 : 0);
 
   // ---- workspace: two complex intermediates of the largest channel count ----
   const int64_t bc = d->batch * cmax;
@@ -193,7 +206,7 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
   im.t_inv = take(t_img);
   im.t_inv_adjoint_of_forward = take(t_img);
   im.z_inv = take(z_img);
-  auto axis_img = [](const AxisCfg& a) { return size_t(a.ktiles) * a.JQ * 3 * 64 * 4; };
+  auto axis_img = [](const AxisCfg& a) { return size_t(a.ktiles) * a.JQ * (a.fold == 2 ? 2 : 1) * 2 * 64 * 4; };
   im.y_fwd = take(axis_img(dv.ay_f));
   im.x_fwd = take(axis_img(dv.ax_f));
   im.y_inv = take(axis_img(dv.ay_i));
@@ -325,32 +338,54 @@ void z_inverse_image(const Derived& dv, float* dst) {
           }
 }
 
-// Axis image: float4 entry ((kt*JQ + q)*3 + part)*64 + lane, component i,
-// holds part (Re, Im, -Im) of basis[k][j], k = 16kt + m, j = 16q + 4g + i.
-// forward: basis[k][j] = B_dim[k][j]; inverse: basis[k][j] = conj(B_dim[j][k]).
+// Axis image, float4 entries indexed by lane (m = lane & 15, g = lane >> 4)
+// and component i; part 0 holds Re, part 1 Im.
+//   fold 0: entry ((kt*JQ + q)*2 + part)*64 + lane = basis[k][j],
+//           k = 16kt + m, j = 16q + 4g + i.
+//   fold 1: same entry layout; tile kt holds parity class c = (kt >= kth),
+//           mode p = 2 (16 (kt - c kth) + m) + c, column j = 16q + 4g + i < J/2.
+//   fold 2: entry (((kt*JQ + q)*2 + c)*2 + part)*64 + lane = basis[y][p],
+//           y = 16kt + m < KO/2, mode p = 2 (16q + 4g + i) + c.
+// forward: basis[k][j] = B_dim[k][j]; inverse: basis[y][p] = conj(B_dim[p][y]).
 void axis_image(const Derived& dv, const AxisCfg& a, int dim, bool inverse, float* dst) {
   const dtst_desc& d = dv.d;
+  const int ncls = a.fold == 2 ? 2 : 1;
   for (int kt = 0; kt < a.ktiles; ++kt)
     for (int q = 0; q < a.JQ; ++q)
-      for (int part = 0; part < 3; ++part)
-        for (int lane = 0; lane < 64; ++lane)
-          for (int i = 0; i < 4; ++i) {
-            const int m = lane & 15, g = lane >> 4;
-            const int k = 16 * kt + m;
-            const int j = 16 * q + 4 * g + i;
-            double v = 0.0;
-            if (k < a.KO && j < a.J) {
-              double re, im;
-              if (inverse) {
-                bval(d, dim, j, k, &re, &im);
-                im = -im;
+      for (int c = 0; c < ncls; ++c)
+        for (int part = 0; part < 2; ++part)
+          for (int lane = 0; lane < 64; ++lane)
+            for (int i = 0; i < 4; ++i) {
+              const int m = lane & 15, g = lane >> 4;
+              int k, j;  // output row, contracted index (before the basis orientation)
+              bool ok;
+              if (a.fold == 1) {
+                const int cls = kt >= a.kth ? 1 : 0;
+                k = 2 * (16 * (kt - cls * a.kth) + m) + cls;
+                j = 16 * q + 4 * g + i;
+                ok = k < a.KO && j < a.J / 2;
+              } else if (a.fold == 2) {
+                k = 16 * kt + m;
+                j = 2 * (16 * q + 4 * g + i) + c;
+                ok = k < a.KO / 2 && j < a.J;
               } else {
-                bval(d, dim, k, j, &re, &im);
+                k = 16 * kt + m;
+                j = 16 * q + 4 * g + i;
+                ok = k < a.KO && j < a.J;
               }
-              v = part == 0 ? re : (part == 1 ? im : -im);
+              double v = 0.0;
+              if (ok) {
+                double re, im;
+                if (inverse) {
+                  bval(d, dim, j, k, &re, &im);
+                  im = -im;
+                } else {
+                  bval(d, dim, k, j, &re, &im);
+                }
+                v = part == 0 ? re : im;
+              }
+              dst[(((((size_t)kt * a.JQ + q) * ncls + c) * 2 + part) * 64 + lane) * 4 + i] = static_cast<float>(v);
             }
-            dst[((((size_t)kt * a.JQ + q) * 3 + part) * 64 + lane) * 4 + i] = static_cast<float>(v);
-          }
 }
 
 }  // namespace
