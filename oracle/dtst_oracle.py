@@ -46,7 +46,7 @@ import numpy as np
 __all__ = [
     "Geometry", "retained_indices", "retained_t", "basis", "half_weights",
     "forward", "inverse", "forward_adj", "inverse_adj", "mix",
-    "mix_data_grad", "mix_wgrad", "forward_at_modes", "inverse_at_points",
+    "mix_data_grad", "mix_wgrad", "forward_at_modes", "inverse_at_points", "forward_adj_at_points",
     "n_modes", "mode_index",
 ]
 
@@ -230,10 +230,18 @@ def inverse(yhat: np.ndarray, g: Geometry) -> np.ndarray:
 def inverse_at_points(yhat_bc: np.ndarray, g: Geometry, points) -> np.ndarray:
     """Inverse of one (b, c) slice at a list of local points (x, y, z, t),
     each one its own sum over all retained modes."""
+    ntot = float(np.prod(np.asarray(g.n_global, dtype=np.float64)))
+    return _expand_at_points(yhat_bc, g, points, half_weights(g.n_global[3], g.kt) / ntot)
+
+
+def forward_adj_at_points(g_xhat_bc: np.ndarray, g: Geometry, points) -> np.ndarray:
+    """``forward_adj`` of one (b, c) slice at a list of local points."""
+    return _expand_at_points(g_xhat_bc, g, points, np.ones(g.kt))
+
+
+def _expand_at_points(yhat_bc, g, points, w):
     yhat_bc = np.asarray(yhat_bc, dtype=np.complex128)
     Bx, By, Bz, Bt = _bases(g)
-    ntot = float(np.prod(np.asarray(g.n_global, dtype=np.float64)))
-    w = half_weights(g.n_global[3], g.kt) / ntot
     res = np.empty(len(points), dtype=np.float64)
     for q, (px, py, pz, pt) in enumerate(points):
         v = np.tensordot(yhat_bc, np.conj(Bt[:, pt]) * w, axes=([3], [0]))

@@ -392,3 +392,21 @@ def test_planted_waves_closed_form_on_slab():
         expect = expect + wave_spectrum_closed_form(g, k, ph, 5.0)
     d = O.forward(noise + waves[None, None], g) - O.forward(noise, g)
     assert rel(d[0, 0], expect) < 1e-11
+
+
+def test_point_evaluators_match_pinned_full_transforms():
+    """The per-coefficient / per-point evaluators used for very large shards
+    agree with the full transforms pinned above (FFT, irfftn, adjoint)."""
+    g = geo("pencil")
+    x = rand_shard(g, 91)
+    X = O.forward(x, g)
+    modes = [(0, 1, 2, 0), (5, 3, 0, 2), (2, 0, 3, 1)]
+    got = O.forward_at_modes(x[1, 0], g, modes)
+    assert np.allclose(got, [X[1, 0][m] for m in modes], rtol=1e-12, atol=1e-12)
+    Y = synth.np_complex_normal((g.batch, g.c_out) + g.K, 92).astype(np.complex128)
+    pts = [(0, 0, 0, 0), (3, 4, 7, 5), (1, 2, 5, 7)]
+    y = O.inverse(Y, g)
+    assert np.allclose(O.inverse_at_points(Y[1, 2], g, pts), [y[1, 2][p] for p in pts], rtol=1e-12, atol=1e-14)
+    ga = O.forward_adj(Y, g)
+    assert np.allclose(O.forward_adj_at_points(Y[0, 1], g, pts), [ga[0, 1][p] for p in pts], rtol=1e-12,
+                       atol=1e-12)
