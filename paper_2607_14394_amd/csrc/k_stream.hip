@@ -31,6 +31,12 @@ __device__ __forceinline__ v4f mfma(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// The inverse's real output is written once and not read again by this
+// library: stream it past the caches.
+__device__ __forceinline__ void store_stream(float* p, float a, float b, float c, float d) {
+  __builtin_nontemporal_store(v4f{a, b, c, d}, reinterpret_cast<v4f*>(p));
+}
+
 struct StreamArgs {
   int64_t rows;
   int nt, nz, kt, kz, zh, zt, vec;
@@ -350,10 +356,8 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
             va[i] = lo ? Y[hf][0][i] : recv;
             vb[i] = lo ? recv : Y[hf][TH - 1][i];
           }
-          if (za < a.zh)
-            *reinterpret_cast<float4*>(yrow + int64_t(za + hf * a.zh) * a.nt + tch) = make_float4(va[0], va[1], va[2], va[3]);
-          if (zb < a.zh)
-            *reinterpret_cast<float4*>(yrow + int64_t(zb + hf * a.zh) * a.nt + tch) = make_float4(vb[0], vb[1], vb[2], vb[3]);
+          if (za < a.zh) store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
+          if (zb < a.zh) store_stream(yrow + int64_t(zb + hf * a.zh) * a.nt + tch, vb[0], vb[1], vb[2], vb[3]);
         }
         continue;
       }
@@ -364,12 +368,11 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
         for (int mt = 0; mt < TH; ++mt) {
           const int t0 = 16 * mt + 4 * g;
           if (VEC) {
-            if (zok && t0 < a.nt)
-              *reinterpret_cast<float4*>(dst + t0) = make_float4(Y[hf][mt][0], Y[hf][mt][1], Y[hf][mt][2], Y[hf][mt][3]);
+            if (zok && t0 < a.nt) store_stream(dst + t0, Y[hf][mt][0], Y[hf][mt][1], Y[hf][mt][2], Y[hf][mt][3]);
           } else {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              if (zok && t0 + i < a.nt) dst[t0 + i] = Y[hf][mt][i];
+              if (zok && t0 + i < a.nt) __builtin_nontemporal_store(Y[hf][mt][i], dst + t0 + i);
           }
         }
       }
