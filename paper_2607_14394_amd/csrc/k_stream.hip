@@ -40,7 +40,13 @@ __device__ __forceinline__ void store_stream(float* p, float a, float b, float c
 struct StreamArgs {
   int64_t rows;
   int nt, nz, kt, kz, zh, zt, vec;
+  int full;  // every z tile and t group is complete: no masking needed
 };
+
+// DPP row rotate by 8 within each 16-lane row: lane m reads lane m ^ 8.
+__device__ __forceinline__ float ror8(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xf, 0xf, false));
+}
 
 // ---------------------------------------------------------------------------
 // Forward: x (rows x N_z x N_t) fp32 -> out (rows x K_z x K_t) complex.
@@ -52,7 +58,9 @@ struct StreamArgs {
 // early wait.  Within a tile the independent accumulator chains are
 // interleaved step by step.
 // ---------------------------------------------------------------------------
-template <int CT, int TH, int MT, int NCLS, bool VEC>
+// MODE 0: scalar loads (N_t % 4 != 0); 1: 16-byte loads with masks;
+// 2: 16-byte loads of complete tiles, no masks.
+template <int CT, int TH, int MT, int NCLS, int MODE>
 __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2* __restrict__ out,
                                             const float (&bt)[TH * 4][CT], const float4* lds,
                                             const StreamArgs& a, int64_t wave, int64_t wstride) {
@@ -62,7 +70,7 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
   const int64_t row_len = int64_t(a.nz) * a.nt;
   const int64_t n_iter = ((a.rows - 1 - wave) / wstride + 1) * a.zt;
 
-  // Load the tile of (row r, z-tile zt) into dst; ok[hf][h] (VEC) or
+  // Load the tile of (row r, z-tile zt) into dst; ok[hf][4h] (MODE 1) or
   // ok[hf][4h + j] (scalar) records which values are inside the row.
   auto load_tile = [&](int64_t r, int zt, float (&dst)[NCLS][TH][4], bool (&ok)[NCLS][TH * 4]) {
     const float* xr = x + r * row_len;
@@ -73,7 +81,11 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
       const int64_t zoff = int64_t(zl + hf * a.zh) * a.nt;
 #pragma unroll
       for (int h = 0; h < TH; ++h) {
-        if (VEC) {
+        if (MODE == 2) {
+          const float4 v = *reinterpret_cast<const float4*>(xr + zoff + 16 * h + 4 * g);
+          dst[hf][h][0] = v.x; dst[hf][h][1] = v.y; dst[hf][h][2] = v.z; dst[hf][h][3] = v.w;
+          ok[hf][4 * h] = true;
+        } else if (MODE == 1) {
           const int t0 = 16 * h + 4 * g;
           const bool v_ok = zok && t0 < a.nt;
           const float4 v = *reinterpret_cast<const float4*>(xr + (v_ok ? zoff + t0 : 0));
@@ -147,7 +159,7 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int hf = 0; hf < NCLS; ++hf) {
-          const float xa = ok[hf][VEC ? 4 * h : 4 * h + j] ? xv[hf][h][j] : 0.f;
+          const float xa = (MODE == 2 || ok[hf][MODE == 1 ? 4 * h : 4 * h + j]) ? xv[hf][h][j] : 0.f;
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct) V[hf][ct] = mfma(xa, bt[h * 4 + j][ct], V[hf][ct]);
         }
@@ -189,8 +201,8 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
           if (CT == 1) {
             const float q = P[cl][mr][0][i];
             const float u = P[cl][mr + MT / 2][0][i];
-            const float qs = __shfl_xor(q, 8);
-            const float us = __shfl_xor(u, 8);
+            const float qs = ror8(q);
+            const float us = ror8(u);
             if (m < KTP && m < a.kt && p < a.kz) orow[p * a.kt + m] = make_float2(q - us, qs + u);
           } else {
             const float rr = P[cl][mr][0][i], ri = P[cl][mr][CT - 1][i];
@@ -227,8 +239,9 @@ fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
   const int64_t wstride = int64_t(gridDim.x) * wpb;
   const int64_t wave = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6);
   if (wave >= a.rows) return;
-  if (a.vec) fwd_tz_body<CT, TH, MT, NCLS, true>(x, out, bt, lds, a, wave, wstride);
-  else fwd_tz_body<CT, TH, MT, NCLS, false>(x, out, bt, lds, a, wave, wstride);
+  if (a.full) fwd_tz_body<CT, TH, MT, NCLS, 2>(x, out, bt, lds, a, wave, wstride);
+  else if (a.vec) fwd_tz_body<CT, TH, MT, NCLS, 1>(x, out, bt, lds, a, wave, wstride);
+  else fwd_tz_body<CT, TH, MT, NCLS, 0>(x, out, bt, lds, a, wave, wstride);
 }
 
 // ---------------------------------------------------------------------------
@@ -239,7 +252,9 @@ fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
 // expansion (one chain per output tile) run as interleaved MFMA phases; all
 // stores of the tile follow them.
 // ---------------------------------------------------------------------------
-template <int CT, int TH, int MT, int NCLS, bool VEC>
+// MODE 0: scalar stores (N_t % 4 != 0); 1: 16-byte stores with masks;
+// 2: 16-byte stores of complete tiles, no masks.
+template <int CT, int TH, int MT, int NCLS, int MODE>
 __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float* __restrict__ y,
                                             const float (&ta)[TH][CT][4], const float4* lds,
                                             const StreamArgs& a, int64_t wave, int64_t wstride) {
@@ -339,7 +354,7 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
 
       const int zl = zt * 16 + m;
       const bool zok = zl < a.zh;
-      if (VEC && TH == 2 && a.nt == 32) {
+      if (MODE != 0 && TH == 2 && a.nt == 32) {
         // Rows of exactly 32 floats: lanes m and m^8 trade one 16-byte
         // chunk (DPP row rotate by 8) so that each store instruction writes
         // 8 whole 128-byte rows instead of 16 half rows.
@@ -356,8 +371,8 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
             va[i] = lo ? Y[hf][0][i] : recv;
             vb[i] = lo ? recv : Y[hf][TH - 1][i];
           }
-          if (za < a.zh) store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
-          if (zb < a.zh) store_stream(yrow + int64_t(zb + hf * a.zh) * a.nt + tch, vb[0], vb[1], vb[2], vb[3]);
+          if (MODE == 2 || za < a.zh) store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
+          if (MODE == 2 || zb < a.zh) store_stream(yrow + int64_t(zb + hf * a.zh) * a.nt + tch, vb[0], vb[1], vb[2], vb[3]);
         }
         continue;
       }
@@ -367,8 +382,9 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
 #pragma unroll
         for (int mt = 0; mt < TH; ++mt) {
           const int t0 = 16 * mt + 4 * g;
-          if (VEC) {
-            if (zok && t0 < a.nt) store_stream(dst + t0, Y[hf][mt][0], Y[hf][mt][1], Y[hf][mt][2], Y[hf][mt][3]);
+          if (MODE != 0) {
+            if (MODE == 2 || (zok && t0 < a.nt))
+              store_stream(dst + t0, Y[hf][mt][0], Y[hf][mt][1], Y[hf][mt][2], Y[hf][mt][3]);
           } else {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -403,8 +419,9 @@ inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
   const int64_t wstride = int64_t(gridDim.x) * wpb;
   const int64_t wave = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6);
   if (wave >= a.rows) return;
-  if (a.vec) inv_zt_body<CT, TH, MT, NCLS, true>(in, y, ta, lds, a, wave, wstride);
-  else inv_zt_body<CT, TH, MT, NCLS, false>(in, y, ta, lds, a, wave, wstride);
+  if (a.full) inv_zt_body<CT, TH, MT, NCLS, 2>(in, y, ta, lds, a, wave, wstride);
+  else if (a.vec) inv_zt_body<CT, TH, MT, NCLS, 1>(in, y, ta, lds, a, wave, wstride);
+  else inv_zt_body<CT, TH, MT, NCLS, 0>(in, y, ta, lds, a, wave, wstride);
 }
 
 typedef void (*fwd_fn)(const float*, float2*, const float*, const float4*, StreamArgs);
@@ -450,6 +467,7 @@ StreamArgs args_of(const StreamCfg& c, int64_t rows) {
   a.zh = c.zh;
   a.zt = c.zt;
   a.vec = c.vec;
+  a.full = (c.vec && c.zh % 16 == 0 && c.nt == 16 * c.th) ? 1 : 0;
   return a;
 }
 
