@@ -33,7 +33,6 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 FP32_MFMA_PEAK_TFS = 157.3   # MI355X dense fp32 matrix
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "hbm_counters.json")
-STREAM_SRC = os.path.join(ROOT, "paper_2607_14394_amd", "csrc", "k_stream.hip")
 
 
 def log(msg):
@@ -192,7 +191,10 @@ def traffic_entry(kernel, launches_per_step):
     except Exception:
         return None
     ent = c.get("kernels", {}).get(kernel)
-    if not ent or ent.get("source_sha") != _sha(STREAM_SRC):
+    if not ent:
+        return None
+    src = os.path.join(ROOT, "paper_2607_14394_amd", "csrc", ent.get("source", "k_stream.hip"))
+    if ent.get("source_sha") != _sha(src):
         return None
     return ent["fetch_kib"] * 1024 * c["fetch_scale"] + ent["write_kib"] * 1024 * c["write_scale"]
 

@@ -51,6 +51,11 @@ class Desc(ctypes.Structure):
 
 
 def _load():
+    # torch ships its own HIP runtime under the same soname (libamdhip64.so.7).
+    # Loading torch first makes libdtst.so bind to that one copy; loading
+    # libdtst.so first would bring a second HIP/HSA runtime into the process,
+    # and one of the two then finds no device.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"libdtst.so not found at {LIB_PATH}; build it with "
                           "`python paper_2607_14394_amd/build.py` (no fallback path exists)")
