@@ -44,8 +44,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4],
-                    help="workload table entry (default 2: 128^3x32 in 8 x-slabs)")
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5],
+                    help="workload table entry (default 2: 128^3x32 in 8 x-slabs; 5 times the backward)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-times", action="store_true",
                     help="skip the per-kernel event pass (used under rocprofv3)")
@@ -108,7 +108,43 @@ def _sha(path):
 
 
 # ---------------------------------------------------------------------------
-def build_workload(torch, D, synth, cfg, device):
+class Workload:
+    """One benchmark step and its accounting.
+
+    step()      launches the whole step on the current stream
+    launches    kernel role -> launches per step
+    work        kernel role -> algorithmic bytes / flops of one launch
+    bytes, flops, mfma_flops   the whole step
+    cpu_sample()  runs the fp64 oracle on a sample of the step and returns
+                  (seconds, fraction of the step's bytes it covered, description)
+    """
+
+
+def _geo(O, g, batch=None, c_in=None, c_out=None):
+    return O.Geometry(g["n_global"], g["n_local"], g["offset"], g["kmax"], g["kt"],
+                      g["batch"] if batch is None else batch, g["c_in"] if c_in is None else c_in,
+                      g["c_out"] if c_out is None else c_out)
+
+
+def _vol(g):
+    v = 1
+    for n in g["n_local"]:
+        v *= n
+    return v
+
+
+def _mix_work(g, m_count, kind):
+    B, ci, co = g["batch"], g["c_in"], g["c_out"]
+    spectra = B * (ci + co) * m_count * 8
+    return dict(bytes=m_count * ci * co * 8 + spectra, flops=8 * B * m_count * ci * co,
+                mfma_flops=8 * B * m_count * ci * co)
+
+
+def forward_workload(torch, D, synth, cfg, device):
+    """Forward partial DFT + mix + inverse over every shard of the workload.
+    Workload 2 runs its 8 slabs one after another: the forwards accumulate
+    into one spectrum, the mix runs over the 8 mode ranges in turn, and every
+    slab is then expanded back."""
     c = synth.CONFIGS[cfg]
     shards = []
     if cfg == 2:
@@ -131,62 +167,175 @@ def build_workload(torch, D, synth, cfg, device):
     xhat = torch.empty(plans[0].spectral_shape(g0["c_in"]), dtype=torch.complex64, device=device)
     yhat = torch.empty(plans[0].spectral_shape(g0["c_out"]), dtype=torch.complex64, device=device)
     ys = [torch.empty(p.spatial_shape(g0["c_out"]), dtype=torch.float32, device=device) for p in plans]
-    P = len(plans) if cfg == 2 else 1
+    P = len(plans)
     bounds = [(M * r) // P for r in range(P + 1)]
     ranges = [(bounds[r], bounds[r + 1]) for r in range(P)]
-    return shards, plans, W, xhat, yhat, ys, ranges
+
+    w = Workload()
+
+    def step():
+        for p, (plan, (_, x)) in enumerate(zip(plans, shards)):
+            plan.forward(x, xhat, accumulate=p > 0)
+        for m0, m1 in ranges:
+            plans[0].mix(xhat, W[m0:m1], yhat, m0, m1)
+        for plan, y in zip(plans, ys):
+            plan.inverse(yhat, y)
+
+    w.step = step
+    per = work(g0, g0["c_in"])
+    per["mix"] = _mix_work(g0, M // P, "mix")
+    w.work = per
+    w.launches = {k: P for k in ("stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "mix", "axis_inv_x",
+                                 "axis_inv_y", "stream_inv_zt")}
+    w.flops = sum(per[k]["flops"] * n for k, n in w.launches.items())
+    w.mfma_flops = sum(per[k]["mfma_flops"] * n for k, n in w.launches.items())
+    B, ci, co = g0["batch"], g0["c_in"], g0["c_out"]
+    w.bytes = P * B * (ci + co) * _vol(g0) * 4 + M * ci * co * 8   # read x, write y, read W
+    w.metric = "spectral-layer ms and GB/s + TFLOP/s per MI355X (fwd partial DFT+mix+inverse)"
+    w.config = {"workload": synth.CONFIGS[cfg]["name"], "global_grid": list(g0["n_global"]),
+                "local_shard": list(g0["n_local"]), "shards_run_in_sequence": P, "batch": B,
+                "c_in": ci, "c_out": co,
+                "modes": [2 * g0["kmax"][0], 2 * g0["kmax"][1], 2 * g0["kmax"][2], g0["kt"]]}
+
+    def cpu_sample(min_seconds=10.0):
+        """Whole fp64 oracle layers of this workload when a layer is small
+        (repeated until min_seconds), else the first channels of shard 0
+        through forward, mix on a mode range, inverse."""
+        import numpy as np
+        import oracle as O
+        if w.bytes <= 16e9:
+            geos = [_geo(O, g) for g, _ in shards]
+            xs = [x.cpu().numpy() for _, x in shards]
+            Ws = W.cpu().numpy()
+            layers = 0
+            t0 = time.perf_counter()
+            while True:
+                X = None
+                for x, geo in zip(xs, geos):
+                    part = O.forward(x, geo)
+                    X = part if X is None else X + part
+                Y = O.mix(X, Ws, 0, M, c_out=co).reshape((X.shape[0], co) + geos[0].K)
+                for geo in geos:
+                    O.inverse(Y, geo)
+                layers += 1
+                dt = time.perf_counter() - t0
+                if dt >= min_seconds:
+                    break
+            return dt, float(layers), (f"fp64 oracle, {layers} whole layer(s) of this workload ({P} shard forwards "
+                                       f"summed, mix over all {M} modes, {P} shard inverses), inputs in host memory")
+        nc = 1
+        ms = 8192
+        g, x = shards[0]
+        geo = _geo(O, g, batch=1, c_in=nc, c_out=nc)
+        xs = x[0:1, 0:nc].cpu().numpy()
+        Ws = W[:ms, :, :].cpu().numpy()
+        Xs = synth.np_complex_normal((B, ci, ms), 12345)
+        Ys = synth.np_complex_normal((1, nc) + geo.K, 12346)
+        t0 = time.perf_counter()
+        O.forward(xs, geo)
+        O.mix(Xs, Ws, 0, ms, c_out=co)
+        O.inverse(Ys, geo)
+        dt = time.perf_counter() - t0
+        frac = (2 * nc * _vol(g) * 4 + ms * ci * co * 8) / w.bytes
+        return dt, frac, (f"fp64 oracle: forward and inverse of one (b, c) slice of shard 0 and the mix over "
+                          f"{ms} modes; GB/s scaled by the share of the layer's bytes it covers ({frac:.2e})")
+
+    w.cpu_sample = cpu_sample
+    return w
 
 
-def layer_step(plans, shards, W, xhat, yhat, ys, ranges):
-    for p, (plan, (_, x)) in enumerate(zip(plans, shards)):
-        plan.forward(x, xhat, accumulate=p > 0)
-    for m0, m1 in ranges:
-        plans[0].mix(xhat, W[m0:m1], yhat, m0, m1)
-    for plan, y in zip(plans, ys):
-        plan.inverse(yhat, y)
+def backward_workload(torch, D, synth, cfg, device):
+    """Backward of the spectral layer on one shard: inverse_adj of the
+    upstream gradient, the mix data gradient (W^H), the weight gradient and
+    forward_adj, over the full mode set."""
+    g = synth.geometry(cfg)
+    plan = D.Plan(g, device)
+    M = plan.n_modes
+    B, ci, co = g["batch"], g["c_in"], g["c_out"]
+    x = synth.torch_input(cfg, g, device)
+    xhat = torch.empty(plan.spectral_shape(ci), dtype=torch.complex64, device=device)
+    plan.forward(x, xhat)            # set-up: the saved forward spectrum
+    torch.cuda.synchronize()
+    del x
+    torch.cuda.empty_cache()
+    W = synth.torch_weights(M, ci, co, synth.seed_of(cfg, "weights"), device)
+    gy = synth.torch_normal(tuple(plan.spatial_shape(co)), synth.seed_of(cfg, "upstream"), device)
+    gyh = torch.empty(plan.spectral_shape(co), dtype=torch.complex64, device=device)
+    gxh = torch.empty(plan.spectral_shape(ci), dtype=torch.complex64, device=device)
+    gW = torch.empty_like(W)
+    gx = torch.empty(plan.spatial_shape(ci), dtype=torch.float32, device=device)
+
+    w = Workload()
+
+    def step():
+        plan.inverse_adj(gy, gyh)
+        plan.mix(gyh, W, gxh, 0, M, op=1)
+        plan.wgrad(xhat, gyh, gW, 0, M)
+        plan.forward_adj(gxh, gx)
+
+    w.step = step
+    per_o = work(g, co)       # inverse_adj runs the forward-direction kernels on C_out channels
+    per_i = work(g, ci)       # forward_adj runs the inverse-direction kernels on C_in channels
+    per = {k: per_o[k] for k in ("stream_fwd_tz", "axis_fwd_y", "axis_fwd_x")}
+    per.update({k: per_i[k] for k in ("axis_inv_x", "axis_inv_y", "stream_inv_zt")})
+    per["mix_h"] = _mix_work(g, M, "mix_h")
+    per["wgrad"] = _mix_work(g, M, "wgrad")
+    w.work = per
+    w.launches = {k: 1 for k in per}
+    w.flops = sum(per[k]["flops"] for k in per)
+    w.mfma_flops = sum(per[k]["mfma_flops"] for k in per)
+    w.bytes = B * (ci + co) * _vol(g) * 4 + 2 * M * ci * co * 8   # read g_y, write g_x, read W, write g_W
+    w.metric = ("spectral-layer backward ms and GB/s + TFLOP/s per MI355X "
+                "(inverse_adj + mix data grad + wgrad + forward_adj)")
+    w.config = {"workload": synth.CONFIGS[cfg]["name"], "global_grid": list(g["n_global"]),
+                "local_shard": list(g["n_local"]), "shards_run_in_sequence": 1, "batch": B,
+                "c_in": ci, "c_out": co,
+                "modes": [2 * g["kmax"][0], 2 * g["kmax"][1], 2 * g["kmax"][2], g["kt"]]}
+
+    def cpu_sample(min_seconds=10.0):
+        """One (b, c) slice through inverse_adj and forward_adj, and the
+        data and weight gradients over a mode range, on the fp64 oracle."""
+        import oracle as O
+        nc = 1
+        ms = 4096
+        geo = _geo(O, g, batch=1, c_in=nc, c_out=nc)
+        gys = gy[0:1, 0:nc].cpu().numpy()
+        Ws = W[:ms].cpu().numpy()
+        Xs = synth.np_complex_normal((B, ci, ms), 12345)
+        Gs = synth.np_complex_normal((B, co, ms), 12346)
+        GXs = synth.np_complex_normal((1, nc) + geo.K, 12347)
+        t0 = time.perf_counter()
+        O.inverse_adj(gys, geo)
+        O.mix_data_grad(Gs, Ws, 0, ms)
+        O.mix_wgrad(Xs, Gs, 0, ms)
+        O.forward_adj(GXs, geo)
+        dt = time.perf_counter() - t0
+        frac = (2 * nc * _vol(g) * 4 + 2 * ms * ci * co * 8) / w.bytes
+        return dt, frac, (f"fp64 oracle: inverse_adj and forward_adj of one (b, c) slice and the data and "
+                          f"weight gradients over {ms} modes; GB/s scaled by the share of the step's bytes "
+                          f"it covers ({frac:.2e})")
+
+    w.cpu_sample = cpu_sample
+    return w
 
 
-def cpu_baseline(torch, synth, cfg, shards, W, layer_bytes, min_seconds=10.0):
-    """The fp64 oracle on the same workload: every shard's forward summed,
-    the mix over all modes, every shard's inverse -- one whole layer,
-    repeated until at least min_seconds of CPU work have been timed."""
-    import numpy as np
-    import oracle as O
+def cpu_baseline(w):
+    """Times the fp64 oracle on the workload's sample with the BLAS threads
+    set to the cores this process may use."""
     try:
         from threadpoolctl import threadpool_info, threadpool_limits
     except Exception:  # pragma: no cover
         threadpool_limits = None
     cores = len(os.sched_getaffinity(0))
-    geos = [O.Geometry(g["n_global"], g["n_local"], g["offset"], g["kmax"], g["kt"], g["batch"], g["c_in"],
-                       g["c_out"]) for g, _ in shards]
-    xs = [x.cpu().numpy() for _, x in shards]
-    Ws = W.cpu().numpy()
-    M = Ws.shape[0]
-    c_out = shards[0][0]["c_out"]
     ctx = threadpool_limits(limits=cores) if threadpool_limits else None
-    layers = 0
     try:
-        t0 = time.perf_counter()
-        while True:
-            X = None
-            for x, geo in zip(xs, geos):
-                part = O.forward(x, geo)
-                X = part if X is None else X + part
-            Y = O.mix(X, Ws, 0, M, c_out=c_out).reshape((X.shape[0], c_out) + geos[0].K)
-            for geo in geos:
-                O.inverse(Y, geo)
-            layers += 1
-            dt = time.perf_counter() - t0
-            if dt >= min_seconds:
-                break
+        dt, frac, desc = w.cpu_sample()
         threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1) if threadpool_limits else cores
     finally:
         if ctx is not None:
             ctx.__exit__(None, None, None)
-    return {"value": round(layer_bytes * layers / dt / 1e9, 3), "unit": "GB/s", "cores": int(threads),
-            "kind": "oracle", "seconds": round(dt, 2),
-            "sample": f"fp64 oracle, {layers} whole layer(s) of this workload ({len(shards)} shard forwards "
-                      f"summed, mix over all {M} modes, {len(shards)} shard inverses), inputs in host memory"}
+    return {"value": round(w.bytes * frac / dt / 1e9, 3), "unit": "GB/s", "cores": int(threads),
+            "kind": "oracle", "seconds": round(dt, 2), "sample": desc}
 
 
 def traffic_entry(kernel, launches_per_step):
@@ -246,13 +395,12 @@ def main():
         del blk
         torch.cuda.empty_cache()
     log(f"building workload {cfg}")
-    shards, plans, W, xhat, yhat, ys, ranges = build_workload(torch, D, synth, cfg, device)
-    g0 = shards[0][0]
+    w = backward_workload(torch, D, synth, cfg, device) if cfg == 5 else forward_workload(torch, D, synth, cfg, device)
     log(f"warmup {args.warmup} steps")
 
     # ---- warmup ----
     for _ in range(args.warmup):
-        layer_step(plans, shards, W, xhat, yhat, ys, ranges)
+        w.step()
     torch.cuda.synchronize()
 
     log(f"timing {args.steps} steps")
@@ -263,7 +411,7 @@ def main():
     torch.cuda.synchronize()
     t0.record(stream)
     for _ in range(args.steps):
-        layer_step(plans, shards, W, xhat, yhat, ys, ranges)
+        w.step()
     t1.record(stream)
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / args.steps
@@ -275,68 +423,51 @@ def main():
         D.dtst_profile_collect()
         torch.cuda.synchronize()
         for _ in range(args.steps):
-            layer_step(plans, shards, W, xhat, yhat, ys, ranges)
+            w.step()
         torch.cuda.synchronize()
         prof = D.dtst_profile_collect()
         D.dtst_profile_enable(False)
         kernel_ms = {k: (n, tot / n) for k, (n, tot) in prof.items()}
 
     # ---- accounting ----
-    P = len(shards)
-    per = work(g0, g0["c_in"])
-    per_mix = work(g0, g0["c_in"], m_count=plans[0].n_modes // P)
-    launches = {"stream_fwd_tz": P, "axis_fwd_y": P, "axis_fwd_x": P, "mix": P, "axis_inv_x": P,
-                "axis_inv_y": P, "stream_inv_zt": P}
-    layer_flops = sum(per[k]["flops"] * n for k, n in launches.items() if k != "mix") + P * per_mix["mix"]["flops"]
-    layer_mfma = sum(per[k]["mfma_flops"] * n for k, n in launches.items() if k != "mix") + P * per_mix["mix"]["flops"]
-    B, ci, co = g0["batch"], g0["c_in"], g0["c_out"]
-    vol = 1
-    for v in g0["n_local"]:
-        vol *= v
-    M = plans[0].n_modes
-    layer_bytes = P * B * (ci + co) * vol * 4 + M * ci * co * 8   # read x, write y, read W
     sec = ms_per_step / 1e3
-    gbs = layer_bytes / sec / 1e9
-
+    gbs = w.bytes / sec / 1e9
     roof = None
     stages = {}
     if kernel_ms:
         for k, (n, avg) in kernel_ms.items():
-            wk = per_mix["mix"] if k == "mix" else per.get(k)
+            wk = w.work.get(k)
             if wk is None:
                 continue
             stages[k] = {"launches_per_step": n // args.steps, "avg_ms": round(avg, 4),
                          "GB_s": round(wk["bytes"] / (avg / 1e3) / 1e9, 1),
                          "TFLOP_s": round(wk["flops"] / (avg / 1e3) / 1e12, 2),
                          "mfma_TFLOP_s": round(wk["mfma_flops"] / (avg / 1e3) / 1e12, 2)}
-        dom = max(kernel_ms, key=lambda k: kernel_ms[k][0] * kernel_ms[k][1])
+        dom = max((k for k in kernel_ms if k in w.work), key=lambda k: kernel_ms[k][0] * kernel_ms[k][1])
         n, avg = kernel_ms[dom]
-        wk = per_mix["mix"] if dom == "mix" else per[dom]
+        wk = w.work[dom]
         ach = wk["bytes"] / (avg / 1e3) / 1e9
-        tr = traffic_entry(dom, n // args.steps)
+        tr = traffic_entry(dom, n // args.steps) if cfg == 2 else None
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None if tr is None else int(tr),
                 "algorithmic_bytes_per_launch": int(wk["bytes"]), "avg_launch_ms": round(avg, 4)}
 
     out = {
-        "metric": "spectral-layer ms and GB/s + TFLOP/s per MI355X (fwd partial DFT+mix+inverse)",
+        "metric": w.metric,
         "value": round(gbs, 2), "unit": "GB/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "layer_ms": round(ms_per_step, 4),
-        "layer_TFLOP_s": round(layer_flops / sec / 1e12, 3),
-        "layer_mfma_TFLOP_s": round(layer_mfma / sec / 1e12, 3),
-        "layer_bytes": int(layer_bytes), "layer_flops": int(layer_flops),
-        "config": {"workload": synth.CONFIGS[cfg]["name"], "global_grid": list(g0["n_global"]),
-                   "local_shard": list(g0["n_local"]), "shards_run_in_sequence": P, "batch": B,
-                   "c_in": ci, "c_out": co, "modes": [2 * g0["kmax"][0], 2 * g0["kmax"][1], 2 * g0["kmax"][2],
-                                                      g0["kt"]]},
+        "layer_TFLOP_s": round(w.flops / sec / 1e12, 3),
+        "layer_mfma_TFLOP_s": round(w.mfma_flops / sec / 1e12, 3),
+        "layer_bytes": int(w.bytes), "layer_flops": int(w.flops),
+        "config": w.config,
         "roofline": roof, "stages": stages,
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on a sample")
-        out["cpu_baseline"] = cpu_baseline(torch, synth, cfg, shards, W, layer_bytes)
+        out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
 
 

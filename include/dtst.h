@@ -89,7 +89,8 @@ typedef struct {
 
 /* Check a descriptor.  DTST_OK, DTST_ERR_INVALID_ARG for a geometry the
  * method does not define, DTST_ERR_UNSUPPORTED for one the kernels do not
- * cover (currently: kt <= 16, N_t^loc <= 64, and per-kernel LDS limits). */
+ * cover (currently: kt <= 16, N_t^loc <= 64, c_out <= 512, and per-kernel
+ * LDS limits). */
 dtst_status dtst_desc_validate(const dtst_desc* d);
 
 /* Workspace bytes the execute calls of this geometry need (>= 0). */

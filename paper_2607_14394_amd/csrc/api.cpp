@@ -229,9 +229,10 @@ dtst_status dtst_desc_validate(const dtst_desc* d) {
   std::string err;
   const dtst_status s = dtst::derive(d, &dv, &err);
   if (s != DTST_OK) return fail(s, err);
-  const size_t mix_max = dtst::mix_lds_bytes(1, dv.d.batch, dv.d.c_in, dv.d.c_out);
-  if (mix_max > 160 * 1024)
-    return fail(DTST_ERR_UNSUPPORTED, "batch * channels too large for one mode of the mix kernels");
+  if (dv.d.c_out > dtst::kMixMaxCout)
+    return fail(DTST_ERR_UNSUPPORTED, "c_out above " + std::to_string(dtst::kMixMaxCout) + " for the mix kernels");
+  if (dtst::mix_lds_bytes(dv.d.batch, dv.d.c_in, dv.d.c_out) > 160 * 1024)
+    return fail(DTST_ERR_UNSUPPORTED, "batch * channels too large for one workgroup of the mix kernels");
   return ok();
 }
 

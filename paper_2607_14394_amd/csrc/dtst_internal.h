@@ -98,8 +98,10 @@ int launch_inv_zt(const StreamCfg& c, const void* in, float* y, int64_t rows,
                   const float* timg, const float* zimg, void* stream);
 int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const float* img,
                 int accumulate, void* stream);
-// LDS bytes per staged mode of a mix launch (op 0: mix / wgrad, 1: mix_h).
-size_t mix_lds_bytes(int op, int64_t B, int64_t ci, int64_t co);
+// LDS bytes of one workgroup of the mix kernels (mix, mix_h and wgrad alike).
+size_t mix_lds_bytes(int64_t B, int64_t ci, int64_t co);
+// Largest C_out the mix kernels cover (64 lanes x 8 columns per row).
+constexpr int64_t kMixMaxCout = 512;
 int launch_mix(const void* xhat, const void* w, void* yhat, int64_t B, int64_t ci, int64_t co,
                int64_t M, int64_t m0, int64_t m1, void* stream);
 int launch_mix_h(const void* gy, const void* w, void* gx, int64_t B, int64_t ci, int64_t co,

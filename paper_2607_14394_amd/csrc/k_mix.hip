@@ -6,11 +6,18 @@
 //   wgrad    g_w[m-m0,i,o] (+)= sum_b conj(xhat[b,i,m]) g_y[b,o,m]
 //
 // With B <= 2 the arithmetic intensity is about 1-2 flop/byte, so all three
-// are bound by HBM traffic on w / g_w (M C_in C_out complex values).  Each
-// workgroup owns a block of consecutive modes: the spectra of those modes
-// (stride M between channels) are staged through LDS so that every global
-// access is coalesced, and w / g_w are streamed in their natural
-// (m, i, o) order.
+// are bound by HBM traffic on w / g_w (M C_in C_out complex values).
+//
+// Layout of the work: a "row group" of LPR lanes (the power of two >= C_out,
+// at most 64) covers one row (m, i, 0..C_out) of w / g_w, lane l holding the
+// columns o = l + LPR s (s < OPL), so every row is read or written with
+// contiguous 8-byte accesses.  A 256-thread workgroup has 256 / LPR groups and
+// owns that many consecutive modes, one per group.  The spectra of those modes
+// (stride M between channels in HBM) are staged through LDS as
+// [b][mode][channel + 1], which turns their strided reads into coalesced ones
+// and gives each group its per-mode vectors.  The first rows of w are loaded
+// into registers before the staging barrier, so their HBM latency overlaps
+// the staging.
 #include <hip/hip_runtime.h>
 
 #include "dtst_internal.h"
@@ -21,28 +28,31 @@ namespace {
 struct MixArgs {
   int64_t M, m0, count;  // count = m1 - m0
   int64_t nblk;           // number of mode blocks
-  int B, ci, co, mpb;     // mpb = modes per block
+  int B, ci, co;
+  int lpr, mpb;           // lanes per row group, modes per block (= 256 / lpr)
   int acc;
 };
 
-__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
-  return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
-}
-// conj(a) * b
-__device__ __forceinline__ float2 cjmul(float2 a, float2 b) {
-  return make_float2(a.x * b.x + a.y * b.y, a.x * b.y - a.y * b.x);
-}
+typedef float v2f __attribute__((ext_vector_type(2)));
 
-constexpr int BCH = 4;  // batch entries accumulated per pass
+// Spectrum entries of one batch chunk processed together.
+constexpr int BCH = 2;
 
-// Stage spec[b][c][mbase .. mbase+nm) (channels C) into LDS as [b][c][mm].
+// w rows held in registers per chunk (times OPL columns per lane).
+template <int OPL>
+struct Rows {
+  static constexpr int value = OPL >= 8 ? 2 : 16 / OPL;
+};
+
+// spec[b][c][mbase + mm] (channel stride M) -> dst[(b * mpb + mm) * (C + 1) + c]
 __device__ __forceinline__ void stage(float2* dst, const float2* __restrict__ spec, int B, int C, int64_t M,
                                       int64_t mbase, int nm, int mpb) {
   const int n = B * C * nm;
   for (int e = threadIdx.x; e < n; e += blockDim.x) {
     const int mm = e % nm;
     const int bc = e / nm;
-    dst[bc * mpb + mm] = spec[int64_t(bc) * M + mbase + mm];
+    const int b = bc / C, c = bc % C;
+    dst[(b * mpb + mm) * (C + 1) + c] = spec[int64_t(bc) * M + mbase + mm];
   }
 }
 
@@ -52,153 +62,271 @@ __device__ __forceinline__ void unstage(float2* __restrict__ spec, const float2*
   for (int e = threadIdx.x; e < n; e += blockDim.x) {
     const int mm = e % nm;
     const int bc = e / nm;
-    spec[int64_t(bc) * M + mbase + mm] = src[bc * mpb + mm];
+    const int b = bc / C, c = bc % C;
+    spec[int64_t(bc) * M + mbase + mm] = src[(b * mpb + mm) * (C + 1) + c];
   }
 }
 
+// Loads rows i0 .. i0 + R - 1 of the (ci x co) matrix at `base` into v;
+// rows or columns outside the matrix (and inactive groups) read its first
+// element and are never used.
+template <int OPL, int R>
+__device__ __forceinline__ void load_rows(float2 (&v)[R][OPL], const float2* __restrict__ base, int i0, int ci,
+                                          int co, int lr, int lpr, bool active) {
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int s = 0; s < OPL; ++s) {
+      const int i = i0 + r, o = lr + lpr * s;
+      const bool ok = active && i < ci && o < co;
+      v[r][s] = base[ok ? int64_t(i) * co + o : 0];
+    }
+}
+
+// Sum of v over each aligned group of LPR lanes (a power of two <= 64),
+// with DPP steps: pairs and quads (quad_perm), 8 and 16 lanes (row half
+// mirror, row mirror), then 32 and 64 lanes by broadcasting the last lane of
+// a row into the next row(s).  The full sum is valid in the group's last
+// lane (lanes >= 16 of a 32-lane group, >= 48 of a 64-lane group; every lane
+// for groups up to 16).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xf, false));
+}
+template <int LPR>
+__device__ __forceinline__ float group_sum(float v) {
+  if (LPR > 1) v += dpp<0xB1, 0xf>(v);   // quad_perm [1, 0, 3, 2]
+  if (LPR > 2) v += dpp<0x4E, 0xf>(v);   // quad_perm [2, 3, 0, 1]
+  if (LPR > 4) v += dpp<0x141, 0xf>(v);  // row_half_mirror
+  if (LPR > 8) v += dpp<0x140, 0xf>(v);  // row_mirror
+  if (LPR > 16) v += dpp<0x142, 0xa>(v); // row_bcast:15 into rows 1 and 3
+  if (LPR > 32) v += dpp<0x143, 0xc>(v); // row_bcast:31 into rows 2 and 3
+  return v;
+}
+
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+  return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+// conj(a) * b
+__device__ __forceinline__ float2 cjmul(float2 a, float2 b) {
+  return make_float2(a.x * b.x + a.y * b.y, a.x * b.y - a.y * b.x);
+}
+
+template <int LPR, int OPL>
 __global__ void __launch_bounds__(256)
 mix_kernel(const float2* __restrict__ x, const float2* __restrict__ w, float2* __restrict__ y, MixArgs a) {
+  constexpr int R = Rows<OPL>::value;
   extern __shared__ float2 sm[];
-  float2* sx = sm;                          // [B][ci][mpb]
-  float2* sy = sm + a.B * a.ci * a.mpb;     // [B][co][mpb]
+  float2* sx = sm;                                // [B][mpb][ci + 1]
+  float2* sy = sm + a.B * a.mpb * (a.ci + 1);     // [B][mpb][co + 1]
+  const int lr = threadIdx.x % LPR, mm = threadIdx.x / LPR;
   for (int64_t blk = blockIdx.x; blk < a.nblk; blk += gridDim.x) {
-  const int64_t lm0 = blk * a.mpb;  // local mode index in [0, count)
-  const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
-  const int64_t mbase = a.m0 + lm0;
-  stage(sx, x, a.B, a.ci, a.M, mbase, nm, a.mpb);
-  __syncthreads();
-  for (int e = threadIdx.x; e < nm * a.co; e += blockDim.x) {
-    const int o = e % a.co;
-    const int mm = e / a.co;
-    const float2* wp = w + (lm0 + mm) * int64_t(a.ci) * a.co + o;
-    for (int b0 = 0; b0 < a.B; b0 += BCH) {
-      float2 acc[BCH];
+    const int64_t lm0 = blk * a.mpb;  // local mode index in [0, count)
+    const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
+    const int64_t mbase = a.m0 + lm0;
+    const bool active = mm < nm;
+    const float2* wm = w + (lm0 + (active ? mm : 0)) * int64_t(a.ci) * a.co;
+    float2 wv[R][OPL];
+    load_rows<OPL, R>(wv, wm, 0, a.ci, a.co, lr, LPR, active);
+    stage(sx, x, a.B, a.ci, a.M, mbase, nm, a.mpb);
+    __syncthreads();
+    for (int i0 = 0; i0 < a.ci; i0 += R) {
+      if (i0 > 0) load_rows<OPL, R>(wv, wm, i0, a.ci, a.co, lr, LPR, active);
+      for (int b0 = 0; b0 < a.B; b0 += BCH) {
+        float2 acc[BCH][OPL];
 #pragma unroll
-      for (int q = 0; q < BCH; ++q) acc[q] = make_float2(0.f, 0.f);
-      for (int i = 0; i < a.ci; ++i) {
-        const float2 wv = wp[int64_t(i) * a.co];
+        for (int q = 0; q < BCH; ++q)
 #pragma unroll
-        for (int q = 0; q < BCH; ++q) {
-          if (b0 + q < a.B) {
-            const float2 xv = sx[((b0 + q) * a.ci + i) * a.mpb + mm];
-            const float2 p = cmul(xv, wv);
-            acc[q].x += p.x;
-            acc[q].y += p.y;
+          for (int s = 0; s < OPL; ++s) acc[q][s] = make_float2(0.f, 0.f);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if (i0 + r >= a.ci) continue;
+#pragma unroll
+          for (int q = 0; q < BCH; ++q) {
+            if (b0 + q >= a.B) continue;
+            const float2 xv = sx[((b0 + q) * a.mpb + mm) * (a.ci + 1) + i0 + r];
+#pragma unroll
+            for (int s = 0; s < OPL; ++s) {
+              const float2 p = cmul(xv, wv[r][s]);
+              acc[q][s].x += p.x;
+              acc[q][s].y += p.y;
+            }
+          }
+        }
+        if (active) {
+#pragma unroll
+          for (int q = 0; q < BCH; ++q) {
+            if (b0 + q >= a.B) continue;
+#pragma unroll
+            for (int s = 0; s < OPL; ++s) {
+              const int o = lr + LPR * s;
+              if (o >= a.co) continue;
+              float2* d = sy + ((b0 + q) * a.mpb + mm) * (a.co + 1) + o;
+              if (i0 > 0) {
+                acc[q][s].x += d->x;
+                acc[q][s].y += d->y;
+              }
+              *d = acc[q][s];
+            }
           }
         }
       }
-#pragma unroll
-      for (int q = 0; q < BCH; ++q)
-        if (b0 + q < a.B) sy[((b0 + q) * a.co + o) * a.mpb + mm] = acc[q];
     }
-  }
-  __syncthreads();
-  unstage(y, sy, a.B, a.co, a.M, mbase, nm, a.mpb);
-  __syncthreads();
+    __syncthreads();
+    unstage(y, sy, a.B, a.co, a.M, mbase, nm, a.mpb);
+    __syncthreads();
   }
 }
 
-// Data gradient: the w block of the workgroup's modes is staged in LDS
-// (row stride 2*co + 2 floats, so lanes reading consecutive rows i hit
-// different banks) and each thread owns one (mode, i) pair.
+// Data gradient: each row (m, i) of w gives g_x[b, i, m] for every b as a
+// sum over the row's C_out columns, reduced across the row group's lanes.
+template <int LPR, int OPL>
 __global__ void __launch_bounds__(256)
 mix_h_kernel(const float2* __restrict__ gy, const float2* __restrict__ w, float2* __restrict__ gx, MixArgs a) {
+  constexpr int R = Rows<OPL>::value;
   extern __shared__ float2 sm[];
-  const int wrow = a.co + 1;                           // float2 stride of one (mode, i) row
-  float2* sw = sm;                                     // [mpb][ci][wrow]
-  float2* sg = sw + a.mpb * a.ci * wrow;               // [B][co][mpb]
-  float2* sx = sg + a.B * a.co * a.mpb;                // [B][ci][mpb]
+  float2* sg = sm;                                // [B][mpb][co + 1]
+  float2* sx = sm + a.B * a.mpb * (a.co + 1);     // [B][mpb][ci + 1]
+  const int lr = threadIdx.x % LPR, mm = threadIdx.x / LPR;
   for (int64_t blk = blockIdx.x; blk < a.nblk; blk += gridDim.x) {
-  const int64_t lm0 = blk * a.mpb;
-  const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
-  const int64_t mbase = a.m0 + lm0;
-  stage(sg, gy, a.B, a.co, a.M, mbase, nm, a.mpb);
-  const int nw = nm * a.ci * a.co;
-  const float2* wb = w + lm0 * int64_t(a.ci) * a.co;
-  for (int e = threadIdx.x; e < nw; e += blockDim.x) {
-    const int o = e % a.co;
-    const int mi = e / a.co;  // mm * ci + i
-    sw[mi * wrow + o] = wb[e];
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < nm * a.ci; e += blockDim.x) {
-    const int i = e % a.ci;
-    const int mm = e / a.ci;
-    const float2* wr = sw + (mm * a.ci + i) * wrow;
-    for (int b0 = 0; b0 < a.B; b0 += BCH) {
-      float2 acc[BCH];
+    const int64_t lm0 = blk * a.mpb;
+    const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
+    const int64_t mbase = a.m0 + lm0;
+    const bool active = mm < nm;
+    const float2* wm = w + (lm0 + (active ? mm : 0)) * int64_t(a.ci) * a.co;
+    float2 wv[R][OPL];
+    load_rows<OPL, R>(wv, wm, 0, a.ci, a.co, lr, LPR, active);
+    stage(sg, gy, a.B, a.co, a.M, mbase, nm, a.mpb);
+    __syncthreads();
+    for (int i0 = 0; i0 < a.ci; i0 += R) {
+      if (i0 > 0) load_rows<OPL, R>(wv, wm, i0, a.ci, a.co, lr, LPR, active);
+      for (int b0 = 0; b0 < a.B; b0 += BCH) {
+        // this lane's columns of g_y for the batch chunk
+        float2 gv[BCH][OPL];
 #pragma unroll
-      for (int q = 0; q < BCH; ++q) acc[q] = make_float2(0.f, 0.f);
-      for (int o = 0; o < a.co; ++o) {
-        const float2 wv = wr[o];
+        for (int q = 0; q < BCH; ++q)
 #pragma unroll
-        for (int q = 0; q < BCH; ++q) {
-          if (b0 + q < a.B) {
-            const float2 gv = sg[((b0 + q) * a.co + o) * a.mpb + mm];
-            const float2 p = cjmul(wv, gv);
-            acc[q].x += p.x;
-            acc[q].y += p.y;
+          for (int s = 0; s < OPL; ++s) {
+            const int o = lr + LPR * s;
+            gv[q][s] = (b0 + q < a.B && o < a.co && active) ? sg[((b0 + q) * a.mpb + mm) * (a.co + 1) + o]
+                                                             : make_float2(0.f, 0.f);
+          }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if (i0 + r >= a.ci) continue;
+#pragma unroll
+          for (int q = 0; q < BCH; ++q) {
+            if (b0 + q >= a.B) continue;
+            float2 t = make_float2(0.f, 0.f);
+#pragma unroll
+            for (int s = 0; s < OPL; ++s) {
+              const float2 p = cjmul(wv[r][s], gv[q][s]);
+              t.x += p.x;
+              t.y += p.y;
+            }
+            t.x = group_sum<LPR>(t.x);
+            t.y = group_sum<LPR>(t.y);
+            if (lr == LPR - 1 && active) sx[((b0 + q) * a.mpb + mm) * (a.ci + 1) + i0 + r] = t;
           }
         }
       }
-#pragma unroll
-      for (int q = 0; q < BCH; ++q)
-        if (b0 + q < a.B) sx[((b0 + q) * a.ci + i) * a.mpb + mm] = acc[q];
     }
-  }
-  __syncthreads();
-  unstage(gx, sx, a.B, a.ci, a.M, mbase, nm, a.mpb);
-  __syncthreads();
+    __syncthreads();
+    unstage(gx, sx, a.B, a.ci, a.M, mbase, nm, a.mpb);
+    __syncthreads();
   }
 }
 
+// Weight gradient: each lane forms its columns of a chunk of rows (m, i) in
+// registers -- its g_y values of the batch chunk held in registers, x
+// broadcast from LDS -- and streams the rows out with non-temporal stores
+// (g_w is written once and not read back here, except for the accumulate
+// read-modify-write).
+template <int LPR, int OPL>
 __global__ void __launch_bounds__(256)
 wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2* __restrict__ gw, MixArgs a) {
+  constexpr int R = Rows<OPL>::value;
   extern __shared__ float2 sm[];
-  float2* sx = sm;                       // [B][ci][mpb]
-  float2* sg = sm + a.B * a.ci * a.mpb;  // [B][co][mpb]
+  float2* sx = sm;                                // [B][mpb][ci + 1]
+  float2* sg = sm + a.B * a.mpb * (a.ci + 1);     // [B][mpb][co + 1]
+  const int lr = threadIdx.x % LPR, mm = threadIdx.x / LPR;
   for (int64_t blk = blockIdx.x; blk < a.nblk; blk += gridDim.x) {
-  const int64_t lm0 = blk * a.mpb;
-  const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
-  const int64_t mbase = a.m0 + lm0;
-  stage(sx, x, a.B, a.ci, a.M, mbase, nm, a.mpb);
-  stage(sg, gy, a.B, a.co, a.M, mbase, nm, a.mpb);
-  __syncthreads();
-  for (int e = threadIdx.x; e < nm * a.co; e += blockDim.x) {
-    const int o = e % a.co;
-    const int mm = e / a.co;
-    float2* gp = gw + (lm0 + mm) * int64_t(a.ci) * a.co + o;
-    for (int i = 0; i < a.ci; ++i) {
-      float2 acc = make_float2(0.f, 0.f);
-      for (int b = 0; b < a.B; ++b) {
-        const float2 p = cjmul(sx[(b * a.ci + i) * a.mpb + mm], sg[(b * a.co + o) * a.mpb + mm]);
-        acc.x += p.x;
-        acc.y += p.y;
+    const int64_t lm0 = blk * a.mpb;
+    const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
+    const int64_t mbase = a.m0 + lm0;
+    const bool active = mm < nm;
+    float2* gm = gw + (lm0 + (active ? mm : 0)) * int64_t(a.ci) * a.co;
+    float2 acc[R][OPL];
+    if (a.acc) load_rows<OPL, R>(acc, gm, 0, a.ci, a.co, lr, LPR, active);
+    stage(sx, x, a.B, a.ci, a.M, mbase, nm, a.mpb);
+    stage(sg, gy, a.B, a.co, a.M, mbase, nm, a.mpb);
+    __syncthreads();
+    if (active) {
+      for (int i0 = 0; i0 < a.ci; i0 += R) {
+        if (a.acc) {
+          if (i0 > 0) load_rows<OPL, R>(acc, gm, i0, a.ci, a.co, lr, LPR, true);
+        } else {
+#pragma unroll
+          for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int s = 0; s < OPL; ++s) acc[r][s] = make_float2(0.f, 0.f);
+        }
+        for (int b0 = 0; b0 < a.B; b0 += BCH) {
+          float2 gv[BCH][OPL];
+#pragma unroll
+          for (int q = 0; q < BCH; ++q)
+#pragma unroll
+            for (int s = 0; s < OPL; ++s) {
+              const int o = lr + LPR * s;
+              gv[q][s] = (b0 + q < a.B && o < a.co) ? sg[((b0 + q) * a.mpb + mm) * (a.co + 1) + o]
+                                                    : make_float2(0.f, 0.f);
+            }
+#pragma unroll
+          for (int r = 0; r < R; ++r) {
+            if (i0 + r >= a.ci) continue;
+#pragma unroll
+            for (int q = 0; q < BCH; ++q) {
+              if (b0 + q >= a.B) continue;
+              const float2 xv = sx[((b0 + q) * a.mpb + mm) * (a.ci + 1) + i0 + r];
+#pragma unroll
+              for (int s = 0; s < OPL; ++s) {
+                const float2 p = cjmul(xv, gv[q][s]);
+                acc[r][s].x += p.x;
+                acc[r][s].y += p.y;
+              }
+            }
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const int i = i0 + r;
+          if (i >= a.ci) continue;
+#pragma unroll
+          for (int s = 0; s < OPL; ++s) {
+            const int o = lr + LPR * s;
+            if (o >= a.co) continue;
+            __builtin_nontemporal_store(v2f{acc[r][s].x, acc[r][s].y},
+                                        reinterpret_cast<v2f*>(gm + int64_t(i) * a.co + o));
+          }
+        }
       }
-      float2* dst = gp + int64_t(i) * a.co;
-      if (a.acc) {
-        const float2 old = *dst;
-        acc.x += old.x;
-        acc.y += old.y;
-      }
-      *dst = acc;
     }
-  }
-  __syncthreads();
+    __syncthreads();
   }
 }
 
-// Modes per block: enough (mode, channel) work items for 256 threads, capped
-// so the staged tiles fit in 64 KiB of LDS.
-int modes_per_block(int per_mode_items, size_t per_mode_lds) {
-  int mpb = 256 / (per_mode_items > 0 ? per_mode_items : 1);
-  if (mpb < 1) mpb = 1;
-  if (mpb > 64) mpb = 64;
-  while (mpb > 1 && size_t(mpb) * per_mode_lds > 64 * 1024) --mpb;
-  return mpb;
+int lanes_per_row(int64_t co) {
+  int l = 1;
+  while (l < co && l < 64) l <<= 1;
+  return l;
 }
 
-MixArgs make_args(int64_t B, int64_t ci, int64_t co, int64_t M, int64_t m0, int64_t m1, int mpb, int acc) {
+int opl_of(int64_t co) {
+  const int64_t o = (co + 63) / 64;
+  return o <= 1 ? 1 : (o <= 2 ? 2 : (o <= 4 ? 4 : 8));
+}
+
+MixArgs make_args(int64_t B, int64_t ci, int64_t co, int64_t M, int64_t m0, int64_t m1, int acc) {
   MixArgs a;
   a.M = M;
   a.m0 = m0;
@@ -206,73 +334,89 @@ MixArgs make_args(int64_t B, int64_t ci, int64_t co, int64_t M, int64_t m0, int6
   a.B = static_cast<int>(B);
   a.ci = static_cast<int>(ci);
   a.co = static_cast<int>(co);
-  a.mpb = mpb;
+  a.lpr = lanes_per_row(co);
+  a.mpb = 256 / a.lpr;
   a.acc = acc;
-  a.nblk = (a.count + mpb - 1) / mpb;
+  a.nblk = (a.count + a.mpb - 1) / a.mpb;
   return a;
+}
+
+typedef void (*mix_fn)(const float2*, const float2*, float2*, MixArgs);
+
+int launch(mix_fn f, size_t lds, const float2* p0, const float2* p1, float2* p2, const MixArgs& a, void* stream) {
+  if (lds > 65536) {
+    const hipError_t e =
+        hipFuncSetAttribute(reinterpret_cast<const void*>(f), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+  }
+  const int64_t blocks = a.nblk < (int64_t(1) << 22) ? a.nblk : (int64_t(1) << 22);
+  hipLaunchKernelGGL(f, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, static_cast<hipStream_t>(stream), p0,
+                     p1, p2, a);
+  return hipGetLastError();
 }
 
 }  // namespace
 
-// Largest LDS a mix launch may need; the host checks this before launching.
-size_t mix_lds_bytes(int op, int64_t B, int64_t ci, int64_t co) {
-  const size_t c8 = sizeof(float2);
-  if (op == 1) return c8 * (size_t(ci) * (co + 1) + size_t(B) * (ci + co));
-  return c8 * size_t(B) * (ci + co);
+// LDS bytes of one mix workgroup (the same for all three kernels).
+size_t mix_lds_bytes(int64_t B, int64_t ci, int64_t co) {
+  const size_t mpb = size_t(256 / lanes_per_row(co));
+  return sizeof(float2) * size_t(B) * mpb * size_t(ci + 1 + co + 1);
 }
+
+namespace {
+
+// Kernel instance for C_out: LPR lanes per row and OPL columns per lane.
+template <template <int, int> class K>
+mix_fn pick(int64_t co) {
+  switch (lanes_per_row(co)) {
+    case 1: return K<1, 1>::fn;
+    case 2: return K<2, 1>::fn;
+    case 4: return K<4, 1>::fn;
+    case 8: return K<8, 1>::fn;
+    case 16: return K<16, 1>::fn;
+    case 32: return K<32, 1>::fn;
+    default: break;
+  }
+  const int opl = opl_of(co);
+  return opl == 1 ? K<64, 1>::fn : opl == 2 ? K<64, 2>::fn : opl == 4 ? K<64, 4>::fn : K<64, 8>::fn;
+}
+template <int L, int O>
+struct MixK {
+  static constexpr mix_fn fn = mix_kernel<L, O>;
+};
+template <int L, int O>
+struct MixHK {
+  static constexpr mix_fn fn = mix_h_kernel<L, O>;
+};
+template <int L, int O>
+struct WgradK {
+  static constexpr mix_fn fn = wgrad_kernel<L, O>;
+};
+
+}  // namespace
 
 int launch_mix(const void* xhat, const void* w, void* yhat, int64_t B, int64_t ci, int64_t co, int64_t M,
                int64_t m0, int64_t m1, void* stream) {
   if (B <= 0 || m1 <= m0) return hipSuccess;
-  const size_t per_mode = mix_lds_bytes(0, B, ci, co);
-  const int mpb = modes_per_block(static_cast<int>(co), per_mode);
-  const MixArgs a = make_args(B, ci, co, M, m0, m1, mpb, 0);
-  const int64_t blocks = a.nblk < (int64_t(1) << 22) ? a.nblk : (int64_t(1) << 22);
-  if (per_mode * mpb > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(mix_kernel),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(per_mode * mpb));
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(mix_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), per_mode * mpb,
-                     static_cast<hipStream_t>(stream), static_cast<const float2*>(xhat),
-                     static_cast<const float2*>(w), static_cast<float2*>(yhat), a);
-  return hipGetLastError();
+  const MixArgs a = make_args(B, ci, co, M, m0, m1, 0);
+  return launch(pick<MixK>(co), mix_lds_bytes(B, ci, co), static_cast<const float2*>(xhat),
+                static_cast<const float2*>(w), static_cast<float2*>(yhat), a, stream);
 }
 
 int launch_mix_h(const void* gy, const void* w, void* gx, int64_t B, int64_t ci, int64_t co, int64_t M,
                  int64_t m0, int64_t m1, void* stream) {
   if (B <= 0 || m1 <= m0) return hipSuccess;
-  const size_t per_mode = mix_lds_bytes(1, B, ci, co);
-  const int mpb = modes_per_block(static_cast<int>(ci), per_mode);
-  const MixArgs a = make_args(B, ci, co, M, m0, m1, mpb, 0);
-  const int64_t blocks = a.nblk < (int64_t(1) << 22) ? a.nblk : (int64_t(1) << 22);
-  if (per_mode * mpb > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(mix_h_kernel),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(per_mode * mpb));
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(mix_h_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), per_mode * mpb,
-                     static_cast<hipStream_t>(stream), static_cast<const float2*>(gy),
-                     static_cast<const float2*>(w), static_cast<float2*>(gx), a);
-  return hipGetLastError();
+  const MixArgs a = make_args(B, ci, co, M, m0, m1, 0);
+  return launch(pick<MixHK>(co), mix_lds_bytes(B, ci, co), static_cast<const float2*>(gy),
+                static_cast<const float2*>(w), static_cast<float2*>(gx), a, stream);
 }
 
 int launch_wgrad(const void* xhat, const void* gy, void* gw, int64_t B, int64_t ci, int64_t co, int64_t M,
                  int64_t m0, int64_t m1, int accumulate, void* stream) {
   if (B <= 0 || m1 <= m0) return hipSuccess;
-  const size_t per_mode = mix_lds_bytes(0, B, ci, co);
-  const int mpb = modes_per_block(static_cast<int>(co), per_mode);
-  const MixArgs a = make_args(B, ci, co, M, m0, m1, mpb, accumulate ? 1 : 0);
-  const int64_t blocks = a.nblk < (int64_t(1) << 22) ? a.nblk : (int64_t(1) << 22);
-  if (per_mode * mpb > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(wgrad_kernel),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(per_mode * mpb));
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(wgrad_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), per_mode * mpb,
-                     static_cast<hipStream_t>(stream), static_cast<const float2*>(xhat),
-                     static_cast<const float2*>(gy), static_cast<float2*>(gw), a);
-  return hipGetLastError();
+  const MixArgs a = make_args(B, ci, co, M, m0, m1, accumulate ? 1 : 0);
+  return launch(pick<WgradK>(co), mix_lds_bytes(B, ci, co), static_cast<const float2*>(xhat),
+                static_cast<const float2*>(gy), static_cast<float2*>(gw), a, stream);
 }
 
 }  // namespace dtst

@@ -190,26 +190,42 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
     // the Re / Im columns of k_t sit 8 lanes apart (CT = 1) or in the two
     // column tiles (CT = 2).
     float2* orow = out + r * int64_t(a.kz) * a.kt;
-#pragma unroll
-    for (int cl = 0; cl < NCLS; ++cl)
+    if (CT == 1) {
+      // Lanes m < 8 finish mode p0 (k_t = m), lanes m >= 8 the next mode
+      // p0 + 1 (k_t = m - 8): z class 1 of the same slot when folded, else
+      // the next accumulator register.  Each lane pair trades the values the
+      // other half needs, and every store instruction writes whole 128-byte
+      // rows of two adjacent modes.
+      const bool hi = m >= KTP;
+      const int kc = hi ? m - KTP : m;
 #pragma unroll
       for (int mr = 0; mr < MT / 2; ++mr)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int s = 16 * mr + 4 * g + i;
-          const int p = s * NCLS + cl;
-          if (CT == 1) {
-            const float q = P[cl][mr][0][i];
-            const float u = P[cl][mr + MT / 2][0][i];
-            const float qs = ror8(q);
-            const float us = ror8(u);
-            if (m < KTP && m < a.kt && p < a.kz) orow[p * a.kt + m] = make_float2(q - us, qs + u);
-          } else {
+        for (int j = 0; j < (NCLS == 2 ? 4 : 2); ++j) {
+          const int i0 = NCLS == 2 ? j : 2 * j, i1 = NCLS == 2 ? j : 2 * j + 1;
+          const int c1 = NCLS - 1;
+          const float q0 = P[0][mr][0][i0], u0 = P[0][mr + MT / 2][0][i0];
+          const float q1 = P[c1][mr][0][i1], u1 = P[c1][mr + MT / 2][0][i1];
+          const float rq = ror8(hi ? q0 : q1);
+          const float ru = ror8(hi ? u0 : u1);
+          const float re = hi ? rq - u1 : q0 - ru;
+          const float im = hi ? q1 + ru : rq + u0;
+          const int p = (NCLS == 2 ? 2 * (16 * mr + 4 * g + i0) : 16 * mr + 4 * g + i0) + (hi ? 1 : 0);
+          if (kc < a.kt && p < a.kz) orow[p * a.kt + kc] = make_float2(re, im);
+        }
+    } else {
+#pragma unroll
+      for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+        for (int mr = 0; mr < MT / 2; ++mr)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int p = (16 * mr + 4 * g + i) * NCLS + cl;
             const float rr = P[cl][mr][0][i], ri = P[cl][mr][CT - 1][i];
             const float ir = P[cl][mr + MT / 2][0][i], ii = P[cl][mr + MT / 2][CT - 1][i];
             if (m < a.kt && p < a.kz) orow[p * a.kt + m] = make_float2(rr - ii, ri + ir);
           }
-        }
+    }
   }
 }
 

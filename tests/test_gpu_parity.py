@@ -147,6 +147,52 @@ def test_mix_ranges_and_wgrad(name):
     assert GW.guards_intact()
 
 
+# (B, C_in, C_out): row groups of 1..64 lanes, one to four columns per lane,
+# batch chunks beyond 4, w row chunks beyond 16, odd counts.
+MIX_SHAPES = [(2, 32, 32), (1, 16, 16), (3, 5, 64), (2, 7, 65), (1, 40, 130), (5, 2, 3), (1, 1, 1)]
+
+
+@pytest.mark.parametrize("shape", MIX_SHAPES, ids=lambda s: "B%d_ci%d_co%d" % s)
+def test_mix_channel_shapes(shape):
+    """mix, its data gradient and the weight gradient (with accumulate) on
+    channel and batch counts that exercise every lane layout of the mix
+    kernels, over the full mode set and a ragged middle range."""
+    B, ci, co = shape
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry((8, 8, 6, 8), (8, 8, 6, 8), (0, 0, 0, 0), (2, 3, 2), 3, B, ci, co)
+    say(f"[mix shape] B={B} Cin={ci} Cout={co}")
+    plan = D.Plan(desc_of(g))
+    M = plan.n_modes
+    X = rand_cplx((B, ci) + g.K, 120)
+    GY = rand_cplx((B, co) + g.K, 121)
+    W = rand_cplx((M, ci, co), 122, var=1.0 / (ci * co))
+    Xd, GYd, Wd = dev(torch, X), dev(torch, GY), dev(torch, W)
+    for m0, m1 in ((0, M), (M // 3 + 1, M - 5)):
+        Wr = Wd[m0:m1].clone()  # its own (aligned) allocation
+        sentinel = rand_cplx((B, co) + g.K, 123)
+        Y = Guarded(torch, plan.spectral_shape(co), torch.complex64, fill=dev(torch, sentinel))
+        plan.mix(Xd, Wr, Y.t, m0, m1, op=0)
+        gx_sent = rand_cplx((B, ci) + g.K, 124)
+        GX = Guarded(torch, plan.spectral_shape(ci), torch.complex64, fill=dev(torch, gx_sent))
+        plan.mix(GYd, Wr, GX.t, m0, m1, op=1)
+        GW = Guarded(torch, (m1 - m0, ci, co), torch.complex64)
+        plan.wgrad(Xd, GYd, GW.t, m0, m1)
+        torch.cuda.synchronize()
+        y_ref = O.mix(X, W[m0:m1], m0, m1, yhat_in=sentinel)
+        check(np_of(Y.t).reshape(B, co, M), y_ref, f"mix [{m0},{m1})")
+        gx_ref = O.mix_data_grad(GY, W[m0:m1], m0, m1, gx_in=gx_sent)
+        check(np_of(GX.t).reshape(B, ci, M), gx_ref, f"mix data grad [{m0},{m1})")
+        gw_ref = O.mix_wgrad(X, GY, m0, m1)
+        check(np_of(GW.t), gw_ref, f"wgrad [{m0},{m1})")
+        plan.wgrad(Xd, GYd, GW.t, m0, m1, accumulate=True)
+        torch.cuda.synchronize()
+        check(np_of(GW.t), 2 * gw_ref, f"wgrad accumulate [{m0},{m1})")
+        for t in (Y, GX, GW):
+            assert t.guards_intact()
+    plan.close()
+
+
 def test_slab_sum_equals_full_domain():
     """Eq. (dtst_reduce) on one GPU: per-slab forwards accumulated into one
     output equal the full-domain coefficients (and the oracle)."""
