@@ -12,13 +12,24 @@
 // at most 64) covers one row (m, i, 0..C_out) of w / g_w, lane l holding the
 // columns o = l + LPR s (s < OPL), so every row is read or written with
 // contiguous 8-byte accesses.  A 256-thread workgroup has 256 / LPR groups and
-// owns that many consecutive modes, one per group.  The spectra of those modes
-// (stride M between channels in HBM) are staged through LDS as
-// [b][mode][channel + 1], which turns their strided reads into coalesced ones
-// and gives each group its per-mode vectors.  The first rows of w are loaded
-// into registers before the staging barrier, so their HBM latency overlaps
-// the staging.
+// handles that many consecutive modes at a time ("mode block"), one per
+// group.  The spectra of a block (stride M between channels in HBM) are
+// staged through LDS as [b][channel][mode + 1], which turns their strided
+// reads into coalesced ones and gives each group its per-mode vectors.
+//
+// mix and mix_h (bound by the reads of w): one workgroup per mode block in
+// an XCD-aware order; the first rows of w are loaded into registers before
+// the staging barrier, so their HBM latency overlaps the staging.
+// wgrad (bound by the writes of g_w): a grid of resident workgroups, each
+// walking a contiguous run of mode blocks (its reads of the spectra advance
+// through the same DRAM rows), fetching the next block's spectra into
+// registers while the current block's rows are written, with the LDS area
+// double-buffered so that one barrier per block separates writers and
+// readers.
 #include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <vector>
 
 #include "dtst_internal.h"
 
@@ -44,27 +55,79 @@ struct Rows {
   static constexpr int value = OPL >= 8 ? 2 : 16 / OPL;
 };
 
-// spec[b][c][mbase + mm] (channel stride M) -> dst[(b * mpb + mm) * (C + 1) + c]
-__device__ __forceinline__ void stage(float2* dst, const float2* __restrict__ spec, int B, int C, int64_t M,
-                                      int64_t mbase, int nm, int mpb) {
-  const int n = B * C * nm;
-  for (int e = threadIdx.x; e < n; e += blockDim.x) {
-    const int mm = e % nm;
-    const int bc = e / nm;
-    const int b = bc / C, c = bc % C;
-    dst[(b * mpb + mm) * (C + 1) + c] = spec[int64_t(bc) * M + mbase + mm];
+// Spectra of a block's modes in LDS: entry (b, c, mm) at
+// [(b * C + c) * (MPB + 1) + mm].  They are read from spec[b][c][mbase + mm]
+// (channel stride M), MPB consecutive modes per (b, c) row; each thread
+// fetches its PRE entries into registers one block ahead and writes them to
+// LDS when that block starts (entries beyond 256 * PRE are copied directly).
+constexpr int PRE = 4;
+
+template <int MPB>
+__device__ __forceinline__ int sidx(int bc, int mm) {
+  return bc * (MPB + 1) + mm;
+}
+
+// Direct staging of a block's spectra (no register prefetch).
+template <int MPB>
+__device__ __forceinline__ void stage(float2* dst, const float2* __restrict__ spec, int BC, int64_t M,
+                                      int64_t mbase, int nm) {
+  for (int e = threadIdx.x; e < BC * MPB; e += 256) {
+    const int mm = e % MPB, bc = e / MPB;
+    if (mm < nm) dst[sidx<MPB>(bc, mm)] = spec[int64_t(bc) * M + mbase + mm];
   }
 }
 
-__device__ __forceinline__ void unstage(float2* __restrict__ spec, const float2* src, int B, int C, int64_t M,
-                                        int64_t mbase, int nm, int mpb) {
-  const int n = B * C * nm;
-  for (int e = threadIdx.x; e < n; e += blockDim.x) {
-    const int mm = e % nm;
-    const int bc = e / nm;
-    const int b = bc / C, c = bc % C;
-    spec[int64_t(bc) * M + mbase + mm] = src[(b * mpb + mm) * (C + 1) + c];
+template <int MPB>
+__device__ __forceinline__ void fetch(float2 (&pre)[PRE], const float2* __restrict__ spec, int BC, int64_t M,
+                                      int64_t mbase, int nm) {
+#pragma unroll
+  for (int j = 0; j < PRE; ++j) {
+    const int e = threadIdx.x + 256 * j;
+    const int mm = e % MPB, bc = e / MPB;
+    const bool ok = bc < BC && mm < nm;
+    pre[j] = spec[ok ? int64_t(bc) * M + mbase + mm : 0];
   }
+}
+
+template <int MPB>
+__device__ __forceinline__ void put(float2* dst, const float2 (&pre)[PRE], const float2* __restrict__ spec, int BC,
+                                    int64_t M, int64_t mbase, int nm) {
+#pragma unroll
+  for (int j = 0; j < PRE; ++j) {
+    const int e = threadIdx.x + 256 * j;
+    const int mm = e % MPB, bc = e / MPB;
+    if (bc < BC && mm < nm) dst[sidx<MPB>(bc, mm)] = pre[j];
+  }
+  for (int e = threadIdx.x + 256 * PRE; e < BC * MPB; e += 256) {
+    const int mm = e % MPB, bc = e / MPB;
+    if (mm < nm) dst[sidx<MPB>(bc, mm)] = spec[int64_t(bc) * M + mbase + mm];
+  }
+}
+
+template <int MPB>
+__device__ __forceinline__ void unstage(float2* __restrict__ spec, const float2* src, int BC, int64_t M,
+                                        int64_t mbase, int nm) {
+  for (int e = threadIdx.x; e < BC * MPB; e += 256) {
+    const int mm = e % MPB, bc = e / MPB;
+    if (mm < nm) spec[int64_t(bc) * M + mbase + mm] = src[sidx<MPB>(bc, mm)];
+  }
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs, each with its own
+// L2.  Give each XCD a contiguous run of mode blocks, so that neighbouring
+// blocks -- which read the two halves of the same 128-byte lines of the
+// spectra -- share an L2 and each line is fetched from HBM once.
+__device__ __forceinline__ int64_t first_block() {
+  const int64_t grid = gridDim.x, bid = blockIdx.x;
+  const int64_t per = grid / 8;
+  if (bid >= per * 8) return bid;
+  return (bid % 8) * per + bid / 8;
+}
+
+// The contiguous run of mode blocks [*k0, *k1) of this workgroup.
+__device__ __forceinline__ void span(int64_t nblk, int64_t* k0, int64_t* k1) {
+  *k0 = nblk * blockIdx.x / gridDim.x;
+  *k1 = nblk * (blockIdx.x + 1) / gridDim.x;
 }
 
 // Loads rows i0 .. i0 + R - 1 of the (ci x co) matrix at `base` into v;
@@ -112,23 +175,26 @@ __device__ __forceinline__ float2 cjmul(float2 a, float2 b) {
   return make_float2(a.x * b.x + a.y * b.y, a.x * b.y - a.y * b.x);
 }
 
+// mix and mix_h: one mode block per workgroup (the grid covers every
+// block), in the XCD-aware order above.
 template <int LPR, int OPL>
 __global__ void __launch_bounds__(256)
 mix_kernel(const float2* __restrict__ x, const float2* __restrict__ w, float2* __restrict__ y, MixArgs a) {
   constexpr int R = Rows<OPL>::value;
+  constexpr int MPB = 256 / LPR;
   extern __shared__ float2 sm[];
-  float2* sx = sm;                                // [B][mpb][ci + 1]
-  float2* sy = sm + a.B * a.mpb * (a.ci + 1);     // [B][mpb][co + 1]
+  float2* sx = sm;                                // B * ci rows
+  float2* sy = sm + a.B * a.ci * (MPB + 1);       // B * co rows
   const int lr = threadIdx.x % LPR, mm = threadIdx.x / LPR;
-  for (int64_t blk = blockIdx.x; blk < a.nblk; blk += gridDim.x) {
-    const int64_t lm0 = blk * a.mpb;  // local mode index in [0, count)
-    const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
+  for (int64_t k = first_block(); k < a.nblk; k += gridDim.x) {
+    const int64_t lm0 = k * MPB;  // local mode index in [0, count)
+    const int nm = static_cast<int>(min(int64_t(MPB), a.count - lm0));
     const int64_t mbase = a.m0 + lm0;
     const bool active = mm < nm;
     const float2* wm = w + (lm0 + (active ? mm : 0)) * int64_t(a.ci) * a.co;
     float2 wv[R][OPL];
     load_rows<OPL, R>(wv, wm, 0, a.ci, a.co, lr, LPR, active);
-    stage(sx, x, a.B, a.ci, a.M, mbase, nm, a.mpb);
+    stage<MPB>(sx, x, a.B * a.ci, a.M, mbase, nm);
     __syncthreads();
     for (int i0 = 0; i0 < a.ci; i0 += R) {
       if (i0 > 0) load_rows<OPL, R>(wv, wm, i0, a.ci, a.co, lr, LPR, active);
@@ -144,7 +210,7 @@ mix_kernel(const float2* __restrict__ x, const float2* __restrict__ w, float2* _
 #pragma unroll
           for (int q = 0; q < BCH; ++q) {
             if (b0 + q >= a.B) continue;
-            const float2 xv = sx[((b0 + q) * a.mpb + mm) * (a.ci + 1) + i0 + r];
+            const float2 xv = sx[sidx<MPB>((b0 + q) * a.ci + i0 + r, mm)];
 #pragma unroll
             for (int s = 0; s < OPL; ++s) {
               const float2 p = cmul(xv, wv[r][s]);
@@ -161,7 +227,7 @@ mix_kernel(const float2* __restrict__ x, const float2* __restrict__ w, float2* _
             for (int s = 0; s < OPL; ++s) {
               const int o = lr + LPR * s;
               if (o >= a.co) continue;
-              float2* d = sy + ((b0 + q) * a.mpb + mm) * (a.co + 1) + o;
+              float2* d = sy + sidx<MPB>((b0 + q) * a.co + o, mm);
               if (i0 > 0) {
                 acc[q][s].x += d->x;
                 acc[q][s].y += d->y;
@@ -173,7 +239,7 @@ mix_kernel(const float2* __restrict__ x, const float2* __restrict__ w, float2* _
       }
     }
     __syncthreads();
-    unstage(y, sy, a.B, a.co, a.M, mbase, nm, a.mpb);
+    unstage<MPB>(y, sy, a.B * a.co, a.M, mbase, nm);
     __syncthreads();
   }
 }
@@ -184,19 +250,20 @@ template <int LPR, int OPL>
 __global__ void __launch_bounds__(256)
 mix_h_kernel(const float2* __restrict__ gy, const float2* __restrict__ w, float2* __restrict__ gx, MixArgs a) {
   constexpr int R = Rows<OPL>::value;
+  constexpr int MPB = 256 / LPR;
   extern __shared__ float2 sm[];
-  float2* sg = sm;                                // [B][mpb][co + 1]
-  float2* sx = sm + a.B * a.mpb * (a.co + 1);     // [B][mpb][ci + 1]
+  float2* sg = sm;                                // B * co rows
+  float2* sx = sm + a.B * a.co * (MPB + 1);       // B * ci rows
   const int lr = threadIdx.x % LPR, mm = threadIdx.x / LPR;
-  for (int64_t blk = blockIdx.x; blk < a.nblk; blk += gridDim.x) {
-    const int64_t lm0 = blk * a.mpb;
-    const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
+  for (int64_t k = first_block(); k < a.nblk; k += gridDim.x) {
+    const int64_t lm0 = k * MPB;
+    const int nm = static_cast<int>(min(int64_t(MPB), a.count - lm0));
     const int64_t mbase = a.m0 + lm0;
     const bool active = mm < nm;
     const float2* wm = w + (lm0 + (active ? mm : 0)) * int64_t(a.ci) * a.co;
     float2 wv[R][OPL];
     load_rows<OPL, R>(wv, wm, 0, a.ci, a.co, lr, LPR, active);
-    stage(sg, gy, a.B, a.co, a.M, mbase, nm, a.mpb);
+    stage<MPB>(sg, gy, a.B * a.co, a.M, mbase, nm);
     __syncthreads();
     for (int i0 = 0; i0 < a.ci; i0 += R) {
       if (i0 > 0) load_rows<OPL, R>(wv, wm, i0, a.ci, a.co, lr, LPR, active);
@@ -208,7 +275,7 @@ mix_h_kernel(const float2* __restrict__ gy, const float2* __restrict__ w, float2
 #pragma unroll
           for (int s = 0; s < OPL; ++s) {
             const int o = lr + LPR * s;
-            gv[q][s] = (b0 + q < a.B && o < a.co && active) ? sg[((b0 + q) * a.mpb + mm) * (a.co + 1) + o]
+            gv[q][s] = (b0 + q < a.B && o < a.co && active) ? sg[sidx<MPB>((b0 + q) * a.co + o, mm)]
                                                              : make_float2(0.f, 0.f);
           }
 #pragma unroll
@@ -226,92 +293,108 @@ mix_h_kernel(const float2* __restrict__ gy, const float2* __restrict__ w, float2
             }
             t.x = group_sum<LPR>(t.x);
             t.y = group_sum<LPR>(t.y);
-            if (lr == LPR - 1 && active) sx[((b0 + q) * a.mpb + mm) * (a.ci + 1) + i0 + r] = t;
+            if (lr == LPR - 1 && active) sx[sidx<MPB>((b0 + q) * a.ci + i0 + r, mm)] = t;
           }
         }
       }
     }
     __syncthreads();
-    unstage(gx, sx, a.B, a.ci, a.M, mbase, nm, a.mpb);
+    unstage<MPB>(gx, sx, a.B * a.ci, a.M, mbase, nm);
     __syncthreads();
   }
 }
 
-// Weight gradient: each lane forms its columns of a chunk of rows (m, i) in
-// registers -- its g_y values of the batch chunk held in registers, x
-// broadcast from LDS -- and streams the rows out with non-temporal stores
-// (g_w is written once and not read back here, except for the accumulate
-// read-modify-write).
+// Weight gradient: a grid of resident workgroups, each walking its run of
+// mode blocks.  Per block its spectra go from registers to one half of a
+// double-buffered LDS area, the next block's are fetched, one barrier; then
+// each lane forms its columns of a chunk of rows (m, i) in registers -- its
+// g_y values of the batch chunk held in registers, x broadcast from LDS --
+// and streams the rows out with non-temporal stores (g_w is written once and
+// not read back here, except for the accumulate read-modify-write).  With
+// almost no reads to overlap, this keeps the stores flowing while the next
+// block's spectra arrive.
 template <int LPR, int OPL>
 __global__ void __launch_bounds__(256)
 wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2* __restrict__ gw, MixArgs a) {
   constexpr int R = Rows<OPL>::value;
+  constexpr int MPB = 256 / LPR;
   extern __shared__ float2 sm[];
-  float2* sx = sm;                                // [B][mpb][ci + 1]
-  float2* sg = sm + a.B * a.mpb * (a.ci + 1);     // [B][mpb][co + 1]
+  const int nx = a.B * a.ci * (MPB + 1), ng = a.B * a.co * (MPB + 1);
   const int lr = threadIdx.x % LPR, mm = threadIdx.x / LPR;
-  for (int64_t blk = blockIdx.x; blk < a.nblk; blk += gridDim.x) {
-    const int64_t lm0 = blk * a.mpb;
-    const int nm = static_cast<int>(min(int64_t(a.mpb), a.count - lm0));
+  int64_t k0, k1;
+  span(a.nblk, &k0, &k1);
+  float2 prex[PRE], preg[PRE];
+  if (k0 < k1) {
+    const int nm0 = int(min(int64_t(MPB), a.count - k0 * MPB));
+    fetch<MPB>(prex, x, a.B * a.ci, a.M, a.m0 + k0 * MPB, nm0);
+    fetch<MPB>(preg, gy, a.B * a.co, a.M, a.m0 + k0 * MPB, nm0);
+  }
+  for (int64_t k = k0; k < k1; ++k) {
+    float2* sx = sm + ((k - k0) & 1) * (nx + ng);  // B * ci rows
+    float2* sg = sx + nx;                          // B * co rows
+    const int64_t lm0 = k * MPB;
+    const int nm = static_cast<int>(min(int64_t(MPB), a.count - lm0));
     const int64_t mbase = a.m0 + lm0;
     const bool active = mm < nm;
     float2* gm = gw + (lm0 + (active ? mm : 0)) * int64_t(a.ci) * a.co;
     float2 acc[R][OPL];
     if (a.acc) load_rows<OPL, R>(acc, gm, 0, a.ci, a.co, lr, LPR, active);
-    stage(sx, x, a.B, a.ci, a.M, mbase, nm, a.mpb);
-    stage(sg, gy, a.B, a.co, a.M, mbase, nm, a.mpb);
+    put<MPB>(sx, prex, x, a.B * a.ci, a.M, mbase, nm);
+    put<MPB>(sg, preg, gy, a.B * a.co, a.M, mbase, nm);
+    if (k + 1 < k1) {
+      const int nm1 = int(min(int64_t(MPB), a.count - lm0 - MPB));
+      fetch<MPB>(prex, x, a.B * a.ci, a.M, mbase + MPB, nm1);
+      fetch<MPB>(preg, gy, a.B * a.co, a.M, mbase + MPB, nm1);
+    }
     __syncthreads();
-    if (active) {
-      for (int i0 = 0; i0 < a.ci; i0 += R) {
-        if (a.acc) {
-          if (i0 > 0) load_rows<OPL, R>(acc, gm, i0, a.ci, a.co, lr, LPR, true);
-        } else {
+    if (!active) continue;
+    for (int i0 = 0; i0 < a.ci; i0 += R) {
+      if (a.acc) {
+        if (i0 > 0) load_rows<OPL, R>(acc, gm, i0, a.ci, a.co, lr, LPR, true);
+      } else {
 #pragma unroll
-          for (int r = 0; r < R; ++r)
+        for (int r = 0; r < R; ++r)
 #pragma unroll
-            for (int s = 0; s < OPL; ++s) acc[r][s] = make_float2(0.f, 0.f);
-        }
-        for (int b0 = 0; b0 < a.B; b0 += BCH) {
-          float2 gv[BCH][OPL];
+          for (int s = 0; s < OPL; ++s) acc[r][s] = make_float2(0.f, 0.f);
+      }
+      for (int b0 = 0; b0 < a.B; b0 += BCH) {
+        float2 gv[BCH][OPL];
 #pragma unroll
-          for (int q = 0; q < BCH; ++q)
-#pragma unroll
-            for (int s = 0; s < OPL; ++s) {
-              const int o = lr + LPR * s;
-              gv[q][s] = (b0 + q < a.B && o < a.co) ? sg[((b0 + q) * a.mpb + mm) * (a.co + 1) + o]
-                                                    : make_float2(0.f, 0.f);
-            }
-#pragma unroll
-          for (int r = 0; r < R; ++r) {
-            if (i0 + r >= a.ci) continue;
-#pragma unroll
-            for (int q = 0; q < BCH; ++q) {
-              if (b0 + q >= a.B) continue;
-              const float2 xv = sx[((b0 + q) * a.mpb + mm) * (a.ci + 1) + i0 + r];
-#pragma unroll
-              for (int s = 0; s < OPL; ++s) {
-                const float2 p = cjmul(xv, gv[q][s]);
-                acc[r][s].x += p.x;
-                acc[r][s].y += p.y;
-              }
-            }
-          }
-        }
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-          const int i = i0 + r;
-          if (i >= a.ci) continue;
+        for (int q = 0; q < BCH; ++q)
 #pragma unroll
           for (int s = 0; s < OPL; ++s) {
             const int o = lr + LPR * s;
-            if (o >= a.co) continue;
-            __builtin_nontemporal_store(v2f{acc[r][s].x, acc[r][s].y},
-                                        reinterpret_cast<v2f*>(gm + int64_t(i) * a.co + o));
+            gv[q][s] = (b0 + q < a.B && o < a.co) ? sg[sidx<MPB>((b0 + q) * a.co + o, mm)] : make_float2(0.f, 0.f);
+          }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if (i0 + r >= a.ci) continue;
+#pragma unroll
+          for (int q = 0; q < BCH; ++q) {
+            if (b0 + q >= a.B) continue;
+            const float2 xv = sx[sidx<MPB>((b0 + q) * a.ci + i0 + r, mm)];
+#pragma unroll
+            for (int s = 0; s < OPL; ++s) {
+              const float2 p = cjmul(xv, gv[q][s]);
+              acc[r][s].x += p.x;
+              acc[r][s].y += p.y;
+            }
           }
         }
       }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int i = i0 + r;
+        if (i >= a.ci) continue;
+#pragma unroll
+        for (int s = 0; s < OPL; ++s) {
+          const int o = lr + LPR * s;
+          if (o >= a.co) continue;
+          __builtin_nontemporal_store(v2f{acc[r][s].x, acc[r][s].y},
+                                      reinterpret_cast<v2f*>(gm + int64_t(i) * a.co + o));
+        }
+      }
     }
-    __syncthreads();
   }
 }
 
@@ -343,13 +426,54 @@ MixArgs make_args(int64_t B, int64_t ci, int64_t co, int64_t M, int64_t m0, int6
 
 typedef void (*mix_fn)(const float2*, const float2*, float2*, MixArgs);
 
-int launch(mix_fn f, size_t lds, const float2* p0, const float2* p1, float2* p2, const MixArgs& a, void* stream) {
+// Workgroups of kernel f with `lds` bytes of LDS the current device holds at
+// once (cached per kernel, LDS size and device).
+int64_t resident_workgroups(mix_fn f, size_t lds) {
+  struct Entry {
+    mix_fn f;
+    size_t lds;
+    int dev;
+    int64_t n;
+  };
+  static std::mutex mu;
+  static std::vector<Entry> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    for (const Entry& e : cache)
+      if (e.f == f && e.lds == lds && e.dev == dev) return e.n;
+  }
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, f, 256, lds) != hipSuccess) return 0;
+  const int64_t n = int64_t(cus) * (per_cu > 0 ? per_cu : 1);
+  std::lock_guard<std::mutex> lock(mu);
+  cache.push_back(Entry{f, lds, dev, n});
+  return n;
+}
+
+// LDS of one mode block's spectra.
+size_t block_lds(int64_t B, int64_t ci, int64_t co) {
+  const size_t mpb = size_t(256 / lanes_per_row(co));
+  return sizeof(float2) * size_t(B) * size_t(ci + co) * (mpb + 1);
+}
+
+// persistent: a grid of resident workgroups walking runs of blocks (wgrad);
+// else one workgroup per block (capped at 2^22, the kernels loop beyond).
+int launch(mix_fn f, size_t lds, bool persistent, const float2* p0, const float2* p1, float2* p2, const MixArgs& a,
+           void* stream) {
   if (lds > 65536) {
     const hipError_t e =
         hipFuncSetAttribute(reinterpret_cast<const void*>(f), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
   }
-  const int64_t blocks = a.nblk < (int64_t(1) << 22) ? a.nblk : (int64_t(1) << 22);
+  int64_t cap = int64_t(1) << 22;
+  if (persistent) {
+    cap = resident_workgroups(f, lds);
+    if (cap <= 0) return hipErrorInvalidConfiguration;
+  }
+  const int64_t blocks = a.nblk < cap ? a.nblk : cap;
   hipLaunchKernelGGL(f, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, static_cast<hipStream_t>(stream), p0,
                      p1, p2, a);
   return hipGetLastError();
@@ -357,11 +481,9 @@ int launch(mix_fn f, size_t lds, const float2* p0, const float2* p1, float2* p2,
 
 }  // namespace
 
-// LDS bytes of one mix workgroup (the same for all three kernels).
-size_t mix_lds_bytes(int64_t B, int64_t ci, int64_t co) {
-  const size_t mpb = size_t(256 / lanes_per_row(co));
-  return sizeof(float2) * size_t(B) * mpb * size_t(ci + 1 + co + 1);
-}
+// Largest LDS of a mix workgroup: wgrad's double-buffered spectra of one
+// mode block (mix and mix_h use half of it).
+size_t mix_lds_bytes(int64_t B, int64_t ci, int64_t co) { return 2 * block_lds(B, ci, co); }
 
 namespace {
 
@@ -399,7 +521,7 @@ int launch_mix(const void* xhat, const void* w, void* yhat, int64_t B, int64_t c
                int64_t m0, int64_t m1, void* stream) {
   if (B <= 0 || m1 <= m0) return hipSuccess;
   const MixArgs a = make_args(B, ci, co, M, m0, m1, 0);
-  return launch(pick<MixK>(co), mix_lds_bytes(B, ci, co), static_cast<const float2*>(xhat),
+  return launch(pick<MixK>(co), block_lds(B, ci, co), false, static_cast<const float2*>(xhat),
                 static_cast<const float2*>(w), static_cast<float2*>(yhat), a, stream);
 }
 
@@ -407,7 +529,7 @@ int launch_mix_h(const void* gy, const void* w, void* gx, int64_t B, int64_t ci,
                  int64_t m0, int64_t m1, void* stream) {
   if (B <= 0 || m1 <= m0) return hipSuccess;
   const MixArgs a = make_args(B, ci, co, M, m0, m1, 0);
-  return launch(pick<MixHK>(co), mix_lds_bytes(B, ci, co), static_cast<const float2*>(gy),
+  return launch(pick<MixHK>(co), block_lds(B, ci, co), false, static_cast<const float2*>(gy),
                 static_cast<const float2*>(w), static_cast<float2*>(gx), a, stream);
 }
 
@@ -415,7 +537,7 @@ int launch_wgrad(const void* xhat, const void* gy, void* gw, int64_t B, int64_t 
                  int64_t m0, int64_t m1, int accumulate, void* stream) {
   if (B <= 0 || m1 <= m0) return hipSuccess;
   const MixArgs a = make_args(B, ci, co, M, m0, m1, accumulate ? 1 : 0);
-  return launch(pick<WgradK>(co), mix_lds_bytes(B, ci, co), static_cast<const float2*>(xhat),
+  return launch(pick<WgradK>(co), mix_lds_bytes(B, ci, co), true, static_cast<const float2*>(xhat),
                 static_cast<const float2*>(gy), static_cast<float2*>(gw), a, stream);
 }
 
