@@ -40,6 +40,8 @@ def desc(**kw):
 def test_valid_descriptor():
     D.dtst_desc_validate(desc())
     D.dtst_desc_validate(desc(batch=0))
+    D.dtst_desc_validate(desc(c_out=512))
+    D.dtst_desc_validate(desc(n_global=(12, 10, 128, 64), n_local=(4, 10, 128, 64), kmax=(3, 2, 64), kt=16))
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -56,6 +58,8 @@ def test_valid_descriptor():
     (dict(c_out=0), 1),
     (dict(n_global=(12, 10, 8, 80), n_local=(4, 10, 8, 80), kt=20), 2),   # kt > 16: not covered
     (dict(n_global=(12, 10, 8, 80), n_local=(4, 10, 8, 80), kt=4), 2),    # N_t local > 64
+    (dict(c_out=513), 2),                                                   # mix kernels take C_out <= 512
+    (dict(n_global=(12, 10, 260, 8), n_local=(4, 10, 260, 8), kmax=(3, 2, 65)), 2),  # > 64 z modes per class
 ])
 def test_invalid_descriptors(kw, status):
     with pytest.raises(D.DtstError) as e:

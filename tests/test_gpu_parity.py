@@ -33,6 +33,8 @@ CASES = {
     "nt64_kt12": ((8, 12, 20, 64), (8, 12, 20, 64), (0, 0, 0, 0), (2, 3, 5), 12, 1, 2, 1),
     "nt21_pdebench_like": ((16, 16, 16, 21), (16, 16, 16, 21), (0, 0, 0, 0), (4, 4, 4), 8, 1, 2, 2),
     "cfg1_full": ((32, 32, 32, 8), (32, 32, 32, 8), (0, 0, 0, 0), (8, 8, 8), 4, 1, 8, 8),
+    # largest tiles the stream kernels take: 64 folded z modes per class, k_t = 16, N_t = 64
+    "max_tiles": ((4, 4, 128, 64), (4, 4, 128, 64), (0, 0, 0, 0), (2, 2, 64), 16, 1, 2, 2),
 }
 
 
@@ -147,9 +149,11 @@ def test_mix_ranges_and_wgrad(name):
     assert GW.guards_intact()
 
 
-# (B, C_in, C_out): row groups of 1..64 lanes, one to four columns per lane,
-# batch chunks beyond 4, w row chunks beyond 16, odd counts.
-MIX_SHAPES = [(2, 32, 32), (1, 16, 16), (3, 5, 64), (2, 7, 65), (1, 40, 130), (5, 2, 3), (1, 1, 1)]
+# (B, C_in, C_out): row groups of 1..64 lanes, one to eight columns per lane
+# (C_out = 512 is the largest the mix kernels take), batch chunks beyond the
+# register chunk, w row chunks beyond 16, odd counts.
+MIX_SHAPES = [(2, 32, 32), (1, 16, 16), (3, 5, 64), (2, 7, 65), (1, 40, 130), (5, 2, 3), (1, 1, 1),
+              (1, 3, 512)]
 
 
 @pytest.mark.parametrize("shape", MIX_SHAPES, ids=lambda s: "B%d_ci%d_co%d" % s)
