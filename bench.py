@@ -76,7 +76,7 @@ def work(g, channels, m_count=None):
     w["stream_fwd_tz"] = dict(
         bytes=rows * (Nz * Nt * 4 + Kz * Kt * 8),
         flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz,
-        mfma_flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz * (0.5 if _folded(g, 2) else 1.0))
+        mfma_flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz / _z_classes(g))
     fy = 0.5 if _folded(g, 1) else 1.0
     fx = 0.5 if _folded(g, 0) else 1.0
     w["axis_fwd_y"] = dict(bytes=B * C * Nx * (Ny + Ky) * Kz * Kt * 8, flops=B * C * Nx * Kz * Kt * 8 * Ky * Ny)
@@ -100,6 +100,18 @@ def work(g, channels, m_count=None):
 def _folded(g, dim):
     """The library folds a dimension whose whole even extent is local."""
     return g["n_local"][dim] == g["n_global"][dim] and g["n_global"][dim] % 2 == 0
+
+
+def _z_classes(g):
+    """z mode classes of the streaming kernels: 4 when z also splits by
+    k mod 4 (N_z % 4 == 0, even k_max, k_t > 8, at most 16 modes per class),
+    2 when it only folds in halves, else 1; the z MFMA work divides by it."""
+    if not _folded(g, 2):
+        return 1
+    Kz = 2 * g["kmax"][2]
+    if g["n_global"][2] % 4 == 0 and g["kmax"][2] % 2 == 0 and g["kt"] > 8 and Kz <= 64:
+        return 4
+    return 2
 
 
 def _sha(path):

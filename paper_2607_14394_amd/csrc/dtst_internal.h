@@ -24,11 +24,15 @@ namespace dtst {
 //   NCLS 1, or 2 when z is folded: with N_z^loc = N_z even,
 //        B[k, z + N/2] = (-1)^k B[k, z], so even k see x[z] + x[z+N/2] and
 //        odd k see x[z] - x[z+N/2]; class c holds the modes p = 2s + c.
+//        4 when in addition N_z % 4 == 0, k_max(z) is even, CT = 2 and
+//        K_z <= 64 (MT = 2):
+//        B[k, z + N/4] = (-i)^k B[k, z], classes by k mod 4 (p = 4s + c),
+//        each contracting the z < N/4 combination sum_j (-i)^(cj) x[z + jN/4].
 // ---------------------------------------------------------------------------
 struct StreamCfg {
   int ct = 1, th = 1, mt = 2, ncls = 1;
   int nt = 0, nz = 0, kt = 0, kz = 0;
-  int zh = 0;   // z extent per class pass (N_z/2 folded, N_z otherwise)
+  int zh = 0;   // z extent per class pass (N_z / ncls)
   int zt = 0;   // ceil(zh / 16)
   int kcp = 0;  // padded slots per class = 8*mt
   int vec = 0;  // 1 when N_t % 4 == 0 (16-byte row chunks)

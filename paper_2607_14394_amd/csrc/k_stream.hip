@@ -49,6 +49,91 @@ __device__ __forceinline__ float ror8(float v) {
 }
 
 // ---------------------------------------------------------------------------
+// z folding.  With z undistributed and N = N_z divisible by NCLS,
+// B[k, z + jN/NCLS] = w^(kj) B[k, z] with w = -1 (NCLS = 2) or -i (NCLS = 4),
+// so the modes split into NCLS classes by k mod NCLS and each class only
+// needs the z < N/NCLS positions of the combination
+//   S_c(z) = sum_j w^(cj) V_j(z),   V_j(z) = V(z + jN/NCLS).
+// The inverse forms the class sums E_c(z) and writes
+//   y(z + jN/NCLS) = sum_c conj(w)^(cj) E_c(z).
+// V and E hold complex values as two column tiles (tile 0 Re, tile 1 Im) when
+// CT = 2, which makes the factors +-i lane-local; NCLS = 4 is only used then.
+// ---------------------------------------------------------------------------
+template <int CT>
+__device__ __forceinline__ void times_i(const v4f (&a)[CT], v4f (&out)[CT]) {
+  // i (re + i im) = -im + i re
+  out[0] = -a[CT - 1];
+  out[CT - 1] = a[0];
+}
+
+template <int NCLS, int CT>
+__device__ __forceinline__ void fold_classes(v4f (&V)[NCLS][CT]) {
+  if constexpr (NCLS == 2) {
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      const v4f s = V[0][ct] + V[1][ct];
+      const v4f d = V[0][ct] - V[1][ct];
+      V[0][ct] = s;
+      V[1][ct] = d;
+    }
+  } else if constexpr (NCLS == 4) {
+    static_assert(CT == 2, "the four-class z fold needs Re and Im in separate column tiles");
+    // S0 = (V0 + V2) + (V1 + V3)      S2 = (V0 + V2) - (V1 + V3)
+    // S1 = (V0 - V2) - i (V1 - V3)    S3 = (V0 - V2) + i (V1 - V3)
+    v4f a[CT], b[CT], c[CT], d[CT], id[CT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      a[ct] = V[0][ct] + V[2][ct];
+      b[ct] = V[1][ct] + V[3][ct];
+      c[ct] = V[0][ct] - V[2][ct];
+      d[ct] = V[1][ct] - V[3][ct];
+    }
+    times_i<CT>(d, id);
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      V[0][ct] = a[ct] + b[ct];
+      V[2][ct] = a[ct] - b[ct];
+      V[1][ct] = c[ct] - id[ct];
+      V[3][ct] = c[ct] + id[ct];
+    }
+  }
+}
+
+template <int NCLS, int CT>
+__device__ __forceinline__ void unfold_classes(v4f (&E)[NCLS][CT]) {
+  if constexpr (NCLS == 2) {
+    // even modes + odd modes at z, even - odd at z + N_z/2
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      const v4f s = E[0][ct] + E[1][ct];
+      const v4f d = E[0][ct] - E[1][ct];
+      E[0][ct] = s;
+      E[1][ct] = d;
+    }
+  } else if constexpr (NCLS == 4) {
+    static_assert(CT == 2, "the four-class z fold needs Re and Im in separate column tiles");
+    // y0 = (E0 + E2) + (E1 + E3)      y2 = (E0 + E2) - (E1 + E3)
+    // y1 = (E0 - E2) + i (E1 - E3)    y3 = (E0 - E2) - i (E1 - E3)
+    v4f a[CT], b[CT], c[CT], d[CT], id[CT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      a[ct] = E[0][ct] + E[2][ct];
+      b[ct] = E[1][ct] + E[3][ct];
+      c[ct] = E[0][ct] - E[2][ct];
+      d[ct] = E[1][ct] - E[3][ct];
+    }
+    times_i<CT>(d, id);
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      E[0][ct] = a[ct] + b[ct];
+      E[2][ct] = a[ct] - b[ct];
+      E[1][ct] = c[ct] + id[ct];
+      E[3][ct] = c[ct] - id[ct];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Forward: x (rows x N_z x N_t) fp32 -> out (rows x K_z x K_t) complex.
 //
 // Every wave walks its (row, z-tile) pairs in order and keeps the next
@@ -163,15 +248,7 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct) V[hf][ct] = mfma(xa, bt[h * 4 + j][ct], V[hf][ct]);
         }
-    if (NCLS == 2) {
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct) {
-        const v4f s = V[0][ct] + V[NCLS - 1][ct];
-        const v4f d = V[0][ct] - V[NCLS - 1][ct];
-        V[0][ct] = s;
-        V[NCLS - 1][ct] = d;
-      }
-    }
+    fold_classes<NCLS, CT>(V);
     // Contract z: accumulator register i of V is the B operand of the
     // step whose K index is z = 16zt + 4g + i.
 #pragma unroll
@@ -190,7 +267,8 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
     // the Re / Im columns of k_t sit 8 lanes apart (CT = 1) or in the two
     // column tiles (CT = 2).
     float2* orow = out + r * int64_t(a.kz) * a.kt;
-    if (CT == 1) {
+    if constexpr (CT == 1) {
+      static_assert(NCLS <= 2, "the four-class z fold needs CT = 2");
       // Lanes m < 8 finish mode p0 (k_t = m), lanes m >= 8 the next mode
       // p0 + 1 (k_t = m - 8): z class 1 of the same slot when folded, else
       // the next accumulator register.  Each lane pair trades the values the
@@ -234,7 +312,7 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
 #define DTST_STREAM_WAVES(CT, MT, NCLS, TH) \
   __attribute__((amdgpu_waves_per_eu(((CT) * (MT) * (NCLS) <= 4 && (TH) <= 2) ? 4 : 1)))
 
-template <int CT, int TH, int MT, int NCLS>
+template <int CT, int TH, int MT, int NCLS, int MODE>
 __global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH)
 fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
               const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
@@ -255,9 +333,7 @@ fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
   const int64_t wstride = int64_t(gridDim.x) * wpb;
   const int64_t wave = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6);
   if (wave >= a.rows) return;
-  if (a.full) fwd_tz_body<CT, TH, MT, NCLS, 2>(x, out, bt, lds, a, wave, wstride);
-  else if (a.vec) fwd_tz_body<CT, TH, MT, NCLS, 1>(x, out, bt, lds, a, wave, wstride);
-  else fwd_tz_body<CT, TH, MT, NCLS, 0>(x, out, bt, lds, a, wave, wstride);
+  fwd_tz_body<CT, TH, MT, NCLS, MODE>(x, out, bt, lds, a, wave, wstride);
 }
 
 // ---------------------------------------------------------------------------
@@ -344,16 +420,7 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
           for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct) W[cl][ct] = mfma(A[cl][ct][q][i], B[cl][q][i], W[cl][ct]);
-      if (NCLS == 2) {
-        // even modes + odd modes at z, even - odd at z + N_z/2
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          const v4f s = W[0][ct] + W[NCLS - 1][ct];
-          const v4f d = W[0][ct] - W[NCLS - 1][ct];
-          W[0][ct] = s;
-          W[NCLS - 1][ct] = d;
-        }
-      }
+      unfold_classes<NCLS, CT>(W);
       v4f Y[NCLS][TH];
 #pragma unroll
       for (int hf = 0; hf < NCLS; ++hf)
@@ -412,7 +479,7 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
   }
 }
 
-template <int CT, int TH, int MT, int NCLS>
+template <int CT, int TH, int MT, int NCLS, int MODE>
 __global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH)
 inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
               const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
@@ -435,42 +502,63 @@ inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
   const int64_t wstride = int64_t(gridDim.x) * wpb;
   const int64_t wave = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6);
   if (wave >= a.rows) return;
-  if (a.full) inv_zt_body<CT, TH, MT, NCLS, 2>(in, y, ta, lds, a, wave, wstride);
-  else if (a.vec) inv_zt_body<CT, TH, MT, NCLS, 1>(in, y, ta, lds, a, wave, wstride);
-  else inv_zt_body<CT, TH, MT, NCLS, 0>(in, y, ta, lds, a, wave, wstride);
+  inv_zt_body<CT, TH, MT, NCLS, MODE>(in, y, ta, lds, a, wave, wstride);
 }
 
 typedef void (*fwd_fn)(const float*, float2*, const float*, const float4*, StreamArgs);
 typedef void (*inv_fn)(const float2*, float*, const float*, const float4*, StreamArgs);
 
-template <int CT, int TH, int MT>
-void pick2(int ncls, fwd_fn* f, inv_fn* v) {
-  if (ncls == 2) {
-    *f = fwd_tz_kernel<CT, TH, MT, 2>;
-    *v = inv_zt_kernel<CT, TH, MT, 2>;
+// Load / store form of a configuration: 0 scalar (N_t % 4 != 0), 1 16-byte
+// with masks, 2 complete tiles (z tiles and t groups all full).  Each form is
+// its own kernel instance, so the registers of one do not limit the others.
+int mode_of(const StreamCfg& c) {
+  if (!c.vec) return 0;
+  return (c.zh % 16 == 0 && c.nt == 16 * c.th) ? 2 : 1;
+}
+
+template <int CT, int TH, int MT, int NCLS>
+void pick3(int mode, fwd_fn* f, inv_fn* v) {
+  if (mode == 2) {
+    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 2>;
+    *v = inv_zt_kernel<CT, TH, MT, NCLS, 2>;
+  } else if (mode == 1) {
+    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 1>;
+    *v = inv_zt_kernel<CT, TH, MT, NCLS, 1>;
   } else {
-    *f = fwd_tz_kernel<CT, TH, MT, 1>;
-    *v = inv_zt_kernel<CT, TH, MT, 1>;
+    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 0>;
+    *v = inv_zt_kernel<CT, TH, MT, NCLS, 0>;
   }
 }
 
+template <int CT, int TH, int MT>
+void pick2(int ncls, int mode, fwd_fn* f, inv_fn* v) {
+  if constexpr (CT == 2 && MT == 2) {
+    if (ncls == 4) {
+      pick3<CT, TH, MT, 4>(mode, f, v);
+      return;
+    }
+  }
+  if (ncls == 2) pick3<CT, TH, MT, 2>(mode, f, v);
+  else pick3<CT, TH, MT, 1>(mode, f, v);
+}
+
 template <int CT, int TH>
-void pick1(int mt, int ncls, fwd_fn* f, inv_fn* v) {
-  if (mt == 2) pick2<CT, TH, 2>(ncls, f, v);
-  else if (mt == 4) pick2<CT, TH, 4>(ncls, f, v);
-  else pick2<CT, TH, 8>(ncls, f, v);
+void pick1(int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
+  if (mt == 2) pick2<CT, TH, 2>(ncls, mode, f, v);
+  else if (mt == 4) pick2<CT, TH, 4>(ncls, mode, f, v);
+  else pick2<CT, TH, 8>(ncls, mode, f, v);
 }
 
 template <int CT>
-void pick0(int th, int mt, int ncls, fwd_fn* f, inv_fn* v) {
-  if (th == 1) pick1<CT, 1>(mt, ncls, f, v);
-  else if (th == 2) pick1<CT, 2>(mt, ncls, f, v);
-  else pick1<CT, 4>(mt, ncls, f, v);
+void pick0(int th, int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
+  if (th == 1) pick1<CT, 1>(mt, ncls, mode, f, v);
+  else if (th == 2) pick1<CT, 2>(mt, ncls, mode, f, v);
+  else pick1<CT, 4>(mt, ncls, mode, f, v);
 }
 
 void pick(const StreamCfg& c, fwd_fn* f, inv_fn* v) {
-  if (c.ct == 1) pick0<1>(c.th, c.mt, c.ncls, f, v);
-  else pick0<2>(c.th, c.mt, c.ncls, f, v);
+  if (c.ct == 1) pick0<1>(c.th, c.mt, c.ncls, mode_of(c), f, v);
+  else pick0<2>(c.th, c.mt, c.ncls, mode_of(c), f, v);
 }
 
 StreamArgs args_of(const StreamCfg& c, int64_t rows) {
@@ -483,7 +571,7 @@ StreamArgs args_of(const StreamCfg& c, int64_t rows) {
   a.zh = c.zh;
   a.zt = c.zt;
   a.vec = c.vec;
-  a.full = (c.vec && c.zh % 16 == 0 && c.nt == 16 * c.th) ? 1 : 0;
+  a.full = mode_of(c) == 2 ? 1 : 0;
   return a;
 }
 

@@ -130,8 +130,16 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
     *err = "local N_t > 64 is not covered by the streaming kernels";
     return DTST_ERR_UNSUPPORTED;
   }
+  // z folds when this shard holds the whole even z extent: into 2 classes by
+  // mode parity, or into 4 by k mod 4 when N_z % 4 == 0, the stored position
+  // of a mode has its residue (k even), Re / Im of k_t sit in separate column
+  // tiles (ct == 2, which keeps the factors +-i lane-local) and each class
+  // holds at most 16 modes (one Re and one Im row tile: the four-class
+  // kernels fit their registers only at that size).
   const bool fold = d->n_local[2] == d->n_global[2] && d->n_global[2] % 2 == 0;
-  sc.ncls = fold ? 2 : 1;
+  const bool fold4 =
+      fold && d->n_global[2] % 4 == 0 && d->kmax[2] % 2 == 0 && sc.ct == 2 && sc.kz <= 4 * 16;
+  sc.ncls = fold4 ? 4 : (fold ? 2 : 1);
   const int slots = static_cast<int>(ceil_div(sc.kz, sc.ncls));
   int kcp = static_cast<int>(round_up(slots, 16));
   if (kcp == 48) kcp = 64;
@@ -141,7 +149,7 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
   }
   sc.kcp = kcp;
   sc.mt = kcp / 8;
-  sc.zh = fold ? sc.nz / 2 : sc.nz;
+  sc.zh = sc.nz / sc.ncls;
   sc.zt = static_cast<int>(ceil_div(sc.zh, 16));
   sc.vec = (sc.nt % 4 == 0) ? 1 : 0;
   sc.lds_bytes = size_t(sc.ncls) * sc.zt * sc.mt * 64 * 16;

@@ -35,6 +35,13 @@ CASES = {
     "cfg1_full": ((32, 32, 32, 8), (32, 32, 32, 8), (0, 0, 0, 0), (8, 8, 8), 4, 1, 8, 8),
     # largest tiles the stream kernels take: 64 folded z modes per class, k_t = 16, N_t = 64
     "max_tiles": ((4, 4, 128, 64), (4, 4, 128, 64), (0, 0, 0, 0), (2, 2, 64), 16, 1, 2, 2),
+    # four-class z fold (N_z % 4 == 0, even k_max(z), k_t > 8): ragged z tile with masked
+    # 16-byte t chunks, scalar t (N_t = 21), complete tiles with every z mode kept
+    "radix4_ragged": ((6, 8, 40, 24), (6, 8, 40, 24), (0, 0, 0, 0), (2, 3, 6), 10, 2, 2, 3),
+    "radix4_scalar_t": ((4, 6, 24, 21), (4, 6, 24, 21), (0, 0, 0, 0), (1, 2, 4), 11, 1, 1, 2),
+    "radix4_full_tiles": ((4, 4, 64, 32), (4, 4, 64, 32), (0, 0, 0, 0), (2, 2, 32), 16, 1, 2, 2),
+    # odd k_max(z) with N_z % 4 == 0 and k_t > 8 keeps the two-class fold
+    "fold2_odd_kz_kt9": ((4, 4, 24, 16), (4, 4, 24, 16), (0, 0, 0, 0), (1, 1, 5), 9, 1, 2, 1),
 }
 
 
