@@ -19,6 +19,9 @@ Distributed Spectral Neural Operators", arXiv 2607.14394):
                                    half-spectrum reading for t (see below)
 * adjoints / weight gradient    -- Sec. V-C (backward pass), worked out with
                                    respect to <a, b> = Re sum conj(a) b
+* block epilogue                -- Sec. V (block structure), Algorithm 1: the
+                                   point-wise bypass W x added to the spectral
+                                   output, through GELU
 
 Readings taken where the paper is silent (each is listed in the design doc):
 
@@ -29,11 +32,14 @@ Readings taken where the paper is silent (each is listed in the design doc):
   w(N_t/2) = 1 for even N_t, w = 2 otherwise.
 * Mix: Yhat[b,o,m] = sum_i Xhat[b,i,m] W[m,i,o], no conjugation.
 * Phases are reduced as exact integers, (k * n) mod N, before any trig call.
+* GELU is the exact form v Phi(v) (erf), the bypass W a real (C_out x C_in)
+  matrix with no bias (Algorithm 1 names neither an approximation nor a bias).
 
 Every routine works in float64 / complex128.  Contractions are done one
 dimension at a time (the DFT kernel is a product over dimensions), in the
 paper's order T, Z, Y, X for the forward and X, Y, Z, T for the inverse
-(Algorithm 1); ``np.tensordot`` is the only library primitive used.
+(Algorithm 1).  The library primitives used are ``np.tensordot`` and
+``np.einsum`` (contractions) and ``math.erf``.
 """
 
 from __future__ import annotations
@@ -47,7 +53,7 @@ __all__ = [
     "Geometry", "retained_indices", "retained_t", "basis", "half_weights",
     "forward", "inverse", "forward_adj", "inverse_adj", "mix",
     "mix_data_grad", "mix_wgrad", "forward_at_modes", "inverse_at_points", "forward_adj_at_points",
-    "n_modes", "mode_index",
+    "n_modes", "mode_index", "gelu", "block_epilogue",
 ]
 
 
@@ -322,3 +328,29 @@ def mix_wgrad(xhat, g_yhat, m0, m1, gw_in=None):
     if gw_in is not None:
         gw = gw + np.asarray(gw_in, dtype=np.complex128)
     return gw
+
+
+# ---------------------------------------------------------------------------
+# Block epilogue (Sec. V "Block Structure", Algorithm 1: first and last step)
+# ---------------------------------------------------------------------------
+_erf = np.frompyfunc(math.erf, 1, 1)
+
+
+def gelu(v):
+    """GELU(v) = v Phi(v) with Phi the standard normal CDF,
+    Phi(v) = (1 + erf(v / sqrt 2)) / 2 (the exact form, not an approximation)."""
+    v = np.asarray(v, dtype=np.float64)
+    return 0.5 * v * (1.0 + _erf(v / math.sqrt(2.0)).astype(np.float64))
+
+
+def block_epilogue(x, w_bypass, y):
+    """out[b,o,n] = GELU(sum_i W[o,i] x[b,i,n] + y[b,o,n]): the point-wise
+    linear bypass W x of the block input added to the spectral output y (the
+    inverse partial DFT of the mixed spectrum), through the activation.
+
+    x: (B, C_in, ...) real, w_bypass: (C_out, C_in) real, y: (B, C_out, ...)."""
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w_bypass, dtype=np.float64)
+    y = np.asarray(y, dtype=np.float64)
+    y0 = np.tensordot(w, x, axes=([1], [1]))          # (C_out, B, ...)
+    return gelu(np.moveaxis(y0, 0, 1) + y)

@@ -410,3 +410,47 @@ def test_point_evaluators_match_pinned_full_transforms():
     ga = O.forward_adj(Y, g)
     assert np.allclose(O.forward_adj_at_points(Y[0, 1], g, pts), [ga[0, 1][p] for p in pts], rtol=1e-12,
                        atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Block epilogue: GELU(W x + y) (Sec. V block structure, Algorithm 1)
+# ---------------------------------------------------------------------------
+def test_gelu_matches_normal_cdf_table():
+    """GELU(v) = v Phi(v) at tabulated values of the normal CDF."""
+    rows = [ln.split() for ln in open(os.path.join(GOLDEN, "normal_cdf.txt")) if ln.strip() and ln[0] != "#"]
+    v = np.array([float(r[0]) for r in rows])
+    phi = np.array([float(r[1]) for r in rows])
+    assert np.allclose(O.gelu(v), v * phi, rtol=0, atol=2e-15)
+
+
+def test_gelu_identities():
+    """GELU(v) - GELU(-v) = v (Phi(v) + Phi(-v) = 1), GELU(0) = 0, and the
+    activation is the identity / zero far out on either side."""
+    v = np.linspace(-6.0, 6.0, 241)
+    assert np.allclose(O.gelu(v) - O.gelu(-v), v, rtol=0, atol=1e-15)
+    assert O.gelu(np.array([0.0]))[0] == 0.0
+    assert abs(O.gelu(np.array([12.0]))[0] - 12.0) < 1e-15
+    assert abs(O.gelu(np.array([-12.0]))[0]) < 1e-15
+
+
+def test_block_epilogue_special_cases_and_brute_force():
+    """W = I and y = 0 give GELU(x); W = 0 gives GELU(y); a random case
+    equals the per-point, per-channel loop written out."""
+    rng = np.random.default_rng(31)
+    B, ci, co, shape = 2, 3, 4, (2, 3, 2, 5)
+    x = rng.standard_normal((B, ci) + shape)
+    y = rng.standard_normal((B, co) + shape)
+    w = rng.standard_normal((co, ci))
+    eye = np.eye(ci)
+    assert np.allclose(O.block_epilogue(x, eye, np.zeros_like(x)), O.gelu(x), rtol=0, atol=1e-15)
+    assert np.allclose(O.block_epilogue(x, np.zeros((co, ci)), y), O.gelu(y), rtol=0, atol=1e-15)
+    got = O.block_epilogue(x, w, y)
+    ref = np.empty_like(y)
+    for b in range(B):
+        for o in range(co):
+            for n in np.ndindex(*shape):
+                s = y[(b, o) + n]
+                for i in range(ci):
+                    s += w[o, i] * x[(b, i) + n]
+                ref[(b, o) + n] = 0.5 * s * (1.0 + math.erf(s / math.sqrt(2.0)))
+    assert np.allclose(got, ref, rtol=0, atol=1e-14)
