@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5],
                     help="workload table entry (default 2: 128^3x32 in 8 x-slabs; 5 times the backward)")
+    ap.add_argument("--block", action="store_true",
+                    help="time the whole block of Algorithm 1: after every shard's inverse, the point-wise "
+                         "bypass of the shard's input and GELU (forward workloads only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-times", action="store_true",
                     help="skip the per-kernel event pass (used under rocprofv3)")
@@ -152,7 +155,7 @@ def _mix_work(g, m_count, kind):
                 mfma_flops=8 * B * m_count * ci * co)
 
 
-def forward_workload(torch, D, synth, cfg, device):
+def forward_workload(torch, D, synth, cfg, device, block=False):
     """Forward partial DFT + mix + inverse over every shard of the workload.
     Workload 2 runs its 8 slabs one after another: the forwards accumulate
     into one spectrum, the mix runs over the 8 mode ranges in turn, and every
@@ -182,6 +185,7 @@ def forward_workload(torch, D, synth, cfg, device):
     P = len(plans)
     bounds = [(M * r) // P for r in range(P + 1)]
     ranges = [(bounds[r], bounds[r + 1]) for r in range(P)]
+    Wb = synth.torch_bypass(g0["c_out"], g0["c_in"], synth.seed_of(cfg, "bypass"), device) if block else None
 
     w = Workload()
 
@@ -190,20 +194,26 @@ def forward_workload(torch, D, synth, cfg, device):
             plan.forward(x, xhat, accumulate=p > 0)
         for m0, m1 in ranges:
             plans[0].mix(xhat, W[m0:m1], yhat, m0, m1)
-        for plan, y in zip(plans, ys):
+        for plan, y, (_, x) in zip(plans, ys, shards):
             plan.inverse(yhat, y)
+            if block:
+                plan.block_epilogue(x, Wb, y)
 
     w.step = step
     per = work(g0, g0["c_in"])
     per["mix"] = _mix_work(g0, M // P, "mix")
+    B0, ci0, co0, V0 = g0["batch"], g0["c_in"], g0["c_out"], _vol(g0)
+    per["block_epilogue"] = dict(bytes=B0 * V0 * (ci0 + 2 * co0) * 4, flops=2 * B0 * V0 * ci0 * co0,
+                                 mfma_flops=2 * B0 * V0 * ci0 * co0)
     w.work = per
-    w.launches = {k: P for k in ("stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "mix", "axis_inv_x",
-                                 "axis_inv_y", "stream_inv_zt")}
+    roles = ("stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "mix", "axis_inv_x", "axis_inv_y", "stream_inv_zt")
+    w.launches = {k: P for k in roles + (("block_epilogue",) if block else ())}
     w.flops = sum(per[k]["flops"] * n for k, n in w.launches.items())
     w.mfma_flops = sum(per[k]["mfma_flops"] * n for k, n in w.launches.items())
     B, ci, co = g0["batch"], g0["c_in"], g0["c_out"]
     w.bytes = P * B * (ci + co) * _vol(g0) * 4 + M * ci * co * 8   # read x, write y, read W
-    w.metric = "spectral-layer ms and GB/s + TFLOP/s per MI355X (fwd partial DFT+mix+inverse)"
+    w.metric = ("DRIFT block ms and GB/s + TFLOP/s per MI355X (fwd partial DFT+mix+inverse, bypass + GELU)"
+                if block else "spectral-layer ms and GB/s + TFLOP/s per MI355X (fwd partial DFT+mix+inverse)")
     w.config = {"workload": synth.CONFIGS[cfg]["name"], "global_grid": list(g0["n_global"]),
                 "local_shard": list(g0["n_local"]), "shards_run_in_sequence": P, "batch": B,
                 "c_in": ci, "c_out": co,
@@ -219,6 +229,7 @@ def forward_workload(torch, D, synth, cfg, device):
             geos = [_geo(O, g) for g, _ in shards]
             xs = [x.cpu().numpy() for _, x in shards]
             Ws = W.cpu().numpy()
+            Wbs = Wb.cpu().numpy() if block else None
             layers = 0
             t0 = time.perf_counter()
             while True:
@@ -227,14 +238,19 @@ def forward_workload(torch, D, synth, cfg, device):
                     part = O.forward(x, geo)
                     X = part if X is None else X + part
                 Y = O.mix(X, Ws, 0, M, c_out=co).reshape((X.shape[0], co) + geos[0].K)
-                for geo in geos:
-                    O.inverse(Y, geo)
+                for geo, x in zip(geos, xs):
+                    y = O.inverse(Y, geo)
+                    if block:
+                        O.block_epilogue(x, Wbs, y)
                 layers += 1
                 dt = time.perf_counter() - t0
                 if dt >= min_seconds:
                     break
-            return dt, float(layers), (f"fp64 oracle, {layers} whole layer(s) of this workload ({P} shard forwards "
-                                       f"summed, mix over all {M} modes, {P} shard inverses), inputs in host memory")
+            what = "block(s)" if block else "layer(s)"
+            extra = ", each followed by the bypass and GELU" if block else ""
+            return dt, float(layers), (f"fp64 oracle, {layers} whole {what} of this workload ({P} shard forwards "
+                                       f"summed, mix over all {M} modes, {P} shard inverses{extra}), inputs in "
+                                       f"host memory")
         nc = 1
         ms = 8192
         g, x = shards[0]
@@ -243,10 +259,13 @@ def forward_workload(torch, D, synth, cfg, device):
         Ws = W[:ms, :, :].cpu().numpy()
         Xs = synth.np_complex_normal((B, ci, ms), 12345)
         Ys = synth.np_complex_normal((1, nc) + geo.K, 12346)
+        Wbs = Wb[:nc, :nc].cpu().numpy() if block else None
         t0 = time.perf_counter()
         O.forward(xs, geo)
         O.mix(Xs, Ws, 0, ms, c_out=co)
-        O.inverse(Ys, geo)
+        ys = O.inverse(Ys, geo)
+        if block:
+            O.block_epilogue(xs, Wbs, ys)
         dt = time.perf_counter() - t0
         frac = (2 * nc * _vol(g) * 4 + ms * ci * co * 8) / w.bytes
         return dt, frac, (f"fp64 oracle: forward and inverse of one (b, c) slice of shard 0 and the mix over "
@@ -407,7 +426,11 @@ def main():
         del blk
         torch.cuda.empty_cache()
     log(f"building workload {cfg}")
-    w = backward_workload(torch, D, synth, cfg, device) if cfg == 5 else forward_workload(torch, D, synth, cfg, device)
+    if args.block and cfg == 5:
+        print("--block applies to the forward workloads (1-4)", file=sys.stderr)
+        sys.exit(2)
+    w = (backward_workload(torch, D, synth, cfg, device) if cfg == 5
+         else forward_workload(torch, D, synth, cfg, device, block=args.block))
     log(f"warmup {args.warmup} steps")
 
     # ---- warmup ----

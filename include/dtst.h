@@ -161,6 +161,18 @@ dtst_status dtst_inverse_adj(dtst_plan_t p, const float* g_y, void* g_yhat, int 
 dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, void* g_w_shard,
                            int64_t m0, int64_t m1, int accumulate, void* stream);
 
+/* Block epilogue (Sec. V block structure; Algorithm 1, first and last step):
+ * the point-wise linear bypass of the block input added to the spectral
+ * output, through the activation, in place on y:
+ *   y[b,o,n] <- GELU( sum_i w_bypass[o,i] x[b,i,n] + y[b,o,n] ),
+ *   GELU(v) = v Phi(v) = v (1 + erf(v / sqrt 2)) / 2  (exact form, no bias).
+ * x: (B, C_in, shard) fp32, the block input; y: (B, C_out, shard) fp32, the
+ * output of dtst_inverse; w_bypass: (C_out, C_in) fp32 row-major.  All are
+ * device arrays owned by the caller, 16-byte aligned; x must not overlap y
+ * (DTST_ERR_INVALID_ARG); C_in * C_out <= 40960 (DTST_ERR_UNSUPPORTED).
+ * Asynchronous on `stream`, no allocation. */
+dtst_status dtst_block_epilogue(dtst_plan_t p, const float* x, const float* w_bypass, float* y, void* stream);
+
 /* ---- instrumentation ----------------------------------------------------- */
 
 /* Per-kernel device time, for callers that time the path (benchmarks,
@@ -168,7 +180,7 @@ dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, 
  * bracketed by a pair of HIP events recorded on the call's stream; nothing
  * else changes.  Process-wide; off by default. */
 typedef struct {
-  char name[40];     /* kernel role, e.g. "stream_fwd_tz", "axis_fwd_y", "mix" */
+  char name[40];     /* kernel role, e.g. "stream_fwd_tz", "axis_fwd_y", "mix", "block_epilogue" */
   int64_t launches;  /* launches collected */
   double total_ms;   /* summed event-to-event device time */
 } dtst_kernel_time;

@@ -39,7 +39,7 @@ Every routine works in float64 / complex128.  Contractions are done one
 dimension at a time (the DFT kernel is a product over dimensions), in the
 paper's order T, Z, Y, X for the forward and X, Y, Z, T for the inverse
 (Algorithm 1).  The library primitives used are ``np.tensordot`` and
-``np.einsum`` (contractions) and ``math.erf``.
+``np.einsum`` (contractions) and ``scipy.special.erf``.
 """
 
 from __future__ import annotations
@@ -333,14 +333,12 @@ def mix_wgrad(xhat, g_yhat, m0, m1, gw_in=None):
 # ---------------------------------------------------------------------------
 # Block epilogue (Sec. V "Block Structure", Algorithm 1: first and last step)
 # ---------------------------------------------------------------------------
-_erf = np.frompyfunc(math.erf, 1, 1)
-
-
 def gelu(v):
     """GELU(v) = v Phi(v) with Phi the standard normal CDF,
     Phi(v) = (1 + erf(v / sqrt 2)) / 2 (the exact form, not an approximation)."""
+    from scipy.special import erf
     v = np.asarray(v, dtype=np.float64)
-    return 0.5 * v * (1.0 + _erf(v / math.sqrt(2.0)).astype(np.float64))
+    return 0.5 * v * (1.0 + erf(v / math.sqrt(2.0)))
 
 
 def block_epilogue(x, w_bypass, y):

@@ -104,9 +104,9 @@ size_t w1_bytes(const dtst::Derived& dv) {
 
 // ---- per-kernel event timing (dtst_profile_enable / dtst_profile_collect) ----
 enum KernelRole { K_FWD_TZ, K_AXIS_FWD_Y, K_AXIS_FWD_X, K_AXIS_INV_X, K_AXIS_INV_Y, K_INV_ZT, K_MIX, K_MIX_H,
-                  K_WGRAD, K_COUNT };
+                  K_WGRAD, K_BLOCK, K_COUNT };
 const char* const kRoleNames[K_COUNT] = {"stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "axis_inv_x", "axis_inv_y",
-                                         "stream_inv_zt", "mix", "mix_h", "wgrad"};
+                                         "stream_inv_zt", "mix", "mix_h", "wgrad", "block_epilogue"};
 
 struct Profiler {
   std::mutex mu;
@@ -417,6 +417,30 @@ dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, 
                               accumulate, stream);
   });
   return device_status(e, "wgrad launch");
+}
+
+dtst_status dtst_block_epilogue(dtst_plan_t p, const float* x, const float* w_bypass, float* y, void* stream) {
+  DTST_TRY(check_plan(p));
+  const dtst::Derived& dv = p->dv;
+  if (dv.d.batch == 0) return ok();
+  DTST_TRY(check_ptr(x, "x"));
+  DTST_TRY(check_ptr(w_bypass, "w_bypass"));
+  DTST_TRY(check_ptr(y, "y"));
+  if (dv.d.c_in * dv.d.c_out * int64_t(sizeof(float)) > 160 * 1024)
+    return fail(DTST_ERR_UNSUPPORTED, "c_in * c_out above 40960: the bypass matrix must fit in LDS");
+  const int64_t V = dv.d.n_local[0] * dv.d.n_local[1] * dv.d.n_local[2] * dv.d.n_local[3];
+  // x must not overlap y (y is rewritten while x is still being read).
+  const char* xb = reinterpret_cast<const char*>(x);
+  const char* yb = reinterpret_cast<const char*>(y);
+  const size_t xbytes = size_t(dv.d.batch) * dv.d.c_in * V * sizeof(float);
+  const size_t ybytes = size_t(dv.d.batch) * dv.d.c_out * V * sizeof(float);
+  if (xb < yb + ybytes && yb < xb + xbytes) return fail(DTST_ERR_INVALID_ARG, "x and y overlap");
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  const int e = timed(K_BLOCK, stream, [&] {
+    return dtst::launch_block_epilogue(x, w_bypass, y, dv.d.batch, dv.d.c_in, dv.d.c_out, V, stream);
+  });
+  return device_status(e, "block epilogue launch");
 }
 
 dtst_status dtst_profile_enable(int on) {

@@ -1,0 +1,124 @@
+// Block epilogue (Sec. V "Block Structure", Algorithm 1 first and last
+// step): the point-wise linear bypass of the block input added to the
+// spectral output, through the activation,
+//
+//   y[b,o,n] <- GELU( sum_i w[o,i] x[b,i,n] + y[b,o,n] ),   GELU(v) = v Phi(v),
+//
+// in place on y (the output of the inverse partial DFT).  Per point this is a
+// (C_out x C_in) matrix-vector product, about 2 C_in C_out / (4 (C_in + 2 C_out))
+// flop per byte (2.7 at C = 16): bound by HBM traffic on x and y, so it runs on
+// the VALU.  Each thread owns four consecutive points of one batch entry
+// (16-byte accesses), reads their C_in input channels once per chunk of 16
+// output channels, and reads w from LDS (the same entry for every lane).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "dtst_internal.h"
+
+namespace dtst {
+namespace {
+
+constexpr int OC = 16;  // output channels per pass over the input channels
+
+__device__ __forceinline__ float gelu(float v) {
+  return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+}
+
+template <int VEC>
+__global__ void __launch_bounds__(256)
+block_epilogue_kernel(const float* __restrict__ x, const float* __restrict__ w, float* __restrict__ y, int64_t V,
+                      int64_t total, int ci, int co) {
+  // VEC: 4 points per thread (V % 4 == 0, 16-byte accesses), else 1.
+  constexpr int P = VEC ? 4 : 1;
+  const int64_t VP = V / P;
+  // w in LDS: every lane reads the same entry (a broadcast), which keeps it
+  // out of the scalar registers.
+  extern __shared__ float sw[];
+  for (int e = threadIdx.x; e < co * ci; e += blockDim.x) sw[e] = w[e];
+  __syncthreads();
+  for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
+       idx += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t b = idx / VP, n = (idx - b * VP) * P;
+    const float* xb = x + b * ci * V + n;
+    float* yb = y + b * co * V + n;
+    for (int o0 = 0; o0 < co; o0 += OC) {
+      // the accumulators start from y, loaded before the x loop so that its
+      // latency overlaps the reads of x
+      float acc[OC][P];
+#pragma unroll
+      for (int oo = 0; oo < OC; ++oo) {
+        const int o = o0 + oo < co ? o0 + oo : co - 1;
+        const float* yp = yb + int64_t(o) * V;
+        if constexpr (VEC) {
+          const float4 v = *reinterpret_cast<const float4*>(yp);
+          acc[oo][0] = v.x;
+          acc[oo][1] = v.y;
+          acc[oo][2] = v.z;
+          acc[oo][3] = v.w;
+        } else {
+          acc[oo][0] = *yp;
+        }
+      }
+#pragma unroll 4
+      for (int i = 0; i < ci; ++i) {
+        float xv[P];
+        if constexpr (VEC) {
+          const float4 v = *reinterpret_cast<const float4*>(xb + int64_t(i) * V);
+          xv[0] = v.x;
+          xv[1] = v.y;
+          xv[2] = v.z;
+          xv[3] = v.w;
+        } else {
+          xv[0] = xb[int64_t(i) * V];
+        }
+#pragma unroll
+        for (int oo = 0; oo < OC; ++oo) {
+          const int o = o0 + oo < co ? o0 + oo : co - 1;
+          const float wv = sw[o * ci + i];
+#pragma unroll
+          for (int p = 0; p < P; ++p) acc[oo][p] += wv * xv[p];
+        }
+      }
+#pragma unroll
+      for (int oo = 0; oo < OC; ++oo) {
+        if (o0 + oo >= co) continue;
+        float* yp = yb + int64_t(o0 + oo) * V;
+        if constexpr (VEC) {
+          *reinterpret_cast<float4*>(yp) =
+              make_float4(gelu(acc[oo][0]), gelu(acc[oo][1]), gelu(acc[oo][2]), gelu(acc[oo][3]));
+        } else {
+          *yp = gelu(acc[oo][0]);
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+int launch_block_epilogue(const float* x, const float* w, float* y, int64_t B, int64_t ci, int64_t co, int64_t V,
+                          void* stream) {
+  if (B <= 0 || V <= 0) return hipSuccess;
+  const bool vec = V % 4 == 0;
+  const int64_t total = B * (vec ? V / 4 : V);
+  const int64_t cap = int64_t(1) << 20;
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, cap);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t lds = size_t(ci) * co * sizeof(float);
+  const void* fn = vec ? reinterpret_cast<const void*>(block_epilogue_kernel<1>)
+                       : reinterpret_cast<const void*>(block_epilogue_kernel<0>);
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+  }
+  if (vec)
+    hipLaunchKernelGGL(block_epilogue_kernel<1>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s, x, w, y, V,
+                       total, static_cast<int>(ci), static_cast<int>(co));
+  else
+    hipLaunchKernelGGL(block_epilogue_kernel<0>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s, x, w, y, V,
+                       total, static_cast<int>(ci), static_cast<int>(co));
+  return hipGetLastError();
+}
+
+}  // namespace dtst

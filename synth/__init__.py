@@ -8,7 +8,7 @@ waves).  Every array it returns is fed unchanged to both the HIP library and
 the fp64 CPU oracle.
 
 Seeds: input 1000*cfg, weights 1000*cfg + 1, upstream gradient 1000*cfg + 2,
-synthetic spectra 1000*cfg + 3.
+synthetic spectra 1000*cfg + 3, bypass weights 1000*cfg + 4.
 
 The paper's workload (PDEBench 3D compressible Navier-Stokes, 128^3 x 21
 steps, d_v = 20, modes (8, 8, 8, 16)) is not available here; these fields
@@ -59,7 +59,7 @@ CFG2_AMPLITUDE = 5.0
 
 
 def seed_of(cfg: int, what: str) -> int:
-    return 1000 * cfg + {"input": 0, "weights": 1, "upstream": 2, "spectrum": 3}[what]
+    return 1000 * cfg + {"input": 0, "weights": 1, "upstream": 2, "spectrum": 3, "bypass": 4}[what]
 
 
 def geometry(cfg: int, shard: int | None = None) -> dict:
@@ -151,6 +151,11 @@ def torch_complex_normal(shape, seed, device, var=1.0):
 def torch_weights(m_count, c_in, c_out, seed, device):
     return torch_complex_normal((m_count, c_in, c_out), seed, device,
                                 var=1.0 / (c_in * c_out))
+
+
+def torch_bypass(c_out, c_in, seed, device):
+    """Real point-wise bypass weights (C_out x C_in), N(0, 1/C_in)."""
+    return torch_normal((c_out, c_in), seed, device, std=1.0 / math.sqrt(c_in))
 
 
 def torch_plane_wave_(out, g, k, phase, amp):

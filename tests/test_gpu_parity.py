@@ -297,3 +297,70 @@ def test_errors_launch_nothing():
     with pytest.raises(D.DtstError) as e:
         D.dtst_forward(h, x, out, 0, small_ws)
     assert "destroyed" in str(e.value)
+
+
+# (n_local, B, C_in, C_out): 16-byte path with one and two chunks of 16 output
+# channels, the scalar path (point count not a multiple of 4), C_in != C_out.
+EPILOGUE_SHAPES = [((4, 6, 8, 8), 2, 16, 16), ((3, 5, 4, 8), 1, 3, 37), ((3, 5, 7, 3), 2, 5, 2),
+                   ((2, 2, 2, 2), 1, 1, 1)]
+
+
+@pytest.mark.parametrize("shape", EPILOGUE_SHAPES, ids=lambda s: "nl%s_B%d_ci%d_co%d" % (
+    "x".join(map(str, s[0])), s[1], s[2], s[3]))
+def test_block_epilogue(shape):
+    """y <- GELU(W x + y) (Algorithm 1, first and last step) against the
+    oracle, element by element."""
+    nl, B, ci, co = shape
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry(nl, nl, (0, 0, 0, 0), (1, 1, 1), 1, B, ci, co)
+    say(f"[block epilogue] n_local={nl} B={B} Cin={ci} Cout={co}")
+    plan = D.Plan(desc_of(g))
+    x = rand_real((B, ci) + nl, 130)
+    y = rand_real((B, co) + nl, 131)
+    w = (rand_real((co, ci), 132) / np.sqrt(ci)).astype(np.float32)
+    Y = Guarded(torch, plan.spatial_shape(co), torch.float32, fill=dev(torch, y))
+    plan.block_epilogue(dev(torch, x), dev(torch, w), Y.t)
+    torch.cuda.synchronize()
+    check(np_of(Y.t), O.block_epilogue(x, w, y), "block epilogue")
+    assert Y.guards_intact()
+    plan.close()
+
+
+def test_block_forward_small():
+    """The whole block of Algorithm 1 on one shard: forward, mix, inverse, then
+    the bypass and GELU, against the oracle composed from the same input."""
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry((16, 12, 24, 16), (16, 12, 24, 16), (0, 0, 0, 0), (4, 3, 5), 6, 2, 3, 4)
+    plan = D.Plan(desc_of(g))
+    M = plan.n_modes
+    x = rand_real((g.batch, g.c_in) + g.n_local, 133)
+    W = rand_cplx((M, g.c_in, g.c_out), 134, var=1.0 / (g.c_in * g.c_out))
+    wb = (rand_real((g.c_out, g.c_in), 135) / np.sqrt(g.c_in)).astype(np.float32)
+    xd = dev(torch, x)
+    xh = torch.empty(plan.spectral_shape(g.c_in), dtype=torch.complex64, device="cuda")
+    yh = torch.empty(plan.spectral_shape(g.c_out), dtype=torch.complex64, device="cuda")
+    y = torch.empty(plan.spatial_shape(g.c_out), dtype=torch.float32, device="cuda")
+    plan.forward(xd, xh)
+    plan.mix(xh, dev(torch, W), yh, 0, M)
+    plan.inverse(yh, y)
+    plan.block_epilogue(xd, dev(torch, wb), y)
+    torch.cuda.synchronize()
+    spec = O.mix(O.forward(x, g), W, 0, M, c_out=g.c_out).reshape((g.batch, g.c_out) + g.K)
+    ref = O.block_epilogue(x, wb, O.inverse(spec, g))
+    check(np_of(y), ref, "block forward (spectral path + bypass + GELU)")
+    plan.close()
+
+
+def test_block_epilogue_rejects_overlap():
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry((4, 4, 4, 4), (4, 4, 4, 4), (0, 0, 0, 0), (1, 1, 1), 1, 1, 2, 2)
+    plan = D.Plan(desc_of(g))
+    buf = torch.zeros((1, 2) + g.n_local, dtype=torch.float32, device="cuda")
+    w = torch.zeros((2, 2), dtype=torch.float32, device="cuda")
+    with pytest.raises(D.DtstError) as e:
+        D.dtst_block_epilogue(plan.handle, buf, w, buf)
+    assert e.value.status == 1
+    plan.close()

@@ -207,3 +207,29 @@ def test_backward_full_size():
     del gxh, gx
     plan.close()
     free(torch)
+
+
+def test_block_epilogue_full_size():
+    """Block epilogue GELU(W x + y) on one 16x128x128x32 slab of workload 2
+    (B1, C16, the launch the block benchmark times), checked on sampled
+    points; the spectral output y is a seeded stand-in."""
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    cfg = 2
+    g = synth.geometry(cfg, 3)
+    say(f"[workload 2 block epilogue] slab 3, n_local={g['n_local']}")
+    plan = D.Plan(g)
+    B, ci, co = g["batch"], g["c_in"], g["c_out"]
+    x = synth.torch_input(cfg, g, "cuda")
+    y = synth.torch_normal((B, co) + tuple(g["n_local"]), synth.seed_of(cfg, "spectrum") + 40, "cuda")
+    wb = synth.torch_bypass(co, ci, synth.seed_of(cfg, "bypass"), "cuda")
+    pts = sampled_points(g["n_local"], 4096, 23)
+    idx = torch.tensor([list(p) for p in pts], device="cuda").T
+    xs = np_of(x[:, :, idx[0], idx[1], idx[2], idx[3]])
+    ys = np_of(y[:, :, idx[0], idx[1], idx[2], idx[3]])
+    plan.block_epilogue(x, wb, y)
+    got = np_of(y[:, :, idx[0], idx[1], idx[2], idx[3]])
+    check(got, O.block_epilogue(xs, np_of(wb), ys), "block epilogue (sampled points)")
+    del x, y
+    plan.close()
+    free(torch)
