@@ -44,8 +44,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5],
-                    help="workload table entry (default 2: 128^3x32 in 8 x-slabs; 5 times the backward)")
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6],
+                    help="workload table entry (default 2: 128^3x32 in 8 x-slabs; 5 times the backward; "
+                         "6: the same grid in 2x4 (x, y) pencils)")
     ap.add_argument("--block", action="store_true",
                     help="time the whole block of Algorithm 1: after every shard's inverse, the point-wise "
                          "bypass of the shard's input and GELU (forward workloads only)")
@@ -162,14 +163,13 @@ def forward_workload(torch, D, synth, cfg, device, block=False):
     slab is then expanded back."""
     c = synth.CONFIGS[cfg]
     shards = []
-    if cfg == 2:
-        full = synth.full_domain(2)
-        x_full = synth.torch_input(2, full, device)
-        P = c["shards"]
-        lx = c["n_local"][0]
-        for p in range(P):
-            g = synth.geometry(2, p)
-            shards.append((g, x_full[:, :, p * lx:(p + 1) * lx].contiguous()))
+    if cfg in synth.ALL_SHARDS:
+        full = synth.full_domain(cfg)
+        x_full = synth.torch_input(cfg, full, device)
+        for p in range(c["shards"]):
+            g = synth.geometry(cfg, p)
+            (x0, y0, _, _), (lx, ly, _, _) = g["offset"], g["n_local"]
+            shards.append((g, x_full[:, :, x0:x0 + lx, y0:y0 + ly].contiguous()))
         del x_full
         torch.cuda.empty_cache()
     else:

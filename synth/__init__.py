@@ -46,7 +46,16 @@ CONFIGS = {
             n_global=(256, 256, 256, 32), n_local=(64, 256, 256, 32), shards=4,
             shard=1, kmax=(32, 32, 32), kt=16, batch=2, c_in=32, c_out=32,
             field="normal"),
+    # Not one of the five reference workloads: the grid of workload 2 under the
+    # paper's 2-D (pencil) decomposition, x and y both distributed.
+    6: dict(name="128^3x32 in 2x4 (x, y) pencils of 64x32, B1 C16, modes 32/32/32/8",
+            n_global=(128, 128, 128, 32), n_local=(64, 32, 128, 32), shards=8, grid=(2, 4),
+            kmax=(16, 16, 16), kt=8, batch=1, c_in=16, c_out=16,
+            field="normal+waves"),
 }
+
+# Workloads whose every shard is run, one after another, on the one GPU.
+ALL_SHARDS = (2, 6)
 
 # Plane waves planted in every channel of workload 2: (k, phase), amplitude 5.
 # k is a signed (x, y, z, t) wavenumber.  The second wave sits on the -k_max
@@ -63,10 +72,12 @@ def seed_of(cfg: int, what: str) -> int:
 
 
 def geometry(cfg: int, shard: int | None = None) -> dict:
-    """Plain-dict description of one shard of workload ``cfg``."""
+    """Plain-dict description of one shard of workload ``cfg``.  Shards are
+    numbered row-major over the (x, y) shard grid (x slabs: grid (P, 1))."""
     c = CONFIGS[cfg]
     p = c.get("shard", 0) if shard is None else shard
-    off = (p * c["n_local"][0], 0, 0, 0)
+    gx, gy = c.get("grid", (c["shards"], 1))
+    off = ((p // gy) * c["n_local"][0], (p % gy) * c["n_local"][1], 0, 0)
     return dict(n_global=tuple(c["n_global"]), n_local=tuple(c["n_local"]),
                 offset=off, kmax=tuple(c["kmax"]), kt=c["kt"],
                 batch=c["batch"], c_in=c["c_in"], c_out=c["c_out"])

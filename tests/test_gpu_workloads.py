@@ -125,35 +125,37 @@ def test_layer_full_size(cfg):
     free(torch)
 
 
-def test_slab_decomposition_128cubed():
-    """Workload 2: 8 x-slabs run one after another and accumulated equal the
-    full-domain spectrum; two channels are checked against the oracle, and
-    the three planted plane waves sit at their closed-form values."""
+@pytest.mark.parametrize("cfg", [2, 6])
+def test_decomposition_128cubed(cfg):
+    """Workload 2 (8 x-slabs) and 6 (2x4 (x, y) pencils): the shards run one
+    after another and accumulated equal the full-domain spectrum; two
+    channels are checked against the oracle, and the three planted plane
+    waves sit at their closed-form values."""
     torch = torch_gpu()
     import paper_2607_14394_amd as D
-    cfg = 2
     full = synth.full_domain(cfg)
-    say(f"[workload 2] {synth.CONFIGS[cfg]['name']}")
+    say(f"[workload {cfg}] {synth.CONFIGS[cfg]['name']}")
     x = synth.torch_input(cfg, full, "cuda")
     P = synth.CONFIGS[cfg]["shards"]
-    lx = synth.CONFIGS[cfg]["n_local"][0]
     pf = D.Plan(full)
     K = pf.K
     B, C = full["batch"], full["c_in"]
     acc = torch.empty((B, C) + K, dtype=torch.complex64, device="cuda")
     for p in range(P):
-        plan = D.Plan(synth.geometry(cfg, p))
-        plan.forward(x[:, :, p * lx:(p + 1) * lx].contiguous(), acc, accumulate=p > 0)
+        g = synth.geometry(cfg, p)
+        (x0, y0, _, _), (lx, ly, _, _) = g["offset"], g["n_local"]
+        plan = D.Plan(g)
+        plan.forward(x[:, :, x0:x0 + lx, y0:y0 + ly].contiguous(), acc, accumulate=p > 0)
         plan.close()
     ref_full = torch.empty_like(acc)
     pf.forward(x, ref_full)
     # Two fp32 results compared with each other: each carries its own rounding
     # (about 3e-7 relative at the planted spikes, which are ~300x the RMS),
     # so the max-abs bound is twice the oracle bar.
-    check(np_of(acc), np_of(ref_full), "sum over 8 slabs vs one full-domain call", maxabs_rms=2e-4)
+    check(np_of(acc), np_of(ref_full), f"sum over {P} shards vs one full-domain call", maxabs_rms=2e-4)
     go = geo_of(full)
     for c in (0, 9):
-        check(np_of(acc[:, c:c + 1]), O.forward(np_of(x[:, c:c + 1]), go), f"slab sum vs oracle c={c}")
+        check(np_of(acc[:, c:c + 1]), O.forward(np_of(x[:, c:c + 1]), go), f"shard sum vs oracle c={c}")
     # planted waves: 5 cos(2 pi k.n/N + phi) -> (5 prod N / 2) e^{i phi} at +k on top of
     # Gaussian noise whose coefficients have standard deviation sqrt(prod N)
     ng = full["n_global"]
@@ -169,7 +171,27 @@ def test_slab_decomposition_128cubed():
             assert err < 8 * noise, (k, c, err, noise)
     say(f"  planted waves: |spike| = {abs(want):.4e}, noise sigma = {noise:.1f}")
     del x, acc, ref_full
+    free(torch)
+    # every shard's inverse of one spectrum is its block of the full-domain
+    # inverse; one shard is also checked against the oracle on sampled points
+    yh = synth.torch_complex_normal((B, C) + K, synth.seed_of(cfg, "spectrum") + 50, "cuda")
+    y_full = torch.empty((B, C) + tuple(full["n_global"]), dtype=torch.float32, device="cuda")
+    pf.inverse(yh, y_full)
+    for p in range(P):
+        g = synth.geometry(cfg, p)
+        (x0, y0, _, _), (lx, ly, _, _) = g["offset"], g["n_local"]
+        plan = D.Plan(g)
+        y = torch.empty((B, C) + tuple(g["n_local"]), dtype=torch.float32, device="cuda")
+        plan.inverse(yh, y)
+        check(np_of(y), np_of(y_full[:, :, x0:x0 + lx, y0:y0 + ly]), f"shard {p} inverse vs full-domain block")
+        if p == P - 1:
+            pts = sampled_points(g["n_local"], 32, 29)
+            ref = O.inverse_at_points(np_of(yh[0, 5]), geo_of(g), pts)
+            check(np.array([y[(0, 5) + q].item() for q in pts]), ref, f"shard {p} inverse vs oracle (points)")
+        plan.close()
+        del y
     pf.close()
+    del yh, y_full
     free(torch)
 
 
