@@ -64,10 +64,12 @@ __device__ __forceinline__ int64_t xcd_logical(int64_t bid, int64_t grid) {
 // lane (row i: value (re[i], im[i]) at column n) with 16-byte stores: even
 // lanes write rows 0 and 2, odd lanes rows 1 and 3, each as the pair of
 // columns (n & ~1, (n & ~1) + 1).  NN is even, so pairs never straddle the
-// end of a row.  rowok(i) says whether row k0 + i exists.
+// end of a row.  rowok(i) says whether row k0 + i exists.  With acc the
+// stored values are added to what the output held: pre[h] when the caller
+// loaded it earlier (same addresses, h = 0, 1), else read here.
 template <class RowPtr, class RowOk>
 __device__ __forceinline__ void store_tile(const float (&re)[4], const float (&im)[4], int n, bool nok, int acc,
-                                           RowPtr rowptr, RowOk rowok) {
+                                           RowPtr rowptr, RowOk rowok, const float4* pre = nullptr) {
   const bool odd = n & 1;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -81,7 +83,7 @@ __device__ __forceinline__ void store_tile(const float (&re)[4], const float (&i
       float4* o = reinterpret_cast<float4*>(rowptr(row) + (n & ~1));
       float4 w = v;
       if (acc) {
-        const float4 old = *o;
+        const float4 old = pre ? pre[h] : *o;
         w.x += old.x;
         w.y += old.y;
         w.z += old.z;
@@ -92,7 +94,7 @@ __device__ __forceinline__ void store_tile(const float (&re)[4], const float (&i
   }
 }
 
-template <int KT, int NT, int FOLD>
+template <int KT, int NT, int FOLD, int ACC>
 __global__ void __launch_bounds__(256)
 axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float4* __restrict__ img,
             AxisArgs a) {
@@ -151,6 +153,34 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
     float2 vn[NC][NS][NT][4];
     bool okn[NT][4];
     load(0, vn, okn);
+
+    // Accumulating launches (forward x, the shard sum): fetch the values the
+    // output holds now right behind the first input loads, so that read is not
+    // a second round trip after the MFMAs.  Output row of tile kt, row i:
+    // FOLD 0: 16kt + 4g + i; FOLD 1: mode 2s + c of class c = (kt >= kth).
+    auto out_row = [&](int kt, int i) {
+      if (FOLD == 1) {
+        const int c = kt >= a.kth ? 1 : 0;
+        return 2 * (16 * (kt - c * a.kth) + 4 * g + i) + c;
+      }
+      return 16 * kt + 4 * g + i;
+    };
+    float4 pre[ACC ? KT : 1][ACC ? NT : 1][2];
+    if constexpr (ACC) {
+      const float2* ob = out + b * int64_t(a.KO) * a.NN;
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int kt = kb * KT + kk;
+            const int n = nw + 16 * nt + m;
+            const int row = out_row(kt, (n & 1) ? 2 * h + 1 : 2 * h);
+            const bool ok = kt < a.ktiles && n < a.NN && row < a.KO;
+            pre[kk][nt][h] = *reinterpret_cast<const float4*>(ob + (ok ? int64_t(row) * a.NN + (n & ~1) : 0));
+          }
+    }
     for (int q = 0; q < a.JQ; ++q) {
       // B operands: V[c or fold class][nt][i] as (re, im, -im)
       constexpr int NV = FOLD == 0 ? 1 : 2;
@@ -227,8 +257,8 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
             im[i] = acci[0][kk][nt][i];
           }
           const int k0 = 16 * kt + 4 * g;
-          store_tile(re, im, n, nok, a.acc, [&](int i) { return ob + int64_t(k0 + i) * a.NN; },
-                     [&](int i) { return k0 + i < a.KO; });
+          store_tile(re, im, n, nok, ACC, [&](int i) { return ob + int64_t(k0 + i) * a.NN; },
+                     [&](int i) { return k0 + i < a.KO; }, ACC ? pre[ACC ? kk : 0][ACC ? nt : 0] : nullptr);
         } else if (FOLD == 1) {
           // tile kt holds class c = kt >= kth, slots s = 16 (kt - c kth) + 4g + i, mode p = 2s + c
           float re[4], im[4];
@@ -239,8 +269,8 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
           }
           const int c = kt >= a.kth ? 1 : 0;
           const int s0 = 16 * (kt - c * a.kth) + 4 * g;
-          store_tile(re, im, n, nok, a.acc, [&](int i) { return ob + int64_t(2 * (s0 + i) + c) * a.NN; },
-                     [&](int i) { return 2 * (s0 + i) + c < a.KO; });
+          store_tile(re, im, n, nok, ACC, [&](int i) { return ob + int64_t(2 * (s0 + i) + c) * a.NN; },
+                     [&](int i) { return 2 * (s0 + i) + c < a.KO; }, ACC ? pre[ACC ? kk : 0][ACC ? nt : 0] : nullptr);
         } else {
           // rows y = 16kt + 4g + i < KO/2: E + O at y, E - O at y + KO/2
           const int y0 = 16 * kt + 4 * g;
@@ -254,7 +284,7 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
               re[i] = hf == 0 ? er + odr : er - odr;
               im[i] = hf == 0 ? ei + odi : ei - odi;
             }
-            store_tile(re, im, n, nok, a.acc,
+            store_tile(re, im, n, nok, ACC,
                        [&](int i) { return ob + int64_t(y0 + i + hf * a.oh) * a.NN; },
                        [&](int i) { return y0 + i < a.oh; });
           }
@@ -264,19 +294,21 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
   }
 }
 
-template <int KT, int FOLD>
+template <int KT, int FOLD, int ACC>
 void launch_kt(int nt, int grid, hipStream_t s, const float2* pin, float2* pout, const float4* pimg,
                const AxisArgs& a) {
-  if (nt == 2) hipLaunchKernelGGL((axis_kernel<KT, 2, FOLD>), dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
-  else hipLaunchKernelGGL((axis_kernel<KT, 1, FOLD>), dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
+  if (nt == 2)
+    hipLaunchKernelGGL((axis_kernel<KT, 2, FOLD, ACC>), dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
+  else
+    hipLaunchKernelGGL((axis_kernel<KT, 1, FOLD, ACC>), dim3(grid), dim3(256), 0, s, pin, pout, pimg, a);
 }
 
-template <int FOLD>
+template <int FOLD, int ACC>
 void launch_fold(int kt, int nt, int grid, hipStream_t s, const float2* pin, float2* pout, const float4* pimg,
                  const AxisArgs& a) {
-  if (kt == 1) launch_kt<1, FOLD>(nt, grid, s, pin, pout, pimg, a);
-  else if (kt == 2) launch_kt<2, FOLD>(nt, grid, s, pin, pout, pimg, a);
-  else launch_kt<4, FOLD>(nt, grid, s, pin, pout, pimg, a);
+  if (kt == 1) launch_kt<1, FOLD, ACC>(nt, grid, s, pin, pout, pimg, a);
+  else if (kt == 2) launch_kt<2, FOLD, ACC>(nt, grid, s, pin, pout, pimg, a);
+  else launch_kt<4, FOLD, ACC>(nt, grid, s, pin, pout, pimg, a);
 }
 
 }  // namespace
@@ -310,9 +342,13 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
   const float2* pin = static_cast<const float2*>(in);
   float2* pout = static_cast<float2*>(out);
   const float4* pimg = reinterpret_cast<const float4*>(img);
-  if (c.fold == 1) launch_fold<1>(kt, nt, grid, s, pin, pout, pimg, a);
-  else if (c.fold == 2) launch_fold<2>(kt, nt, grid, s, pin, pout, pimg, a);
-  else launch_fold<0>(kt, nt, grid, s, pin, pout, pimg, a);
+  // Accumulation only happens on forward-direction launches (fold 0 or 1).
+  if (c.fold == 2 && a.acc) return hipErrorInvalidValue;
+  if (c.fold == 2) launch_fold<2, 0>(kt, nt, grid, s, pin, pout, pimg, a);
+  else if (c.fold == 1) a.acc ? launch_fold<1, 1>(kt, nt, grid, s, pin, pout, pimg, a)
+                              : launch_fold<1, 0>(kt, nt, grid, s, pin, pout, pimg, a);
+  else a.acc ? launch_fold<0, 1>(kt, nt, grid, s, pin, pout, pimg, a)
+             : launch_fold<0, 0>(kt, nt, grid, s, pin, pout, pimg, a);
   return hipGetLastError();
 }
 
