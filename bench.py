@@ -195,9 +195,10 @@ def forward_workload(torch, D, synth, cfg, device, block=False):
         for m0, m1 in ranges:
             plans[0].mix(xhat, W[m0:m1], yhat, m0, m1)
         for plan, y, (_, x) in zip(plans, ys, shards):
-            plan.inverse(yhat, y)
             if block:
-                plan.block_epilogue(x, Wb, y)
+                plan.inverse_block(yhat, x, Wb, y)
+            else:
+                plan.inverse(yhat, y)
 
     w.step = step
     per = work(g0, g0["c_in"])

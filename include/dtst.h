@@ -173,6 +173,14 @@ dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, 
  * Asynchronous on `stream`, no allocation. */
 dtst_status dtst_block_epilogue(dtst_plan_t p, const float* x, const float* w_bypass, float* y, void* stream);
 
+/* The block's last step in one call: the inverse partial DFT of yhat (as
+ * dtst_inverse) followed by the block epilogue (as dtst_block_epilogue),
+ *   y = GELU( w_bypass x + inverse(yhat) ),
+ * with the same arrays, layouts, alignment and overlap rules; both steps are
+ * enqueued on `stream` one after the other.  No allocation. */
+dtst_status dtst_inverse_block(dtst_plan_t p, const void* yhat, const float* x, const float* w_bypass, float* y,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---- instrumentation ----------------------------------------------------- */
 
 /* Per-kernel device time, for callers that time the path (benchmarks,

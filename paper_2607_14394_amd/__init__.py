@@ -17,6 +17,7 @@ __all__ = [
     "DtstError", "Desc", "lib", "make_desc", "dtst_desc_validate", "dtst_desc_workspace_bytes",
     "dtst_basis_host", "dtst_plan", "dtst_plan_destroy", "dtst_plan_info", "dtst_forward", "dtst_mix",
     "dtst_inverse", "dtst_forward_adj", "dtst_inverse_adj", "dtst_mix_wgrad", "dtst_block_epilogue",
+    "dtst_inverse_block",
     "dtst_profile_enable",
     "dtst_profile_collect", "Plan", "LIB_PATH",
 ]
@@ -76,6 +77,7 @@ def _load():
         "dtst_inverse_adj": [P, VP, VP, I, VP, SZ, VP],
         "dtst_mix_wgrad": [P, VP, VP, VP, I64, I64, I, VP],
         "dtst_block_epilogue": [P, VP, VP, VP, VP],
+        "dtst_inverse_block": [P, VP, VP, VP, VP, VP, SZ, VP],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -208,6 +210,11 @@ def dtst_block_epilogue(plan, x, w_bypass, y, stream=None):
     _check(lib.dtst_block_epilogue(plan, _ptr(x), _ptr(w_bypass), _ptr(y), _stream(stream)))
 
 
+def dtst_inverse_block(plan, yhat, x, w_bypass, y, ws, stream=None):
+    _check(lib.dtst_inverse_block(plan, _ptr(yhat), _ptr(x), _ptr(w_bypass), _ptr(y), *_wsargs(ws),
+                                  _stream(stream)))
+
+
 def dtst_mix_wgrad(plan, xhat, g_yhat, g_w_shard, m0, m1, accumulate, stream=None):
     _check(lib.dtst_mix_wgrad(plan, _ptr(xhat), _ptr(g_yhat), _ptr(g_w_shard), int(m0), int(m1), int(accumulate),
                               _stream(stream)))
@@ -306,6 +313,15 @@ class Plan:
         self._need(g_yhat, self.spectral_shape(self.desc.c_out), torch.complex64, "g_yhat")
         self._need(g_w, (m1 - m0, self.desc.c_in, self.desc.c_out), torch.complex64, "g_w")
         dtst_mix_wgrad(self.handle, xhat, g_yhat, g_w, m0, m1, accumulate, stream)
+
+    def inverse_block(self, yhat, x, w_bypass, y, stream=None):
+        """y = GELU(w_bypass x + inverse(yhat)) (the block's last step)."""
+        import torch
+        self._need(yhat, self.spectral_shape(self.desc.c_out), torch.complex64, "yhat")
+        self._need(x, self.spatial_shape(self.desc.c_in), torch.float32, "x")
+        self._need(w_bypass, (self.desc.c_out, self.desc.c_in), torch.float32, "w_bypass")
+        self._need(y, self.spatial_shape(self.desc.c_out), torch.float32, "y")
+        dtst_inverse_block(self.handle, yhat, x, w_bypass, y, self.ws, stream)
 
     def block_epilogue(self, x, w_bypass, y, stream=None):
         """y <- GELU(w_bypass x + y) in place (the block's bypass and activation)."""

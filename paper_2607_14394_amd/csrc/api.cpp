@@ -419,28 +419,63 @@ dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, 
   return device_status(e, "wgrad launch");
 }
 
-dtst_status dtst_block_epilogue(dtst_plan_t p, const float* x, const float* w_bypass, float* y, void* stream) {
-  DTST_TRY(check_plan(p));
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by the two block calls: pointers, the LDS limit on
+// the bypass matrix, and x not overlapping y (y is written while x is read).
+dtst_status check_block(const dtst_plan_st* p, const float* x, const float* w_bypass, const float* y) {
   const dtst::Derived& dv = p->dv;
-  if (dv.d.batch == 0) return ok();
   DTST_TRY(check_ptr(x, "x"));
   DTST_TRY(check_ptr(w_bypass, "w_bypass"));
   DTST_TRY(check_ptr(y, "y"));
   if (dv.d.c_in * dv.d.c_out * int64_t(sizeof(float)) > 160 * 1024)
     return fail(DTST_ERR_UNSUPPORTED, "c_in * c_out above 40960: the bypass matrix must fit in LDS");
   const int64_t V = dv.d.n_local[0] * dv.d.n_local[1] * dv.d.n_local[2] * dv.d.n_local[3];
-  // x must not overlap y (y is rewritten while x is still being read).
   const char* xb = reinterpret_cast<const char*>(x);
   const char* yb = reinterpret_cast<const char*>(y);
   const size_t xbytes = size_t(dv.d.batch) * dv.d.c_in * V * sizeof(float);
   const size_t ybytes = size_t(dv.d.batch) * dv.d.c_out * V * sizeof(float);
   if (xb < yb + ybytes && yb < xb + xbytes) return fail(DTST_ERR_INVALID_ARG, "x and y overlap");
-  DeviceGuard guard(p->device);
-  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  return ok();
+}
+
+dtst_status run_block_epilogue(const dtst_plan_st* p, const float* x, const float* w_bypass, float* y,
+                               void* stream) {
+  const dtst::Derived& dv = p->dv;
+  const int64_t V = dv.d.n_local[0] * dv.d.n_local[1] * dv.d.n_local[2] * dv.d.n_local[3];
   const int e = timed(K_BLOCK, stream, [&] {
     return dtst::launch_block_epilogue(x, w_bypass, y, dv.d.batch, dv.d.c_in, dv.d.c_out, V, stream);
   });
   return device_status(e, "block epilogue launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+dtst_status dtst_block_epilogue(dtst_plan_t p, const float* x, const float* w_bypass, float* y, void* stream) {
+  DTST_TRY(check_plan(p));
+  if (p->dv.d.batch == 0) return ok();
+  DTST_TRY(check_block(p, x, w_bypass, y));
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  return run_block_epilogue(p, x, w_bypass, y, stream);
+}
+
+dtst_status dtst_inverse_block(dtst_plan_t p, const void* yhat, const float* x, const float* w_bypass, float* y,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  DTST_TRY(check_plan(p));
+  const dtst::Derived& dv = p->dv;
+  if (dv.d.batch == 0) return ok();
+  DTST_TRY(check_ptr(yhat, "yhat"));
+  DTST_TRY(check_block(p, x, w_bypass, y));
+  DTST_TRY(check_ws(p, workspace, workspace_bytes));
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  DTST_TRY(run_inverse_chain(p, dv.d.c_out, yhat, y, workspace, p->blob + dv.img.t_inv, stream));
+  return run_block_epilogue(p, x, w_bypass, y, stream);
 }
 
 dtst_status dtst_profile_enable(int on) {

@@ -364,3 +364,35 @@ def test_block_epilogue_rejects_overlap():
         D.dtst_block_epilogue(plan.handle, buf, w, buf)
     assert e.value.status == 1
     plan.close()
+
+
+# (n_global, n_local, offset, kmax, kt, B, C_in, C_out): folded and sharded z,
+# many input channels, both k_t column layouts, scalar t.
+INVERSE_BLOCK_CASES = {
+    "fold": ((8, 6, 32, 32), (8, 6, 32, 32), (0, 0, 0, 0), (2, 2, 8), 5, 2, 3, 6),
+    "z_shard": ((8, 6, 64, 16), (8, 6, 32, 16), (0, 0, 16, 0), (2, 2, 4), 4, 1, 20, 16),
+    "many_inputs": ((4, 4, 32, 32), (4, 4, 32, 32), (0, 0, 0, 0), (1, 1, 4), 3, 1, 64, 16),
+    "kt12": ((4, 4, 16, 32), (4, 4, 16, 32), (0, 0, 0, 0), (1, 2, 4), 12, 1, 2, 3),
+    "nt21": ((4, 6, 8, 21), (4, 6, 8, 21), (0, 0, 0, 0), (2, 2, 2), 6, 2, 2, 2),
+}
+
+
+@pytest.mark.parametrize("name", list(INVERSE_BLOCK_CASES))
+def test_inverse_block(name):
+    """y = GELU(W x + inverse(yhat)) in one call against the oracle's
+    inverse followed by its block epilogue."""
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry(*INVERSE_BLOCK_CASES[name])
+    say(f"[inverse block {name}] n_global={g.n_global} n_local={g.n_local} kmax={g.kmax} kt={g.kt} "
+        f"B={g.batch} Cin={g.c_in} Cout={g.c_out}")
+    plan = D.Plan(desc_of(g))
+    yh = rand_cplx((g.batch, g.c_out) + g.K, 140)
+    x = rand_real((g.batch, g.c_in) + g.n_local, 141)
+    wb = (rand_real((g.c_out, g.c_in), 142) / np.sqrt(g.c_in)).astype(np.float32)
+    Y = Guarded(torch, plan.spatial_shape(g.c_out), torch.float32)
+    plan.inverse_block(dev(torch, yh), dev(torch, x), dev(torch, wb), Y.t)
+    torch.cuda.synchronize()
+    check(np_of(Y.t), O.block_epilogue(x, wb, O.inverse(yh, g)), "inverse + block epilogue")
+    assert Y.guards_intact()
+    plan.close()
