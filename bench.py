@@ -392,7 +392,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build runs every shard of the decomposition one after "
+        print("bench.py measures one GPU only: every shard of the decomposition runs one after "
               "another on a single MI355X (no collectives); run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 

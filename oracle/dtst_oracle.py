@@ -23,7 +23,7 @@ Distributed Spectral Neural Operators", arXiv 2607.14394):
                                    point-wise bypass W x added to the spectral
                                    output, through GELU
 
-Readings taken where the paper is silent (each is listed in the design doc):
+Readings taken where the paper is silent:
 
 * x, y, z keep {0..k-1} U {N-k..N-1} (Sec. III); t keeps {0..K_t-1} only, the
   half spectrum of a real signal (Table 3 contracts T 30 -> 16 for k_t = 16).
