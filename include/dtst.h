@@ -107,7 +107,15 @@ dtst_status dtst_basis_host(const dtst_desc* d, int dim, int kind, float* out, s
 
 /* Validate `d`, build every basis table on the host in fp64, round to fp32
  * and upload them to the current HIP device (synchronously).  The plan is
- * bound to that device.  On success *out receives the plan. */
+ * bound to that device.  On success *out receives the plan.
+ *
+ * The plan also fixes the kernel schedule of the forward-direction chain
+ * (dtst_forward, dtst_inverse_adj): where the shapes allow it (K_t <= 8, at
+ * most 16 z modes per fold class, N_t^loc <= 32 and a multiple of 4,
+ * K_y <= 32, K_z K_t <= 256) the t, z and y contractions run as one launch;
+ * otherwise t + z and y are separate launches.  Setting the environment
+ * variable DTST_SCHEDULE=split before dtst_plan keeps them separate (for
+ * comparing the two schedules); results agree to rounding. */
 dtst_status dtst_plan(const dtst_desc* d, dtst_plan_t* out);
 
 /* Free the plan's device tables.  Using a destroyed plan afterwards returns
@@ -188,7 +196,7 @@ dtst_status dtst_inverse_block(dtst_plan_t p, const void* yhat, const float* x, 
  * bracketed by a pair of HIP events recorded on the call's stream; nothing
  * else changes.  Process-wide; off by default. */
 typedef struct {
-  char name[40];     /* kernel role, e.g. "stream_fwd_tz", "axis_fwd_y", "mix", "block_epilogue" */
+  char name[40];     /* kernel role, e.g. "stream_fwd_tzy", "stream_fwd_tz", "axis_fwd_y", "mix" */
   int64_t launches;  /* launches collected */
   double total_ms;   /* summed event-to-event device time */
 } dtst_kernel_time;

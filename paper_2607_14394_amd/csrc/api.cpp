@@ -104,9 +104,10 @@ size_t w1_bytes(const dtst::Derived& dv) {
 
 // ---- per-kernel event timing (dtst_profile_enable / dtst_profile_collect) ----
 enum KernelRole { K_FWD_TZ, K_AXIS_FWD_Y, K_AXIS_FWD_X, K_AXIS_INV_X, K_AXIS_INV_Y, K_INV_ZT, K_MIX, K_MIX_H,
-                  K_WGRAD, K_BLOCK, K_COUNT };
+                  K_WGRAD, K_BLOCK, K_FWD_TZY, K_INV_YZT, K_COUNT };
 const char* const kRoleNames[K_COUNT] = {"stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "axis_inv_x", "axis_inv_y",
-                                         "stream_inv_zt", "mix", "mix_h", "wgrad", "block_epilogue"};
+                                         "stream_inv_zt", "mix", "mix_h", "wgrad", "block_epilogue",
+                                         "stream_fwd_tzy", "stream_inv_yzt"};
 
 struct Profiler {
   std::mutex mu;
@@ -161,7 +162,8 @@ int timed(int role, void* stream, F&& launch) {
   return e;
 }
 
-// Forward-direction chain: streaming t+z, then y, then x (with accumulate).
+// Forward-direction chain: streaming t+z, then y (one fused launch when the
+// plan allows it), then x (with accumulate).
 dtst_status run_forward_chain(const dtst_plan_st* p, int64_t channels, const float* x, void* xhat,
                               int accumulate, void* ws, const float* timg, void* stream) {
   const dtst::Derived& dv = p->dv;
@@ -169,14 +171,24 @@ dtst_status run_forward_chain(const dtst_plan_st* p, int64_t channels, const flo
   if (B == 0) return ok();
   char* w1 = static_cast<char*>(ws);
   char* w2 = w1 + w1_bytes(dv);
-  const int64_t rows = B * channels * dv.d.n_local[0] * dv.d.n_local[1];
-  int e = timed(K_FWD_TZ, stream,
-                [&] { return dtst::launch_fwd_tz(dv.sc, x, w1, rows, timg, p->blob + dv.img.z_fwd, stream); });
-  if (e != hipSuccess) return device_status(e, "t+z contraction launch");
-  e = timed(K_AXIS_FWD_Y, stream, [&] {
-    return dtst::launch_axis(dv.ay_f, B * channels * dv.d.n_local[0], w1, w2, p->blob + dv.img.y_fwd, 0, stream);
-  });
-  if (e != hipSuccess) return device_status(e, "y contraction launch");
+  const int64_t planes = B * channels * dv.d.n_local[0];
+  const int64_t rows = planes * dv.d.n_local[1];
+  int e;
+  if (dv.sc.fuse_y) {
+    e = timed(K_FWD_TZY, stream, [&] {
+      return dtst::launch_fwd_tzy(dv.sc, dv.ay_f, x, w2, planes, static_cast<int>(dv.d.n_local[1]), timg,
+                                  p->blob + dv.img.z_fwd, p->blob + dv.img.y_fwd, stream);
+    });
+    if (e != hipSuccess) return device_status(e, "t+z+y contraction launch");
+  } else {
+    e = timed(K_FWD_TZ, stream,
+              [&] { return dtst::launch_fwd_tz(dv.sc, x, w1, rows, timg, p->blob + dv.img.z_fwd, stream); });
+    if (e != hipSuccess) return device_status(e, "t+z contraction launch");
+    e = timed(K_AXIS_FWD_Y, stream, [&] {
+      return dtst::launch_axis(dv.ay_f, planes, w1, w2, p->blob + dv.img.y_fwd, 0, stream);
+    });
+    if (e != hipSuccess) return device_status(e, "y contraction launch");
+  }
   e = timed(K_AXIS_FWD_X, stream, [&] {
     return dtst::launch_axis(dv.ax_f, B * channels, w2, xhat, p->blob + dv.img.x_fwd, accumulate, stream);
   });
@@ -184,7 +196,8 @@ dtst_status run_forward_chain(const dtst_plan_st* p, int64_t channels, const flo
   return ok();
 }
 
-// Inverse-direction chain: x, then y, then streaming z+t with Re.
+// Inverse-direction chain: x, then y, then streaming z+t with Re (y, z and t
+// in one launch when the plan allows it).
 dtst_status run_inverse_chain(const dtst_plan_st* p, int64_t channels, const void* yhat, float* y, void* ws,
                               const float* timg, void* stream) {
   const dtst::Derived& dv = p->dv;
@@ -196,11 +209,20 @@ dtst_status run_inverse_chain(const dtst_plan_st* p, int64_t channels, const voi
     return dtst::launch_axis(dv.ax_i, B * channels, yhat, v1, p->blob + dv.img.x_inv, 0, stream);
   });
   if (e != hipSuccess) return device_status(e, "x expansion launch");
+  const int64_t planes = B * channels * dv.d.n_local[0];
+  if (dv.sc.fuse_y) {
+    e = timed(K_INV_YZT, stream, [&] {
+      return dtst::launch_inv_yzt(dv.sc, dv.ay_i, v1, y, planes, static_cast<int>(dv.d.n_local[1]), timg,
+                                  p->blob + dv.img.z_inv, p->blob + dv.img.y_inv, stream);
+    });
+    if (e != hipSuccess) return device_status(e, "y+z+t expansion launch");
+    return ok();
+  }
   e = timed(K_AXIS_INV_Y, stream, [&] {
-    return dtst::launch_axis(dv.ay_i, B * channels * dv.d.n_local[0], v1, v2, p->blob + dv.img.y_inv, 0, stream);
+    return dtst::launch_axis(dv.ay_i, planes, v1, v2, p->blob + dv.img.y_inv, 0, stream);
   });
   if (e != hipSuccess) return device_status(e, "y expansion launch");
-  const int64_t rows = B * channels * dv.d.n_local[0] * dv.d.n_local[1];
+  const int64_t rows = planes * dv.d.n_local[1];
   e = timed(K_INV_ZT, stream,
             [&] { return dtst::launch_inv_zt(dv.sc, v2, y, rows, timg, p->blob + dv.img.z_inv, stream); });
   if (e != hipSuccess) return device_status(e, "z+t expansion launch");

@@ -37,8 +37,17 @@ struct StreamCfg {
   int kcp = 0;  // padded slots per class = 8*mt
   int vec = 0;  // 1 when N_t % 4 == 0 (16-byte row chunks)
   size_t lds_bytes = 0;
+  // Fused t + z + y (fwd_tzy_kernel) and y + z + t (inv_yzt_kernel), used
+  // when fuse_y is set:
+  //   ncy        y classes: 2 when y is folded (slot = row pair), else 1
+  //   kyt        16-wide tiles of K_y per class: k tiles of the forward y
+  //              image, K steps of the inverse y image
+  //   fused_mrow LDS row stride (complex values) of the exchanged row results
+  int fuse_y = 0, ncy = 1, kyt = 1, fused_mrow = 0;
+  size_t fused_lds_bytes = 0;
   // filled at plan creation on the plan's device (prepare_stream)
   int grid_fwd = 0, grid_inv = 0;  // resident workgroups of each kernel
+  int grid_fused = 0;  // resident workgroups of fwd_tzy_kernel
 };
 
 // Generic complex contraction along a middle axis:
@@ -98,6 +107,16 @@ int64_t retained_index(const dtst_desc& d, int dim, int64_t p);
 int prepare_stream(StreamCfg* c);
 int launch_fwd_tz(const StreamCfg& c, const float* x, void* out, int64_t rows,
                   const float* timg, const float* zimg, void* stream);
+// Forward t + z + y of `planes` (b, c, x) planes of ny rows into the
+// (planes x K_y x K_z K_t) complex output; ay is the forward y contraction
+// whose image (yimg) supplies the y basis.
+int launch_fwd_tzy(const StreamCfg& c, const AxisCfg& ay, const float* x, void* out, int64_t planes, int ny,
+                   const float* timg, const float* zimg, const float* yimg, void* stream);
+// Inverse y + z + t of `planes` planes: (planes x K_y x K_z K_t) complex in,
+// (planes x ny x N_z x N_t) real out; ay is the inverse y expansion whose
+// image (yimg) supplies the y basis.
+int launch_inv_yzt(const StreamCfg& c, const AxisCfg& ay, const void* in, float* y, int64_t planes, int ny,
+                   const float* timg, const float* zimg, const float* yimg, void* stream);
 int launch_inv_zt(const StreamCfg& c, const void* in, float* y, int64_t rows,
                   const float* timg, const float* zimg, void* stream);
 int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const float* img,

@@ -136,62 +136,171 @@ __device__ __forceinline__ void unfold_classes(v4f (&E)[NCLS][CT]) {
 // ---------------------------------------------------------------------------
 // Forward: x (rows x N_z x N_t) fp32 -> out (rows x K_z x K_t) complex.
 //
-// Every wave walks its (row, z-tile) pairs in order and keeps the next
-// pair's loads in flight while it computes the current one.  Loads are
-// unconditional (out-of-range lanes read the row start) and masked when the
-// values are used, so nothing between the loads and the MFMAs forces an
-// early wait.  Within a tile the independent accumulator chains are
-// interleaved step by step.
-// ---------------------------------------------------------------------------
+// A row is taken in z tiles (16 z per class).  load_tile fetches one tile,
+// tz_tile contracts its t then z into the row's accumulators, and tz_finish
+// turns the accumulators of a finished row into complex coefficients.
 // MODE 0: scalar loads (N_t % 4 != 0); 1: 16-byte loads with masks;
-// 2: 16-byte loads of complete tiles, no masks.
+// 2: 16-byte loads of complete tiles, no masks.  Loads are unconditional
+// (out-of-range lanes read the row start) and masked when the values are
+// used, so nothing between the loads and the MFMAs forces an early wait.
+// ---------------------------------------------------------------------------
+template <int TH, int NCLS, int MODE>
+__device__ __forceinline__ void load_tile(const float* __restrict__ x, const StreamArgs& a, int m, int g, int64_t r,
+                                          int zt, float (&dst)[NCLS][TH][4], bool (&ok)[NCLS][TH * 4]) {
+  const float* xr = x + r * (int64_t(a.nz) * a.nt);
+  const int zl = zt * 16 + m;
+  const bool zok = zl < a.zh;
+#pragma unroll
+  for (int hf = 0; hf < NCLS; ++hf) {
+    const int64_t zoff = int64_t(zl + hf * a.zh) * a.nt;
+#pragma unroll
+    for (int h = 0; h < TH; ++h) {
+      if (MODE == 2) {
+        const float4 v = *reinterpret_cast<const float4*>(xr + zoff + 16 * h + 4 * g);
+        dst[hf][h][0] = v.x; dst[hf][h][1] = v.y; dst[hf][h][2] = v.z; dst[hf][h][3] = v.w;
+        ok[hf][4 * h] = true;
+      } else if (MODE == 1) {
+        const int t0 = 16 * h + 4 * g;
+        const bool v_ok = zok && t0 < a.nt;
+        const float4 v = *reinterpret_cast<const float4*>(xr + (v_ok ? zoff + t0 : 0));
+        dst[hf][h][0] = v.x; dst[hf][h][1] = v.y; dst[hf][h][2] = v.z; dst[hf][h][3] = v.w;
+        ok[hf][4 * h] = v_ok;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int t = 16 * h + 4 * g + j;
+          const bool v_ok = zok && t < a.nt;
+          dst[hf][h][j] = xr[v_ok ? zoff + t : 0];
+          ok[hf][4 * h + j] = v_ok;
+        }
+      }
+    }
+  }
+}
+
+// Contracts t of the tile held in xv (z = 16zt + m and the partner z of
+// every other class) into V, then folds the classes.
+template <int CT, int TH, int NCLS, int MODE>
+__device__ __forceinline__ void t_part(const float (&xv)[NCLS][TH][4], const bool (&ok)[NCLS][TH * 4],
+                                       const float (&bt)[TH * 4][CT], v4f (&V)[NCLS][CT]) {
+#pragma unroll
+  for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) V[hf][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int h = 0; h < TH; ++h)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int hf = 0; hf < NCLS; ++hf) {
+        const float xa = (MODE == 2 || ok[hf][MODE == 1 ? 4 * h : 4 * h + j]) ? xv[hf][h][j] : 0.f;
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) V[hf][ct] = mfma(xa, bt[h * 4 + j][ct], V[hf][ct]);
+      }
+  fold_classes<NCLS, CT>(V);
+}
+
+// Contracts z of the t-contracted tile V (z tile zt) into P; P is cleared
+// first when zt == 0.  Accumulator register i of V is the B operand of the
+// step whose K index is z = 16zt + 4g + i.
+template <int CT, int MT, int NCLS>
+__device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* lds, const StreamArgs& a, int zt,
+                                       int lane, v4f (&P)[NCLS][MT][CT]) {
+  float4 A[NCLS][MT];
+#pragma unroll
+  for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) A[cl][mt] = lds[((cl * a.zt + zt) * MT + mt) * 64 + lane];
+  if (zt == 0) {
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = mfma(A[cl][mt][i], V[cl][ct][i], P[cl][mt][ct]);
+}
+
+// Contracts t, then z, of the tile (z tile zt) held in xv into P.  Within the
+// tile the independent accumulator chains are interleaved step by step.
+template <int CT, int TH, int MT, int NCLS, int MODE>
+__device__ __forceinline__ void tz_tile(const float (&xv)[NCLS][TH][4], const bool (&ok)[NCLS][TH * 4],
+                                        const float (&bt)[TH * 4][CT], const float4* lds, const StreamArgs& a,
+                                        int zt, int lane, v4f (&P)[NCLS][MT][CT]) {
+  v4f V[NCLS][CT];
+  t_part<CT, TH, NCLS, MODE>(xv, ok, bt, V);
+  z_part<CT, MT, NCLS>(V, lds, a, zt, lane, P);
+}
+
+// Combines the real-stacked products of a finished row into complex
+// coefficients and hands each one to st(index p * K_t + k_t, re, im):
+// (Re B) V and (Im B) V sit in row tiles mt and mt + MT/2 of the same lane;
+// the Re / Im columns of k_t sit 8 lanes apart (CT = 1) or in the two
+// column tiles (CT = 2).
+template <int CT, int MT, int NCLS, class Store>
+__device__ __forceinline__ void tz_finish(const v4f (&P)[NCLS][MT][CT], const StreamArgs& a, int m, int g,
+                                          Store&& st) {
+  constexpr int KTP = 8 * CT;
+  if constexpr (CT == 1) {
+    static_assert(NCLS <= 2, "the four-class z fold needs CT = 2");
+    // Lanes m < 8 finish mode p0 (k_t = m), lanes m >= 8 the next mode
+    // p0 + 1 (k_t = m - 8): z class 1 of the same slot when folded, else
+    // the next accumulator register.  Each lane pair trades the values the
+    // other half needs, so every store instruction covers whole 128-byte
+    // rows of two adjacent modes.
+    const bool hi = m >= KTP;
+    const int kc = hi ? m - KTP : m;
+#pragma unroll
+    for (int mr = 0; mr < MT / 2; ++mr)
+#pragma unroll
+      for (int j = 0; j < (NCLS == 2 ? 4 : 2); ++j) {
+        const int i0 = NCLS == 2 ? j : 2 * j, i1 = NCLS == 2 ? j : 2 * j + 1;
+        const int c1 = NCLS - 1;
+        const float q0 = P[0][mr][0][i0], u0 = P[0][mr + MT / 2][0][i0];
+        const float q1 = P[c1][mr][0][i1], u1 = P[c1][mr + MT / 2][0][i1];
+        const float rq = ror8(hi ? q0 : q1);
+        const float ru = ror8(hi ? u0 : u1);
+        const float re = hi ? rq - u1 : q0 - ru;
+        const float im = hi ? q1 + ru : rq + u0;
+        const int p = (NCLS == 2 ? 2 * (16 * mr + 4 * g + i0) : 16 * mr + 4 * g + i0) + (hi ? 1 : 0);
+        if (kc < a.kt && p < a.kz) st(p * a.kt + kc, re, im);
+      }
+  } else {
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int mr = 0; mr < MT / 2; ++mr)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int p = (16 * mr + 4 * g + i) * NCLS + cl;
+          const float rr = P[cl][mr][0][i], ri = P[cl][mr][CT - 1][i];
+          const float ir = P[cl][mr + MT / 2][0][i], ii = P[cl][mr + MT / 2][CT - 1][i];
+          if (m < a.kt && p < a.kz) st(p * a.kt + m, rr - ii, ri + ir);
+        }
+  }
+}
+
+// Every wave walks its (row, z-tile) pairs in order and keeps the next
+// pair's loads in flight while it computes the current one.
 template <int CT, int TH, int MT, int NCLS, int MODE>
 __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2* __restrict__ out,
                                             const float (&bt)[TH * 4][CT], const float4* lds,
                                             const StreamArgs& a, int64_t wave, int64_t wstride) {
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
-  constexpr int KTP = 8 * CT;
-  const int64_t row_len = int64_t(a.nz) * a.nt;
   const int64_t n_iter = ((a.rows - 1 - wave) / wstride + 1) * a.zt;
-
-  // Load the tile of (row r, z-tile zt) into dst; ok[hf][4h] (MODE 1) or
-  // ok[hf][4h + j] (scalar) records which values are inside the row.
-  auto load_tile = [&](int64_t r, int zt, float (&dst)[NCLS][TH][4], bool (&ok)[NCLS][TH * 4]) {
-    const float* xr = x + r * row_len;
-    const int zl = zt * 16 + m;
-    const bool zok = zl < a.zh;
-#pragma unroll
-    for (int hf = 0; hf < NCLS; ++hf) {
-      const int64_t zoff = int64_t(zl + hf * a.zh) * a.nt;
-#pragma unroll
-      for (int h = 0; h < TH; ++h) {
-        if (MODE == 2) {
-          const float4 v = *reinterpret_cast<const float4*>(xr + zoff + 16 * h + 4 * g);
-          dst[hf][h][0] = v.x; dst[hf][h][1] = v.y; dst[hf][h][2] = v.z; dst[hf][h][3] = v.w;
-          ok[hf][4 * h] = true;
-        } else if (MODE == 1) {
-          const int t0 = 16 * h + 4 * g;
-          const bool v_ok = zok && t0 < a.nt;
-          const float4 v = *reinterpret_cast<const float4*>(xr + (v_ok ? zoff + t0 : 0));
-          dst[hf][h][0] = v.x; dst[hf][h][1] = v.y; dst[hf][h][2] = v.z; dst[hf][h][3] = v.w;
-          ok[hf][4 * h] = v_ok;
-        } else {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int t = 16 * h + 4 * g + j;
-            const bool v_ok = zok && t < a.nt;
-            dst[hf][h][j] = xr[v_ok ? zoff + t : 0];
-            ok[hf][4 * h + j] = v_ok;
-          }
-        }
-      }
-    }
-  };
 
   float xn[NCLS][TH][4];
   bool okn[NCLS][TH * 4];
-  load_tile(wave, 0, xn, okn);
+  load_tile<TH, NCLS, MODE>(x, a, m, g, wave, 0, xn, okn);
   int64_t rn = wave;
   int ztn = 0;
   v4f P[NCLS][MT][CT];
@@ -214,96 +323,198 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
       ztn = 0;
       rn += wstride;
     }
-    if (it + 1 < n_iter) load_tile(rn, ztn, xn, okn);
+    if (it + 1 < n_iter) load_tile<TH, NCLS, MODE>(x, a, m, g, rn, ztn, xn, okn);
 
-    // z basis of this tile (independent of the loads).
-    float4 A[NCLS][MT];
-#pragma unroll
-    for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) A[cl][mt] = lds[((cl * a.zt + zt) * MT + mt) * 64 + lane];
+    tz_tile<CT, TH, MT, NCLS, MODE>(xv, ok, bt, lds, a, zt, lane, P);
+    if (zt != a.zt - 1) continue;
 
-    if (zt == 0) {
-#pragma unroll
-      for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+    float2* orow = out + r * int64_t(a.kz) * a.kt;
+    tz_finish<CT, MT, NCLS>(P, a, m, g, [&](int idx, float re, float im) { orow[idx] = make_float2(re, im); });
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Forward t + z + y in one pass (used when the y contraction fits: K_t <= 8,
+// at most 16 z modes per class, K_y <= 32, K_z K_t <= 256).
+//
+// A workgroup of 16 waves owns one (b, c, x) plane at a time (persistent over
+// planes).  The plane's y rows come in groups of 16 slots: with y folded (the
+// shard holds the whole even N_y) a slot is the row pair (y, y + N_y/2),
+// otherwise a single row.  Wave w contracts t and z of the row(s) of slot w
+// exactly as fwd_tz_body does and leaves the (K_z x K_t) results in LDS.
+// After a barrier, wave w < ceil(K_z K_t / 16) contracts y for the columns
+// 16w..16w+15 of every slot of the group (the slots are the MFMA K index, the
+// y basis image of the separate y contraction supplies the A operand; folded,
+// even modes take the pair's sum and odd modes its difference), accumulating
+// over the plane's groups in registers; a second barrier frees the LDS rows.
+// The (K_y x K_z K_t) result of the plane is written once.  The shard is read
+// once and the (N_y x K_z K_t) intermediate never reaches HBM.
+// ---------------------------------------------------------------------------
+struct FusedArgs {
+  int64_t planes;  // B * C * N_x
+  int ny;          // local N_y (rows per plane)
+  int slots;       // slots per plane: N_y / 2 folded, else N_y
+  int half;        // N_y / 2 folded (second row of a slot), else 0
+  int jq;          // groups of 16 slots per plane
+  int kth;         // k tiles per y class in the y image
+  int ky;          // K_y
+  int mcols;       // K_z * K_t
+  int mrow;        // LDS row stride in complex values
+  int nwy;         // waves running the y contraction: ceil(mcols / 16)
+  int yimg_n4;     // float4 entries of the y image (staged in LDS after the row exchange)
+};
+
+template <int TH, int NCLS, int MODE, int NCY, int KYT>
+__global__ void __launch_bounds__(1024)
+fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const float* __restrict__ timg,
+               const float4* __restrict__ zimg, const float4* __restrict__ yimg, StreamArgs a, FusedArgs f) {
+  constexpr int CT = 1, MT = 2;
+  extern __shared__ float4 lds[];
+  const int nimg = NCLS * a.zt * MT * 64;
+  float2* vlds = reinterpret_cast<float2*>(lds + nimg);
+  const int lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  const int w = threadIdx.x >> 6;
+  if (blockIdx.x >= f.planes) return;  // the host never launches more workgroups than planes
+
+  // Position of a tile: (plane, slot group, row of the slot, z tile).
+  struct Cur {
+    int64_t pl;
+    int q, h, zt;
+  };
+  auto advance = [&](Cur c) {
+    if (++c.zt == a.zt) {
+      c.zt = 0;
+      if (++c.h == NCY) {
+        c.h = 0;
+        if (++c.q == f.jq) {
+          c.q = 0;
+          c.pl += gridDim.x;
+        }
+      }
     }
+    return c;
+  };
+  // Row of a tile for this wave; slots past the plane's end read its first
+  // row and contribute zeros.
+  auto row_of = [&](const Cur& c, bool* valid) {
+    const int s = 16 * c.q + w;
+    *valid = s < f.slots;
+    return c.pl * f.ny + (*valid ? s + c.h * f.half : 0);
+  };
 
-    // Contract t for z = 16zt + m (and z + N_z/2 when folded).
-    v4f V[NCLS][CT];
+  // One tile ahead: the next tile's loads are in flight while the current
+  // one is contracted.  The first loads go out before the z image is staged.
+  Cur cur{static_cast<int64_t>(blockIdx.x), 0, 0, 0};
+  bool valid;
+  float xn[NCLS][TH][4];
+  bool okn[NCLS][TH * 4];
+  load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cur, &valid), 0, xn, okn);
+
+  // LDS: z image, the exchanged row results, the y image.
+  float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
+  for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
+  for (int i = threadIdx.x; i < f.yimg_n4; i += blockDim.x) ylds[i] = yimg[i];
+  __syncthreads();
+
+  float bt[TH * 4][CT];
+#pragma unroll
+  for (int s = 0; s < TH * 4; ++s) bt[s][0] = timg[s * 64 + lane];
+
+  v4f yr[NCY][KYT], yi[NCY][KYT];
+#pragma unroll
+  for (int c = 0; c < NCY; ++c)
+#pragma unroll
+    for (int k = 0; k < KYT; ++k) {
+      yr[c][k] = v4f{0.f, 0.f, 0.f, 0.f};
+      yi[c][k] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
+  v4f P[NCLS][MT][CT];
+
+  while (true) {
+    float xv[NCLS][TH][4];
+    bool ok[NCLS][TH * 4];
 #pragma unroll
     for (int hf = 0; hf < NCLS; ++hf)
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct) V[hf][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int hh = 0; hh < TH; ++hh)
 #pragma unroll
-    for (int h = 0; h < TH; ++h)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int hf = 0; hf < NCLS; ++hf) {
-          const float xa = (MODE == 2 || ok[hf][MODE == 1 ? 4 * h : 4 * h + j]) ? xv[hf][h][j] : 0.f;
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) V[hf][ct] = mfma(xa, bt[h * 4 + j][ct], V[hf][ct]);
+        for (int j = 0; j < 4; ++j) {
+          xv[hf][hh][j] = xn[hf][hh][j];
+          ok[hf][4 * hh + j] = okn[hf][4 * hh + j];
         }
-    fold_classes<NCLS, CT>(V);
-    // Contract z: accumulator register i of V is the B operand of the
-    // step whose K index is z = 16zt + 4g + i.
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = mfma(A[cl][mt][i], V[cl][ct][i], P[cl][mt][ct]);
+    const Cur c = cur;
+    const bool c_valid = valid;
+    cur = advance(cur);
+    if (cur.pl < f.planes) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cur, &valid), cur.zt, xn, okn);
 
-    if (zt != a.zt - 1) continue;
-
-    // Combine the real-stacked products into complex coefficients:
-    // (Re B) V and (Im B) V sit in row tiles mt and mt + MT/2 of the same lane;
-    // the Re / Im columns of k_t sit 8 lanes apart (CT = 1) or in the two
-    // column tiles (CT = 2).
-    float2* orow = out + r * int64_t(a.kz) * a.kt;
-    if constexpr (CT == 1) {
-      static_assert(NCLS <= 2, "the four-class z fold needs CT = 2");
-      // Lanes m < 8 finish mode p0 (k_t = m), lanes m >= 8 the next mode
-      // p0 + 1 (k_t = m - 8): z class 1 of the same slot when folded, else
-      // the next accumulator register.  Each lane pair trades the values the
-      // other half needs, and every store instruction writes whole 128-byte
-      // rows of two adjacent modes.
-      const bool hi = m >= KTP;
-      const int kc = hi ? m - KTP : m;
+    tz_tile<CT, TH, MT, NCLS, MODE>(xv, ok, bt, lds, a, c.zt, lane, P);
+    if (c.zt == a.zt - 1) {
+      // Row done: leave its results in LDS; after the group's last row,
+      // contract y over the group's slots.
+      float2* vrow = vlds + (c.h * 16 + w) * f.mrow;
+      tz_finish<CT, MT, NCLS>(P, a, m, g, [&](int idx, float re, float im) {
+        vrow[idx] = c_valid ? make_float2(re, im) : make_float2(0.f, 0.f);
+      });
+      if (c.h == NCY - 1) {
+        __syncthreads();
+        if (w < f.nwy) {
+          const int mc = 16 * w + m;
+          float4 br[NCY][KYT], bi[NCY][KYT];
 #pragma unroll
-      for (int mr = 0; mr < MT / 2; ++mr)
+          for (int cl = 0; cl < NCY; ++cl)
 #pragma unroll
-        for (int j = 0; j < (NCLS == 2 ? 4 : 2); ++j) {
-          const int i0 = NCLS == 2 ? j : 2 * j, i1 = NCLS == 2 ? j : 2 * j + 1;
-          const int c1 = NCLS - 1;
-          const float q0 = P[0][mr][0][i0], u0 = P[0][mr + MT / 2][0][i0];
-          const float q1 = P[c1][mr][0][i1], u1 = P[c1][mr + MT / 2][0][i1];
-          const float rq = ror8(hi ? q0 : q1);
-          const float ru = ror8(hi ? u0 : u1);
-          const float re = hi ? rq - u1 : q0 - ru;
-          const float im = hi ? q1 + ru : rq + u0;
-          const int p = (NCLS == 2 ? 2 * (16 * mr + 4 * g + i0) : 16 * mr + 4 * g + i0) + (hi ? 1 : 0);
-          if (kc < a.kt && p < a.kz) orow[p * a.kt + kc] = make_float2(re, im);
-        }
-    } else {
-#pragma unroll
-      for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-        for (int mr = 0; mr < MT / 2; ++mr)
+            for (int k = 0; k < KYT; ++k) {
+              const int kt = NCY == 2 ? cl * f.kth + k : k;
+              const float4* ip = ylds + (kt * f.jq + c.q) * 2 * 64 + lane;
+              br[cl][k] = ip[0];
+              bi[cl][k] = ip[64];
+            }
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int p = (16 * mr + 4 * g + i) * NCLS + cl;
-            const float rr = P[cl][mr][0][i], ri = P[cl][mr][CT - 1][i];
-            const float ir = P[cl][mr + MT / 2][0][i], ii = P[cl][mr + MT / 2][CT - 1][i];
-            if (m < a.kt && p < a.kz) orow[p * a.kt + m] = make_float2(rr - ii, ri + ir);
+            const int s = 4 * g + i;
+            const float2 va = vlds[s * f.mrow + mc];
+            float2 xs[NCY];
+            if constexpr (NCY == 2) {
+              const float2 vbv = vlds[(16 + s) * f.mrow + mc];
+              xs[0] = make_float2(va.x + vbv.x, va.y + vbv.y);
+              xs[1] = make_float2(va.x - vbv.x, va.y - vbv.y);
+            } else {
+              xs[0] = va;
+            }
+#pragma unroll
+            for (int cl = 0; cl < NCY; ++cl)
+#pragma unroll
+              for (int k = 0; k < KYT; ++k) {
+                yr[cl][k] = mfma(br[cl][k][i], xs[cl].x, yr[cl][k]);
+                yi[cl][k] = mfma(br[cl][k][i], xs[cl].y, yi[cl][k]);
+                yr[cl][k] = mfma(bi[cl][k][i], -xs[cl].y, yr[cl][k]);
+                yi[cl][k] = mfma(bi[cl][k][i], xs[cl].x, yi[cl][k]);
+              }
           }
+          if (c.q == f.jq - 1) {
+            // Plane done: rows p of K_y (class cl, slot 16k + 4g + i), columns mc.
+            float2* op = out + c.pl * int64_t(f.ky) * f.mcols;
+#pragma unroll
+            for (int cl = 0; cl < NCY; ++cl)
+#pragma unroll
+              for (int k = 0; k < KYT; ++k) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                  const int sl = 16 * k + 4 * g + i;
+                  const int p = NCY == 2 ? 2 * sl + cl : sl;
+                  if (p < f.ky && mc < f.mcols)
+                    op[int64_t(p) * f.mcols + mc] = make_float2(yr[cl][k][i], yi[cl][k][i]);
+                }
+                yr[cl][k] = v4f{0.f, 0.f, 0.f, 0.f};
+                yi[cl][k] = v4f{0.f, 0.f, 0.f, 0.f};
+              }
+          }
+        }
+        __syncthreads();
+      }
     }
+    if (cur.pl >= f.planes) break;
   }
 }
 
@@ -339,143 +550,160 @@ fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
 // ---------------------------------------------------------------------------
 // Inverse: in (rows x K_z x K_t) complex -> y (rows x N_z x N_t) fp32.
 //
-// Each row's spectrum is loaded one row ahead.  Per z-tile the z expansion
-// (one accumulator chain per class and column tile), the unfold, and the t
-// expansion (one chain per output tile) run as interleaved MFMA phases; all
-// stores of the tile follow them.
-// ---------------------------------------------------------------------------
+// load_u fetches the spectrum values of one row that this lane needs,
+// build_a arranges them as the A operand of the z expansion, and inv_row runs,
+// per z-tile, the z expansion (one accumulator chain per class and column
+// tile), the unfold, and the t expansion (one chain per output tile) as
+// interleaved MFMA phases, with all stores of the tile after them.
 // MODE 0: scalar stores (N_t % 4 != 0); 1: 16-byte stores with masks;
 // 2: 16-byte stores of complete tiles, no masks.
+// ---------------------------------------------------------------------------
+// Spectrum values this lane needs from one row: slot s = 16qh + 4g + i of
+// class cl at k_t column c = 16ct + m (Re and Im columns read the same value).
+template <int CT, int MT, int NCLS>
+__device__ __forceinline__ void load_u(const float2* urow, const StreamArgs& a, int m, int g,
+                                       float2 (&dst)[NCLS][CT][MT / 2][4], bool (&ok)[NCLS][CT][MT / 2][4]) {
+  constexpr int KTP = 8 * CT;
+#pragma unroll
+  for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int qh = 0; qh < MT / 2; ++qh)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int s = 16 * qh + 4 * g + i;
+          const int p = s * NCLS + cl;
+          const int c = 16 * ct + m;
+          const int kt = c < KTP ? c : c - KTP;
+          const bool v_ok = p < a.kz && kt < a.kt;
+          dst[cl][ct][qh][i] = urow[v_ok ? p * a.kt + kt : 0];
+          ok[cl][ct][qh][i] = v_ok;
+        }
+}
+
+// A operand of the z expansion (rows c, K index kz' = 16q + 4g + i):
+// kz' < KCP pairs with Re C_z, kz' >= KCP with Im C_z.
+template <int CT, int MT, int NCLS>
+__device__ __forceinline__ void build_a(const float2 (&u)[NCLS][CT][MT / 2][4], const bool (&ok)[NCLS][CT][MT / 2][4],
+                                        int m, float (&A)[NCLS][CT][MT][4]) {
+  constexpr int KTP = 8 * CT;
+#pragma unroll
+  for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int qh = 0; qh < MT / 2; ++qh)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool is_re = 16 * ct + m < KTP;
+          const float2 v = ok[cl][ct][qh][i] ? u[cl][ct][qh][i] : make_float2(0.f, 0.f);
+          A[cl][ct][qh][i] = is_re ? v.x : v.y;
+          A[cl][ct][qh + MT / 2][i] = is_re ? -v.y : v.x;
+        }
+}
+
+template <int CT, int TH, int MT, int NCLS, int MODE>
+__device__ __forceinline__ void inv_row(const float (&A)[NCLS][CT][MT][4], float* __restrict__ yrow,
+                                        const float (&ta)[TH][CT][4], const float4* lds, const StreamArgs& a,
+                                        int lane) {
+  const int m = lane & 15, g = lane >> 4;
+  for (int zt = 0; zt < a.zt; ++zt) {
+    float4 B[NCLS][MT];
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int q = 0; q < MT; ++q) B[cl][q] = lds[((cl * a.zt + zt) * MT + q) * 64 + lane];
+
+    v4f W[NCLS][CT];
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) W[cl][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < MT; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) W[cl][ct] = mfma(A[cl][ct][q][i], B[cl][q][i], W[cl][ct]);
+    unfold_classes<NCLS, CT>(W);
+    v4f Y[NCLS][TH];
+#pragma unroll
+    for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+      for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+          for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = mfma(ta[mt][ct][i], W[hf][ct][i], Y[hf][mt]);
+
+    const int zl = zt * 16 + m;
+    const bool zok = zl < a.zh;
+    if (MODE != 0 && TH == 2 && a.nt == 32) {
+      // Rows of exactly 32 floats: lanes m and m^8 trade one 16-byte
+      // chunk (DPP row rotate by 8) so that each store instruction writes
+      // 8 whole 128-byte rows instead of 16 half rows.
+      const bool lo = m < 8;
+      const int za = zt * 16 + (m & 7), zb = za + 8;
+      const int tch = (lo ? 0 : 16) + 4 * g;
+#pragma unroll
+      for (int hf = 0; hf < NCLS; ++hf) {
+        float va[4], vb[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float send = lo ? Y[hf][TH - 1][i] : Y[hf][0][i];
+          const float recv = ror8(send);
+          va[i] = lo ? Y[hf][0][i] : recv;
+          vb[i] = lo ? recv : Y[hf][TH - 1][i];
+        }
+        if (MODE == 2 || za < a.zh) store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
+        if (MODE == 2 || zb < a.zh) store_stream(yrow + int64_t(zb + hf * a.zh) * a.nt + tch, vb[0], vb[1], vb[2], vb[3]);
+      }
+      continue;
+    }
+#pragma unroll
+    for (int hf = 0; hf < NCLS; ++hf) {
+      float* dst = yrow + int64_t(zl + hf * a.zh) * a.nt;
+#pragma unroll
+      for (int mt = 0; mt < TH; ++mt) {
+        const int t0 = 16 * mt + 4 * g;
+        if (MODE != 0) {
+          if (MODE == 2 || (zok && t0 < a.nt))
+            store_stream(dst + t0, Y[hf][mt][0], Y[hf][mt][1], Y[hf][mt][2], Y[hf][mt][3]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (zok && t0 + i < a.nt) __builtin_nontemporal_store(Y[hf][mt][i], dst + t0 + i);
+        }
+      }
+    }
+  }
+}
+
+// Each row's spectrum is loaded one row ahead.
 template <int CT, int TH, int MT, int NCLS, int MODE>
 __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float* __restrict__ y,
                                             const float (&ta)[TH][CT][4], const float4* lds,
                                             const StreamArgs& a, int64_t wave, int64_t wstride) {
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
-  constexpr int KTP = 8 * CT;
   const int64_t row_len = int64_t(a.nz) * a.nt;
-
-  // Spectrum values this lane needs from one row: slot s = 16qh + 4g + i of
-  // class cl at k_t column c = 16ct + m (Re and Im columns read the same value).
-  auto load_u = [&](int64_t r, float2 (&dst)[NCLS][CT][MT / 2][4], bool (&ok)[NCLS][CT][MT / 2][4]) {
-    const float2* urow = in + r * int64_t(a.kz) * a.kt;
-#pragma unroll
-    for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-        for (int qh = 0; qh < MT / 2; ++qh)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int s = 16 * qh + 4 * g + i;
-            const int p = s * NCLS + cl;
-            const int c = 16 * ct + m;
-            const int kt = c < KTP ? c : c - KTP;
-            const bool v_ok = p < a.kz && kt < a.kt;
-            dst[cl][ct][qh][i] = urow[v_ok ? p * a.kt + kt : 0];
-            ok[cl][ct][qh][i] = v_ok;
-          }
-  };
+  const int64_t spec_len = int64_t(a.kz) * a.kt;
 
   float2 un[NCLS][CT][MT / 2][4];
   bool okn[NCLS][CT][MT / 2][4];
-  load_u(wave, un, okn);
+  load_u<CT, MT, NCLS>(in + wave * spec_len, a, m, g, un, okn);
   for (int64_t r = wave; r < a.rows; r += wstride) {
-    // A operand of the z expansion (rows c, K index kz' = 16q + 4g + i):
-    // kz' < KCP pairs with Re C_z, kz' >= KCP with Im C_z.
     float A[NCLS][CT][MT][4];
-#pragma unroll
-    for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-        for (int qh = 0; qh < MT / 2; ++qh)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const bool is_re = 16 * ct + m < KTP;
-            const float2 u = okn[cl][ct][qh][i] ? un[cl][ct][qh][i] : make_float2(0.f, 0.f);
-            A[cl][ct][qh][i] = is_re ? u.x : u.y;
-            A[cl][ct][qh + MT / 2][i] = is_re ? -u.y : u.x;
-          }
-    if (r + wstride < a.rows) load_u(r + wstride, un, okn);
-
-    float* yrow = y + r * row_len;
-    for (int zt = 0; zt < a.zt; ++zt) {
-      float4 B[NCLS][MT];
-#pragma unroll
-      for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-        for (int q = 0; q < MT; ++q) B[cl][q] = lds[((cl * a.zt + zt) * MT + q) * 64 + lane];
-
-      v4f W[NCLS][CT];
-#pragma unroll
-      for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) W[cl][ct] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int q = 0; q < MT; ++q)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct) W[cl][ct] = mfma(A[cl][ct][q][i], B[cl][q][i], W[cl][ct]);
-      unfold_classes<NCLS, CT>(W);
-      v4f Y[NCLS][TH];
-#pragma unroll
-      for (int hf = 0; hf < NCLS; ++hf)
-#pragma unroll
-        for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int hf = 0; hf < NCLS; ++hf)
-#pragma unroll
-            for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = mfma(ta[mt][ct][i], W[hf][ct][i], Y[hf][mt]);
-
-      const int zl = zt * 16 + m;
-      const bool zok = zl < a.zh;
-      if (MODE != 0 && TH == 2 && a.nt == 32) {
-        // Rows of exactly 32 floats: lanes m and m^8 trade one 16-byte
-        // chunk (DPP row rotate by 8) so that each store instruction writes
-        // 8 whole 128-byte rows instead of 16 half rows.
-        const bool lo = m < 8;
-        const int za = zt * 16 + (m & 7), zb = za + 8;
-        const int tch = (lo ? 0 : 16) + 4 * g;
-#pragma unroll
-        for (int hf = 0; hf < NCLS; ++hf) {
-          float va[4], vb[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float send = lo ? Y[hf][TH - 1][i] : Y[hf][0][i];
-            const float recv = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(send), 0x128, 0xf, 0xf, false));
-            va[i] = lo ? Y[hf][0][i] : recv;
-            vb[i] = lo ? recv : Y[hf][TH - 1][i];
-          }
-          if (MODE == 2 || za < a.zh) store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
-          if (MODE == 2 || zb < a.zh) store_stream(yrow + int64_t(zb + hf * a.zh) * a.nt + tch, vb[0], vb[1], vb[2], vb[3]);
-        }
-        continue;
-      }
-#pragma unroll
-      for (int hf = 0; hf < NCLS; ++hf) {
-        float* dst = yrow + int64_t(zl + hf * a.zh) * a.nt;
-#pragma unroll
-        for (int mt = 0; mt < TH; ++mt) {
-          const int t0 = 16 * mt + 4 * g;
-          if (MODE != 0) {
-            if (MODE == 2 || (zok && t0 < a.nt))
-              store_stream(dst + t0, Y[hf][mt][0], Y[hf][mt][1], Y[hf][mt][2], Y[hf][mt][3]);
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if (zok && t0 + i < a.nt) __builtin_nontemporal_store(Y[hf][mt][i], dst + t0 + i);
-          }
-        }
-      }
-    }
+    build_a<CT, MT, NCLS>(un, okn, m, A);
+    if (r + wstride < a.rows) load_u<CT, MT, NCLS>(in + (r + wstride) * spec_len, a, m, g, un, okn);
+    inv_row<CT, TH, MT, NCLS, MODE>(A, y + r * row_len, ta, lds, a, lane);
   }
 }
 
@@ -505,7 +733,129 @@ inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
   inv_zt_body<CT, TH, MT, NCLS, MODE>(in, y, ta, lds, a, wave, wstride);
 }
 
+// ---------------------------------------------------------------------------
+// Inverse y + z + t in one pass (same shape conditions as fwd_tzy_kernel).
+//
+// A workgroup of 16 waves owns one (b, c, x) plane (one workgroup per plane:
+// a persistent loop would make every plane's operand loads wait behind the
+// previous plane's outstanding row stores, which share the wave's memory
+// counter).  Wave w < ceil(K_z K_t / 16) loads the columns 16w..16w+15 of the
+// plane's (K_y x K_z K_t) spectrum as MFMA B operands (K index = y mode).  For
+// every group of 16 slots (one y tile of the inverse y image) those waves
+// expand y for the group's slots -- folded, the even-mode sum E and odd-mode
+// sum O give E + O at y and E - O at y + N_y/2 -- and leave the rows in LDS;
+// after a barrier, wave w expands z and t of the row(s) of slot w exactly as
+// inv_zt_body does and streams them out; a second barrier frees the LDS rows.
+// The (N_y x K_z K_t) intermediate never reaches HBM.
+// ---------------------------------------------------------------------------
+template <int TH, int NCLS, int MODE, int NCY, int JQY>
+__global__ void __launch_bounds__(1024)
+inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float* __restrict__ timg,
+               const float4* __restrict__ zimg, const float4* __restrict__ yimg, StreamArgs a, FusedArgs f) {
+  constexpr int CT = 1, MT = 2;
+  extern __shared__ float4 lds[];
+  const int nimg = NCLS * a.zt * MT * 64;
+  float2* vlds = reinterpret_cast<float2*>(lds + nimg);
+  const int lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  const int w = threadIdx.x >> 6;
+  if (blockIdx.x >= f.planes) return;  // the host launches one workgroup per plane
+  const int64_t pl = blockIdx.x;
+  const int mc = 16 * w + m;
+  const bool col_ok = mc < f.mcols;
+
+  // B operands of the y expansion: spectrum row p (class cl, K index
+  // 16q + 4g + i), column mc; zero outside the spectrum.  Issued first, so
+  // their latency overlaps the LDS staging.
+  float2 u[NCY][JQY][4];
+  {
+    const float2* sp = in + pl * int64_t(f.ky) * f.mcols;
+#pragma unroll
+    for (int cl = 0; cl < NCY; ++cl)
+#pragma unroll
+      for (int q = 0; q < JQY; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kk = 16 * q + 4 * g + i;
+          const int p = NCY == 2 ? 2 * kk + cl : kk;
+          const bool ok = col_ok && p < f.ky;
+          const float2 v = sp[ok ? int64_t(p) * f.mcols + mc : 0];
+          u[cl][q][i] = ok ? v : make_float2(0.f, 0.f);
+        }
+  }
+
+  // LDS: z image, the exchanged rows, the y image.
+  float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
+  for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
+  for (int i = threadIdx.x; i < f.yimg_n4; i += blockDim.x) ylds[i] = yimg[i];
+  __syncthreads();
+
+  // A operand of the t expansion: rows t = 16mt + m, K index c = 4g + i.
+  float ta[TH][CT][4];
+#pragma unroll
+  for (int mt = 0; mt < TH; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ta[mt][0][i] = timg[(mt * 4 + i) * 64 + lane];
+
+  const int64_t row_len = int64_t(a.nz) * a.nt;
+  {
+    for (int gq = 0; gq < f.jq; ++gq) {
+      if (w < f.nwy) {
+        v4f er[NCY], ei[NCY];
+#pragma unroll
+        for (int cl = 0; cl < NCY; ++cl) {
+          er[cl] = v4f{0.f, 0.f, 0.f, 0.f};
+          ei[cl] = v4f{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int q = 0; q < JQY; ++q)
+#pragma unroll
+          for (int cl = 0; cl < NCY; ++cl) {
+            // image entry (((tile * JQ + q) * NCY + class) * 2 + part) * 64 + lane
+            const float4* ip = ylds + ((gq * JQY + q) * NCY + cl) * 2 * 64 + lane;
+            const float4 br = ip[0], bi = ip[64];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float2 v = u[cl][q][i];
+              er[cl] = mfma(br[i], v.x, er[cl]);
+              ei[cl] = mfma(br[i], v.y, ei[cl]);
+              er[cl] = mfma(bi[i], -v.y, er[cl]);
+              ei[cl] = mfma(bi[i], v.x, ei[cl]);
+            }
+          }
+        // accumulator register i holds slot 4g + i, column mc
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int sl = 4 * g + i;
+          if constexpr (NCY == 2) {
+            vlds[sl * f.mrow + mc] = make_float2(er[0][i] + er[1][i], ei[0][i] + ei[1][i]);
+            vlds[(16 + sl) * f.mrow + mc] = make_float2(er[0][i] - er[1][i], ei[0][i] - ei[1][i]);
+          } else {
+            vlds[sl * f.mrow + mc] = make_float2(er[0][i], ei[0][i]);
+          }
+        }
+      }
+      __syncthreads();
+      const int s = 16 * gq + w;
+      if (s < f.slots) {
+#pragma unroll
+        for (int h = 0; h < NCY; ++h) {
+          float2 uu[NCLS][CT][MT / 2][4];
+          bool ok[NCLS][CT][MT / 2][4];
+          load_u<CT, MT, NCLS>(vlds + (h * 16 + w) * f.mrow, a, m, g, uu, ok);
+          float A[NCLS][CT][MT][4];
+          build_a<CT, MT, NCLS>(uu, ok, m, A);
+          inv_row<CT, TH, MT, NCLS, MODE>(A, y + (pl * f.ny + s + h * f.half) * row_len, ta, lds, a, lane);
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
 typedef void (*fwd_fn)(const float*, float2*, const float*, const float4*, StreamArgs);
+typedef void (*ifused_fn)(const float2*, float*, const float*, const float4*, const float4*, StreamArgs, FusedArgs);
+typedef void (*fused_fn)(const float*, float2*, const float*, const float4*, const float4*, StreamArgs, FusedArgs);
 typedef void (*inv_fn)(const float2*, float*, const float*, const float4*, StreamArgs);
 
 // Load / store form of a configuration: 0 scalar (N_t % 4 != 0), 1 16-byte
@@ -556,6 +906,45 @@ void pick0(int th, int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
   else pick1<CT, 4>(mt, ncls, mode, f, v);
 }
 
+template <int TH, int NCLS, int MODE>
+fused_fn pick_fused3(int ncy, int kyt) {
+  if (ncy == 2) return fwd_tzy_kernel<TH, NCLS, MODE, 2, 1>;
+  if (kyt == 1) return fwd_tzy_kernel<TH, NCLS, MODE, 1, 1>;
+  return fwd_tzy_kernel<TH, NCLS, MODE, 1, 2>;
+}
+
+template <int TH, int NCLS>
+fused_fn pick_fused2(int mode, int ncy, int kyt) {
+  return mode == 2 ? pick_fused3<TH, NCLS, 2>(ncy, kyt) : pick_fused3<TH, NCLS, 1>(ncy, kyt);
+}
+
+template <int TH, int NCLS, int MODE>
+ifused_fn pick_ifused3(int ncy, int jqy) {
+  if (ncy == 2) return inv_yzt_kernel<TH, NCLS, MODE, 2, 1>;
+  if (jqy == 1) return inv_yzt_kernel<TH, NCLS, MODE, 1, 1>;
+  return inv_yzt_kernel<TH, NCLS, MODE, 1, 2>;
+}
+
+template <int TH, int NCLS>
+ifused_fn pick_ifused2(int mode, int ncy, int jqy) {
+  return mode == 2 ? pick_ifused3<TH, NCLS, 2>(ncy, jqy) : pick_ifused3<TH, NCLS, 1>(ncy, jqy);
+}
+
+// Fused y + z + t instances: as below, with JQY 16-wide K steps per y class.
+ifused_fn pick_ifused(const StreamCfg& c) {
+  const int mode = mode_of(c);
+  if (c.th == 1) return c.ncls == 2 ? pick_ifused2<1, 2>(mode, c.ncy, c.kyt) : pick_ifused2<1, 1>(mode, c.ncy, c.kyt);
+  return c.ncls == 2 ? pick_ifused2<2, 2>(mode, c.ncy, c.kyt) : pick_ifused2<2, 1>(mode, c.ncy, c.kyt);
+}
+
+// Fused t + z + y instances: CT = 1, MT = 2, TH <= 2, NCLS <= 2, 16-byte
+// loads; (NCY, KYT) = (2, 1) folded, (1, 1) or (1, 2) otherwise.
+fused_fn pick_fused(const StreamCfg& c) {
+  const int mode = mode_of(c);
+  if (c.th == 1) return c.ncls == 2 ? pick_fused2<1, 2>(mode, c.ncy, c.kyt) : pick_fused2<1, 1>(mode, c.ncy, c.kyt);
+  return c.ncls == 2 ? pick_fused2<2, 2>(mode, c.ncy, c.kyt) : pick_fused2<2, 1>(mode, c.ncy, c.kyt);
+}
+
 void pick(const StreamCfg& c, fwd_fn* f, inv_fn* v) {
   if (c.ct == 1) pick0<1>(c.th, c.mt, c.ncls, mode_of(c), f, v);
   else pick0<2>(c.th, c.mt, c.ncls, mode_of(c), f, v);
@@ -600,6 +989,23 @@ int prepare_stream(StreamCfg* c) {
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(v), hipFuncAttributeMaxDynamicSharedMemorySize,
                           int(c->lds_bytes));
   if (e != hipSuccess) return e;
+  if (c->fuse_y) {
+    const void* ff = reinterpret_cast<const void*>(pick_fused(*c));
+    e = hipFuncSetAttribute(ff, hipFuncAttributeMaxDynamicSharedMemorySize, int(c->fused_lds_bytes));
+    if (e != hipSuccess) return e;
+    int dev = 0, cus = 0, per_cu = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ff, 1024, c->fused_lds_bytes)) != hipSuccess)
+      return e;
+    c->grid_fused = cus * (per_cu > 0 ? per_cu : 1);
+    const void* fi = reinterpret_cast<const void*>(pick_ifused(*c));
+    e = hipFuncSetAttribute(fi, hipFuncAttributeMaxDynamicSharedMemorySize, int(c->fused_lds_bytes));
+    if (e != hipSuccess) return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fi, 1024, c->fused_lds_bytes)) != hipSuccess)
+      return e;
+    if (per_cu <= 0) return hipErrorInvalidConfiguration;
+  }
   c->grid_fwd = resident_grid(reinterpret_cast<const void*>(f), c->lds_bytes);
   c->grid_inv = resident_grid(reinterpret_cast<const void*>(v), c->lds_bytes);
   if (c->grid_fwd <= 0 || c->grid_inv <= 0) return hipErrorInvalidConfiguration;
@@ -626,6 +1032,54 @@ int launch_inv_zt(const StreamCfg& c, const void* in, float* y, int64_t rows, co
   hipLaunchKernelGGL(v, dim3(grid_for(c.grid_inv, rows)), dim3(256), c.lds_bytes, static_cast<hipStream_t>(stream),
                      static_cast<const float2*>(in), y, timg, reinterpret_cast<const float4*>(zimg),
                      args_of(c, rows));
+  return hipGetLastError();
+}
+
+int launch_fwd_tzy(const StreamCfg& c, const AxisCfg& ay, const float* x, void* out, int64_t planes, int ny,
+                   const float* timg, const float* zimg, const float* yimg, void* stream) {
+  if (planes <= 0) return hipSuccess;
+  FusedArgs f;
+  f.planes = planes;
+  f.ny = ny;
+  f.slots = ay.fold == 1 ? ny / 2 : ny;
+  f.half = ay.fold == 1 ? ny / 2 : 0;
+  f.jq = ay.JQ;
+  f.kth = ay.kth;
+  f.ky = ay.KO;
+  f.mcols = c.kz * c.kt;
+  f.mrow = c.fused_mrow;
+  f.nwy = (f.mcols + 15) / 16;
+  f.yimg_n4 = ay.ktiles * ay.JQ * 2 * 64;
+  const int64_t grid = planes < c.grid_fused ? planes : c.grid_fused;
+  hipLaunchKernelGGL(pick_fused(c), dim3(static_cast<unsigned>(grid)), dim3(1024), c.fused_lds_bytes,
+                     static_cast<hipStream_t>(stream), x, static_cast<float2*>(out), timg,
+                     reinterpret_cast<const float4*>(zimg), reinterpret_cast<const float4*>(yimg),
+                     args_of(c, planes * ny), f);
+  return hipGetLastError();
+}
+
+int launch_inv_yzt(const StreamCfg& c, const AxisCfg& ay, const void* in, float* y, int64_t planes, int ny,
+                   const float* timg, const float* zimg, const float* yimg, void* stream) {
+  if (planes <= 0) return hipSuccess;
+  // The y expansion's image must have the K steps and tiles the kernel assumes.
+  if (ay.JQ != c.kyt || (ay.fold == 2) != (c.ncy == 2)) return hipErrorInvalidValue;
+  FusedArgs f;
+  f.planes = planes;
+  f.ny = ny;
+  f.slots = ay.fold == 2 ? ny / 2 : ny;
+  f.half = ay.fold == 2 ? ny / 2 : 0;
+  f.jq = ay.ktiles;
+  f.kth = 0;
+  f.ky = ay.J;
+  f.mcols = c.kz * c.kt;
+  f.mrow = c.fused_mrow;
+  f.nwy = (f.mcols + 15) / 16;
+  f.yimg_n4 = ay.ktiles * ay.JQ * (ay.fold == 2 ? 2 : 1) * 2 * 64;
+  if (planes > int64_t(0x7fffffff)) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(pick_ifused(c), dim3(static_cast<unsigned>(planes)), dim3(1024), c.fused_lds_bytes,
+                     static_cast<hipStream_t>(stream), static_cast<const float2*>(in), y, timg,
+                     reinterpret_cast<const float4*>(zimg), reinterpret_cast<const float4*>(yimg),
+                     args_of(c, planes * ny), f);
   return hipGetLastError();
 }
 

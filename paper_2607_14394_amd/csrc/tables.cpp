@@ -9,6 +9,7 @@
 // large k*n products (k*n reaches 2.6e5 at N = 512).
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
 
@@ -191,6 +192,29 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
   dv.ax_f = axis(static_cast<int>(d->n_local[0]), static_cast<int>(dv.K[0]), nn_x, fold_x ? 1 : 0);
   dv.ax_i = axis(static_cast<int>(dv.K[0]), static_cast<int>(d->n_local[0]), nn_x, fold_x ? 2 : 0);
   dv.ay_i = axis(static_cast<int>(dv.K[1]), static_cast<int>(d->n_local[1]), nn_y, fold_y ? 2 : 0);
+
+  // ---- fused forward t + z + y ----
+  // Taken when the y contraction fits the fused kernel's registers (one
+  // 16-column tile of K_z K_t per wave of 16, at most two 16-row k tiles of
+  // K_y per wave) and its LDS.  DTST_SCHEDULE=split in the environment at
+  // plan time keeps the separate t + z and y launches.
+  {
+    const char* sched = std::getenv("DTST_SCHEDULE");
+    const bool split = sched != nullptr && std::strcmp(sched, "split") == 0;
+    sc.ncy = fold_y ? 2 : 1;
+    sc.kyt = fold_y ? dv.ay_f.kth : dv.ay_f.ktiles;
+    const int mcols = static_cast<int>(nn_y);
+    sc.fused_mrow = static_cast<int>(round_up(mcols, 32)) + 16;
+    // z image, the 16 slots' exchanged rows, and the larger of the forward and
+    // inverse y images
+    const size_t yf = size_t(dv.ay_f.ktiles) * dv.ay_f.JQ * 2 * 64 * 16;
+    const size_t yi = size_t(dv.ay_i.ktiles) * dv.ay_i.JQ * (fold_y ? 2 : 1) * 2 * 64 * 16;
+    sc.fused_lds_bytes = sc.lds_bytes + size_t(16) * sc.ncy * sc.fused_mrow * 8 + std::max(yf, yi);
+    sc.fuse_y = (!split && sc.ct == 1 && sc.mt == 2 && sc.th <= 2 && sc.ncls <= 2 && sc.vec && dv.K[1] <= 32 &&
+                 mcols <= 256 && sc.kyt <= (fold_y ? 1 : 2) && sc.fused_lds_bytes <= 160 * 1024)
+                    ? 1
+                    : 0;
+  }
 
   // ---- workspace: two complex intermediates of the largest channel count ----
   const int64_t bc = d->batch * cmax;

@@ -42,7 +42,16 @@ CASES = {
     "radix4_full_tiles": ((4, 4, 64, 32), (4, 4, 64, 32), (0, 0, 0, 0), (2, 2, 32), 16, 1, 2, 2),
     # odd k_max(z) with N_z % 4 == 0 and k_t > 8 keeps the two-class fold
     "fold2_odd_kz_kt9": ((4, 4, 24, 16), (4, 4, 24, 16), (0, 0, 0, 0), (1, 1, 5), 9, 1, 2, 1),
+    # more (b, c, x) planes than the fused t+z+y kernel has resident workgroups
+    "many_planes": ((48, 8, 16, 8), (48, 8, 16, 8), (0, 0, 0, 0), (4, 2, 4), 3, 2, 4, 3),
 }
+
+# Geometries whose plan takes the fused t + z + y forward kernel (K_t <= 8, at
+# most 16 z modes per class, N_t <= 32 and a multiple of 4, K_y <= 32,
+# K_z K_t <= 256): folded y with a ragged last slot group, unfolded y (pencil),
+# K above the local extent, several slot groups, many planes.
+FUSED_CASES = ["tiny_baseline", "tiny_slab", "tiny_pencil", "k_above_nloc", "fold_ragged", "slab_like_cfg2",
+               "cfg1_full", "many_planes"]
 
 
 def _setup(name):
@@ -396,3 +405,73 @@ def test_inverse_block(name):
     check(np_of(Y.t), O.block_epilogue(x, wb, O.inverse(yh, g)), "inverse + block epilogue")
     assert Y.guards_intact()
     plan.close()
+
+
+@pytest.mark.parametrize("schedule", ["fused", "split"])
+@pytest.mark.parametrize("name", FUSED_CASES)
+def test_forward_schedules(name, schedule, monkeypatch):
+    """Both forward schedules (one t+z+y launch, or t+z then y) against the
+    oracle; the library's own per-kernel timing names the kernels that ran."""
+    if schedule == "split":
+        monkeypatch.setenv("DTST_SCHEDULE", "split")
+    else:
+        monkeypatch.delenv("DTST_SCHEDULE", raising=False)
+    torch, D, g, plan = _setup(name)
+    x = rand_real((g.batch, g.c_in) + g.n_local, 111)
+    ref = O.forward(x, g)
+    out = Guarded(torch, plan.spectral_shape(g.c_in), torch.complex64)
+    D.dtst_profile_collect()
+    D.dtst_profile_enable(True)
+    try:
+        plan.forward(dev(torch, x), out.t)
+        plan.forward(dev(torch, x), out.t, accumulate=True)
+        torch.cuda.synchronize()
+        ran = {k for k, (n, _) in D.dtst_profile_collect().items() if n > 0}
+    finally:
+        D.dtst_profile_enable(False)
+    check(np_of(out.t), 2 * ref, f"forward ({schedule}) + accumulate")
+    assert out.guards_intact()
+    if schedule == "fused":
+        assert "stream_fwd_tzy" in ran and "stream_fwd_tz" not in ran and "axis_fwd_y" not in ran, ran
+    else:
+        assert "stream_fwd_tz" in ran and "axis_fwd_y" in ran and "stream_fwd_tzy" not in ran, ran
+    gy = rand_real((g.batch, g.c_out) + g.n_local, 112)
+    out2 = Guarded(torch, plan.spectral_shape(g.c_out), torch.complex64)
+    plan.inverse_adj(dev(torch, gy), out2.t)
+    torch.cuda.synchronize()
+    check(np_of(out2.t), O.inverse_adj(gy, g), f"inverse_adj ({schedule})")
+    assert out2.guards_intact()
+
+
+@pytest.mark.parametrize("schedule", ["fused", "split"])
+@pytest.mark.parametrize("name", FUSED_CASES)
+def test_inverse_schedules(name, schedule, monkeypatch):
+    """Both inverse schedules (y + z + t in one launch, or y then z + t) for
+    the inverse and forward_adj against the oracle, with the kernels that ran."""
+    if schedule == "split":
+        monkeypatch.setenv("DTST_SCHEDULE", "split")
+    else:
+        monkeypatch.delenv("DTST_SCHEDULE", raising=False)
+    torch, D, g, plan = _setup(name)
+    yh = rand_cplx((g.batch, g.c_out) + g.K, 113)
+    out = Guarded(torch, plan.spatial_shape(g.c_out), torch.float32)
+    D.dtst_profile_collect()
+    D.dtst_profile_enable(True)
+    try:
+        plan.inverse(dev(torch, yh), out.t)
+        torch.cuda.synchronize()
+        ran = {k for k, (n, _) in D.dtst_profile_collect().items() if n > 0}
+    finally:
+        D.dtst_profile_enable(False)
+    check(np_of(out.t), O.inverse(yh, g), f"inverse ({schedule})")
+    assert out.guards_intact()
+    if schedule == "fused":
+        assert "stream_inv_yzt" in ran and "stream_inv_zt" not in ran and "axis_inv_y" not in ran, ran
+    else:
+        assert "stream_inv_zt" in ran and "axis_inv_y" in ran and "stream_inv_yzt" not in ran, ran
+    G = rand_cplx((g.batch, g.c_in) + g.K, 114)
+    out2 = Guarded(torch, plan.spatial_shape(g.c_in), torch.float32)
+    plan.forward_adj(dev(torch, G), out2.t)
+    torch.cuda.synchronize()
+    check(np_of(out2.t), O.forward_adj(G, g), f"forward_adj ({schedule})")
+    assert out2.guards_intact()
