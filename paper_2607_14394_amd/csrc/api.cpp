@@ -90,12 +90,6 @@ dtst_status check_ws(const dtst_plan_st* p, const void* ws, size_t ws_bytes) {
   return DTST_OK;
 }
 
-size_t w1_bytes(const dtst::Derived& dv) {
-  const int64_t cmax = dv.d.c_in > dv.d.c_out ? dv.d.c_in : dv.d.c_out;
-  size_t b = size_t(dv.d.batch) * cmax * dv.d.n_local[0] * dv.d.n_local[1] * dv.K[2] * dv.K[3] * 8;
-  return (b + 255) / 256 * 256;
-}
-
 #define DTST_TRY(expr)                 \
   do {                                 \
     dtst_status s_ = (expr);           \
@@ -170,7 +164,7 @@ dtst_status run_forward_chain(const dtst_plan_st* p, int64_t channels, const flo
   const int64_t B = dv.d.batch;
   if (B == 0) return ok();
   char* w1 = static_cast<char*>(ws);
-  char* w2 = w1 + w1_bytes(dv);
+  char* w2 = w1 + dv.w1_bytes;
   const int64_t planes = B * channels * dv.d.n_local[0];
   const int64_t rows = planes * dv.d.n_local[1];
   int e;
@@ -204,7 +198,7 @@ dtst_status run_inverse_chain(const dtst_plan_st* p, int64_t channels, const voi
   const int64_t B = dv.d.batch;
   if (B == 0) return ok();
   char* v2 = static_cast<char*>(ws);    // (.., Nx, Ny, Kz, Kt)
-  char* v1 = v2 + w1_bytes(dv);         // (.., Nx, Ky, Kz, Kt)
+  char* v1 = v2 + dv.w1_bytes;          // (.., Nx, Ky, Kz, Kt)
   int e = timed(K_AXIS_INV_X, stream, [&] {
     return dtst::launch_axis(dv.ax_i, B * channels, yhat, v1, p->blob + dv.img.x_inv, 0, stream);
   });

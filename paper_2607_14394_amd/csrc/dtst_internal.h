@@ -43,7 +43,9 @@ struct StreamCfg {
   //   kyt        16-wide tiles of K_y per class: k tiles of the forward y
   //              image, K steps of the inverse y image
   //   fused_mrow LDS row stride (complex values) of the exchanged row results
-  int fuse_y = 0, ncy = 1, kyt = 1, fused_mrow = 0;
+  //   fused_y_lds 1 when the y basis images are staged in LDS (else read from
+  //              global memory)
+  int fuse_y = 0, ncy = 1, kyt = 1, fused_mrow = 0, fused_y_lds = 0;
   size_t fused_lds_bytes = 0;
   // filled at plan creation on the plan's device (prepare_stream)
   int grid_fwd = 0, grid_inv = 0;  // resident workgroups of each kernel
@@ -86,6 +88,7 @@ struct Derived {
   StreamCfg sc;
   AxisCfg ay_f, ax_f, ax_i, ay_i;  // per-channel shapes; nb is per (b, c) below
   size_t ws_bytes = 0;
+  size_t w1_bytes = 0;  // workspace offset of W2 (0 with the fused y: no W1)
   Images img;
 };
 

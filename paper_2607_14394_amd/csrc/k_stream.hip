@@ -20,6 +20,8 @@
 // without any data movement.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "dtst_internal.h"
 
 namespace dtst {
@@ -350,6 +352,10 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
 // The (K_y x K_z K_t) result of the plane is written once.  The shard is read
 // once and the (N_y x K_z K_t) intermediate never reaches HBM.
 // ---------------------------------------------------------------------------
+// Waves per workgroup and tile buffers per wave of fwd_tzy_kernel.
+constexpr int kFusedWaves = 8;
+constexpr int kFusedBufs = 4;
+
 struct FusedArgs {
   int64_t planes;  // B * C * N_x
   int ny;          // local N_y (rows per plane)
@@ -361,14 +367,17 @@ struct FusedArgs {
   int mcols;       // K_z * K_t
   int mrow;        // LDS row stride in complex values
   int nwy;         // waves running the y contraction: ceil(mcols / 16)
-  int yimg_n4;     // float4 entries of the y image (staged in LDS after the row exchange)
+  int yimg_n4;     // float4 entries of the y image staged in LDS after the row exchange;
+                   // 0: read from global memory (the image does not fit in LDS)
 };
 
-template <int TH, int NCLS, int MODE, int NCY, int KYT>
-__global__ void __launch_bounds__(1024)
+template <int TH, int NCLS, int MODE, int NCY, int KYT, int NW, int NB>
+__global__ void __launch_bounds__(64 * NW)
 fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const float* __restrict__ timg,
                const float4* __restrict__ zimg, const float4* __restrict__ yimg, StreamArgs a, FusedArgs f) {
   constexpr int CT = 1, MT = 2;
+  constexpr int SPW = 16 / NW;  // slots of a group per wave
+  constexpr int MTW = 16 / NW;  // 16-column tiles of the y contraction per wave
   extern __shared__ float4 lds[];
   const int nimg = NCLS * a.zt * MT * 64;
   float2* vlds = reinterpret_cast<float2*>(lds + nimg);
@@ -377,19 +386,23 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
   const int w = threadIdx.x >> 6;
   if (blockIdx.x >= f.planes) return;  // the host never launches more workgroups than planes
 
-  // Position of a tile: (plane, slot group, row of the slot, z tile).
+  // Position of a tile: (plane, slot group, slot of this wave, row of the
+  // slot, z tile), z tile fastest.
   struct Cur {
     int64_t pl;
-    int q, h, zt;
+    int q, j, h, zt;
   };
   auto advance = [&](Cur c) {
     if (++c.zt == a.zt) {
       c.zt = 0;
       if (++c.h == NCY) {
         c.h = 0;
-        if (++c.q == f.jq) {
-          c.q = 0;
-          c.pl += gridDim.x;
+        if (++c.j == SPW) {
+          c.j = 0;
+          if (++c.q == f.jq) {
+            c.q = 0;
+            c.pl += gridDim.x;
+          }
         }
       }
     }
@@ -398,18 +411,27 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
   // Row of a tile for this wave; slots past the plane's end read its first
   // row and contribute zeros.
   auto row_of = [&](const Cur& c, bool* valid) {
-    const int s = 16 * c.q + w;
+    const int s = 16 * c.q + w + NW * c.j;
     *valid = s < f.slots;
     return c.pl * f.ny + (*valid ? s + c.h * f.half : 0);
   };
 
-  // One tile ahead: the next tile's loads are in flight while the current
-  // one is contracted.  The first loads go out before the z image is staged.
-  Cur cur{static_cast<int64_t>(blockIdx.x), 0, 0, 0};
-  bool valid;
-  float xn[NCLS][TH][4];
-  bool okn[NCLS][TH * 4];
-  load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cur, &valid), 0, xn, okn);
+  // NB tile buffers: buffer k holds the tile at cb[k] and is refilled, once
+  // contracted, with the tile NB positions further on, so NB - 1 tiles are in
+  // flight while one is contracted.  The first loads go out before the
+  // images are staged.
+  float xb[NB][NCLS][TH][4];
+  bool okb[NB][NCLS][TH * 4];
+  bool vb[NB];
+  Cur cb[NB];
+  cb[0] = Cur{static_cast<int64_t>(blockIdx.x), 0, 0, 0, 0};
+#pragma unroll
+  for (int k = 1; k < NB; ++k) cb[k] = advance(cb[k - 1]);
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    vb[k] = false;
+    if (cb[k].pl < f.planes) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cb[k], &vb[k]), cb[k].zt, xb[k], okb[k]);
+  }
 
   // LDS: z image, the exchanged row results, the y image.
   float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
@@ -419,102 +441,122 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
 
   float bt[TH * 4][CT];
 #pragma unroll
-  for (int s = 0; s < TH * 4; ++s) bt[s][0] = timg[s * 64 + lane];
+  for (int st = 0; st < TH * 4; ++st) bt[st][0] = timg[st * 64 + lane];
 
-  v4f yr[NCY][KYT], yi[NCY][KYT];
+  v4f yr[NCY][KYT][MTW], yi[NCY][KYT][MTW];
 #pragma unroll
   for (int c = 0; c < NCY; ++c)
 #pragma unroll
-    for (int k = 0; k < KYT; ++k) {
-      yr[c][k] = v4f{0.f, 0.f, 0.f, 0.f};
-      yi[c][k] = v4f{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int k = 0; k < KYT; ++k)
+#pragma unroll
+      for (int t = 0; t < MTW; ++t) {
+        yr[c][k][t] = v4f{0.f, 0.f, 0.f, 0.f};
+        yi[c][k][t] = v4f{0.f, 0.f, 0.f, 0.f};
+      }
   v4f P[NCLS][MT][CT];
 
-  while (true) {
-    float xv[NCLS][TH][4];
-    bool ok[NCLS][TH * 4];
+  // Contract buffer k's tile and refill the buffer; at a row's end leave its
+  // results in LDS, and after the wave's last row of a slot group run the
+  // group's y contraction.
+  auto process = [&](int k) __attribute__((always_inline)) {
+    const Cur c = cb[k];
+    const bool valid = vb[k];
+    v4f V[NCLS][CT];
+    t_part<CT, TH, NCLS, MODE>(xb[k], okb[k], bt, V);
+    const Cur far = advance(cb[(k + NB - 1) % NB]);
+    cb[k] = far;
+    if (far.pl < f.planes) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(far, &vb[k]), far.zt, xb[k], okb[k]);
+    z_part<CT, MT, NCLS>(V, lds, a, c.zt, lane, P);
+    if (c.zt != a.zt - 1) return;
+    float2* vrow = vlds + (c.h * 16 + w + NW * c.j) * f.mrow;
+    tz_finish<CT, MT, NCLS>(P, a, m, g, [&](int idx, float re, float im) {
+      vrow[idx] = valid ? make_float2(re, im) : make_float2(0.f, 0.f);
+    });
+    if (c.h != NCY - 1 || c.j != SPW - 1) return;
+    __syncthreads();
+    float4 br[NCY][KYT], bi[NCY][KYT];
 #pragma unroll
-    for (int hf = 0; hf < NCLS; ++hf)
+    for (int cl = 0; cl < NCY; ++cl)
 #pragma unroll
-      for (int hh = 0; hh < TH; ++hh)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          xv[hf][hh][j] = xn[hf][hh][j];
-          ok[hf][4 * hh + j] = okn[hf][4 * hh + j];
+      for (int kk = 0; kk < KYT; ++kk) {
+        const int kt = NCY == 2 ? cl * f.kth + kk : kk;
+        const int e = (kt * f.jq + c.q) * 2 * 64 + lane;
+        if (f.yimg_n4 > 0) {
+          br[cl][kk] = ylds[e];
+          bi[cl][kk] = ylds[e + 64];
+        } else {
+          br[cl][kk] = yimg[e];
+          bi[cl][kk] = yimg[e + 64];
         }
-    const Cur c = cur;
-    const bool c_valid = valid;
-    cur = advance(cur);
-    if (cur.pl < f.planes) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cur, &valid), cur.zt, xn, okn);
-
-    tz_tile<CT, TH, MT, NCLS, MODE>(xv, ok, bt, lds, a, c.zt, lane, P);
-    if (c.zt == a.zt - 1) {
-      // Row done: leave its results in LDS; after the group's last row,
-      // contract y over the group's slots.
-      float2* vrow = vlds + (c.h * 16 + w) * f.mrow;
-      tz_finish<CT, MT, NCLS>(P, a, m, g, [&](int idx, float re, float im) {
-        vrow[idx] = c_valid ? make_float2(re, im) : make_float2(0.f, 0.f);
-      });
-      if (c.h == NCY - 1) {
-        __syncthreads();
-        if (w < f.nwy) {
-          const int mc = 16 * w + m;
-          float4 br[NCY][KYT], bi[NCY][KYT];
+      }
 #pragma unroll
-          for (int cl = 0; cl < NCY; ++cl)
+    for (int t = 0; t < MTW; ++t) {
+      const int mt = w + NW * t;
+      if (mt >= f.nwy) continue;
+      const int mc = 16 * mt + m;
 #pragma unroll
-            for (int k = 0; k < KYT; ++k) {
-              const int kt = NCY == 2 ? cl * f.kth + k : k;
-              const float4* ip = ylds + (kt * f.jq + c.q) * 2 * 64 + lane;
-              br[cl][k] = ip[0];
-              bi[cl][k] = ip[64];
-            }
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int s = 4 * g + i;
-            const float2 va = vlds[s * f.mrow + mc];
-            float2 xs[NCY];
-            if constexpr (NCY == 2) {
-              const float2 vbv = vlds[(16 + s) * f.mrow + mc];
-              xs[0] = make_float2(va.x + vbv.x, va.y + vbv.y);
-              xs[1] = make_float2(va.x - vbv.x, va.y - vbv.y);
-            } else {
-              xs[0] = va;
-            }
-#pragma unroll
-            for (int cl = 0; cl < NCY; ++cl)
-#pragma unroll
-              for (int k = 0; k < KYT; ++k) {
-                yr[cl][k] = mfma(br[cl][k][i], xs[cl].x, yr[cl][k]);
-                yi[cl][k] = mfma(br[cl][k][i], xs[cl].y, yi[cl][k]);
-                yr[cl][k] = mfma(bi[cl][k][i], -xs[cl].y, yr[cl][k]);
-                yi[cl][k] = mfma(bi[cl][k][i], xs[cl].x, yi[cl][k]);
-              }
-          }
-          if (c.q == f.jq - 1) {
-            // Plane done: rows p of K_y (class cl, slot 16k + 4g + i), columns mc.
-            float2* op = out + c.pl * int64_t(f.ky) * f.mcols;
-#pragma unroll
-            for (int cl = 0; cl < NCY; ++cl)
-#pragma unroll
-              for (int k = 0; k < KYT; ++k) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                  const int sl = 16 * k + 4 * g + i;
-                  const int p = NCY == 2 ? 2 * sl + cl : sl;
-                  if (p < f.ky && mc < f.mcols)
-                    op[int64_t(p) * f.mcols + mc] = make_float2(yr[cl][k][i], yi[cl][k][i]);
-                }
-                yr[cl][k] = v4f{0.f, 0.f, 0.f, 0.f};
-                yi[cl][k] = v4f{0.f, 0.f, 0.f, 0.f};
-              }
-          }
+      for (int i = 0; i < 4; ++i) {
+        const int sl = 4 * g + i;
+        const float2 va = vlds[sl * f.mrow + mc];
+        float2 xs[NCY];
+        if constexpr (NCY == 2) {
+          const float2 vbv = vlds[(16 + sl) * f.mrow + mc];
+          xs[0] = make_float2(va.x + vbv.x, va.y + vbv.y);
+          xs[1] = make_float2(va.x - vbv.x, va.y - vbv.y);
+        } else {
+          xs[0] = va;
         }
-        __syncthreads();
+#pragma unroll
+        for (int cl = 0; cl < NCY; ++cl)
+#pragma unroll
+          for (int kk = 0; kk < KYT; ++kk) {
+            yr[cl][kk][t] = mfma(br[cl][kk][i], xs[cl].x, yr[cl][kk][t]);
+            yi[cl][kk][t] = mfma(br[cl][kk][i], xs[cl].y, yi[cl][kk][t]);
+            yr[cl][kk][t] = mfma(bi[cl][kk][i], -xs[cl].y, yr[cl][kk][t]);
+            yi[cl][kk][t] = mfma(bi[cl][kk][i], xs[cl].x, yi[cl][kk][t]);
+          }
+      }
+      if (c.q == f.jq - 1) {
+        // Plane done: rows p of K_y (class cl, slot 16kk + 4g + i), columns mc.
+        float2* op = out + c.pl * int64_t(f.ky) * f.mcols;
+#pragma unroll
+        for (int cl = 0; cl < NCY; ++cl)
+#pragma unroll
+          for (int kk = 0; kk < KYT; ++kk) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int sl = 16 * kk + 4 * g + i;
+              const int p = NCY == 2 ? 2 * sl + cl : sl;
+              if (p < f.ky && mc < f.mcols)
+                op[int64_t(p) * f.mcols + mc] = make_float2(yr[cl][kk][t][i], yi[cl][kk][t][i]);
+            }
+            yr[cl][kk][t] = v4f{0.f, 0.f, 0.f, 0.f};
+            yi[cl][kk][t] = v4f{0.f, 0.f, 0.f, 0.f};
+          }
       }
     }
-    if (cur.pl >= f.planes) break;
+    __syncthreads();
+  };
+
+  // Tiles in order through buffers 0, 1, ..., NB - 1, 0, ...; the loop ends
+  // after the tile whose successor lies past the last plane.  The buffer
+  // index is a compile-time constant at every step (the buffers stay in
+  // registers).
+  static_assert(NB >= 1 && NB <= 4, "one to four tile buffers");
+  auto step = [&](auto kc) __attribute__((always_inline)) {
+    constexpr int k = decltype(kc)::value;
+    const bool more = cb[(k + 1) % NB].pl < f.planes;
+    process(k);
+    return more;
+  };
+  while (true) {
+    if (!step(std::integral_constant<int, 0>{})) return;
+    if constexpr (NB > 1)
+      if (!step(std::integral_constant<int, 1>{})) return;
+    if constexpr (NB > 2)
+      if (!step(std::integral_constant<int, 2>{})) return;
+    if constexpr (NB > 3)
+      if (!step(std::integral_constant<int, 3>{})) return;
   }
 }
 
@@ -812,8 +854,9 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
 #pragma unroll
           for (int cl = 0; cl < NCY; ++cl) {
             // image entry (((tile * JQ + q) * NCY + class) * 2 + part) * 64 + lane
-            const float4* ip = ylds + ((gq * JQY + q) * NCY + cl) * 2 * 64 + lane;
-            const float4 br = ip[0], bi = ip[64];
+            const int e = ((gq * JQY + q) * NCY + cl) * 2 * 64 + lane;
+            const float4 br = f.yimg_n4 > 0 ? ylds[e] : yimg[e];
+            const float4 bi = f.yimg_n4 > 0 ? ylds[e + 64] : yimg[e + 64];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const float2 v = u[cl][q][i];
@@ -908,9 +951,9 @@ void pick0(int th, int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
 
 template <int TH, int NCLS, int MODE>
 fused_fn pick_fused3(int ncy, int kyt) {
-  if (ncy == 2) return fwd_tzy_kernel<TH, NCLS, MODE, 2, 1>;
-  if (kyt == 1) return fwd_tzy_kernel<TH, NCLS, MODE, 1, 1>;
-  return fwd_tzy_kernel<TH, NCLS, MODE, 1, 2>;
+  if (ncy == 2) return fwd_tzy_kernel<TH, NCLS, MODE, 2, 1, kFusedWaves, kFusedBufs>;
+  if (kyt == 1) return fwd_tzy_kernel<TH, NCLS, MODE, 1, 1, kFusedWaves, kFusedBufs>;
+  return fwd_tzy_kernel<TH, NCLS, MODE, 1, 2, kFusedWaves, kFusedBufs>;
 }
 
 template <int TH, int NCLS>
@@ -996,7 +1039,8 @@ int prepare_stream(StreamCfg* c) {
     int dev = 0, cus = 0, per_cu = 0;
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ff, 1024, c->fused_lds_bytes)) != hipSuccess)
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, ff, 64 * kFusedWaves, c->fused_lds_bytes)) !=
+        hipSuccess)
       return e;
     c->grid_fused = cus * (per_cu > 0 ? per_cu : 1);
     const void* fi = reinterpret_cast<const void*>(pick_ifused(*c));
@@ -1049,9 +1093,9 @@ int launch_fwd_tzy(const StreamCfg& c, const AxisCfg& ay, const float* x, void* 
   f.mcols = c.kz * c.kt;
   f.mrow = c.fused_mrow;
   f.nwy = (f.mcols + 15) / 16;
-  f.yimg_n4 = ay.ktiles * ay.JQ * 2 * 64;
+  f.yimg_n4 = c.fused_y_lds ? ay.ktiles * ay.JQ * 2 * 64 : 0;
   const int64_t grid = planes < c.grid_fused ? planes : c.grid_fused;
-  hipLaunchKernelGGL(pick_fused(c), dim3(static_cast<unsigned>(grid)), dim3(1024), c.fused_lds_bytes,
+  hipLaunchKernelGGL(pick_fused(c), dim3(static_cast<unsigned>(grid)), dim3(64 * kFusedWaves), c.fused_lds_bytes,
                      static_cast<hipStream_t>(stream), x, static_cast<float2*>(out), timg,
                      reinterpret_cast<const float4*>(zimg), reinterpret_cast<const float4*>(yimg),
                      args_of(c, planes * ny), f);
@@ -1074,7 +1118,7 @@ int launch_inv_yzt(const StreamCfg& c, const AxisCfg& ay, const void* in, float*
   f.mcols = c.kz * c.kt;
   f.mrow = c.fused_mrow;
   f.nwy = (f.mcols + 15) / 16;
-  f.yimg_n4 = ay.ktiles * ay.JQ * (ay.fold == 2 ? 2 : 1) * 2 * 64;
+  f.yimg_n4 = c.fused_y_lds ? ay.ktiles * ay.JQ * (ay.fold == 2 ? 2 : 1) * 2 * 64 : 0;
   if (planes > int64_t(0x7fffffff)) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL(pick_ifused(c), dim3(static_cast<unsigned>(planes)), dim3(1024), c.fused_lds_bytes,
                      static_cast<hipStream_t>(stream), static_cast<const float2*>(in), y, timg,

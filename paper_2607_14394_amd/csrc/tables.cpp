@@ -193,6 +193,13 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
   dv.ax_i = axis(static_cast<int>(dv.K[0]), static_cast<int>(d->n_local[0]), nn_x, fold_x ? 2 : 0);
   dv.ay_i = axis(static_cast<int>(dv.K[1]), static_cast<int>(d->n_local[1]), nn_y, fold_y ? 2 : 0);
 
+  // ---- workspace: the complex intermediates of the largest channel count ----
+  // W1 = (.., N_x, N_y, K_z, K_t) between the t+z and y steps, W2 = (.., N_x,
+  // K_y, K_z, K_t) between the y and x steps (W1 only without the fused y).
+  const int64_t bc = d->batch * cmax;
+  const size_t w1 = round_up(size_t(bc) * d->n_local[0] * d->n_local[1] * nn_y * 8, 256);
+  const size_t w2 = round_up(size_t(bc) * d->n_local[0] * dv.K[1] * nn_y * 8, 256);
+
   // ---- fused forward t + z + y ----
   // Taken when the y contraction fits the fused kernel's registers (one
   // 16-column tile of K_z K_t per wave of 16, at most two 16-row k tiles of
@@ -206,21 +213,21 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
     const int mcols = static_cast<int>(nn_y);
     sc.fused_mrow = static_cast<int>(round_up(mcols, 32)) + 16;
     // z image, the 16 slots' exchanged rows, and the larger of the forward and
-    // inverse y images
+    // inverse y images when that still fits (else the y images are read from
+    // global memory)
     const size_t yf = size_t(dv.ay_f.ktiles) * dv.ay_f.JQ * 2 * 64 * 16;
     const size_t yi = size_t(dv.ay_i.ktiles) * dv.ay_i.JQ * (fold_y ? 2 : 1) * 2 * 64 * 16;
-    sc.fused_lds_bytes = sc.lds_bytes + size_t(16) * sc.ncy * sc.fused_mrow * 8 + std::max(yf, yi);
+    sc.fused_lds_bytes = sc.lds_bytes + size_t(16) * sc.ncy * sc.fused_mrow * 8;
+    sc.fused_y_lds = sc.fused_lds_bytes + std::max(yf, yi) <= 160 * 1024 ? 1 : 0;
+    if (sc.fused_y_lds) sc.fused_lds_bytes += std::max(yf, yi);
     sc.fuse_y = (!split && sc.ct == 1 && sc.mt == 2 && sc.th <= 2 && sc.ncls <= 2 && sc.vec && dv.K[1] <= 32 &&
                  mcols <= 256 && sc.kyt <= (fold_y ? 1 : 2) && sc.fused_lds_bytes <= 160 * 1024)
                     ? 1
                     : 0;
   }
+  dv.w1_bytes = sc.fuse_y ? 0 : w1;
+  dv.ws_bytes = dv.w1_bytes + w2;
 
-  // ---- workspace: two complex intermediates of the largest channel count ----
-  const int64_t bc = d->batch * cmax;
-  const size_t w1 = round_up(size_t(bc) * d->n_local[0] * d->n_local[1] * nn_y * 8, 256);
-  const size_t w2 = round_up(size_t(bc) * d->n_local[0] * dv.K[1] * nn_y * 8, 256);
-  dv.ws_bytes = w1 + w2;
 
   // ---- image offsets (floats, 256-byte aligned) ----
   Images& im = dv.img;

@@ -68,14 +68,21 @@ def test_invalid_descriptors(kw, status):
     assert str(e.value)
 
 
-def test_workspace_bytes():
+def test_workspace_bytes(monkeypatch):
     d = desc(batch=2, c_in=2, c_out=3)
-    # two complex intermediates (.., Nx, Ny, Kz, Kt) and (.., Nx, Ky, Kz, Kt), largest channel count
+    # complex intermediates of the largest channel count: (.., Nx, Ky, Kz, Kt) between the y and x
+    # steps, and (.., Nx, Ny, Kz, Kt) between the t+z and y steps when those are separate launches
     w1 = 2 * 3 * 4 * 10 * 4 * 3 * 8
     w2 = 2 * 3 * 4 * 4 * 4 * 3 * 8
     r = lambda v: (v + 255) // 256 * 256
-    assert D.dtst_desc_workspace_bytes(d) == r(w1) + r(w2)
+    monkeypatch.delenv("DTST_SCHEDULE", raising=False)
+    assert D.dtst_desc_workspace_bytes(d) == r(w2)          # y fused into the stream kernels
     assert D.dtst_desc_workspace_bytes(desc(batch=0)) == 0
+    # N_t = 6 (not a multiple of 4) keeps the separate launches
+    d6 = desc(batch=2, c_in=2, c_out=3, n_global=(12, 10, 8, 6), n_local=(4, 10, 8, 6))
+    assert D.dtst_desc_workspace_bytes(d6) == r(2 * 3 * 4 * 10 * 4 * 3 * 8) + r(w2)
+    monkeypatch.setenv("DTST_SCHEDULE", "split")
+    assert D.dtst_desc_workspace_bytes(d) == r(w1) + r(w2)
 
 
 @pytest.mark.parametrize("g", [

@@ -44,14 +44,18 @@ CASES = {
     "fold2_odd_kz_kt9": ((4, 4, 24, 16), (4, 4, 24, 16), (0, 0, 0, 0), (1, 1, 5), 9, 1, 2, 1),
     # more (b, c, x) planes than the fused t+z+y kernel has resident workgroups
     "many_planes": ((48, 8, 16, 8), (48, 8, 16, 8), (0, 0, 0, 0), (4, 2, 4), 3, 2, 4, 3),
+    # N_y = N_z = 512: the fused kernels' y basis images do not fit next to the z image and the
+    # row exchange in LDS and are read from global memory
+    "y_image_global": ((2, 512, 512, 8), (2, 512, 512, 8), (0, 0, 0, 0), (1, 16, 16), 4, 1, 1, 1),
 }
 
 # Geometries whose plan takes the fused t + z + y forward kernel (K_t <= 8, at
 # most 16 z modes per class, N_t <= 32 and a multiple of 4, K_y <= 32,
 # K_z K_t <= 256): folded y with a ragged last slot group, unfolded y (pencil),
-# K above the local extent, several slot groups, many planes.
+# K above the local extent, several slot groups, many planes, y basis images
+# read from global memory.
 FUSED_CASES = ["tiny_baseline", "tiny_slab", "tiny_pencil", "k_above_nloc", "fold_ragged", "slab_like_cfg2",
-               "cfg1_full", "many_planes"]
+               "cfg1_full", "many_planes", "y_image_global"]
 
 
 def _setup(name):
