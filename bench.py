@@ -44,12 +44,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6],
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7],
                     help="workload table entry (default 2: 128^3x32 in 8 x-slabs; 5 times the backward; "
                          "6: the same grid in 2x4 (x, y) pencils)")
     ap.add_argument("--block", action="store_true",
                     help="time the whole block of Algorithm 1: after every shard's inverse, the point-wise "
                          "bypass of the shard's input and GELU (forward workloads only)")
+    ap.add_argument("--fno", action="store_true",
+                    help="time the whole FNO forward (lift, 4 Fourier layers, projection) on workload 7, the "
+                         "paper's model shape (d_v 20, modes (8, 8, 8, 16)) on 128^3 x 32 in 4 x-slabs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-times", action="store_true",
                     help="skip the per-kernel event pass (used under rocprofv3)")
@@ -353,6 +356,69 @@ def backward_workload(torch, D, synth, cfg, device):
     return w
 
 
+def fno_workload(torch, D, synth, cfg, device):
+    """FNO forward (lift, Fourier layers as Algorithm 1, projection) over
+    every shard of the workload, run one after another on this GPU."""
+    from paper_2607_14394_amd.fno import FNO
+    c = synth.CONFIGS[cfg]
+    spec = c["fno"]
+    cin, cout, L = spec["c_data_in"], spec["c_data_out"], spec["layers"]
+    shards = [synth.geometry(cfg, p) for p in range(c["shards"])]
+    g0 = shards[0]
+    dv, B = g0["c_in"], g0["batch"]
+    M = synth.n_modes(g0)
+    lift, layers, proj = synth.fno_params_np(M, dv, cin, cout, L, 1000 * cfg)
+    t = lambda a: torch.from_numpy(a).to(device)
+    fno = FNO(shards, (t(lift[0]), t(lift[1])), [(t(r), t(wb)) for r, wb in layers], (t(proj[0]), t(proj[1])),
+              device)
+    xs = [synth.torch_normal(tuple(fno.input_shape(p)), synth.seed_of(cfg, "input") + p, device)
+          for p in range(len(shards))]
+    outs = [torch.empty(fno.output_shape(p), dtype=torch.float32, device=device) for p in range(len(shards))]
+    P = len(shards)
+
+    w = Workload()
+    w.step = lambda: fno.forward(xs, outs)
+    per = work(g0, dv)
+    per["mix"] = _mix_work(g0, M // P, "mix")
+    V = _vol(g0)
+    per["block_epilogue"] = dict(bytes=B * V * 3 * dv * 4, flops=2 * B * V * dv * dv, mfma_flops=2 * B * V * dv * dv)
+    # lift (C_in -> d_v) and projection (d_v -> C_out) move and compute the same per point when C_in = C_out
+    pw = [B * V * (cin + dv) * 4, B * V * (dv + cout) * 4]
+    per["pointwise"] = dict(bytes=sum(pw) / 2, flops=B * V * dv * (cin + cout), mfma_flops=B * V * dv * (cin + cout))
+    w.work = per
+    # Minimum traffic of the network: the input and output fields once, and per Fourier layer its
+    # input activation read once, its output written once and its spectral weights read once.
+    w.bytes = P * B * V * (cin + cout) * 4 + L * (2 * P * B * V * dv * 4 + M * dv * dv * 8)
+    w.metric = "FNO forward ms and GB/s per MI355X (lift, 4 Fourier layers of Algorithm 1, projection)"
+    w.config = {"workload": c["name"], "global_grid": list(g0["n_global"]), "local_shard": list(g0["n_local"]),
+                "shards_run_in_sequence": P, "batch": B, "d_v": dv, "c_data_in": cin, "c_data_out": cout,
+                "fourier_layers": L, "modes": [2 * g0["kmax"][0], 2 * g0["kmax"][1], 2 * g0["kmax"][2], g0["kt"]]}
+
+    def cpu_sample(min_seconds=10.0):
+        """One Fourier layer of one (b, c) slice of shard 0 (forward, inverse,
+        bypass and GELU of that channel) and the mix over a mode range, on the
+        fp64 oracle."""
+        import numpy as np
+        import oracle as O
+        nc, ms = 1, 4096
+        geo = _geo(O, g0, batch=1, c_in=nc, c_out=nc)
+        xs0 = xs[0][0:1, 0:nc].cpu().numpy()
+        Rs = layers[0][0][:ms]
+        Xs = synth.np_complex_normal((B, dv, ms), 12345)
+        Ys = synth.np_complex_normal((1, nc) + geo.K, 12346)
+        t0 = time.perf_counter()
+        O.forward(xs0, geo)
+        O.mix(Xs, Rs, 0, ms, c_out=dv)
+        O.block_epilogue(xs0, np.eye(nc), O.inverse(Ys, geo))
+        dt = time.perf_counter() - t0
+        frac = (2 * nc * V * 4 + ms * dv * dv * 8) / w.bytes
+        return dt, frac, (f"fp64 oracle: one Fourier layer of one (b, c) slice of shard 0 and the mix over {ms} "
+                          f"modes; GB/s scaled by the share of the forward's bytes it covers ({frac:.2e})")
+
+    w.cpu_sample = cpu_sample
+    return w
+
+
 def cpu_baseline(w):
     """Times the fp64 oracle on the workload's sample with the BLAS threads
     set to the cores this process may use."""
@@ -415,7 +481,10 @@ def main():
     import synth
 
     device = "cuda"
-    cfg = args.workload
+    cfg = 7 if args.fno else args.workload
+    if args.fno and args.block:
+        print("--fno already includes every block's bypass and GELU", file=sys.stderr)
+        sys.exit(2)
     if args.hbm_warmup_gb > 0:
         # Set-up only, outside every timed region: the stream kernels run up to
         # 13% slower on the first large buffers a fresh process places in HBM;
@@ -432,8 +501,14 @@ def main():
     if args.block and cfg == 5:
         print("--block applies to the forward workloads (1-4)", file=sys.stderr)
         sys.exit(2)
-    w = (backward_workload(torch, D, synth, cfg, device) if cfg == 5
-         else forward_workload(torch, D, synth, cfg, device, block=args.block))
+    if cfg == 7 and not args.fno:
+        print("workload 7 is the FNO forward: run it with --fno", file=sys.stderr)
+        sys.exit(2)
+    if args.fno:
+        w = fno_workload(torch, D, synth, cfg, device)
+    else:
+        w = (backward_workload(torch, D, synth, cfg, device) if cfg == 5
+             else forward_workload(torch, D, synth, cfg, device, block=args.block))
     log(f"warmup {args.warmup} steps")
 
     # ---- warmup ----

@@ -169,6 +169,20 @@ dtst_status dtst_inverse_adj(dtst_plan_t p, const float* g_y, void* g_yhat, int 
 dtst_status dtst_mix_wgrad(dtst_plan_t p, const void* xhat, const void* g_yhat, void* g_w_shard,
                            int64_t m0, int64_t m1, int accumulate, void* stream);
 
+/* Point-wise linear layer over the points of a (B, C, points) tensor: the
+ * lift P and the projection Q that the FNO applies before and after its
+ * Fourier layers (Sec. II), read as single linear layers with a bias:
+ *   y[b,o,n] = act( sum_i w[o,i] x[b,i,n] + bias[o] ),
+ * act = 0: identity, act = 1: GELU(v) = v (1 + erf(v / sqrt 2)) / 2.
+ * x: (batch, c_in, points) fp32; y: (batch, c_out, points) fp32; w: (c_out,
+ * c_in) fp32 row-major; bias: c_out fp32, or NULL for none.  Device arrays
+ * owned by the caller, 16-byte aligned; x must not overlap y
+ * (DTST_ERR_INVALID_ARG); c_in * c_out + c_out <= 40960 (DTST_ERR_UNSUPPORTED).
+ * Independent of any plan; runs on the current device, asynchronous on
+ * `stream`, no allocation. */
+dtst_status dtst_pointwise(const float* x, const float* w, const float* bias, float* y, int64_t batch,
+                           int64_t c_in, int64_t c_out, int64_t points, int act, void* stream);
+
 /* Block epilogue (Sec. V block structure; Algorithm 1, first and last step):
  * the point-wise linear bypass of the block input added to the spectral
  * output, through the activation, in place on y:

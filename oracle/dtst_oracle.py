@@ -22,6 +22,8 @@ Distributed Spectral Neural Operators", arXiv 2607.14394):
 * block epilogue                -- Sec. V (block structure), Algorithm 1: the
                                    point-wise bypass W x added to the spectral
                                    output, through GELU
+* FNO forward                   -- Sec. II: lift P, L Fourier layers (each as
+                                   Algorithm 1), projection Q
 
 Readings taken where the paper is silent:
 
@@ -34,6 +36,9 @@ Readings taken where the paper is silent:
 * Phases are reduced as exact integers, (k * n) mod N, before any trig call.
 * GELU is the exact form v Phi(v) (erf), the bypass W a real (C_out x C_in)
   matrix with no bias (Algorithm 1 names neither an approximation nor a bias).
+* The point-wise networks P and Q of the FNO (Sec. II names them, not their
+  depth) are single linear layers with a bias; every Fourier layer, the last
+  included, ends in GELU as Algorithm 1 returns it.
 
 Every routine works in float64 / complex128.  Contractions are done one
 dimension at a time (the DFT kernel is a product over dimensions), in the
@@ -53,7 +58,7 @@ __all__ = [
     "Geometry", "retained_indices", "retained_t", "basis", "half_weights",
     "forward", "inverse", "forward_adj", "inverse_adj", "mix",
     "mix_data_grad", "mix_wgrad", "forward_at_modes", "inverse_at_points", "forward_adj_at_points",
-    "n_modes", "mode_index", "gelu", "block_epilogue",
+    "n_modes", "mode_index", "gelu", "block_epilogue", "pointwise", "fno_forward",
 ]
 
 
@@ -352,3 +357,43 @@ def block_epilogue(x, w_bypass, y):
     y = np.asarray(y, dtype=np.float64)
     y0 = np.tensordot(w, x, axes=([1], [1]))          # (C_out, B, ...)
     return gelu(np.moveaxis(y0, 0, 1) + y)
+
+
+# ---------------------------------------------------------------------------
+# FNO forward (Sec. II: lift P, L Fourier layers, projection Q)
+# ---------------------------------------------------------------------------
+def pointwise(x, w, bias=None, act=False):
+    """y[b,o,n] = act(sum_i W[o,i] x[b,i,n] + bias[o]): a point-wise linear
+    layer, the reading of the lift P and the projection Q; act applies GELU.
+
+    x: (B, C_in, ...) real, w: (C_out, C_in) real, bias: (C_out,) or None."""
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    y = np.moveaxis(np.tensordot(w, x, axes=([1], [1])), 0, 1)   # (B, C_out, ...)
+    if bias is not None:
+        b = np.asarray(bias, dtype=np.float64)
+        y = y + b.reshape((1, -1) + (1,) * (y.ndim - 2))
+    return gelu(y) if act else y
+
+
+def fno_forward(x, g: Geometry, lift, blocks, proj):
+    """FNO forward on the whole domain g (offset 0, c_in = c_out = d_v):
+
+        v_0     = P(x)                                   lift, (C_data_in -> d_v)
+        v_{l+1} = GELU(W_l v_l + I(R_l F(v_l)))          Fourier layer l (Algorithm 1)
+        out     = Q(v_L)                                 projection, (d_v -> C_data_out)
+
+    F and I are the forward and inverse partial DFTs over the retained modes
+    (``forward``, ``inverse``), R_l the mode-wise channel mix (``mix`` over all
+    M modes), W_l the point-wise bypass.  lift = (w, bias), proj = (w, bias),
+    blocks = [(R_l (M, d_v, d_v) complex, W_l (d_v, d_v) real), ...].  The
+    result does not depend on how the domain is split into shards: the shard
+    spectra sum to the whole-domain spectrum (Eq. dtst_reduce) and the inverse
+    is evaluated point by point."""
+    v = pointwise(x, lift[0], lift[1])
+    M = n_modes(g)
+    for r_l, w_l in blocks:
+        xh = forward(v, g)
+        yh = mix(xh, r_l, 0, M).reshape((v.shape[0], np.asarray(r_l).shape[2]) + g.K)
+        v = block_epilogue(v, w_l, inverse(yh, g))
+    return pointwise(v, proj[0], proj[1])

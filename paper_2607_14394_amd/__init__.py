@@ -17,7 +17,7 @@ __all__ = [
     "DtstError", "Desc", "lib", "make_desc", "dtst_desc_validate", "dtst_desc_workspace_bytes",
     "dtst_basis_host", "dtst_plan", "dtst_plan_destroy", "dtst_plan_info", "dtst_forward", "dtst_mix",
     "dtst_inverse", "dtst_forward_adj", "dtst_inverse_adj", "dtst_mix_wgrad", "dtst_block_epilogue",
-    "dtst_inverse_block",
+    "dtst_inverse_block", "dtst_pointwise",
     "dtst_profile_enable",
     "dtst_profile_collect", "Plan", "LIB_PATH",
 ]
@@ -78,6 +78,7 @@ def _load():
         "dtst_mix_wgrad": [P, VP, VP, VP, I64, I64, I, VP],
         "dtst_block_epilogue": [P, VP, VP, VP, VP],
         "dtst_inverse_block": [P, VP, VP, VP, VP, VP, SZ, VP],
+        "dtst_pointwise": [VP, VP, VP, VP, I64, I64, I64, I64, I, VP],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -213,6 +214,24 @@ def dtst_block_epilogue(plan, x, w_bypass, y, stream=None):
 def dtst_inverse_block(plan, yhat, x, w_bypass, y, ws, stream=None):
     _check(lib.dtst_inverse_block(plan, _ptr(yhat), _ptr(x), _ptr(w_bypass), _ptr(y), *_wsargs(ws),
                                   _stream(stream)))
+
+
+def dtst_pointwise(x, w, bias, y, act=0, stream=None):
+    """y = act(w x + bias) over the points of x (batch, c_in, ...) into y
+    (batch, c_out, ...); bias may be None.  Shape checks here, arithmetic in
+    the library."""
+    import torch
+    if x.dim() < 2 or y.dim() != x.dim() or x.shape[0] != y.shape[0] or x.shape[2:] != y.shape[2:]:
+        raise ValueError(f"x {tuple(x.shape)} and y {tuple(y.shape)} must be (batch, channels, points...)")
+    for t, name in ((x, "x"), (w, "w"), (y, "y")) + (((bias, "bias"),) if bias is not None else ()):
+        if t.device.type != "cuda" or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 device tensor")
+    B, ci, co = x.shape[0], x.shape[1], y.shape[1]
+    if tuple(w.shape) != (co, ci) or (bias is not None and tuple(bias.shape) != (co,)):
+        raise ValueError(f"w must be ({co}, {ci}) and bias ({co},)")
+    points = x[0, 0].numel()
+    _check(lib.dtst_pointwise(_ptr(x), _ptr(w), _ptr(bias), _ptr(y), int(B), int(ci), int(co), int(points), int(act),
+                              _stream(stream)))
 
 
 def dtst_mix_wgrad(plan, xhat, g_yhat, g_w_shard, m0, m1, accumulate, stream=None):

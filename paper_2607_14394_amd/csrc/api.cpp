@@ -98,10 +98,10 @@ dtst_status check_ws(const dtst_plan_st* p, const void* ws, size_t ws_bytes) {
 
 // ---- per-kernel event timing (dtst_profile_enable / dtst_profile_collect) ----
 enum KernelRole { K_FWD_TZ, K_AXIS_FWD_Y, K_AXIS_FWD_X, K_AXIS_INV_X, K_AXIS_INV_Y, K_INV_ZT, K_MIX, K_MIX_H,
-                  K_WGRAD, K_BLOCK, K_FWD_TZY, K_INV_YZT, K_COUNT };
+                  K_WGRAD, K_BLOCK, K_FWD_TZY, K_INV_YZT, K_POINTWISE, K_COUNT };
 const char* const kRoleNames[K_COUNT] = {"stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "axis_inv_x", "axis_inv_y",
                                          "stream_inv_zt", "mix", "mix_h", "wgrad", "block_epilogue",
-                                         "stream_fwd_tzy", "stream_inv_yzt"};
+                                         "stream_fwd_tzy", "stream_inv_yzt", "pointwise"};
 
 struct Profiler {
   std::mutex mu;
@@ -470,6 +470,32 @@ dtst_status run_block_epilogue(const dtst_plan_st* p, const float* x, const floa
 }  // namespace
 
 extern "C" {
+
+dtst_status dtst_pointwise(const float* x, const float* w, const float* bias, float* y, int64_t batch, int64_t c_in,
+                           int64_t c_out, int64_t points, int act, void* stream) {
+  if (batch < 0 || points < 0 || c_in < 1 || c_out < 1)
+    return fail(DTST_ERR_INVALID_ARG, "need batch >= 0, points >= 0, c_in >= 1, c_out >= 1");
+  if (act != 0 && act != 1) return fail(DTST_ERR_INVALID_ARG, "act must be 0 (identity) or 1 (GELU)");
+  if ((c_in * c_out + c_out) * int64_t(sizeof(float)) > 160 * 1024)
+    return fail(DTST_ERR_UNSUPPORTED, "c_in * c_out + c_out above 40960: the weights must fit in LDS");
+  if (batch == 0 || points == 0) return ok();
+  DTST_TRY(check_ptr(x, "x"));
+  DTST_TRY(check_ptr(w, "w"));
+  if (bias != nullptr) DTST_TRY(check_ptr(bias, "bias"));
+  DTST_TRY(check_ptr(y, "y"));
+  int64_t nx = 0, ny = 0;
+  if (__builtin_mul_overflow(batch * c_in, points, &nx) || __builtin_mul_overflow(batch * c_out, points, &ny) ||
+      nx > (int64_t(1) << 50) || ny > (int64_t(1) << 50))
+    return fail(DTST_ERR_INVALID_ARG, "problem size overflows the supported element counts");
+  const char* xb = reinterpret_cast<const char*>(x);
+  const char* yb = reinterpret_cast<const char*>(y);
+  if (xb < yb + size_t(ny) * sizeof(float) && yb < xb + size_t(nx) * sizeof(float))
+    return fail(DTST_ERR_INVALID_ARG, "x and y overlap");
+  const int e = timed(K_POINTWISE, stream, [&] {
+    return dtst::launch_pointwise(x, w, bias, y, batch, c_in, c_out, points, act, stream);
+  });
+  return device_status(e, "point-wise launch");
+}
 
 dtst_status dtst_block_epilogue(dtst_plan_t p, const float* x, const float* w_bypass, float* y, void* stream) {
   DTST_TRY(check_plan(p));

@@ -135,6 +135,10 @@ int launch_mix_h(const void* gy, const void* w, void* gx, int64_t B, int64_t ci,
 // y <- GELU(w x + y) over B batch entries of V points (block epilogue).
 int launch_block_epilogue(const float* x, const float* w, float* y, int64_t B, int64_t ci, int64_t co, int64_t V,
                           void* stream);
+// y = act(w x + bias) over B batch entries of V points (lift / projection);
+// bias may be null (zero); act 1 = GELU.
+int launch_pointwise(const float* x, const float* w, const float* bias, float* y, int64_t B, int64_t ci, int64_t co,
+                     int64_t V, int act, void* stream);
 int launch_wgrad(const void* xhat, const void* gy, void* gw, int64_t B, int64_t ci, int64_t co,
                  int64_t M, int64_t m0, int64_t m1, int accumulate, void* stream);
 

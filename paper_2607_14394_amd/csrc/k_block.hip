@@ -1,15 +1,17 @@
-// Block epilogue (Sec. V "Block Structure", Algorithm 1 first and last
-// step): the point-wise linear bypass of the block input added to the
-// spectral output, through the activation,
+// Point-wise linear layers over the points of a (B, C, V) tensor:
 //
-//   y[b,o,n] <- GELU( sum_i w[o,i] x[b,i,n] + y[b,o,n] ),   GELU(v) = v Phi(v),
+//   block epilogue (Sec. V "Block Structure", Algorithm 1 first and last
+//   step), in place on the spectral output y:
+//     y[b,o,n] <- GELU( sum_i w[o,i] x[b,i,n] + y[b,o,n] ),   GELU(v) = v Phi(v);
+//   lift P and projection Q of the FNO (Sec. II), into a separate y:
+//     y[b,o,n]  = act( sum_i w[o,i] x[b,i,n] + bias[o] ),   act = identity or GELU.
 //
-// in place on y (the output of the inverse partial DFT).  Per point this is a
-// (C_out x C_in) matrix-vector product, about 2 C_in C_out / (4 (C_in + 2 C_out))
-// flop per byte (2.7 at C = 16): bound by HBM traffic on x and y, so it runs on
-// the VALU.  Each thread owns four consecutive points of one batch entry
-// (16-byte accesses), reads their C_in input channels once per chunk of 16
-// output channels, and reads w from LDS (the same entry for every lane).
+// Per point this is a (C_out x C_in) matrix-vector product, about
+// 2 C_in C_out / (4 (C_in + 2 C_out)) flop per byte (2.7 at C = 16): bound by
+// HBM traffic on x and y, so it runs on the VALU.  Each thread owns four
+// consecutive points of one batch entry (16-byte accesses), reads their C_in
+// input channels once per chunk of 16 output channels, and reads w (and the
+// bias) from LDS (the same entry for every lane).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -25,17 +27,22 @@ __device__ __forceinline__ float gelu(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
 }
 
-template <int VEC>
+// ADDY: the accumulators start from y (block epilogue), else from the bias
+// (zero without one).  ACT: 1 applies GELU, 0 none.
+template <int VEC, int ADDY, int ACT>
 __global__ void __launch_bounds__(256)
-block_epilogue_kernel(const float* __restrict__ x, const float* __restrict__ w, float* __restrict__ y, int64_t V,
-                      int64_t total, int ci, int co) {
+pointwise_kernel(const float* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
+                 float* __restrict__ y, int64_t V, int64_t total, int ci, int co) {
   // VEC: 4 points per thread (V % 4 == 0, 16-byte accesses), else 1.
   constexpr int P = VEC ? 4 : 1;
   const int64_t VP = V / P;
-  // w in LDS: every lane reads the same entry (a broadcast), which keeps it
-  // out of the scalar registers.
+  // w (and the bias) in LDS: every lane reads the same entry (a broadcast),
+  // which keeps them out of the scalar registers.
   extern __shared__ float sw[];
+  float* sb = sw + co * ci;
   for (int e = threadIdx.x; e < co * ci; e += blockDim.x) sw[e] = w[e];
+  if (!ADDY)
+    for (int e = threadIdx.x; e < co; e += blockDim.x) sb[e] = bias ? bias[e] : 0.f;
   __syncthreads();
   for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
        idx += int64_t(gridDim.x) * blockDim.x) {
@@ -43,14 +50,17 @@ block_epilogue_kernel(const float* __restrict__ x, const float* __restrict__ w, 
     const float* xb = x + b * ci * V + n;
     float* yb = y + b * co * V + n;
     for (int o0 = 0; o0 < co; o0 += OC) {
-      // the accumulators start from y, loaded before the x loop so that its
-      // latency overlaps the reads of x
+      // the accumulators start from y (loaded before the x loop so that its
+      // latency overlaps the reads of x) or from the bias
       float acc[OC][P];
 #pragma unroll
       for (int oo = 0; oo < OC; ++oo) {
         const int o = o0 + oo < co ? o0 + oo : co - 1;
         const float* yp = yb + int64_t(o) * V;
-        if constexpr (VEC) {
+        if constexpr (!ADDY) {
+#pragma unroll
+          for (int p = 0; p < P; ++p) acc[oo][p] = sb[o];
+        } else if constexpr (VEC) {
           const float4 v = *reinterpret_cast<const float4*>(yp);
           acc[oo][0] = v.x;
           acc[oo][1] = v.y;
@@ -84,41 +94,56 @@ block_epilogue_kernel(const float* __restrict__ x, const float* __restrict__ w, 
       for (int oo = 0; oo < OC; ++oo) {
         if (o0 + oo >= co) continue;
         float* yp = yb + int64_t(o0 + oo) * V;
+        float r[P];
+#pragma unroll
+        for (int p = 0; p < P; ++p) r[p] = ACT ? gelu(acc[oo][p]) : acc[oo][p];
         if constexpr (VEC) {
-          *reinterpret_cast<float4*>(yp) =
-              make_float4(gelu(acc[oo][0]), gelu(acc[oo][1]), gelu(acc[oo][2]), gelu(acc[oo][3]));
+          *reinterpret_cast<float4*>(yp) = make_float4(r[0], r[1], r[2], r[3]);
         } else {
-          *yp = gelu(acc[oo][0]);
+          *yp = r[0];
         }
       }
     }
   }
 }
 
-}  // namespace
 
-int launch_block_epilogue(const float* x, const float* w, float* y, int64_t B, int64_t ci, int64_t co, int64_t V,
-                          void* stream) {
+template <int ADDY, int ACT>
+int launch_pw(const float* x, const float* w, const float* bias, float* y, int64_t B, int64_t ci, int64_t co,
+              int64_t V, void* stream) {
   if (B <= 0 || V <= 0) return hipSuccess;
   const bool vec = V % 4 == 0;
   const int64_t total = B * (vec ? V / 4 : V);
   const int64_t cap = int64_t(1) << 20;
   const int64_t blocks = std::min<int64_t>((total + 255) / 256, cap);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const size_t lds = size_t(ci) * co * sizeof(float);
-  const void* fn = vec ? reinterpret_cast<const void*>(block_epilogue_kernel<1>)
-                       : reinterpret_cast<const void*>(block_epilogue_kernel<0>);
+  const size_t lds = (size_t(ci) * co + (ADDY ? 0 : co)) * sizeof(float);
+  const void* fn = vec ? reinterpret_cast<const void*>(pointwise_kernel<1, ADDY, ACT>)
+                       : reinterpret_cast<const void*>(pointwise_kernel<0, ADDY, ACT>);
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
   }
   if (vec)
-    hipLaunchKernelGGL(block_epilogue_kernel<1>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s, x, w, y, V,
-                       total, static_cast<int>(ci), static_cast<int>(co));
+    hipLaunchKernelGGL((pointwise_kernel<1, ADDY, ACT>), dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s, x, w,
+                       bias, y, V, total, static_cast<int>(ci), static_cast<int>(co));
   else
-    hipLaunchKernelGGL(block_epilogue_kernel<0>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s, x, w, y, V,
-                       total, static_cast<int>(ci), static_cast<int>(co));
+    hipLaunchKernelGGL((pointwise_kernel<0, ADDY, ACT>), dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s, x, w,
+                       bias, y, V, total, static_cast<int>(ci), static_cast<int>(co));
   return hipGetLastError();
+}
+
+}  // namespace
+
+int launch_block_epilogue(const float* x, const float* w, float* y, int64_t B, int64_t ci, int64_t co, int64_t V,
+                          void* stream) {
+  return launch_pw<1, 1>(x, w, nullptr, y, B, ci, co, V, stream);
+}
+
+int launch_pointwise(const float* x, const float* w, const float* bias, float* y, int64_t B, int64_t ci, int64_t co,
+                     int64_t V, int act, void* stream) {
+  return act ? launch_pw<0, 1>(x, w, bias, y, B, ci, co, V, stream)
+             : launch_pw<0, 0>(x, w, bias, y, B, ci, co, V, stream);
 }
 
 }  // namespace dtst

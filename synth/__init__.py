@@ -8,7 +8,9 @@ waves).  Every array it returns is fed unchanged to both the HIP library and
 the fp64 CPU oracle.
 
 Seeds: input 1000*cfg, weights 1000*cfg + 1, upstream gradient 1000*cfg + 2,
-synthetic spectra 1000*cfg + 3, bypass weights 1000*cfg + 4.
+synthetic spectra 1000*cfg + 3, bypass weights 1000*cfg + 4, lift 1000*cfg + 5,
+projection 1000*cfg + 6 (the Fourier layer l of an FNO adds 10*l to the weight
+and bypass seeds).
 
 The paper's workload (PDEBench 3D compressible Navier-Stokes, 128^3 x 21
 steps, d_v = 20, modes (8, 8, 8, 16)) is not available here; these fields
@@ -52,10 +54,17 @@ CONFIGS = {
             n_global=(128, 128, 128, 32), n_local=(64, 32, 128, 32), shards=8, grid=(2, 4),
             kmax=(16, 16, 16), kt=8, batch=1, c_in=16, c_out=16,
             field="normal+waves"),
+    # The paper's model (Sec. VI-A): d_v = 20, 4 Fourier layers, modes (8, 8, 8, 16),
+    # 128^3 grid in 4 x-slabs; 5 input and 5 output fields as in 3D compressible
+    # Navier-Stokes; N_t = 32 so that k_t = 16 is a half spectrum.
+    7: dict(name="FNO forward: 128^3x32 in 4 x-slabs of 32, B1, lift 5->20, 4 blocks, modes 16/16/16/16, proj 20->5",
+            n_global=(128, 128, 128, 32), n_local=(32, 128, 128, 32), shards=4,
+            kmax=(8, 8, 8), kt=16, batch=1, c_in=20, c_out=20, field="normal",
+            fno=dict(c_data_in=5, c_data_out=5, layers=4)),
 }
 
 # Workloads whose every shard is run, one after another, on the one GPU.
-ALL_SHARDS = (2, 6)
+ALL_SHARDS = (2, 6, 7)
 
 # Plane waves planted in every channel of workload 2: (k, phase), amplitude 5.
 # k is a signed (x, y, z, t) wavenumber.  The second wave sits on the -k_max
@@ -68,7 +77,20 @@ CFG2_AMPLITUDE = 5.0
 
 
 def seed_of(cfg: int, what: str) -> int:
-    return 1000 * cfg + {"input": 0, "weights": 1, "upstream": 2, "spectrum": 3, "bypass": 4}[what]
+    return 1000 * cfg + {"input": 0, "weights": 1, "upstream": 2, "spectrum": 3, "bypass": 4, "lift": 5,
+                         "proj": 6}[what]
+
+
+def fno_params_np(M, dv, c_in, c_out, layers, seed):
+    """Seeded FNO parameters as host arrays: lift (w (dv, c_in), b (dv,)),
+    layers [(R (M, dv, dv) complex64 with E|R|^2 = 1/dv^2, W (dv, dv) float32
+    ~ N(0, 1/dv))], projection (w (c_out, dv), b (c_out,)); the scales keep the
+    activations of order one through the layers."""
+    lift = (np_normal((dv, c_in), seed + 5, std=1.0 / math.sqrt(c_in)), np_normal((dv,), seed + 15, std=0.1))
+    blocks = [(np_weights(M, dv, dv, seed + 1 + 10 * l), np_normal((dv, dv), seed + 4 + 10 * l, std=1.0 / math.sqrt(dv)))
+              for l in range(layers)]
+    proj = (np_normal((c_out, dv), seed + 6, std=1.0 / math.sqrt(dv)), np_normal((c_out,), seed + 16, std=0.1))
+    return lift, blocks, proj
 
 
 def geometry(cfg: int, shard: int | None = None) -> dict:

@@ -454,3 +454,67 @@ def test_block_epilogue_special_cases_and_brute_force():
                     s += w[o, i] * x[(b, i) + n]
                 ref[(b, o) + n] = 0.5 * s * (1.0 + math.erf(s / math.sqrt(2.0)))
     assert np.allclose(got, ref, rtol=0, atol=1e-14)
+
+
+def test_pointwise_brute_force_and_special_cases():
+    """The point-wise layer equals the per-point loop written out; with the
+    identity matrix and no bias it returns x, and with act it returns GELU."""
+    rng = np.random.default_rng(41)
+    B, ci, co, shape = 2, 3, 2, (2, 3, 2, 4)
+    x = rng.standard_normal((B, ci) + shape)
+    w = rng.standard_normal((co, ci))
+    b = rng.standard_normal(co)
+    got = O.pointwise(x, w, b)
+    ref = np.empty((B, co) + shape)
+    for bb in range(B):
+        for o in range(co):
+            for n in np.ndindex(*shape):
+                s = b[o]
+                for i in range(ci):
+                    s += w[o, i] * x[(bb, i) + n]
+                ref[(bb, o) + n] = s
+    assert np.allclose(got, ref, rtol=0, atol=1e-14)
+    assert np.allclose(O.pointwise(x, np.eye(ci)), x, rtol=0, atol=0)
+    g = O.pointwise(x, np.eye(ci), act=True)
+    assert np.allclose(g, [[[[[[0.5 * v * (1 + math.erf(v / math.sqrt(2))) for v in r3] for r3 in r2] for r2 in r1]
+                             for r1 in c] for c in bx] for bx in x], rtol=0, atol=1e-15)
+
+
+def _fno_fft(x, g, lift, blocks, proj):
+    """The FNO forward written with numpy's FFT: rfftn, gather of the
+    retained modes, per-mode channel mix, scatter into the zero spectrum,
+    irfftn; bypass and GELU (math.erf) per point; lift and projection as
+    matrix products over the channel axis."""
+    erf = np.vectorize(math.erf)
+    act = lambda v: 0.5 * v * (1.0 + erf(v / math.sqrt(2.0)))
+    chan = lambda w, v: np.einsum("oi,bi...->bo...", w, v)
+    v = chan(lift[0], x) + lift[1][None, :, None, None, None, None]
+    for r, wb in blocks:
+        F = _fft_forward(v, g)                                   # (B, C, Kx, Ky, Kz, Kt)
+        B, C = F.shape[:2]
+        Fm = F.reshape(B, C, -1)                                  # m = flattened mode index
+        Y = np.einsum("bim,mio->bom", Fm, r).reshape((B, r.shape[2]) + g.K)
+        v = act(chan(wb, v) + _fft_inverse(Y, g))
+    return chan(proj[0], v) + proj[1][None, :, None, None, None, None]
+
+
+@pytest.mark.parametrize("n_global,kmax,kt", [((8, 6, 4, 6), (2, 2, 1), 3), ((6, 5, 8, 8), (3, 2, 3), 5)])
+def test_fno_forward_matches_fft_formulation(n_global, kmax, kt):
+    """The oracle's FNO forward (direct partial DFTs) equals the same network
+    evaluated through numpy's FFT, four Fourier layers deep; with no Fourier
+    layer it is the projection of the lift."""
+    rng = np.random.default_rng(43)
+    dv, cin, cout, B = 3, 2, 2, 2
+    g = O.Geometry(n_global, n_global, (0, 0, 0, 0), kmax, kt, B, dv, dv)
+    M = O.n_modes(g)
+    x = rng.standard_normal((B, cin) + tuple(n_global))
+    lift = (rng.standard_normal((dv, cin)), rng.standard_normal(dv))
+    proj = (rng.standard_normal((cout, dv)), rng.standard_normal(cout))
+    blocks = [((rng.standard_normal((M, dv, dv)) + 1j * rng.standard_normal((M, dv, dv))) / dv,
+               rng.standard_normal((dv, dv)) / math.sqrt(dv)) for _ in range(4)]
+    got = O.fno_forward(x, g, lift, blocks, proj)
+    ref = _fno_fft(x, g, lift, blocks, proj)
+    assert got.shape == (B, cout) + tuple(n_global)
+    assert rel(got, ref) < 1e-12
+    direct = np.einsum("oi,bi...->bo...", proj[0] @ lift[0], x) + (proj[0] @ lift[1] + proj[1])[None, :, None, None, None, None]
+    assert rel(O.fno_forward(x, g, lift, [], proj), direct) < 1e-13
