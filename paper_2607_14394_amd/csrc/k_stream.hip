@@ -367,11 +367,10 @@ struct FusedArgs {
   int mcols;       // K_z * K_t
   int mrow;        // LDS row stride in complex values
   int nwy;         // waves running the y contraction: ceil(mcols / 16)
-  int yimg_n4;     // float4 entries of the y image staged in LDS after the row exchange;
-                   // 0: read from global memory (the image does not fit in LDS)
+  int yimg_n4;     // float4 entries of the y image (staged in LDS when the kernel's YL is 1)
 };
 
-template <int TH, int NCLS, int MODE, int NCY, int KYT, int NW, int NB>
+template <int TH, int NCLS, int MODE, int NCY, int KYT, int NW, int NB, int YL>
 __global__ void __launch_bounds__(64 * NW)
 fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const float* __restrict__ timg,
                const float4* __restrict__ zimg, const float4* __restrict__ yimg, StreamArgs a, FusedArgs f) {
@@ -409,17 +408,23 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
     return c;
   };
   // Row of a tile for this wave; slots past the plane's end read its first
-  // row and contribute zeros.
+  // row and contribute zeros, and positions past the last plane (loaded but
+  // never contracted) read the last plane.  Every load is unconditional: a
+  // load behind a branch would make the compiler wait for all outstanding
+  // loads (one memory counter) before each tile instead of for that tile's.
   auto row_of = [&](const Cur& c, bool* valid) {
     const int s = 16 * c.q + w + NW * c.j;
     *valid = s < f.slots;
-    return c.pl * f.ny + (*valid ? s + c.h * f.half : 0);
+    const int64_t pl = c.pl < f.planes ? c.pl : f.planes - 1;
+    return pl * f.ny + (*valid ? s + c.h * f.half : 0);
   };
 
   // NB tile buffers: buffer k holds the tile at cb[k] and is refilled, once
   // contracted, with the tile NB positions further on, so NB - 1 tiles are in
-  // flight while one is contracted.  The first loads go out before the
-  // images are staged.
+  // flight while one is contracted.  The first tile's loads go out before the
+  // images are staged, the others after: the staging loads wait for every
+  // load issued before them (one memory counter), and the first tiles of the
+  // whole grid take several microseconds to arrive.
   float xb[NB][NCLS][TH][4];
   bool okb[NB][NCLS][TH * 4];
   bool vb[NB];
@@ -428,20 +433,28 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
 #pragma unroll
   for (int k = 1; k < NB; ++k) cb[k] = advance(cb[k - 1]);
 #pragma unroll
-  for (int k = 0; k < NB; ++k) {
-    vb[k] = false;
-    if (cb[k].pl < f.planes) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cb[k], &vb[k]), cb[k].zt, xb[k], okb[k]);
-  }
-
-  // LDS: z image, the exchanged row results, the y image.
-  float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
-  for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
-  for (int i = threadIdx.x; i < f.yimg_n4; i += blockDim.x) ylds[i] = yimg[i];
-  __syncthreads();
-
+  for (int k = 0; k < NB; ++k) vb[k] = false;
+  load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cb[0], &vb[0]), cb[0].zt, xb[0], okb[0]);
+  // B operand of the t contraction.
   float bt[TH * 4][CT];
 #pragma unroll
   for (int st = 0; st < TH * 4; ++st) bt[st][0] = timg[st * 64 + lane];
+
+  // LDS: z image, the exchanged row results, the y image (YL = 1; with
+  // YL = 0 the y image is read from global memory).
+  float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
+  for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
+  if (YL)
+    for (int i = threadIdx.x; i < f.yimg_n4; i += blockDim.x) ylds[i] = yimg[i];
+  __syncthreads();
+  // Every load so far (the first tile, the t basis, the staging) completes
+  // here, before the other buffers' loads go out.  Without this explicit
+  // wait the compiler cannot tell, inside the tile loop, that those loads
+  // are done, and it makes each pass of the loop wait for all outstanding
+  // loads (one memory counter), which empties the prefetch.
+  __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+  for (int k = 1; k < NB; ++k) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cb[k], &vb[k]), cb[k].zt, xb[k], okb[k]);
 
   v4f yr[NCY][KYT][MTW], yi[NCY][KYT][MTW];
 #pragma unroll
@@ -458,14 +471,18 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
   // Contract buffer k's tile and refill the buffer; at a row's end leave its
   // results in LDS, and after the wave's last row of a slot group run the
   // group's y contraction.
+  // Tiles past the last plane (live = false, the same for the whole
+  // workgroup) are loaded but not contracted.
   auto process = [&](int k) __attribute__((always_inline)) {
     const Cur c = cb[k];
     const bool valid = vb[k];
+    const bool live = c.pl < f.planes;
     v4f V[NCLS][CT];
-    t_part<CT, TH, NCLS, MODE>(xb[k], okb[k], bt, V);
+    if (live) t_part<CT, TH, NCLS, MODE>(xb[k], okb[k], bt, V);
     const Cur far = advance(cb[(k + NB - 1) % NB]);
     cb[k] = far;
-    if (far.pl < f.planes) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(far, &vb[k]), far.zt, xb[k], okb[k]);
+    load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(far, &vb[k]), far.zt, xb[k], okb[k]);
+    if (!live) return;
     z_part<CT, MT, NCLS>(V, lds, a, c.zt, lane, P);
     if (c.zt != a.zt - 1) return;
     float2* vrow = vlds + (c.h * 16 + w + NW * c.j) * f.mrow;
@@ -481,7 +498,7 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
       for (int kk = 0; kk < KYT; ++kk) {
         const int kt = NCY == 2 ? cl * f.kth + kk : kk;
         const int e = (kt * f.jq + c.q) * 2 * 64 + lane;
-        if (f.yimg_n4 > 0) {
+        if constexpr (YL) {
           br[cl][kk] = ylds[e];
           bi[cl][kk] = ylds[e + 64];
         } else {
@@ -538,26 +555,24 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
     __syncthreads();
   };
 
-  // Tiles in order through buffers 0, 1, ..., NB - 1, 0, ...; the loop ends
-  // after the tile whose successor lies past the last plane.  The buffer
-  // index is a compile-time constant at every step (the buffers stay in
-  // registers).
+  // Tiles in order through buffers 0, 1, ..., NB - 1, 0, ...; every pass runs
+  // all NB steps (steps past the last plane only load), and the only exit is
+  // at the end of a pass.  The buffer index is a compile-time constant at
+  // every step (the buffers stay in registers), and no path leaves a step
+  // early: an exit between steps would give the compiler a path on which a
+  // buffer's loads are followed by fewer loads than the other buffers', and
+  // its waits for that buffer would then cover all outstanding loads.
   static_assert(NB >= 1 && NB <= 4, "one to four tile buffers");
   auto step = [&](auto kc) __attribute__((always_inline)) {
     constexpr int k = decltype(kc)::value;
-    const bool more = cb[(k + 1) % NB].pl < f.planes;
     process(k);
-    return more;
   };
-  while (true) {
-    if (!step(std::integral_constant<int, 0>{})) return;
-    if constexpr (NB > 1)
-      if (!step(std::integral_constant<int, 1>{})) return;
-    if constexpr (NB > 2)
-      if (!step(std::integral_constant<int, 2>{})) return;
-    if constexpr (NB > 3)
-      if (!step(std::integral_constant<int, 3>{})) return;
-  }
+  do {
+    step(std::integral_constant<int, 0>{});
+    if constexpr (NB > 1) step(std::integral_constant<int, 1>{});
+    if constexpr (NB > 2) step(std::integral_constant<int, 2>{});
+    if constexpr (NB > 3) step(std::integral_constant<int, 3>{});
+  } while (cb[0].pl < f.planes);
 }
 
 // Register budget: the common shapes fit 4 waves per SIMD (128 registers);
@@ -790,7 +805,7 @@ inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
 // inv_zt_body does and streams them out; a second barrier frees the LDS rows.
 // The (N_y x K_z K_t) intermediate never reaches HBM.
 // ---------------------------------------------------------------------------
-template <int TH, int NCLS, int MODE, int NCY, int JQY>
+template <int TH, int NCLS, int MODE, int NCY, int JQY, int YL>
 __global__ void __launch_bounds__(1024)
 inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float* __restrict__ timg,
                const float4* __restrict__ zimg, const float4* __restrict__ yimg, StreamArgs a, FusedArgs f) {
@@ -826,10 +841,12 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
         }
   }
 
-  // LDS: z image, the exchanged rows, the y image.
+  // LDS: z image, the exchanged rows, the y image (YL = 1; with YL = 0 the
+  // y image is read from global memory).
   float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
   for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
-  for (int i = threadIdx.x; i < f.yimg_n4; i += blockDim.x) ylds[i] = yimg[i];
+  if (YL)
+    for (int i = threadIdx.x; i < f.yimg_n4; i += blockDim.x) ylds[i] = yimg[i];
   __syncthreads();
 
   // A operand of the t expansion: rows t = 16mt + m, K index c = 4g + i.
@@ -855,8 +872,8 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
           for (int cl = 0; cl < NCY; ++cl) {
             // image entry (((tile * JQ + q) * NCY + class) * 2 + part) * 64 + lane
             const int e = ((gq * JQY + q) * NCY + cl) * 2 * 64 + lane;
-            const float4 br = f.yimg_n4 > 0 ? ylds[e] : yimg[e];
-            const float4 bi = f.yimg_n4 > 0 ? ylds[e + 64] : yimg[e + 64];
+            const float4 br = YL ? ylds[e] : yimg[e];
+            const float4 bi = YL ? ylds[e + 64] : yimg[e + 64];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const float2 v = u[cl][q][i];
@@ -949,43 +966,56 @@ void pick0(int th, int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
   else pick1<CT, 4>(mt, ncls, mode, f, v);
 }
 
-template <int TH, int NCLS, int MODE>
-fused_fn pick_fused3(int ncy, int kyt) {
-  if (ncy == 2) return fwd_tzy_kernel<TH, NCLS, MODE, 2, 1, kFusedWaves, kFusedBufs>;
-  if (kyt == 1) return fwd_tzy_kernel<TH, NCLS, MODE, 1, 1, kFusedWaves, kFusedBufs>;
-  return fwd_tzy_kernel<TH, NCLS, MODE, 1, 2, kFusedWaves, kFusedBufs>;
-}
-
-template <int TH, int NCLS>
-fused_fn pick_fused2(int mode, int ncy, int kyt) {
-  return mode == 2 ? pick_fused3<TH, NCLS, 2>(ncy, kyt) : pick_fused3<TH, NCLS, 1>(ncy, kyt);
+template <int TH, int NCLS, int MODE, int YL>
+fused_fn pick_fused4(int ncy, int kyt) {
+  if (ncy == 2) return fwd_tzy_kernel<TH, NCLS, MODE, 2, 1, kFusedWaves, kFusedBufs, YL>;
+  if (kyt == 1) return fwd_tzy_kernel<TH, NCLS, MODE, 1, 1, kFusedWaves, kFusedBufs, YL>;
+  return fwd_tzy_kernel<TH, NCLS, MODE, 1, 2, kFusedWaves, kFusedBufs, YL>;
 }
 
 template <int TH, int NCLS, int MODE>
-ifused_fn pick_ifused3(int ncy, int jqy) {
-  if (ncy == 2) return inv_yzt_kernel<TH, NCLS, MODE, 2, 1>;
-  if (jqy == 1) return inv_yzt_kernel<TH, NCLS, MODE, 1, 1>;
-  return inv_yzt_kernel<TH, NCLS, MODE, 1, 2>;
+fused_fn pick_fused3(int ncy, int kyt, int yl) {
+  return yl ? pick_fused4<TH, NCLS, MODE, 1>(ncy, kyt) : pick_fused4<TH, NCLS, MODE, 0>(ncy, kyt);
 }
 
 template <int TH, int NCLS>
-ifused_fn pick_ifused2(int mode, int ncy, int jqy) {
-  return mode == 2 ? pick_ifused3<TH, NCLS, 2>(ncy, jqy) : pick_ifused3<TH, NCLS, 1>(ncy, jqy);
+fused_fn pick_fused2(int mode, int ncy, int kyt, int yl) {
+  return mode == 2 ? pick_fused3<TH, NCLS, 2>(ncy, kyt, yl) : pick_fused3<TH, NCLS, 1>(ncy, kyt, yl);
 }
 
-// Fused y + z + t instances: as below, with JQY 16-wide K steps per y class.
+template <int TH, int NCLS, int MODE, int YL>
+ifused_fn pick_ifused4(int ncy, int jqy) {
+  if (ncy == 2) return inv_yzt_kernel<TH, NCLS, MODE, 2, 1, YL>;
+  if (jqy == 1) return inv_yzt_kernel<TH, NCLS, MODE, 1, 1, YL>;
+  return inv_yzt_kernel<TH, NCLS, MODE, 1, 2, YL>;
+}
+
+template <int TH, int NCLS, int MODE>
+ifused_fn pick_ifused3(int ncy, int jqy, int yl) {
+  return yl ? pick_ifused4<TH, NCLS, MODE, 1>(ncy, jqy) : pick_ifused4<TH, NCLS, MODE, 0>(ncy, jqy);
+}
+
+template <int TH, int NCLS>
+ifused_fn pick_ifused2(int mode, int ncy, int jqy, int yl) {
+  return mode == 2 ? pick_ifused3<TH, NCLS, 2>(ncy, jqy, yl) : pick_ifused3<TH, NCLS, 1>(ncy, jqy, yl);
+}
+
+// Fused y + z + t instances: as below, with JQY 16-wide K steps per y class
+// and the y image in LDS (YL = 1) or read from global memory.
 ifused_fn pick_ifused(const StreamCfg& c) {
-  const int mode = mode_of(c);
-  if (c.th == 1) return c.ncls == 2 ? pick_ifused2<1, 2>(mode, c.ncy, c.kyt) : pick_ifused2<1, 1>(mode, c.ncy, c.kyt);
-  return c.ncls == 2 ? pick_ifused2<2, 2>(mode, c.ncy, c.kyt) : pick_ifused2<2, 1>(mode, c.ncy, c.kyt);
+  const int mode = mode_of(c), yl = c.fused_y_lds;
+  if (c.th == 1)
+    return c.ncls == 2 ? pick_ifused2<1, 2>(mode, c.ncy, c.kyt, yl) : pick_ifused2<1, 1>(mode, c.ncy, c.kyt, yl);
+  return c.ncls == 2 ? pick_ifused2<2, 2>(mode, c.ncy, c.kyt, yl) : pick_ifused2<2, 1>(mode, c.ncy, c.kyt, yl);
 }
 
 // Fused t + z + y instances: CT = 1, MT = 2, TH <= 2, NCLS <= 2, 16-byte
 // loads; (NCY, KYT) = (2, 1) folded, (1, 1) or (1, 2) otherwise.
 fused_fn pick_fused(const StreamCfg& c) {
-  const int mode = mode_of(c);
-  if (c.th == 1) return c.ncls == 2 ? pick_fused2<1, 2>(mode, c.ncy, c.kyt) : pick_fused2<1, 1>(mode, c.ncy, c.kyt);
-  return c.ncls == 2 ? pick_fused2<2, 2>(mode, c.ncy, c.kyt) : pick_fused2<2, 1>(mode, c.ncy, c.kyt);
+  const int mode = mode_of(c), yl = c.fused_y_lds;
+  if (c.th == 1)
+    return c.ncls == 2 ? pick_fused2<1, 2>(mode, c.ncy, c.kyt, yl) : pick_fused2<1, 1>(mode, c.ncy, c.kyt, yl);
+  return c.ncls == 2 ? pick_fused2<2, 2>(mode, c.ncy, c.kyt, yl) : pick_fused2<2, 1>(mode, c.ncy, c.kyt, yl);
 }
 
 void pick(const StreamCfg& c, fwd_fn* f, inv_fn* v) {
@@ -1093,7 +1123,7 @@ int launch_fwd_tzy(const StreamCfg& c, const AxisCfg& ay, const float* x, void* 
   f.mcols = c.kz * c.kt;
   f.mrow = c.fused_mrow;
   f.nwy = (f.mcols + 15) / 16;
-  f.yimg_n4 = c.fused_y_lds ? ay.ktiles * ay.JQ * 2 * 64 : 0;
+  f.yimg_n4 = ay.ktiles * ay.JQ * 2 * 64;
   const int64_t grid = planes < c.grid_fused ? planes : c.grid_fused;
   hipLaunchKernelGGL(pick_fused(c), dim3(static_cast<unsigned>(grid)), dim3(64 * kFusedWaves), c.fused_lds_bytes,
                      static_cast<hipStream_t>(stream), x, static_cast<float2*>(out), timg,
@@ -1118,7 +1148,7 @@ int launch_inv_yzt(const StreamCfg& c, const AxisCfg& ay, const void* in, float*
   f.mcols = c.kz * c.kt;
   f.mrow = c.fused_mrow;
   f.nwy = (f.mcols + 15) / 16;
-  f.yimg_n4 = c.fused_y_lds ? ay.ktiles * ay.JQ * (ay.fold == 2 ? 2 : 1) * 2 * 64 : 0;
+  f.yimg_n4 = ay.ktiles * ay.JQ * (ay.fold == 2 ? 2 : 1) * 2 * 64;
   if (planes > int64_t(0x7fffffff)) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL(pick_ifused(c), dim3(static_cast<unsigned>(planes)), dim3(1024), c.fused_lds_bytes,
                      static_cast<hipStream_t>(stream), static_cast<const float2*>(in), y, timg,
