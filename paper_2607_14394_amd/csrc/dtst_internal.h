@@ -36,6 +36,9 @@ struct StreamCfg {
   int zt = 0;   // ceil(zh / 16)
   int kcp = 0;  // padded slots per class = 8*mt
   int vec = 0;  // 1 when N_t % 4 == 0 (16-byte row chunks)
+  // 1 when t folds: CT = 2, N_t = 32 and the shard holds the whole t extent
+  // (the t images then hold the folded layout of the split kernels)
+  int tf = 0;
   size_t lds_bytes = 0;
   // Fused t + z + y (fwd_tzy_kernel) and y + z + t (inv_yzt_kernel), used
   // when fuse_y is set:

@@ -60,6 +60,15 @@ __device__ __forceinline__ float ror8(float v) {
 //   y(z + jN/NCLS) = sum_c conj(w)^(cj) E_c(z).
 // V and E hold complex values as two column tiles (tile 0 Re, tile 1 Im) when
 // CT = 2, which makes the factors +-i lane-local; NCLS = 4 is only used then.
+//
+// t folding (TF = 1; CT = 2, N_t = 16 TH with TH even, t undistributed).
+// B_t[k, t + N_t/2] = (-1)^k B_t[k, t], so even k_t only need the sums
+// x(t) + x(t + N_t/2) and odd k_t the differences, over t < N_t/2: half the
+// t products.  Column tile 0 then holds the even k_t and tile 1 the odd ones.
+// In the forward's t-contracted values (columns = lanes) Re of k_t = 2c + ct
+// sits in lane m = c and Im in lane m = c + 8; in the inverse's z-expanded
+// values (rows = accumulator registers 4g + i) k_t = 2(2g + (i & 1)) + ct
+// with Re in registers 0, 1 and Im in registers 2, 3.
 // ---------------------------------------------------------------------------
 template <int CT>
 __device__ __forceinline__ void times_i(const v4f (&a)[CT], v4f (&out)[CT]) {
@@ -68,7 +77,24 @@ __device__ __forceinline__ void times_i(const v4f (&a)[CT], v4f (&out)[CT]) {
   out[CT - 1] = a[0];
 }
 
-template <int NCLS, int CT>
+// i * a for the forward's t-folded tiles: Re and Im 8 lanes apart.
+template <int CT>
+__device__ __forceinline__ void times_i_lanes(const v4f (&a)[CT], v4f (&out)[CT]) {
+  const float sgn = (threadIdx.x & 15) < 8 ? -1.f : 1.f;
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[ct][i] = sgn * ror8(a[ct][i]);
+}
+
+// i * a for the inverse's t-folded tiles: Re in registers 0, 1, Im in 2, 3.
+template <int CT>
+__device__ __forceinline__ void times_i_regs(const v4f (&a)[CT], v4f (&out)[CT]) {
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) out[ct] = v4f{-a[ct][2], -a[ct][3], a[ct][0], a[ct][1]};
+}
+
+template <int NCLS, int CT, int TF = 0>
 __device__ __forceinline__ void fold_classes(v4f (&V)[NCLS][CT]) {
   if constexpr (NCLS == 2) {
 #pragma unroll
@@ -90,7 +116,8 @@ __device__ __forceinline__ void fold_classes(v4f (&V)[NCLS][CT]) {
       c[ct] = V[0][ct] - V[2][ct];
       d[ct] = V[1][ct] - V[3][ct];
     }
-    times_i<CT>(d, id);
+    if constexpr (TF) times_i_lanes<CT>(d, id);
+    else times_i<CT>(d, id);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
       V[0][ct] = a[ct] + b[ct];
@@ -101,7 +128,7 @@ __device__ __forceinline__ void fold_classes(v4f (&V)[NCLS][CT]) {
   }
 }
 
-template <int NCLS, int CT>
+template <int NCLS, int CT, int TF = 0>
 __device__ __forceinline__ void unfold_classes(v4f (&E)[NCLS][CT]) {
   if constexpr (NCLS == 2) {
     // even modes + odd modes at z, even - odd at z + N_z/2
@@ -124,7 +151,8 @@ __device__ __forceinline__ void unfold_classes(v4f (&E)[NCLS][CT]) {
       c[ct] = E[0][ct] - E[2][ct];
       d[ct] = E[1][ct] - E[3][ct];
     }
-    times_i<CT>(d, id);
+    if constexpr (TF) times_i_regs<CT>(d, id);
+    else times_i<CT>(d, id);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
       E[0][ct] = a[ct] + b[ct];
@@ -181,14 +209,32 @@ __device__ __forceinline__ void load_tile(const float* __restrict__ x, const Str
 }
 
 // Contracts t of the tile held in xv (z = 16zt + m and the partner z of
-// every other class) into V, then folds the classes.
-template <int CT, int TH, int NCLS, int MODE>
+// every other class) into V, then folds the classes.  With TF the lane's
+// t and t + N_t/2 (groups h and h + TH/2) are combined first; only the
+// first 4 TH / 2 steps of bt are used then.
+template <int CT, int TH, int NCLS, int MODE, int TF = 0>
 __device__ __forceinline__ void t_part(const float (&xv)[NCLS][TH][4], const bool (&ok)[NCLS][TH * 4],
                                        const float (&bt)[TH * 4][CT], v4f (&V)[NCLS][CT]) {
 #pragma unroll
   for (int hf = 0; hf < NCLS; ++hf)
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) V[hf][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+  if constexpr (TF) {
+    static_assert(CT == 2 && TH % 2 == 0 && MODE != 0, "t folding needs two k_t tiles and whole 16-byte t groups");
+#pragma unroll
+    for (int h = 0; h < TH / 2; ++h)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int hf = 0; hf < NCLS; ++hf) {
+          const float lo = (MODE == 2 || ok[hf][4 * h]) ? xv[hf][h][j] : 0.f;
+          const float hi = (MODE == 2 || ok[hf][4 * (h + TH / 2)]) ? xv[hf][h + TH / 2][j] : 0.f;
+          V[hf][0] = mfma(lo + hi, bt[h * 4 + j][0], V[hf][0]);
+          V[hf][1] = mfma(lo - hi, bt[h * 4 + j][1], V[hf][1]);
+        }
+    fold_classes<NCLS, CT, TF>(V);
+    return;
+  }
 #pragma unroll
   for (int h = 0; h < TH; ++h)
 #pragma unroll
@@ -233,25 +279,45 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
 
 // Contracts t, then z, of the tile (z tile zt) held in xv into P.  Within the
 // tile the independent accumulator chains are interleaved step by step.
-template <int CT, int TH, int MT, int NCLS, int MODE>
+template <int CT, int TH, int MT, int NCLS, int MODE, int TF = 0>
 __device__ __forceinline__ void tz_tile(const float (&xv)[NCLS][TH][4], const bool (&ok)[NCLS][TH * 4],
                                         const float (&bt)[TH * 4][CT], const float4* lds, const StreamArgs& a,
                                         int zt, int lane, v4f (&P)[NCLS][MT][CT]) {
   v4f V[NCLS][CT];
-  t_part<CT, TH, NCLS, MODE>(xv, ok, bt, V);
+  t_part<CT, TH, NCLS, MODE, TF>(xv, ok, bt, V);
   z_part<CT, MT, NCLS>(V, lds, a, zt, lane, P);
 }
 
 // Combines the real-stacked products of a finished row into complex
 // coefficients and hands each one to st(index p * K_t + k_t, re, im):
 // (Re B) V and (Im B) V sit in row tiles mt and mt + MT/2 of the same lane;
-// the Re / Im columns of k_t sit 8 lanes apart (CT = 1) or in the two
-// column tiles (CT = 2).
-template <int CT, int MT, int NCLS, class Store>
+// the Re / Im columns of k_t sit 8 lanes apart (CT = 1, and CT = 2 with TF)
+// or in the two column tiles (CT = 2).
+template <int CT, int MT, int NCLS, int TF = 0, class Store>
 __device__ __forceinline__ void tz_finish(const v4f (&P)[NCLS][MT][CT], const StreamArgs& a, int m, int g,
                                           Store&& st) {
   constexpr int KTP = 8 * CT;
-  if constexpr (CT == 1) {
+  if constexpr (TF) {
+    // Lanes m < 8 finish the even k_t = 2m of tile 0, lanes m >= 8 the odd
+    // k_t = 2(m - 8) + 1 of tile 1, trading values as in the CT = 1 case.
+    const bool hi = m >= 8;
+    const int kc = 2 * (m & 7) + (hi ? 1 : 0);
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int mr = 0; mr < MT / 2; ++mr)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float q0 = P[cl][mr][0][i], u0 = P[cl][mr + MT / 2][0][i];
+          const float q1 = P[cl][mr][1][i], u1 = P[cl][mr + MT / 2][1][i];
+          const float rq = ror8(hi ? q0 : q1);
+          const float ru = ror8(hi ? u0 : u1);
+          const float re = hi ? rq - u1 : q0 - ru;
+          const float im = hi ? q1 + ru : rq + u0;
+          const int p = (16 * mr + 4 * g + i) * NCLS + cl;
+          if (kc < a.kt && p < a.kz) st(p * a.kt + kc, re, im);
+        }
+  } else if constexpr (CT == 1) {
     static_assert(NCLS <= 2, "the four-class z fold needs CT = 2");
     // Lanes m < 8 finish mode p0 (k_t = m), lanes m >= 8 the next mode
     // p0 + 1 (k_t = m - 8): z class 1 of the same slot when folded, else
@@ -292,7 +358,7 @@ __device__ __forceinline__ void tz_finish(const v4f (&P)[NCLS][MT][CT], const St
 
 // Every wave walks its (row, z-tile) pairs in order and keeps the next
 // pair's loads in flight while it computes the current one.
-template <int CT, int TH, int MT, int NCLS, int MODE>
+template <int CT, int TH, int MT, int NCLS, int MODE, int TF>
 __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2* __restrict__ out,
                                             const float (&bt)[TH * 4][CT], const float4* lds,
                                             const StreamArgs& a, int64_t wave, int64_t wstride) {
@@ -327,11 +393,11 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
     }
     if (it + 1 < n_iter) load_tile<TH, NCLS, MODE>(x, a, m, g, rn, ztn, xn, okn);
 
-    tz_tile<CT, TH, MT, NCLS, MODE>(xv, ok, bt, lds, a, zt, lane, P);
+    tz_tile<CT, TH, MT, NCLS, MODE, TF>(xv, ok, bt, lds, a, zt, lane, P);
     if (zt != a.zt - 1) continue;
 
     float2* orow = out + r * int64_t(a.kz) * a.kt;
-    tz_finish<CT, MT, NCLS>(P, a, m, g, [&](int idx, float re, float im) { orow[idx] = make_float2(re, im); });
+    tz_finish<CT, MT, NCLS, TF>(P, a, m, g, [&](int idx, float re, float im) { orow[idx] = make_float2(re, im); });
   }
 }
 
@@ -576,12 +642,15 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
 }
 
 // Register budget: the common shapes fit 4 waves per SIMD (128 registers);
+// the t-folded forward up to 16 accumulator tiles fits 2 (256 registers);
 // the widest ones (many z classes / k_t tiles) are left to the compiler.
-#define DTST_STREAM_WAVES(CT, MT, NCLS, TH) \
-  __attribute__((amdgpu_waves_per_eu(((CT) * (MT) * (NCLS) <= 4 && (TH) <= 2) ? 4 : 1)))
+#define DTST_STREAM_WAVES(CT, MT, NCLS, TH, TWO) \
+  __attribute__((amdgpu_waves_per_eu(((CT) * (MT) * (NCLS) <= 4 && (TH) <= 2)   ? 4 \
+                                     : ((TWO) && (CT) * (MT) * (NCLS) <= 16) ? 2 \
+                                                                             : 1)))
 
-template <int CT, int TH, int MT, int NCLS, int MODE>
-__global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH)
+template <int CT, int TH, int MT, int NCLS, int MODE, int TF>
+__global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH, TF)
 fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
               const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
   extern __shared__ float4 lds[];
@@ -590,18 +659,19 @@ fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
-  // B operand of the t contraction, step s = 4h + j covers t = 16h + 4g + j.
+  // B operand of the t contraction, step s = 4h + j covers t = 16h + 4g + j
+  // (with TF only the first half: the folded t < N_t/2).
   float bt[TH * 4][CT];
 #pragma unroll
   for (int s = 0; s < TH * 4; ++s)
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) bt[s][ct] = timg[(s * CT + ct) * 64 + lane];
+    for (int ct = 0; ct < CT; ++ct) bt[s][ct] = (TF && s >= TH * 2) ? 0.f : timg[(s * CT + ct) * 64 + lane];
 
   const int wpb = blockDim.x >> 6;
   const int64_t wstride = int64_t(gridDim.x) * wpb;
   const int64_t wave = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6);
   if (wave >= a.rows) return;
-  fwd_tz_body<CT, TH, MT, NCLS, MODE>(x, out, bt, lds, a, wave, wstride);
+  fwd_tz_body<CT, TH, MT, NCLS, MODE, TF>(x, out, bt, lds, a, wave, wstride);
 }
 
 // ---------------------------------------------------------------------------
@@ -615,12 +685,27 @@ fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
 // MODE 0: scalar stores (N_t % 4 != 0); 1: 16-byte stores with masks;
 // 2: 16-byte stores of complete tiles, no masks.
 // ---------------------------------------------------------------------------
+// k_t and part (0 Re, 1 Im) of row m of column tile ct of the inverse's z
+// expansion: c = 16ct + m with c < 8CT the Re rows of k_t = c and the rest
+// the Im rows of k_t = c - 8CT; with TF k_t = 2(2(m >> 2) + (m & 1)) + ct
+// and part (m >> 1) & 1.
+template <int CT, int TF>
+__device__ __forceinline__ void inv_row_kt(int ct, int m, int* kt, bool* is_re) {
+  if constexpr (TF) {
+    *kt = 2 * (2 * (m >> 2) + (m & 1)) + ct;
+    *is_re = ((m >> 1) & 1) == 0;
+  } else {
+    const int c = 16 * ct + m;
+    *is_re = c < 8 * CT;
+    *kt = *is_re ? c : c - 8 * CT;
+  }
+}
+
 // Spectrum values this lane needs from one row: slot s = 16qh + 4g + i of
-// class cl at k_t column c = 16ct + m (Re and Im columns read the same value).
-template <int CT, int MT, int NCLS>
+// class cl at the k_t of row m of tile ct (Re and Im rows read the same value).
+template <int CT, int MT, int NCLS, int TF = 0>
 __device__ __forceinline__ void load_u(const float2* urow, const StreamArgs& a, int m, int g,
                                        float2 (&dst)[NCLS][CT][MT / 2][4], bool (&ok)[NCLS][CT][MT / 2][4]) {
-  constexpr int KTP = 8 * CT;
 #pragma unroll
   for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
@@ -631,8 +716,9 @@ __device__ __forceinline__ void load_u(const float2* urow, const StreamArgs& a, 
         for (int i = 0; i < 4; ++i) {
           const int s = 16 * qh + 4 * g + i;
           const int p = s * NCLS + cl;
-          const int c = 16 * ct + m;
-          const int kt = c < KTP ? c : c - KTP;
+          int kt;
+          bool is_re;
+          inv_row_kt<CT, TF>(ct, m, &kt, &is_re);
           const bool v_ok = p < a.kz && kt < a.kt;
           dst[cl][ct][qh][i] = urow[v_ok ? p * a.kt + kt : 0];
           ok[cl][ct][qh][i] = v_ok;
@@ -641,10 +727,9 @@ __device__ __forceinline__ void load_u(const float2* urow, const StreamArgs& a, 
 
 // A operand of the z expansion (rows c, K index kz' = 16q + 4g + i):
 // kz' < KCP pairs with Re C_z, kz' >= KCP with Im C_z.
-template <int CT, int MT, int NCLS>
+template <int CT, int MT, int NCLS, int TF = 0>
 __device__ __forceinline__ void build_a(const float2 (&u)[NCLS][CT][MT / 2][4], const bool (&ok)[NCLS][CT][MT / 2][4],
                                         int m, float (&A)[NCLS][CT][MT][4]) {
-  constexpr int KTP = 8 * CT;
 #pragma unroll
   for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
@@ -653,14 +738,16 @@ __device__ __forceinline__ void build_a(const float2 (&u)[NCLS][CT][MT / 2][4], 
       for (int qh = 0; qh < MT / 2; ++qh)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const bool is_re = 16 * ct + m < KTP;
+          int kt;
+          bool is_re;
+          inv_row_kt<CT, TF>(ct, m, &kt, &is_re);
           const float2 v = ok[cl][ct][qh][i] ? u[cl][ct][qh][i] : make_float2(0.f, 0.f);
           A[cl][ct][qh][i] = is_re ? v.x : v.y;
           A[cl][ct][qh + MT / 2][i] = is_re ? -v.y : v.x;
         }
 }
 
-template <int CT, int TH, int MT, int NCLS, int MODE>
+template <int CT, int TH, int MT, int NCLS, int MODE, int TF = 0>
 __device__ __forceinline__ void inv_row(const float (&A)[NCLS][CT][MT][4], float* __restrict__ yrow,
                                         const float (&ta)[TH][CT][4], const float4* lds, const StreamArgs& a,
                                         int lane) {
@@ -685,20 +772,42 @@ __device__ __forceinline__ void inv_row(const float (&A)[NCLS][CT][MT][4], float
         for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct) W[cl][ct] = mfma(A[cl][ct][q][i], B[cl][q][i], W[cl][ct]);
-    unfold_classes<NCLS, CT>(W);
+    unfold_classes<NCLS, CT, TF>(W);
     v4f Y[NCLS][TH];
 #pragma unroll
     for (int hf = 0; hf < NCLS; ++hf)
 #pragma unroll
       for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
+    if constexpr (TF) {
+      // Even k_t (tile 0) into Y[.][mt], odd k_t (tile 1) into
+      // Y[.][mt + TH/2], for t < N_t/2; then E + O at t, E - O at t + N_t/2.
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int hf = 0; hf < NCLS; ++hf)
 #pragma unroll
-          for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = mfma(ta[mt][ct][i], W[hf][ct][i], Y[hf][mt]);
+          for (int mt = 0; mt < TH / 2; ++mt) {
+            Y[hf][mt] = mfma(ta[mt][0][i], W[hf][0][i], Y[hf][mt]);
+            Y[hf][mt + TH / 2] = mfma(ta[mt][1][i], W[hf][1][i], Y[hf][mt + TH / 2]);
+          }
+#pragma unroll
+      for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+        for (int mt = 0; mt < TH / 2; ++mt) {
+          const v4f e = Y[hf][mt], o = Y[hf][mt + TH / 2];
+          Y[hf][mt] = e + o;
+          Y[hf][mt + TH / 2] = e - o;
+        }
+    } else {
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int hf = 0; hf < NCLS; ++hf)
+#pragma unroll
+            for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = mfma(ta[mt][ct][i], W[hf][ct][i], Y[hf][mt]);
+    }
 
     const int zl = zt * 16 + m;
     const bool zok = zl < a.zh;
@@ -744,7 +853,7 @@ __device__ __forceinline__ void inv_row(const float (&A)[NCLS][CT][MT][4], float
 }
 
 // Each row's spectrum is loaded one row ahead.
-template <int CT, int TH, int MT, int NCLS, int MODE>
+template <int CT, int TH, int MT, int NCLS, int MODE, int TF>
 __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float* __restrict__ y,
                                             const float (&ta)[TH][CT][4], const float4* lds,
                                             const StreamArgs& a, int64_t wave, int64_t wstride) {
@@ -755,17 +864,17 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
 
   float2 un[NCLS][CT][MT / 2][4];
   bool okn[NCLS][CT][MT / 2][4];
-  load_u<CT, MT, NCLS>(in + wave * spec_len, a, m, g, un, okn);
+  load_u<CT, MT, NCLS, TF>(in + wave * spec_len, a, m, g, un, okn);
   for (int64_t r = wave; r < a.rows; r += wstride) {
     float A[NCLS][CT][MT][4];
-    build_a<CT, MT, NCLS>(un, okn, m, A);
-    if (r + wstride < a.rows) load_u<CT, MT, NCLS>(in + (r + wstride) * spec_len, a, m, g, un, okn);
-    inv_row<CT, TH, MT, NCLS, MODE>(A, y + r * row_len, ta, lds, a, lane);
+    build_a<CT, MT, NCLS, TF>(un, okn, m, A);
+    if (r + wstride < a.rows) load_u<CT, MT, NCLS, TF>(in + (r + wstride) * spec_len, a, m, g, un, okn);
+    inv_row<CT, TH, MT, NCLS, MODE, TF>(A, y + r * row_len, ta, lds, a, lane);
   }
 }
 
-template <int CT, int TH, int MT, int NCLS, int MODE>
-__global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH)
+template <int CT, int TH, int MT, int NCLS, int MODE, int TF>
+__global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH, 0)
 inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
               const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
   extern __shared__ float4 lds[];
@@ -774,20 +883,22 @@ inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
-  // A operand of the t expansion: rows t = 16mt + m, K index c = 16ct + 4g + i.
+  // A operand of the t expansion: rows t = 16mt + m, K index c = 16ct + 4g + i
+  // (with TF only mt < TH/2: the folded t < N_t/2).
   float ta[TH][CT][4];
 #pragma unroll
   for (int mt = 0; mt < TH; ++mt)
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) ta[mt][ct][i] = timg[((mt * CT + ct) * 4 + i) * 64 + lane];
+      for (int i = 0; i < 4; ++i)
+        ta[mt][ct][i] = (TF && mt >= TH / 2) ? 0.f : timg[((mt * CT + ct) * 4 + i) * 64 + lane];
 
   const int wpb = blockDim.x >> 6;
   const int64_t wstride = int64_t(gridDim.x) * wpb;
   const int64_t wave = int64_t(blockIdx.x) * wpb + (threadIdx.x >> 6);
   if (wave >= a.rows) return;
-  inv_zt_body<CT, TH, MT, NCLS, MODE>(in, y, ta, lds, a, wave, wstride);
+  inv_zt_body<CT, TH, MT, NCLS, MODE, TF>(in, y, ta, lds, a, wave, wstride);
 }
 
 // ---------------------------------------------------------------------------
@@ -926,44 +1037,47 @@ int mode_of(const StreamCfg& c) {
   return (c.zh % 16 == 0 && c.nt == 16 * c.th) ? 2 : 1;
 }
 
-template <int CT, int TH, int MT, int NCLS>
+template <int CT, int TH, int MT, int NCLS, int TF>
 void pick3(int mode, fwd_fn* f, inv_fn* v) {
   if (mode == 2) {
-    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 2>;
-    *v = inv_zt_kernel<CT, TH, MT, NCLS, 2>;
+    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 2, TF>;
+    *v = inv_zt_kernel<CT, TH, MT, NCLS, 2, TF>;
   } else if (mode == 1) {
-    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 1>;
-    *v = inv_zt_kernel<CT, TH, MT, NCLS, 1>;
+    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 1, TF>;
+    *v = inv_zt_kernel<CT, TH, MT, NCLS, 1, TF>;
+  } else if constexpr (!TF) {
+    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 0, TF>;
+    *v = inv_zt_kernel<CT, TH, MT, NCLS, 0, TF>;
   } else {
-    *f = fwd_tz_kernel<CT, TH, MT, NCLS, 0>;
-    *v = inv_zt_kernel<CT, TH, MT, NCLS, 0>;
+    *f = nullptr;  // no scalar-load form of the t-folded kernels
+    *v = nullptr;
   }
 }
 
-template <int CT, int TH, int MT>
+template <int CT, int TH, int MT, int TF>
 void pick2(int ncls, int mode, fwd_fn* f, inv_fn* v) {
   if constexpr (CT == 2 && MT == 2) {
     if (ncls == 4) {
-      pick3<CT, TH, MT, 4>(mode, f, v);
+      pick3<CT, TH, MT, 4, TF>(mode, f, v);
       return;
     }
   }
-  if (ncls == 2) pick3<CT, TH, MT, 2>(mode, f, v);
-  else pick3<CT, TH, MT, 1>(mode, f, v);
+  if (ncls == 2) pick3<CT, TH, MT, 2, TF>(mode, f, v);
+  else pick3<CT, TH, MT, 1, TF>(mode, f, v);
 }
 
-template <int CT, int TH>
+template <int CT, int TH, int TF>
 void pick1(int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
-  if (mt == 2) pick2<CT, TH, 2>(ncls, mode, f, v);
-  else if (mt == 4) pick2<CT, TH, 4>(ncls, mode, f, v);
-  else pick2<CT, TH, 8>(ncls, mode, f, v);
+  if (mt == 2) pick2<CT, TH, 2, TF>(ncls, mode, f, v);
+  else if (mt == 4) pick2<CT, TH, 4, TF>(ncls, mode, f, v);
+  else pick2<CT, TH, 8, TF>(ncls, mode, f, v);
 }
 
 template <int CT>
 void pick0(int th, int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
-  if (th == 1) pick1<CT, 1>(mt, ncls, mode, f, v);
-  else if (th == 2) pick1<CT, 2>(mt, ncls, mode, f, v);
-  else pick1<CT, 4>(mt, ncls, mode, f, v);
+  if (th == 1) pick1<CT, 1, 0>(mt, ncls, mode, f, v);
+  else if (th == 2) pick1<CT, 2, 0>(mt, ncls, mode, f, v);
+  else pick1<CT, 4, 0>(mt, ncls, mode, f, v);
 }
 
 template <int TH, int NCLS, int MODE, int YL>
@@ -1018,8 +1132,11 @@ fused_fn pick_fused(const StreamCfg& c) {
   return c.ncls == 2 ? pick_fused2<2, 2>(mode, c.ncy, c.kyt, yl) : pick_fused2<2, 1>(mode, c.ncy, c.kyt, yl);
 }
 
+// Split t + z and z + t instances; the t-folded ones (tf: CT = 2, N_t = 32,
+// 16-byte loads) are their own set.
 void pick(const StreamCfg& c, fwd_fn* f, inv_fn* v) {
-  if (c.ct == 1) pick0<1>(c.th, c.mt, c.ncls, mode_of(c), f, v);
+  if (c.tf) pick1<2, 2, 1>(c.mt, c.ncls, mode_of(c), f, v);
+  else if (c.ct == 1) pick0<1>(c.th, c.mt, c.ncls, mode_of(c), f, v);
   else pick0<2>(c.th, c.mt, c.ncls, mode_of(c), f, v);
 }
 
@@ -1056,6 +1173,7 @@ int prepare_stream(StreamCfg* c) {
   fwd_fn f;
   inv_fn v;
   pick(*c, &f, &v);
+  if (f == nullptr || v == nullptr) return hipErrorInvalidConfiguration;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(c->lds_bytes));
   if (e != hipSuccess) return e;

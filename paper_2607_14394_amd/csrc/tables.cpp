@@ -153,6 +153,9 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
   sc.zh = sc.nz / sc.ncls;
   sc.zt = static_cast<int>(ceil_div(sc.zh, 16));
   sc.vec = (sc.nt % 4 == 0) ? 1 : 0;
+  // t folds (even k_t from x(t) + x(t + N_t/2), odd k_t from the difference)
+  // in the split kernels when the shard holds the whole t extent of 32.
+  sc.tf = (sc.ct == 2 && sc.th == 2 && sc.nt == 32 && d->n_local[3] == d->n_global[3]) ? 1 : 0;
   sc.lds_bytes = size_t(sc.ncls) * sc.zt * sc.mt * 64 * 16;
   if (sc.lds_bytes > 160 * 1024) {
     *err = "z basis image exceeds the 160 KiB LDS of a workgroup";
@@ -266,12 +269,15 @@ inline void bval(const dtst_desc& d, int dim, int64_t p, int64_t j, double* re, 
 // t image of the forward streaming kernel (B operand of the first MFMA):
 // entry ((h*4 + j)*CT + ct)*64 + lane holds Bt'[t][c] with t = 16h + 4g + j,
 // c = 16ct + m (m = lane & 15, g = lane >> 4); c < 8CT is Re B_t[kt=c][t],
-// otherwise Im B_t[kt = c - 8CT][t]; times scale(kt).
+// otherwise Im B_t[kt = c - 8CT][t]; times scale(kt).  t-folded (tf), only
+// t < N_t/2 is filled and column m of tile ct is k_t = 2(m & 7) + ct, Re for
+// m < 8 and Im otherwise (the kernel forms x(t) +- x(t + N_t/2)).
 void t_forward_image(const Derived& dv, bool adjoint_of_inverse, float* dst) {
   const StreamCfg& sc = dv.sc;
   const dtst_desc& d = dv.d;
   const int ktp = 8 * sc.ct;
   const double ntot = double(d.n_global[0]) * d.n_global[1] * d.n_global[2] * d.n_global[3];
+  const int tlim = sc.tf ? sc.nt / 2 : sc.nt;
   for (int h = 0; h < sc.th; ++h)
     for (int j = 0; j < 4; ++j)
       for (int ct = 0; ct < sc.ct; ++ct)
@@ -279,10 +285,10 @@ void t_forward_image(const Derived& dv, bool adjoint_of_inverse, float* dst) {
           const int m = lane & 15, g = lane >> 4;
           const int t = 16 * h + 4 * g + j;
           const int c = 16 * ct + m;
-          const bool is_re = c < ktp;
-          const int kt = is_re ? c : c - ktp;
+          const bool is_re = sc.tf ? m < 8 : c < ktp;
+          const int kt = sc.tf ? 2 * (m & 7) + ct : (is_re ? c : c - ktp);
           double v = 0.0;
-          if (t < sc.nt && kt < sc.kt) {
+          if (t < tlim && kt < sc.kt) {
             double re, im;
             bval(d, 3, kt, t, &re, &im);
             double s = adjoint_of_inverse ? half_weight(d.n_global[3], kt) / ntot : 1.0;
@@ -323,12 +329,15 @@ void z_forward_image(const Derived& dv, float* dst) {
 // t image of the inverse streaming kernel (A operand of its second MFMA):
 // entry ((mt*CT + ct)*4 + i)*64 + lane holds A[t][c] with t = 16mt + m,
 // c = 16ct + 4g + i: Re C_t[t][kt] for c < 8CT, -Im C_t[t][kt] otherwise,
-// where C_t[t][kt] = scale(kt) conj(B_t[kt][t]).
+// where C_t[t][kt] = scale(kt) conj(B_t[kt][t]).  t-folded (tf), only
+// t < N_t/2 is filled and K index 4g + i of tile ct is
+// k_t = 2(2g + (i & 1)) + ct, Re for i < 2 and Im otherwise.
 void t_inverse_image(const Derived& dv, bool is_inverse, float* dst) {
   const StreamCfg& sc = dv.sc;
   const dtst_desc& d = dv.d;
   const int ktp = 8 * sc.ct;
   const double ntot = double(d.n_global[0]) * d.n_global[1] * d.n_global[2] * d.n_global[3];
+  const int tlim = sc.tf ? sc.nt / 2 : sc.nt;
   for (int mt = 0; mt < sc.th; ++mt)
     for (int ct = 0; ct < sc.ct; ++ct)
       for (int i = 0; i < 4; ++i)
@@ -336,10 +345,10 @@ void t_inverse_image(const Derived& dv, bool is_inverse, float* dst) {
           const int m = lane & 15, g = lane >> 4;
           const int t = 16 * mt + m;
           const int c = 16 * ct + 4 * g + i;
-          const bool is_re = c < ktp;
-          const int kt = is_re ? c : c - ktp;
+          const bool is_re = sc.tf ? i < 2 : c < ktp;
+          const int kt = sc.tf ? 2 * (2 * g + (i & 1)) + ct : (is_re ? c : c - ktp);
           double v = 0.0;
-          if (t < sc.nt && kt < sc.kt) {
+          if (t < tlim && kt < sc.kt) {
             double re, im;
             bval(d, 3, kt, t, &re, &im);  // B_t = re + i im; conj(B_t) = re - i im
             const double s = is_inverse ? half_weight(d.n_global[3], kt) / ntot : 1.0;

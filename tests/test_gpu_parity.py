@@ -42,6 +42,13 @@ CASES = {
     "radix4_full_tiles": ((4, 4, 64, 32), (4, 4, 64, 32), (0, 0, 0, 0), (2, 2, 32), 16, 1, 2, 2),
     # odd k_max(z) with N_z % 4 == 0 and k_t > 8 keeps the two-class fold
     "fold2_odd_kz_kt9": ((4, 4, 24, 16), (4, 4, 24, 16), (0, 0, 0, 0), (1, 1, 5), 9, 1, 2, 1),
+    # t fold (k_t > 8, whole N_t = 32): two z classes with a ragged z tile and an odd k_t count,
+    # 64 slots of unfolded sharded z, 32 slots per class in an x slab; with N_t = 32 of a
+    # sharded t the unfolded two-tile kernels run instead
+    "tfold_two_class_ragged": ((6, 8, 36, 32), (6, 8, 36, 32), (0, 0, 0, 0), (2, 3, 9), 13, 1, 2, 3),
+    "tfold_z_shard_mt8": ((4, 6, 96, 32), (4, 6, 40, 32), (0, 0, 24, 0), (1, 2, 20), 16, 1, 1, 2),
+    "tfold_mt4_slab": ((8, 6, 90, 32), (4, 6, 90, 32), (4, 0, 0, 0), (2, 2, 20), 16, 2, 1, 1),
+    "t_shard_nt32_kt16": ((4, 4, 16, 64), (4, 4, 16, 32), (0, 0, 0, 32), (1, 2, 4), 16, 1, 2, 2),
     # more (b, c, x) planes than the fused t+z+y kernel has resident workgroups
     "many_planes": ((48, 8, 16, 8), (48, 8, 16, 8), (0, 0, 0, 0), (4, 2, 4), 3, 2, 4, 3),
     # N_y = N_z = 512: the fused kernels' y basis images do not fit next to the z image and the
