@@ -701,11 +701,25 @@ __device__ __forceinline__ void inv_row_kt(int ct, int m, int* kt, bool* is_re) 
   }
 }
 
-// Spectrum values this lane needs from one row: slot s = 16qh + 4g + i of
-// class cl at the k_t of row m of tile ct (Re and Im rows read the same value).
+// Spectrum index (p * K_t + k_t) of the value this lane needs for slot
+// s = 16qh + 4g + i of class cl at the k_t of row m of tile ct, or -1 when
+// the mode is not retained.  A pure function of the lane and the shape, so
+// the validity is recomputed where it is used instead of being kept in
+// registers across the row-ahead load.
+template <int CT, int NCLS, int TF>
+__device__ __forceinline__ int u_index(const StreamArgs& a, int m, int g, int cl, int ct, int qh, int i, bool* is_re) {
+  const int s = 16 * qh + 4 * g + i;
+  const int p = s * NCLS + cl;
+  int kt;
+  inv_row_kt<CT, TF>(ct, m, &kt, is_re);
+  return (p < a.kz && kt < a.kt) ? p * a.kt + kt : -1;
+}
+
+// Spectrum values this lane needs from one row (Re and Im rows read the same
+// value; lanes of modes that are not retained read the row start).
 template <int CT, int MT, int NCLS, int TF = 0>
 __device__ __forceinline__ void load_u(const float2* urow, const StreamArgs& a, int m, int g,
-                                       float2 (&dst)[NCLS][CT][MT / 2][4], bool (&ok)[NCLS][CT][MT / 2][4]) {
+                                       float2 (&dst)[NCLS][CT][MT / 2][4]) {
 #pragma unroll
   for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
@@ -714,22 +728,17 @@ __device__ __forceinline__ void load_u(const float2* urow, const StreamArgs& a, 
       for (int qh = 0; qh < MT / 2; ++qh)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int s = 16 * qh + 4 * g + i;
-          const int p = s * NCLS + cl;
-          int kt;
           bool is_re;
-          inv_row_kt<CT, TF>(ct, m, &kt, &is_re);
-          const bool v_ok = p < a.kz && kt < a.kt;
-          dst[cl][ct][qh][i] = urow[v_ok ? p * a.kt + kt : 0];
-          ok[cl][ct][qh][i] = v_ok;
+          const int idx = u_index<CT, NCLS, TF>(a, m, g, cl, ct, qh, i, &is_re);
+          dst[cl][ct][qh][i] = urow[idx < 0 ? 0 : idx];
         }
 }
 
 // A operand of the z expansion (rows c, K index kz' = 16q + 4g + i):
 // kz' < KCP pairs with Re C_z, kz' >= KCP with Im C_z.
 template <int CT, int MT, int NCLS, int TF = 0>
-__device__ __forceinline__ void build_a(const float2 (&u)[NCLS][CT][MT / 2][4], const bool (&ok)[NCLS][CT][MT / 2][4],
-                                        int m, float (&A)[NCLS][CT][MT][4]) {
+__device__ __forceinline__ void build_a(const float2 (&u)[NCLS][CT][MT / 2][4], const StreamArgs& a, int m, int g,
+                                        float (&A)[NCLS][CT][MT][4]) {
 #pragma unroll
   for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
@@ -738,10 +747,9 @@ __device__ __forceinline__ void build_a(const float2 (&u)[NCLS][CT][MT / 2][4], 
       for (int qh = 0; qh < MT / 2; ++qh)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          int kt;
           bool is_re;
-          inv_row_kt<CT, TF>(ct, m, &kt, &is_re);
-          const float2 v = ok[cl][ct][qh][i] ? u[cl][ct][qh][i] : make_float2(0.f, 0.f);
+          const bool ok = u_index<CT, NCLS, TF>(a, m, g, cl, ct, qh, i, &is_re) >= 0;
+          const float2 v = ok ? u[cl][ct][qh][i] : make_float2(0.f, 0.f);
           A[cl][ct][qh][i] = is_re ? v.x : v.y;
           A[cl][ct][qh + MT / 2][i] = is_re ? -v.y : v.x;
         }
@@ -852,7 +860,8 @@ __device__ __forceinline__ void inv_row(const float (&A)[NCLS][CT][MT][4], float
   }
 }
 
-// Each row's spectrum is loaded one row ahead.
+// Each row's spectrum is loaded one row ahead (except in the t-folded
+// instances, see below).
 template <int CT, int TH, int MT, int NCLS, int MODE, int TF>
 __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float* __restrict__ y,
                                             const float (&ta)[TH][CT][4], const float4* lds,
@@ -863,18 +872,28 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
   const int64_t spec_len = int64_t(a.kz) * a.kt;
 
   float2 un[NCLS][CT][MT / 2][4];
-  bool okn[NCLS][CT][MT / 2][4];
-  load_u<CT, MT, NCLS, TF>(in + wave * spec_len, a, m, g, un, okn);
+  if constexpr (TF) {
+    // The t-folded instances run two waves per SIMD, which hide each row's
+    // spectrum load; the registers of a row-ahead copy would not fit.
+    for (int64_t r = wave; r < a.rows; r += wstride) {
+      float A[NCLS][CT][MT][4];
+      load_u<CT, MT, NCLS, TF>(in + r * spec_len, a, m, g, un);
+      build_a<CT, MT, NCLS, TF>(un, a, m, g, A);
+      inv_row<CT, TH, MT, NCLS, MODE, TF>(A, y + r * row_len, ta, lds, a, lane);
+    }
+    return;
+  }
+  load_u<CT, MT, NCLS, TF>(in + wave * spec_len, a, m, g, un);
   for (int64_t r = wave; r < a.rows; r += wstride) {
     float A[NCLS][CT][MT][4];
-    build_a<CT, MT, NCLS, TF>(un, okn, m, A);
-    if (r + wstride < a.rows) load_u<CT, MT, NCLS, TF>(in + (r + wstride) * spec_len, a, m, g, un, okn);
+    build_a<CT, MT, NCLS, TF>(un, a, m, g, A);
+    if (r + wstride < a.rows) load_u<CT, MT, NCLS, TF>(in + (r + wstride) * spec_len, a, m, g, un);
     inv_row<CT, TH, MT, NCLS, MODE, TF>(A, y + r * row_len, ta, lds, a, lane);
   }
 }
 
 template <int CT, int TH, int MT, int NCLS, int MODE, int TF>
-__global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH, 0)
+__global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH, TF)
 inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
               const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
   extern __shared__ float4 lds[];
@@ -1012,10 +1031,9 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
 #pragma unroll
         for (int h = 0; h < NCY; ++h) {
           float2 uu[NCLS][CT][MT / 2][4];
-          bool ok[NCLS][CT][MT / 2][4];
-          load_u<CT, MT, NCLS>(vlds + (h * 16 + w) * f.mrow, a, m, g, uu, ok);
+          load_u<CT, MT, NCLS>(vlds + (h * 16 + w) * f.mrow, a, m, g, uu);
           float A[NCLS][CT][MT][4];
-          build_a<CT, MT, NCLS>(uu, ok, m, A);
+          build_a<CT, MT, NCLS>(uu, a, m, g, A);
           inv_row<CT, TH, MT, NCLS, MODE>(A, y + (pl * f.ny + s + h * f.half) * row_len, ta, lds, a, lane);
         }
       }
