@@ -83,7 +83,7 @@ def work(g, channels, m_count=None):
     w["stream_fwd_tz"] = dict(
         bytes=rows * (Nz * Nt * 4 + Kz * Kt * 8),
         flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz,
-        mfma_flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz / _z_classes(g))
+        mfma_flops=rows * Nz * 4 * Kt * Nt / _t_classes(g) + rows * Kt * 8 * Kz * Nz / _z_classes(g))
     fy = 0.5 if _folded(g, 1) else 1.0
     fx = 0.5 if _folded(g, 0) else 1.0
     w["axis_fwd_y"] = dict(bytes=B * C * Nx * (Ny + Ky) * Kz * Kt * 8, flops=B * C * Nx * Kz * Kt * 8 * Ky * Ny)
@@ -116,6 +116,14 @@ def work(g, channels, m_count=None):
 def _folded(g, dim):
     """The library folds a dimension whose whole even extent is local."""
     return g["n_local"][dim] == g["n_global"][dim] and g["n_global"][dim] % 2 == 0
+
+
+def _t_classes(g):
+    """2 when the streaming kernels fold t (8 < k_t <= 16 and the whole
+    N_t = 32 local: even k_t from the sums of t and t + N_t/2, odd k_t from
+    the differences), else 1; the t MFMA work divides by it."""
+    nt = g["n_local"][3]
+    return 2 if 8 < g["kt"] <= 16 and nt == 32 and g["n_global"][3] == nt else 1
 
 
 def _z_classes(g):
@@ -438,16 +446,17 @@ def cpu_baseline(w):
             "kind": "oracle", "seconds": round(dt, 2), "sample": desc}
 
 
-def traffic_entry(kernel, launches_per_step):
-    """HBM bytes per launch from committed FETCH_SIZE / WRITE_SIZE counters,
-    scaled by the copy-kernel calibration; None when the kernel source
-    changed since the counters were taken."""
+def traffic_entry(cfg, kernel):
+    """HBM bytes per launch of one kernel role of workload cfg from committed
+    FETCH_SIZE / WRITE_SIZE counters, scaled by the copy-kernel calibration;
+    None when the workload has no counters or the kernel source changed
+    since they were taken."""
     try:
         with open(COUNTERS_FILE) as f:
             c = json.load(f)
     except Exception:
         return None
-    ent = c.get("kernels", {}).get(kernel)
+    ent = c.get("workloads", {}).get(str(cfg), {}).get("kernels", {}).get(kernel)
     if not ent:
         return None
     src = os.path.join(ROOT, "paper_2607_14394_amd", "csrc", ent.get("source", "k_stream.hip"))
@@ -567,6 +576,7 @@ def main():
             if wk is None:
                 continue
             stages[k] = {"launches_per_step": n // args.steps, "avg_ms": round(avg, 4),
+                         "bytes_per_launch": int(wk["bytes"]), "flops_per_launch": int(wk["flops"]),
                          "GB_s": round(wk["bytes"] / (avg / 1e3) / 1e9, 1),
                          "TFLOP_s": round(wk["flops"] / (avg / 1e3) / 1e12, 2),
                          "mfma_TFLOP_s": round(wk["mfma_flops"] / (avg / 1e3) / 1e12, 2)}
@@ -574,7 +584,7 @@ def main():
         n, avg = kernel_ms[dom]
         wk = w.work[dom]
         ach = wk["bytes"] / (avg / 1e3) / 1e9
-        tr = traffic_entry(dom, n // args.steps) if cfg == 2 else None
+        tr = None if args.block or args.fno else traffic_entry(cfg, dom)
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None if tr is None else int(tr),
                 "algorithmic_bytes_per_launch": int(wk["bytes"]), "avg_launch_ms": round(avg, 4)}
