@@ -421,6 +421,60 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
 // Waves per workgroup and tile buffers per wave of fwd_tzy_kernel.
 constexpr int kFusedWaves = 8;
 constexpr int kFusedBufs = 4;
+// Staging of the fused kernels' basis images in LDS: entries [0, nimg) of
+// the staged range are the z image, the next ny4 the y image, which sits
+// yshift float4 further on in LDS (after the row exchange).  The copy runs in
+// passes of four float4 per thread.  stage_begin copies every pass but the
+// last and issues the last pass's loads; the caller then issues its own
+// first loads and calls stage_end, whose LDS stores wait only for the
+// staging loads (the memory counter retires loads in order), so the
+// caller's loads stay in flight across the barrier that follows.  Lanes past
+// the end copy the last entry again (the same value to the same address),
+// so no pass has a branch.
+struct StageLast {
+  float4 v0, v1, v2, v3;
+  int d0, d1, d2, d3;
+};
+
+__device__ __forceinline__ StageLast stage_begin(float4* lds, const float4* __restrict__ zimg,
+                                                 const float4* __restrict__ yimg, int nimg, int ny4, int yshift) {
+  const int tot = nimg + ny4;
+  const int bd = static_cast<int>(blockDim.x), tid = static_cast<int>(threadIdx.x);
+  auto src_of = [&](int i) { return i < nimg ? zimg[i] : yimg[i - nimg]; };
+  auto dst_of = [&](int i) { return i < nimg ? i : i + yshift; };
+  const int full = (tot - 1) / (4 * bd);
+#pragma unroll 1
+  for (int p = 0; p < full; ++p) {
+    const int i0 = 4 * p * bd + tid;
+    const float4 v0 = src_of(i0), v1 = src_of(i0 + bd), v2 = src_of(i0 + 2 * bd), v3 = src_of(i0 + 3 * bd);
+    lds[dst_of(i0)] = v0;
+    lds[dst_of(i0 + bd)] = v1;
+    lds[dst_of(i0 + 2 * bd)] = v2;
+    lds[dst_of(i0 + 3 * bd)] = v3;
+  }
+  const int l0 = 4 * full * bd + tid;
+  const int i0 = min(l0, tot - 1), i1 = min(l0 + bd, tot - 1), i2 = min(l0 + 2 * bd, tot - 1),
+            i3 = min(l0 + 3 * bd, tot - 1);
+  StageLast r;
+  r.v0 = src_of(i0);
+  r.v1 = src_of(i1);
+  r.v2 = src_of(i2);
+  r.v3 = src_of(i3);
+  r.d0 = dst_of(i0);
+  r.d1 = dst_of(i1);
+  r.d2 = dst_of(i2);
+  r.d3 = dst_of(i3);
+  // Keep the scheduler from moving the caller's loads above these.
+  __builtin_amdgcn_sched_barrier(0);
+  return r;
+}
+
+__device__ __forceinline__ void stage_end(float4* lds, const StageLast& r) {
+  lds[r.d0] = r.v0;
+  lds[r.d1] = r.v1;
+  lds[r.d2] = r.v2;
+  lds[r.d3] = r.v3;
+}
 
 struct FusedArgs {
   int64_t planes;  // B * C * N_x
@@ -487,10 +541,7 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
 
   // NB tile buffers: buffer k holds the tile at cb[k] and is refilled, once
   // contracted, with the tile NB positions further on, so NB - 1 tiles are in
-  // flight while one is contracted.  The first tile's loads go out before the
-  // images are staged, the others after: the staging loads wait for every
-  // load issued before them (one memory counter), and the first tiles of the
-  // whole grid take several microseconds to arrive.
+  // flight while one is contracted.
   float xb[NB][NCLS][TH][4];
   bool okb[NB][NCLS][TH * 4];
   bool vb[NB];
@@ -500,27 +551,22 @@ fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const floa
   for (int k = 1; k < NB; ++k) cb[k] = advance(cb[k - 1]);
 #pragma unroll
   for (int k = 0; k < NB; ++k) vb[k] = false;
-  load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cb[0], &vb[0]), cb[0].zt, xb[0], okb[0]);
+
+  // LDS: z image, the exchanged row results, the y image (YL = 1; with
+  // YL = 0 the y image is read from global memory).  The staging loads go
+  // out first, then the t basis and all NB tiles; the tile loop then starts
+  // with every buffer in flight, the same outstanding loads as at the end of
+  // each of its passes.
+  float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
+  const StageLast stl = stage_begin(lds, zimg, yimg, nimg, YL ? f.yimg_n4 : 0, 8 * NCY * f.mrow);
   // B operand of the t contraction.
   float bt[TH * 4][CT];
 #pragma unroll
   for (int st = 0; st < TH * 4; ++st) bt[st][0] = timg[st * 64 + lane];
-
-  // LDS: z image, the exchanged row results, the y image (YL = 1; with
-  // YL = 0 the y image is read from global memory).
-  float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
-  for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
-  if (YL)
-    for (int i = threadIdx.x; i < f.yimg_n4; i += blockDim.x) ylds[i] = yimg[i];
-  __syncthreads();
-  // Every load so far (the first tile, the t basis, the staging) completes
-  // here, before the other buffers' loads go out.  Without this explicit
-  // wait the compiler cannot tell, inside the tile loop, that those loads
-  // are done, and it makes each pass of the loop wait for all outstanding
-  // loads (one memory counter), which empties the prefetch.
-  __builtin_amdgcn_s_waitcnt(0);
 #pragma unroll
-  for (int k = 1; k < NB; ++k) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cb[k], &vb[k]), cb[k].zt, xb[k], okb[k]);
+  for (int k = 0; k < NB; ++k) load_tile<TH, NCLS, MODE>(x, a, m, g, row_of(cb[k], &vb[k]), cb[k].zt, xb[k], okb[k]);
+  stage_end(lds, stl);
+  __syncthreads();
 
   v4f yr[NCY][KYT][MTW], yi[NCY][KYT][MTW];
 #pragma unroll
@@ -951,9 +997,23 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
   const int mc = 16 * w + m;
   const bool col_ok = mc < f.mcols;
 
+  // LDS: z image, the exchanged rows, the y image (YL = 1; with YL = 0 the
+  // y image is read from global memory).  The staging loads go out first,
+  // then the spectrum operands and the t basis, which stay in flight across
+  // the staging barrier.
+  float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
+  const StageLast stl = stage_begin(lds, zimg, yimg, nimg, YL ? f.yimg_n4 : 0, 8 * NCY * f.mrow);
+
   // B operands of the y expansion: spectrum row p (class cl, K index
-  // 16q + 4g + i), column mc; zero outside the spectrum.  Issued first, so
-  // their latency overlaps the LDS staging.
+  // 16q + 4g + i), column mc.  The loads are unconditional (lanes outside the
+  // spectrum read its first value) and u_ok masks them where they are used:
+  // a load under a condition would make the staging stores below wait for
+  // every outstanding load.
+  auto u_ok = [&](int cl, int q, int i) {
+    const int kk = 16 * q + 4 * g + i;
+    const int p = NCY == 2 ? 2 * kk + cl : kk;
+    return col_ok && p < f.ky;
+  };
   float2 u[NCY][JQY][4];
   {
     const float2* sp = in + pl * int64_t(f.ky) * f.mcols;
@@ -965,19 +1025,9 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
         for (int i = 0; i < 4; ++i) {
           const int kk = 16 * q + 4 * g + i;
           const int p = NCY == 2 ? 2 * kk + cl : kk;
-          const bool ok = col_ok && p < f.ky;
-          const float2 v = sp[ok ? int64_t(p) * f.mcols + mc : 0];
-          u[cl][q][i] = ok ? v : make_float2(0.f, 0.f);
+          u[cl][q][i] = sp[u_ok(cl, q, i) ? int64_t(p) * f.mcols + mc : 0];
         }
   }
-
-  // LDS: z image, the exchanged rows, the y image (YL = 1; with YL = 0 the
-  // y image is read from global memory).
-  float4* ylds = reinterpret_cast<float4*>(vlds + 16 * NCY * f.mrow);
-  for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
-  if (YL)
-    for (int i = threadIdx.x; i < f.yimg_n4; i += blockDim.x) ylds[i] = yimg[i];
-  __syncthreads();
 
   // A operand of the t expansion: rows t = 16mt + m, K index c = 4g + i.
   float ta[TH][CT][4];
@@ -985,6 +1035,8 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
   for (int mt = 0; mt < TH; ++mt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) ta[mt][0][i] = timg[(mt * 4 + i) * 64 + lane];
+  stage_end(lds, stl);
+  __syncthreads();
 
   const int64_t row_len = int64_t(a.nz) * a.nt;
   {
@@ -1006,7 +1058,7 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
             const float4 bi = YL ? ylds[e + 64] : yimg[e + 64];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const float2 v = u[cl][q][i];
+              const float2 v = u_ok(cl, q, i) ? u[cl][q][i] : make_float2(0.f, 0.f);
               er[cl] = mfma(br[i], v.x, er[cl]);
               ei[cl] = mfma(br[i], v.y, ei[cl]);
               er[cl] = mfma(bi[i], -v.y, er[cl]);
