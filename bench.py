@@ -442,8 +442,18 @@ def cpu_baseline(w):
     finally:
         if ctx is not None:
             ctx.__exit__(None, None, None)
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
+    blas = None
+    if threadpool_limits:
+        libs = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        blas = ", ".join(sorted({"%s %s" % (i.get("internal_api"), i.get("version")) for i in libs})) or None
     return {"value": round(w.bytes * frac / dt / 1e9, 3), "unit": "GB/s", "cores": int(threads),
-            "kind": "oracle", "seconds": round(dt, 2), "sample": desc}
+            "kind": "oracle", "seconds": round(dt, 2), "sample": desc, "cpu_model": cpu_model, "blas": blas}
 
 
 def traffic_entry(cfg, kernel):
@@ -552,6 +562,16 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / args.steps
 
+    # ---- per-step pass: each step bracketed by its own events (median, min) ----
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record(stream)
+        w.step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    per_step = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+
     # ---- per-kernel pass: every launch bracketed by HIP events ----
     kernel_ms = {}
     if not args.no_kernel_times:
@@ -594,6 +614,9 @@ def main():
         "value": round(gbs, 2), "unit": "GB/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "step_ms": {"mean": round(ms_per_step, 4), "median": round(per_step[len(per_step) // 2], 4),
+                    "min": round(per_step[0], 4), "note": "median and min from a separate pass that brackets "
+                                                          "each step with its own events"},
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "layer_ms": round(ms_per_step, 4),
         "layer_TFLOP_s": round(w.flops / sec / 1e12, 3),
