@@ -23,7 +23,8 @@
 // per wave) and a block of up to KT 16-row tiles of k.  Every lane streams
 // in[b][j][n] for its n with 8-byte loads (16 lanes cover 128 contiguous
 // bytes), one 16-row step ahead of the MFMAs that consume it; the basis image
-// is read with 16-byte loads that hit in L1/L2.  The epilogue trades values
+// is read with 16-byte loads that hit in L1/L2, each step's tiles issued
+// after the next step's input rows.  The epilogue trades values
 // between neighbouring lanes so that every store writes two complex values
 // (16 bytes) and each store instruction covers whole 128-byte lines.
 #include <hip/hip_runtime.h>
@@ -38,6 +39,11 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ v4f mfma(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
+
+// Hides a value from the optimizer: a load from an address chosen by a
+// select would otherwise be split into a branch with one load per arm, and
+// the compiler's waits after such a branch cover every outstanding load.
+__device__ __forceinline__ void opaque(int64_t& v) { __asm__ volatile("" : "+v"(v)); }
 
 // Value of the neighbouring lane (lane ^ 1) via DPP quad_perm [1, 0, 3, 2].
 __device__ __forceinline__ float swap_adjacent(float v) {
@@ -114,6 +120,10 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
 
     const int nw = nbk * (64 * NT) + wave * (16 * NT);  // first column of this wave
     const float2* inb = in + b * int64_t(a.J) * a.NN;
+    // Entry read by lanes outside the tile (masked when used): per lane, so
+    // that the compiler does not turn the load into a branch with a scalar
+    // load of a uniform address for those lanes.
+    const int64_t spare = m < int64_t(a.J) * a.NN ? m : 0;
 
     // K index jj = 16q + 4g + i.  FOLD 0: row jj.  FOLD 1: rows jj and
     // jj + J/2.  FOLD 2: rows 2jj (even modes) and 2jj + 1 (odd modes).
@@ -132,7 +142,9 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
               const int row = FOLD == 0 ? jj : (FOLD == 1 ? jj + s * a.jh : 2 * jj + c);
-              dst[c][s][nt][i] = inb[v_ok ? int64_t(row) * a.NN + n : 0];
+              int64_t idx = v_ok ? int64_t(row) * a.NN + n : spare;
+              opaque(idx);
+              dst[c][s][nt][i] = inb[idx];
             }
         }
     };
@@ -168,6 +180,8 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
     float4 pre[ACC ? KT : 1][ACC ? NT : 1][2];
     if constexpr (ACC) {
       const float2* ob = out + b * int64_t(a.KO) * a.NN;
+      // even entry for lanes outside the tile (see spare above)
+      const int64_t pspare = (m & 14) + 1 < int64_t(a.KO) * a.NN ? (m & 14) : 0;
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk)
 #pragma unroll
@@ -178,9 +192,30 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
             const int n = nw + 16 * nt + m;
             const int row = out_row(kt, (n & 1) ? 2 * h + 1 : 2 * h);
             const bool ok = kt < a.ktiles && n < a.NN && row < a.KO;
-            pre[kk][nt][h] = *reinterpret_cast<const float4*>(ob + (ok ? int64_t(row) * a.NN + (n & ~1) : 0));
+            int64_t idx = ok ? int64_t(row) * a.NN + (n & ~1) : pspare;
+            opaque(idx);
+            pre[kk][nt][h] = *reinterpret_cast<const float4*>(ob + idx);
           }
     }
+    // Basis tiles of step q (A operands, from L1 / L2): loaded at the end of
+    // the previous step, after the input rows of step q + 1 went out, so that
+    // waiting for them (the memory counter retires loads in order) never
+    // waits for that input prefetch.
+    float4 bre[KT][NE], bim[KT][NE];
+    auto load_basis = [&](int q) {
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) {
+        const int kt = min(kb * KT + kk, a.ktiles - 1);
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+          // image: FOLD 2 -> [kt][q][class][part], else [kt][q][part]
+          const float4* ip = img + ((int64_t(kt) * a.JQ + q) * NE + e) * 2 * 64 + lane;
+          bre[kk][e] = ip[0];
+          bim[kk][e] = ip[64];
+        }
+      }
+    };
+    load_basis(0);
     for (int q = 0; q < a.JQ; ++q) {
       // B operands: V[c or fold class][nt][i] as (re, im, -im)
       constexpr int NV = FOLD == 0 ? 1 : 2;
@@ -212,9 +247,7 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
         const int kt = min(kb * KT + kk, a.ktiles - 1);
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
-          // image: FOLD 2 -> [kt][q][class][part], else [kt][q][part]
-          const float4* ip = img + ((int64_t(kt) * a.JQ + q) * NE + e) * 2 * 64 + lane;
-          const float4 br = ip[0], bi = ip[64];
+          const float4 br = bre[kk][e], bi = bim[kk][e];
           const int v = FOLD == 1 ? (kt >= a.kth ? 1 : 0) : (FOLD == 2 ? e : 0);
 #pragma unroll
           for (int i = 0; i < 4; ++i)
@@ -238,6 +271,7 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
             }
         }
       }
+      if (q + 1 < a.JQ) load_basis(q + 1);
     }
 
 #pragma unroll
