@@ -181,7 +181,7 @@ def forward_workload(torch, D, synth, cfg, device, block=False):
     Workload 2 runs its 8 slabs one after another: the forwards accumulate
     into one spectrum, the mix runs over the 8 mode ranges in turn, and every
     slab is then expanded back."""
-    c = synth.CONFIGS[cfg]
+    c = synth.WORKLOADS[cfg]
     shards = []
     if cfg in synth.ALL_SHARDS:
         full = synth.full_domain(cfg)
@@ -231,7 +231,7 @@ def forward_workload(torch, D, synth, cfg, device, block=False):
     w.bytes = P * B * (ci + co) * _vol(g0) * 4 + M * ci * co * 8   # read x, write y, read W
     w.metric = ("DRIFT block ms and GB/s + TFLOP/s per MI355X (fwd partial DFT+mix+inverse, bypass + GELU)"
                 if block else "spectral-layer ms and GB/s + TFLOP/s per MI355X (fwd partial DFT+mix+inverse)")
-    w.config = {"workload": synth.CONFIGS[cfg]["name"], "global_grid": list(g0["n_global"]),
+    w.config = {"workload": synth.WORKLOADS[cfg]["name"], "global_grid": list(g0["n_global"]),
                 "local_shard": list(g0["n_local"]), "shards_run_in_sequence": P, "batch": B,
                 "c_in": ci, "c_out": co,
                 "modes": [2 * g0["kmax"][0], 2 * g0["kmax"][1], 2 * g0["kmax"][2], g0["kt"]]}
@@ -332,7 +332,7 @@ def backward_workload(torch, D, synth, cfg, device):
     w.bytes = B * (ci + co) * _vol(g) * 4 + 2 * M * ci * co * 8   # read g_y, write g_x, read W, write g_W
     w.metric = ("spectral-layer backward ms and GB/s + TFLOP/s per MI355X "
                 "(inverse_adj + mix data grad + wgrad + forward_adj)")
-    w.config = {"workload": synth.CONFIGS[cfg]["name"], "global_grid": list(g["n_global"]),
+    w.config = {"workload": synth.WORKLOADS[cfg]["name"], "global_grid": list(g["n_global"]),
                 "local_shard": list(g["n_local"]), "shards_run_in_sequence": 1, "batch": B,
                 "c_in": ci, "c_out": co,
                 "modes": [2 * g["kmax"][0], 2 * g["kmax"][1], 2 * g["kmax"][2], g["kt"]]}
@@ -368,7 +368,7 @@ def fno_workload(torch, D, synth, cfg, device):
     """FNO forward (lift, Fourier layers as Algorithm 1, projection) over
     every shard of the workload, run one after another on this GPU."""
     from paper_2607_14394_amd.fno import FNO
-    c = synth.CONFIGS[cfg]
+    c = synth.WORKLOADS[cfg]
     spec = c["fno"]
     cin, cout, L = spec["c_data_in"], spec["c_data_out"], spec["layers"]
     shards = [synth.geometry(cfg, p) for p in range(c["shards"])]

@@ -28,7 +28,7 @@ import numpy as np
 # Workload table.  Sizes are (x, y, z, t).  kmax = (kx, ky, kz): x, y, z keep
 # 2*k indices; kt: t keeps 0..kt-1.
 # ---------------------------------------------------------------------------
-CONFIGS = {
+WORKLOADS = {
     1: dict(name="full-domain 32^3x8, B1 C8, modes 16/16/16/4",
             n_global=(32, 32, 32, 8), n_local=(32, 32, 32, 8), shards=1,
             kmax=(8, 8, 8), kt=4, batch=1, c_in=8, c_out=8, field="normal"),
@@ -96,7 +96,7 @@ def fno_params_np(M, dv, c_in, c_out, layers, seed):
 def geometry(cfg: int, shard: int | None = None) -> dict:
     """Plain-dict description of one shard of workload ``cfg``.  Shards are
     numbered row-major over the (x, y) shard grid (x slabs: grid (P, 1))."""
-    c = CONFIGS[cfg]
+    c = WORKLOADS[cfg]
     p = c.get("shard", 0) if shard is None else shard
     gx, gy = c.get("grid", (c["shards"], 1))
     off = ((p // gy) * c["n_local"][0], (p % gy) * c["n_local"][1], 0, 0)
@@ -246,7 +246,7 @@ def torch_smooth_field(g, channels, seed, device, waves=48, width=8.0, noise_std
 def torch_input(cfg: int, g: dict, device, channels_first=True):
     """Input shard x (B, C_in, *n_local) float32 for workload ``cfg``."""
     torch = _torch()
-    c = CONFIGS[cfg]
+    c = WORKLOADS[cfg]
     shape = (g["batch"], g["c_in"]) + tuple(g["n_local"])
     kind = c["field"]
     if kind == "smooth":

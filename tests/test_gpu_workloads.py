@@ -88,7 +88,7 @@ def test_layer_full_size(cfg):
     import paper_2607_14394_amd as D
     g = synth.geometry(cfg)
     go = geo_of(g)
-    say(f"[workload {cfg}] {synth.CONFIGS[cfg]['name']}")
+    say(f"[workload {cfg}] {synth.WORKLOADS[cfg]['name']}")
     plan = D.Plan(g)
     M = plan.n_modes
     B, ci, co = g["batch"], g["c_in"], g["c_out"]
@@ -134,9 +134,9 @@ def test_decomposition_128cubed(cfg):
     torch = torch_gpu()
     import paper_2607_14394_amd as D
     full = synth.full_domain(cfg)
-    say(f"[workload {cfg}] {synth.CONFIGS[cfg]['name']}")
+    say(f"[workload {cfg}] {synth.WORKLOADS[cfg]['name']}")
     x = synth.torch_input(cfg, full, "cuda")
-    P = synth.CONFIGS[cfg]["shards"]
+    P = synth.WORKLOADS[cfg]["shards"]
     pf = D.Plan(full)
     K = pf.K
     B, C = full["batch"], full["c_in"]
@@ -204,7 +204,7 @@ def test_backward_full_size():
     cfg = 5
     g = synth.geometry(cfg)
     go = geo_of(g)
-    say(f"[workload 5] {synth.CONFIGS[cfg]['name']}")
+    say(f"[workload 5] {synth.WORKLOADS[cfg]['name']}")
     plan = D.Plan(g)
     M = plan.n_modes
     B, ci, co = g["batch"], g["c_in"], g["c_out"]
