@@ -13,14 +13,19 @@ from gpu_common import Guarded, check, desc_of, dev, geometry, np_of, rand_cplx,
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 48
+N_SMALL = 48   # extents up to 16 x 24 x 48
+N_LARGE = 16   # y up to 80 and z up to 96: several fused slot groups and z tiles
 _T_EXTENTS = (3, 4, 5, 6, 8, 10, 12, 16, 21, 24, 32)
 
 
-def _draw(seed):
+def _draw(seed, large):
     rng = np.random.default_rng(seed)
-    ng = [int(rng.integers(2, 17)), int(rng.integers(2, 25)), int(rng.integers(2, 49)),
-          int(rng.choice(_T_EXTENTS))]
+    if large:
+        ng = [int(rng.integers(2, 9)), int(rng.integers(16, 81)), int(rng.integers(16, 97)),
+              int(rng.choice((8, 12, 16, 24, 32)))]
+    else:
+        ng = [int(rng.integers(2, 17)), int(rng.integers(2, 25)), int(rng.integers(2, 49)),
+              int(rng.choice(_T_EXTENTS))]
     split_prob = (0.5, 0.3, 0.2, 0.15)
     nl, off = [], []
     for d in range(4):
@@ -33,18 +38,17 @@ def _draw(seed):
             off.append(0)
     kmax = [int(rng.integers(1, ng[d] // 2 + 1)) for d in range(3)]
     kt = int(rng.integers(1, min(16, ng[3] // 2 + 1) + 1))
+    if large:
+        return (tuple(ng), tuple(nl), tuple(off), tuple(kmax), kt, 1, int(rng.integers(1, 4)),
+                int(rng.integers(1, 4)))
     return (tuple(ng), tuple(nl), tuple(off), tuple(kmax), kt, int(rng.integers(1, 3)),
             int(rng.integers(1, 6)), int(rng.integers(1, 6)))
 
 
-def _cases():
-    try:
-        import paper_2607_14394_amd as D
-    except Exception:  # library not built: the module is skipped below
-        return []
-    out, seed = [], 7000
-    while len(out) < N_CASES and seed < 7000 + 40 * N_CASES:
-        args = _draw(seed)
+def _family(first_seed, count, large, D):
+    out, seed = [], first_seed
+    while len(out) < count and seed < first_seed + 40 * count:
+        args = _draw(seed, large)
         seed += 1
         g = geometry(*args)
         try:
@@ -54,6 +58,14 @@ def _cases():
             continue
         out.append((seed - 1, args))
     return out
+
+
+def _cases():
+    try:
+        import paper_2607_14394_amd as D
+    except Exception:  # library not built: the module is skipped below
+        return []
+    return _family(7000, N_SMALL, False, D) + _family(9000, N_LARGE, True, D)
 
 
 CASES = _cases()
