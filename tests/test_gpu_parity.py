@@ -486,3 +486,33 @@ def test_inverse_schedules(name, schedule, monkeypatch):
     torch.cuda.synchronize()
     check(np_of(out2.t), O.forward_adj(G, g), f"forward_adj ({schedule})")
     assert out2.guards_intact()
+
+
+@pytest.mark.parametrize("name", ["fold_ragged", "kt16_two_col_tiles"])
+def test_one_plan_two_streams(name):
+    """A plan used from two streams at once, each call with its own
+    workspace (the concurrency contract of the C ABI): forward and inverse
+    calls interleaved on two default-priority streams give each stream's
+    oracle result."""
+    torch, D, g, plan = _setup(name)
+    xs = [rand_real((g.batch, g.c_in) + g.n_local, 120 + s) for s in range(2)]
+    yhs = [rand_cplx((g.batch, g.c_out) + g.K, 130 + s) for s in range(2)]
+    xd = [dev(torch, a) for a in xs]
+    yd = [dev(torch, a) for a in yhs]
+    wss = [torch.empty(max(plan.ws_bytes, 16), dtype=torch.uint8, device="cuda") for _ in range(2)]
+    outs = [torch.empty(plan.spectral_shape(g.c_in), dtype=torch.complex64, device="cuda") for _ in range(2)]
+    backs = [torch.empty(plan.spatial_shape(g.c_out), dtype=torch.float32, device="cuda") for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    cur = torch.cuda.current_stream()
+    for st in streams:
+        st.wait_stream(cur)
+    for _ in range(3):
+        for s, st in enumerate(streams):
+            D.dtst_forward(plan.handle, xd[s], outs[s], 0, wss[s], stream=st.cuda_stream)
+            D.dtst_inverse(plan.handle, yd[s], backs[s], wss[s], stream=st.cuda_stream)
+    for st in streams:
+        cur.wait_stream(st)
+    torch.cuda.synchronize()
+    for s in range(2):
+        check(np_of(outs[s]), O.forward(xs[s], g), f"forward on stream {s}")
+        check(np_of(backs[s]), O.inverse(yhs[s], g), f"inverse on stream {s}")
