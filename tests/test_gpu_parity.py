@@ -516,3 +516,47 @@ def test_one_plan_two_streams(name):
     for s in range(2):
         check(np_of(outs[s]), O.forward(xs[s], g), f"forward on stream {s}")
         check(np_of(backs[s]), O.inverse(yhs[s], g), f"inverse on stream {s}")
+
+
+@pytest.mark.parametrize("name", ["fold_ragged", "kt16_two_col_tiles"])
+def test_graph_capture_replays(name):
+    """The execute calls allocate nothing, synchronise nothing and record
+    no memset, so a layer step (forward, mix, inverse) can be captured in a
+    HIP graph.  The graph is replayed several times, with eager work and
+    synchronisation between the replays, and every replay is checked
+    against the eager result."""
+    torch, D, g, plan = _setup(name)
+    M = plan.n_modes
+    x = dev(torch, rand_real((g.batch, g.c_in) + g.n_local, 140))
+    W = dev(torch, rand_cplx((M, g.c_in, g.c_out), 141, var=1.0 / (g.c_in * g.c_out)))
+    xhat = torch.empty(plan.spectral_shape(g.c_in), dtype=torch.complex64, device="cuda")
+    yhat = torch.empty(plan.spectral_shape(g.c_out), dtype=torch.complex64, device="cuda")
+    y = torch.empty(plan.spatial_shape(g.c_out), dtype=torch.float32, device="cuda")
+
+    def step():
+        plan.forward(x, xhat)
+        plan.mix(xhat, W, yhat, 0, M, op=0)
+        plan.inverse(yhat, y)
+
+    step()
+    torch.cuda.synchronize()
+    eager = np_of(y).copy()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        step()
+    for r in range(3):
+        y.fill_(-3.0)
+        xhat.fill_(0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = np_of(y)
+        assert np.array_equal(got, eager), f"replay {r} differs from the eager step"
+    check(eager, O.inverse(O.mix(O.forward(np_of(x), g), np_of(W), 0, M).reshape(plan.spectral_shape(g.c_out)), g),
+          "eager step vs oracle")
