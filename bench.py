@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--fno", action="store_true",
                     help="time the whole FNO forward (lift, 4 Fourier layers, projection) on workload 7, the "
                          "paper's model shape (d_v 20, modes (8, 8, 8, 16)) on 128^3 x 32 in 4 x-slabs")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step in a HIP graph after the warm-up and replay it in the timed "
+                         "region (the same kernels; removes the host's per-launch cost)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-times", action="store_true",
                     help="skip the per-kernel event pass (used under rocprofv3)")
@@ -549,6 +552,23 @@ def main():
     w.mfma_flops = sum(w.work[k]["mfma_flops"] * n for k, n in w.launches.items())
     log(f"kernels per step: {w.launches}")
 
+    # ---- optional HIP graph of one step (the execute calls are capturable:
+    # kernel launches only) ----
+    run = w.step
+    if args.graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            w.step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            w.step()
+        run = graph.replay
+        run()
+        torch.cuda.synchronize()
+
     log(f"timing {args.steps} steps")
     # ---- timed region: K steps bracketed by events on the launch stream ----
     stream = torch.cuda.current_stream()
@@ -557,7 +577,7 @@ def main():
     torch.cuda.synchronize()
     t0.record(stream)
     for _ in range(args.steps):
-        w.step()
+        run()
     t1.record(stream)
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / args.steps
@@ -567,7 +587,7 @@ def main():
     torch.cuda.synchronize()
     for e0, e1 in evs:
         e0.record(stream)
-        w.step()
+        run()
         e1.record(stream)
     torch.cuda.synchronize()
     per_step = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
@@ -614,6 +634,7 @@ def main():
         "value": round(gbs, 2), "unit": "GB/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "launch": "hip_graph" if args.graph else "eager",
         "step_ms": {"mean": round(ms_per_step, 4), "median": round(per_step[len(per_step) // 2], 4),
                     "min": round(per_step[0], 4), "note": "median and min from a separate pass that brackets "
                                                           "each step with its own events"},
