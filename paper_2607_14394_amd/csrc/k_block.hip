@@ -21,15 +21,16 @@
 namespace dtst {
 namespace {
 
-constexpr int OC = 16;  // output channels per pass over the input channels
 
 __device__ __forceinline__ float gelu(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
 }
 
 // ADDY: the accumulators start from y (block epilogue), else from the bias
-// (zero without one).  ACT: 1 applies GELU, 0 none.
-template <int VEC, int ADDY, int ACT>
+// (zero without one).  ACT: 1 applies GELU, 0 none.  OC: output channels per
+// pass over the input channels (the launcher picks C_out rounded up to a
+// multiple of 4 when that is at most 16, else 16).
+template <int VEC, int ADDY, int ACT, int OC>
 __global__ void __launch_bounds__(256)
 pointwise_kernel(const float* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
                  float* __restrict__ y, int64_t V, int64_t total, int ci, int co) {
@@ -108,29 +109,43 @@ pointwise_kernel(const float* __restrict__ x, const float* __restrict__ w, const
 }
 
 
-template <int ADDY, int ACT>
-int launch_pw(const float* x, const float* w, const float* bias, float* y, int64_t B, int64_t ci, int64_t co,
-              int64_t V, void* stream) {
-  if (B <= 0 || V <= 0) return hipSuccess;
+template <int ADDY, int ACT, int OC>
+int launch_pw_oc(const float* x, const float* w, const float* bias, float* y, int64_t B, int64_t ci, int64_t co,
+                 int64_t V, void* stream) {
   const bool vec = V % 4 == 0;
   const int64_t total = B * (vec ? V / 4 : V);
   const int64_t cap = int64_t(1) << 20;
   const int64_t blocks = std::min<int64_t>((total + 255) / 256, cap);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const size_t lds = (size_t(ci) * co + (ADDY ? 0 : co)) * sizeof(float);
-  const void* fn = vec ? reinterpret_cast<const void*>(pointwise_kernel<1, ADDY, ACT>)
-                       : reinterpret_cast<const void*>(pointwise_kernel<0, ADDY, ACT>);
+  const void* fn = vec ? reinterpret_cast<const void*>(pointwise_kernel<1, ADDY, ACT, OC>)
+                       : reinterpret_cast<const void*>(pointwise_kernel<0, ADDY, ACT, OC>);
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
   }
   if (vec)
-    hipLaunchKernelGGL((pointwise_kernel<1, ADDY, ACT>), dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s, x, w,
-                       bias, y, V, total, static_cast<int>(ci), static_cast<int>(co));
+    hipLaunchKernelGGL((pointwise_kernel<1, ADDY, ACT, OC>), dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s,
+                       x, w, bias, y, V, total, static_cast<int>(ci), static_cast<int>(co));
   else
-    hipLaunchKernelGGL((pointwise_kernel<0, ADDY, ACT>), dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s, x, w,
-                       bias, y, V, total, static_cast<int>(ci), static_cast<int>(co));
+    hipLaunchKernelGGL((pointwise_kernel<0, ADDY, ACT, OC>), dim3(static_cast<unsigned>(blocks)), dim3(256), lds, s,
+                       x, w, bias, y, V, total, static_cast<int>(ci), static_cast<int>(co));
   return hipGetLastError();
+}
+
+template <int ADDY, int ACT>
+int launch_pw(const float* x, const float* w, const float* bias, float* y, int64_t B, int64_t ci, int64_t co,
+              int64_t V, void* stream) {
+  if (B <= 0 || V <= 0) return hipSuccess;
+  // C_out <= 16: one pass of C_out rounded up to a multiple of 4 (no wasted
+  // products); wider layers take passes of 16 (a wider pass held more
+  // registers and fewer waves, and measured slower at C_out = 20).
+  switch (co <= 16 ? (co + 3) / 4 : 4) {
+    case 1: return launch_pw_oc<ADDY, ACT, 4>(x, w, bias, y, B, ci, co, V, stream);
+    case 2: return launch_pw_oc<ADDY, ACT, 8>(x, w, bias, y, B, ci, co, V, stream);
+    case 3: return launch_pw_oc<ADDY, ACT, 12>(x, w, bias, y, B, ci, co, V, stream);
+    default: return launch_pw_oc<ADDY, ACT, 16>(x, w, bias, y, B, ci, co, V, stream);
+  }
 }
 
 }  // namespace
