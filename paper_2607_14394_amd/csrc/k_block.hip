@@ -29,7 +29,7 @@ __device__ __forceinline__ float gelu(float v) {
 // ADDY: the accumulators start from y (block epilogue), else from the bias
 // (zero without one).  ACT: 1 applies GELU, 0 none.  OC: output channels per
 // pass over the input channels (the launcher picks C_out rounded up to a
-// multiple of 4 when that is at most 16, else 16).
+// multiple of 4 when that is at most 16, else 12 or 16).
 template <int VEC, int ADDY, int ACT, int OC>
 __global__ void __launch_bounds__(256)
 pointwise_kernel(const float* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
@@ -138,9 +138,11 @@ int launch_pw(const float* x, const float* w, const float* bias, float* y, int64
               int64_t V, void* stream) {
   if (B <= 0 || V <= 0) return hipSuccess;
   // C_out <= 16: one pass of C_out rounded up to a multiple of 4 (no wasted
-  // products); wider layers take passes of 16 (a wider pass held more
-  // registers and fewer waves, and measured slower at C_out = 20).
-  switch (co <= 16 ? (co + 3) / 4 : 4) {
+  // products).  Wider layers take passes of 12 or 16, whichever computes
+  // fewer unused outputs (a single wider pass held more registers and fewer
+  // waves, and measured slower at C_out = 20).
+  const int64_t waste12 = (co + 11) / 12 * 12 - co, waste16 = (co + 15) / 16 * 16 - co;
+  switch (co <= 16 ? (co + 3) / 4 : (waste12 < waste16 ? 3 : 4)) {
     case 1: return launch_pw_oc<ADDY, ACT, 4>(x, w, bias, y, B, ci, co, V, stream);
     case 2: return launch_pw_oc<ADDY, ACT, 8>(x, w, bias, y, B, ci, co, V, stream);
     case 3: return launch_pw_oc<ADDY, ACT, 12>(x, w, bias, y, B, ci, co, V, stream);
