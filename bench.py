@@ -3,17 +3,24 @@
 channel mix + inverse partial DFT) on one MI355X.
 
 A step is one pass of the whole layer over one batch of synthetic input
-already resident in HBM.  The default workload is the 128^3 x 32 global grid
-split into 8 x-slabs of 16 (B = 1, C = 16, modes 32/32/32/8), run the way the
-method runs on 8 GPUs but one shard after another on this GPU: the slab
-forwards accumulate into one spectrum (the sum that replaces the AllReduce),
-the mix runs over the 8 mode ranges S_p in turn (which assembles the full
-spectrum the AllGather would), and every slab is then expanded back.
+already resident in HBM.  The default workload is one GPU's share of a
+256^3 x 32 grid split 4 ways along x: the 64 x 256 x 256 x 32 shard at x
+offset 64, B = 2, C_in = C_out = 32, modes 32/32/32/8 -- the largest
+single-GPU forward configuration.  The workloads that cover a whole
+decomposition (--workload 2: 128^3 x 32 in 8 x-slabs) run the shards one
+after another on this GPU: the shard forwards accumulate into one spectrum
+(the sum that replaces the AllReduce), the mix runs over the mode ranges S_p
+in turn (which assembles the spectrum the AllGather would), and every shard
+is then expanded back.
 
-Prints one JSON line with the step time, the layer's GB/s and TFLOP/s, a
-roofline entry for the kernel that takes the most time (its average launch
-time measured here with HIP events on the launch stream), and the fp64 CPU
-oracle timed on a bounded sample of the same workload on this host.
+Prints one JSON line with the step time, the layer's GB/s and TFLOP/s
+(executed flops after the exact folds, and the direct-definition count of
+Table 3's stages), an HBM roofline entry for the kernel that takes the most
+time and an fp32-MFMA roofline entry for the contraction kernel that
+executes the most matrix work (average launch times measured here with HIP
+events on the launch stream; rocprof counter figures from profiles/ where
+they match the kernel source), and the fp64 CPU oracle timed on a bounded
+sample of the same workload on this host.
 """
 
 from __future__ import annotations
@@ -33,6 +40,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 FP32_MFMA_PEAK_TFS = 157.3   # MI355X dense fp32 matrix
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "hbm_counters.json")
+MFMA_COUNTERS_FILE = os.path.join(ROOT, "profiles", "mfma_counters.json")
 
 
 def log(msg):
@@ -44,9 +52,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7],
-                    help="workload table entry (default 2: 128^3x32 in 8 x-slabs; 5 times the backward; "
-                         "6: the same grid in 2x4 (x, y) pencils)")
+    ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4, 5, 6, 7],
+                    help="workload table entry (default 3: the 64x256x256x32 shard of 256^3x32, B2 C32, the "
+                         "largest single-GPU forward configuration; 2: 128^3x32 in 8 x-slabs; 5 times the "
+                         "backward; 6: 128^3x32 in 2x4 (x, y) pencils)")
     ap.add_argument("--block", action="store_true",
                     help="time the whole block of Algorithm 1: after every shard's inverse, the point-wise "
                          "bypass of the shard's input and GELU (forward workloads only)")
@@ -70,11 +79,36 @@ def parse():
 
 
 # ---------------------------------------------------------------------------
-# Algorithmic work of each kernel role (direct-definition counts: a real x
-# complex multiply-add is 4 flops, complex x complex 8; bytes are the
-# tensors each kernel must read and write once).
+# Algorithmic work of each kernel role.  Flops are real flops: a real x complex
+# multiply-add is 4, complex x complex 8.  "flops" are the direct-definition
+# counts of each per-dimension contraction (Table 3's stages, in its order
+# T, Z, Y, X), "mfma_flops" the products the kernels execute after the exact
+# even / odd and four-class folds (no padding).  Bytes are the tensors each
+# kernel must read and write once.
 # ---------------------------------------------------------------------------
-def work(g, channels, m_count=None):
+def stage_flops(g, channels):
+    """Direct-definition real flops of the four per-dimension contractions of
+    one forward (Sec. V-B, Table 3), contracting t, then z, y, x:
+      t: 4 K_t N_t per (b, c, x, y, z) line (real input, complex basis)
+      z: 8 K_z N_z per (b, c, x, y, k_t) line
+      y: 8 K_y N_y per (b, c, x, k_z, k_t) line
+      x: 8 K_x N_x per (b, c, k_y, k_z, k_t) line
+    The inverse expansions mirror them."""
+    B = g["batch"]
+    Nx, Ny, Nz, Nt = g["n_local"]
+    k = g["kmax"]
+    Kx, Ky, Kz, Kt = 2 * k[0], 2 * k[1], 2 * k[2], g["kt"]
+    lines = B * channels
+    return {"t": lines * Nx * Ny * Nz * 4 * Kt * Nt,
+            "z": lines * Nx * Ny * Kt * 8 * Kz * Nz,
+            "y": lines * Nx * Kz * Kt * 8 * Ky * Ny,
+            "x": lines * Ky * Kz * Kt * 8 * Kx * Nx}
+
+
+def work(g, channels, m_count=None, acc_share=0.0):
+    """Per-launch work of every kernel role.  acc_share: the share of the
+    x-contraction launches that accumulate into the spectrum (they also read
+    it back)."""
     B = g["batch"]
     Nx, Ny, Nz, Nt = g["n_local"]
     k = g["kmax"]
@@ -82,27 +116,25 @@ def work(g, channels, m_count=None):
     C = channels
     M = Kx * Ky * Kz * Kt
     rows = B * C * Nx * Ny
+    sf = stage_flops(g, C)
+    fy = 0.5 if _folded(g, 1) else 1.0
+    fx = 0.5 if _folded(g, 0) else 1.0
     w = {}
     w["stream_fwd_tz"] = dict(
         bytes=rows * (Nz * Nt * 4 + Kz * Kt * 8),
-        flops=rows * Nz * 4 * Kt * Nt + rows * Kt * 8 * Kz * Nz,
-        mfma_flops=rows * Nz * 4 * Kt * Nt / _t_classes(g) + rows * Kt * 8 * Kz * Nz / _z_classes(g))
-    fy = 0.5 if _folded(g, 1) else 1.0
-    fx = 0.5 if _folded(g, 0) else 1.0
-    w["axis_fwd_y"] = dict(bytes=B * C * Nx * (Ny + Ky) * Kz * Kt * 8, flops=B * C * Nx * Kz * Kt * 8 * Ky * Ny)
+        flops=sf["t"] + sf["z"],
+        mfma_flops=sf["t"] / _t_classes(g) + sf["z"] / _z_classes(g))
+    w["axis_fwd_y"] = dict(bytes=B * C * Nx * (Ny + Ky) * Kz * Kt * 8, flops=sf["y"], mfma_flops=sf["y"] * fy)
     # t + z + y in one launch: reads the shard once, writes the y-contracted rows
-    y_flops = w["axis_fwd_y"]["flops"]
     w["stream_fwd_tzy"] = dict(
         bytes=rows * Nz * Nt * 4 + B * C * Nx * Ky * Kz * Kt * 8,
-        flops=w["stream_fwd_tz"]["flops"] + y_flops,
-        mfma_flops=w["stream_fwd_tz"]["mfma_flops"] + y_flops * fy)
-    w["axis_fwd_x"] = dict(bytes=B * C * (Nx + Kx) * Ky * Kz * Kt * 8, flops=B * C * Ky * Kz * Kt * 8 * Kx * Nx)
-    w["axis_fwd_y"]["mfma_flops"] = w["axis_fwd_y"]["flops"] * fy
-    w["axis_fwd_x"]["mfma_flops"] = w["axis_fwd_x"]["flops"] * fx
-    w["axis_inv_x"] = dict(bytes=w["axis_fwd_x"]["bytes"], flops=w["axis_fwd_x"]["flops"],
-                           mfma_flops=w["axis_fwd_x"]["mfma_flops"])
-    w["axis_inv_y"] = dict(bytes=w["axis_fwd_y"]["bytes"], flops=w["axis_fwd_y"]["flops"],
-                           mfma_flops=w["axis_fwd_y"]["mfma_flops"])
+        flops=w["stream_fwd_tz"]["flops"] + sf["y"],
+        mfma_flops=w["stream_fwd_tz"]["mfma_flops"] + sf["y"] * fy)
+    spec = B * C * M * 8
+    w["axis_fwd_x"] = dict(bytes=B * C * Nx * Ky * Kz * Kt * 8 + spec + acc_share * spec, flops=sf["x"],
+                           mfma_flops=sf["x"] * fx)
+    w["axis_inv_x"] = dict(bytes=B * C * Nx * Ky * Kz * Kt * 8 + spec, flops=sf["x"], mfma_flops=sf["x"] * fx)
+    w["axis_inv_y"] = dict(bytes=w["axis_fwd_y"]["bytes"], flops=sf["y"], mfma_flops=sf["y"] * fy)
     w["stream_inv_zt"] = dict(bytes=w["stream_fwd_tz"]["bytes"], flops=w["stream_fwd_tz"]["flops"],
                               mfma_flops=w["stream_fwd_tz"]["mfma_flops"])
     # y + z + t in one launch: reads the x-expanded spectrum, writes the shard
@@ -114,6 +146,13 @@ def work(g, channels, m_count=None):
     for v in w.values():
         v.setdefault("mfma_flops", v["flops"])
     return w
+
+
+# Kernel roles whose products run on the matrix cores (the per-dimension
+# contractions); the mix, its gradients and the point-wise layers run on the
+# vector ALUs.
+CONTRACTION_ROLES = ("stream_fwd_tzy", "stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "axis_inv_x", "axis_inv_y",
+                     "stream_inv_zt", "stream_inv_yzt")
 
 
 def _folded(g, dim):
@@ -224,7 +263,8 @@ def forward_workload(torch, D, synth, cfg, device, block=False):
                 plan.inverse(yhat, y)
 
     w.step = step
-    per = work(g0, g0["c_in"])
+    # every shard's forward after the first accumulates into the spectrum
+    per = work(g0, g0["c_in"], acc_share=(P - 1) / P)
     per["mix"] = _mix_work(g0, M // P, "mix")
     B0, ci0, co0, V0 = g0["batch"], g0["c_in"], g0["c_out"], _vol(g0)
     per["block_epilogue"] = dict(bytes=B0 * V0 * (ci0 + 2 * co0) * 4, flops=2 * B0 * V0 * ci0 * co0,
@@ -459,6 +499,24 @@ def cpu_baseline(w):
             "kind": "oracle", "seconds": round(dt, 2), "sample": desc, "cpu_model": cpu_model, "blas": blas}
 
 
+def counter_flops(cfg, kernel):
+    """fp32 MFMA flops per launch of one kernel role of workload cfg from
+    committed rocprof counters (SQ_INSTS_VALU_MFMA_MOPS_F32 x 512); None when
+    there are none or the kernel source changed since they were taken."""
+    try:
+        with open(MFMA_COUNTERS_FILE) as f:
+            c = json.load(f)
+    except Exception:
+        return None
+    ent = c.get("workloads", {}).get(str(cfg), {}).get("kernels", {}).get(kernel)
+    if not ent:
+        return None
+    src = os.path.join(ROOT, "paper_2607_14394_amd", "csrc", ent.get("source", "k_stream.hip"))
+    if ent.get("source_sha") != _sha(src):
+        return None
+    return ent["mfma_flops_per_launch"]
+
+
 def traffic_entry(cfg, kernel):
     """HBM bytes per launch of one kernel role of workload cfg from committed
     FETCH_SIZE / WRITE_SIZE counters, scaled by the copy-kernel calibration;
@@ -609,17 +667,26 @@ def main():
     sec = ms_per_step / 1e3
     gbs = w.bytes / sec / 1e9
     roof = None
+    roof_mfma = None
     stages = {}
     if kernel_ms:
         for k, (n, avg) in kernel_ms.items():
             wk = w.work.get(k)
             if wk is None:
                 continue
-            stages[k] = {"launches_per_step": n // args.steps, "avg_ms": round(avg, 4),
-                         "bytes_per_launch": int(wk["bytes"]), "flops_per_launch": int(wk["flops"]),
-                         "GB_s": round(wk["bytes"] / (avg / 1e3) / 1e9, 1),
-                         "TFLOP_s": round(wk["flops"] / (avg / 1e3) / 1e12, 2),
-                         "mfma_TFLOP_s": round(wk["mfma_flops"] / (avg / 1e3) / 1e12, 2)}
+            st = {"launches_per_step": n // args.steps, "avg_ms": round(avg, 4),
+                  "bytes_per_launch": int(wk["bytes"]), "executed_flops_per_launch": int(wk["mfma_flops"]),
+                  "direct_flops_per_launch": int(wk["flops"]),
+                  "GB_s": round(wk["bytes"] / (avg / 1e3) / 1e9, 1),
+                  "TFLOP_s": round(wk["mfma_flops"] / (avg / 1e3) / 1e12, 2),
+                  "direct_TFLOP_s": round(wk["flops"] / (avg / 1e3) / 1e12, 2)}
+            if k in CONTRACTION_ROLES:
+                st["mfma_frac"] = round(wk["mfma_flops"] / (avg / 1e3) / 1e12 / FP32_MFMA_PEAK_TFS, 4)
+                cf = counter_flops(cfg, k)
+                if cf is not None and not (args.block or args.fno):
+                    st["counter_TFLOP_s"] = round(cf / (avg / 1e3) / 1e12, 2)
+                    st["counter_mfma_frac"] = round(cf / (avg / 1e3) / 1e12 / FP32_MFMA_PEAK_TFS, 4)
+            stages[k] = st
         dom = max((k for k in kernel_ms if k in w.work), key=lambda k: kernel_ms[k][0] * kernel_ms[k][1])
         n, avg = kernel_ms[dom]
         wk = w.work[dom]
@@ -628,6 +695,26 @@ def main():
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None if tr is None else int(tr),
                 "algorithmic_bytes_per_launch": int(wk["bytes"]), "avg_launch_ms": round(avg, 4)}
+        # The contraction kernel that executes the most MFMA work per step,
+        # against the fp32 matrix peak: executed flops (after the folds) per
+        # launch over its event-timed launch, and, where committed rocprof
+        # counters of the same kernel source exist, the counted MFMA flops.
+        cons = [k for k in kernel_ms if k in w.work and k in CONTRACTION_ROLES]
+        if cons:
+            dm = max(cons, key=lambda k: kernel_ms[k][0] * w.work[k]["mfma_flops"])
+            n, avg = kernel_ms[dm]
+            ex = w.work[dm]["mfma_flops"] / (avg / 1e3) / 1e12
+            cf = None if args.block or args.fno else counter_flops(cfg, dm)
+            roof_mfma = {"kernel": dm, "bound": "mfma", "achieved": round(ex, 2), "peak": FP32_MFMA_PEAK_TFS,
+                         "unit": "TFLOP/s", "frac": round(ex / FP32_MFMA_PEAK_TFS, 4),
+                         "executed_flops_per_launch": int(w.work[dm]["mfma_flops"]),
+                         "counter_flops_per_launch": None if cf is None else int(cf),
+                         "counter_frac": None if cf is None else round(cf / (avg / 1e3) / 1e12 / FP32_MFMA_PEAK_TFS, 4),
+                         "avg_launch_ms": round(avg, 4)}
+            # every contraction kernel together: executed MFMA flops over their summed time
+            tot_f = sum(w.work[k]["mfma_flops"] * kernel_ms[k][0] for k in cons)
+            tot_s = sum(kernel_ms[k][0] * kernel_ms[k][1] / 1e3 for k in cons)
+            roof_mfma["all_contraction_kernels_frac"] = round(tot_f / tot_s / 1e12 / FP32_MFMA_PEAK_TFS, 4)
 
     out = {
         "metric": w.metric,
@@ -640,11 +727,13 @@ def main():
                                                           "each step with its own events"},
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "layer_ms": round(ms_per_step, 4),
-        "layer_TFLOP_s": round(w.flops / sec / 1e12, 3),
-        "layer_mfma_TFLOP_s": round(w.mfma_flops / sec / 1e12, 3),
-        "layer_bytes": int(w.bytes), "layer_flops": int(w.flops),
+        # executed flops: the products the kernels perform after the exact folds
+        "layer_TFLOP_s": round(w.mfma_flops / sec / 1e12, 3),
+        # the per-dimension contractions as defined (Table 3's stage counts, in real flops)
+        "layer_direct_TFLOP_s": round(w.flops / sec / 1e12, 3),
+        "layer_bytes": int(w.bytes), "layer_executed_flops": int(w.mfma_flops), "layer_direct_flops": int(w.flops),
         "config": w.config,
-        "roofline": roof, "stages": stages,
+        "roofline": roof, "roofline_mfma": roof_mfma, "stages": stages,
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on a sample")

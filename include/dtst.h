@@ -93,8 +93,12 @@ typedef struct {
  * LDS limits). */
 dtst_status dtst_desc_validate(const dtst_desc* d);
 
-/* Workspace bytes the execute calls of this geometry need (>= 0). */
+/* Workspace bytes the execute calls of this geometry need (>= 0), for a
+ * plan made with dtst_plan (the default schedule). */
 dtst_status dtst_desc_workspace_bytes(const dtst_desc* d, size_t* bytes);
+
+/* The same for a plan made with dtst_plan_ex(d, flags, ...). */
+dtst_status dtst_desc_workspace_bytes_ex(const dtst_desc* d, uint32_t flags, size_t* bytes);
 
 /* Write the fp32 basis matrix of dimension `dim` (0..3 = x, y, z, t) that
  * the plan uploads, as an interleaved complex (K_dim x N_dim^loc) host array
@@ -109,14 +113,27 @@ dtst_status dtst_basis_host(const dtst_desc* d, int dim, int kind, float* out, s
  * and upload them to the current HIP device (synchronously).  The plan is
  * bound to that device.  On success *out receives the plan.
  *
- * The plan also fixes the kernel schedule of the forward-direction chain
- * (dtst_forward, dtst_inverse_adj): where the shapes allow it (K_t <= 8, at
- * most 16 z modes per fold class, N_t^loc <= 32 and a multiple of 4,
- * K_y <= 32, K_z K_t <= 256) the t, z and y contractions run as one launch;
- * otherwise t + z and y are separate launches.  Setting the environment
- * variable DTST_SCHEDULE=split before dtst_plan keeps them separate (for
- * comparing the two schedules); results agree to rounding. */
+ * The plan also fixes the kernel schedule of both chains (dtst_forward and
+ * dtst_inverse_adj; dtst_inverse and dtst_forward_adj): where the shapes
+ * allow it (K_t <= 8, at most 16 z modes per fold class, N_t^loc <= 32 and a
+ * multiple of 4, K_y <= 32, K_z K_t <= 256) the t, z and y contractions run
+ * as one launch; otherwise t + z and y are separate launches.  Same as
+ * dtst_plan_ex(d, 0, out). */
 dtst_status dtst_plan(const dtst_desc* d, dtst_plan_t* out);
+
+/* Plan options (bit flags of dtst_plan_ex / dtst_desc_workspace_bytes_ex). */
+enum {
+  /* Keep the t + z and y contractions (and the y and z + t expansions) as
+   * separate launches even where the shapes allow one launch.  The result
+   * agrees with the default schedule to rounding (the contraction order of
+   * Sec. V-B is the same); the workspace then also holds the (.., N_x, N_y,
+   * K_z, K_t) intermediate. */
+  DTST_PLAN_SPLIT_SCHEDULE = 1u
+};
+
+/* dtst_plan with options: `flags` is 0 or a combination of the DTST_PLAN_*
+ * flags above; any other bit is DTST_ERR_INVALID_ARG. */
+dtst_status dtst_plan_ex(const dtst_desc* d, uint32_t flags, dtst_plan_t* out);
 
 /* Free the plan's device tables.  Using a destroyed plan afterwards returns
  * DTST_ERR_INVALID_ARG. */

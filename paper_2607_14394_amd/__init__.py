@@ -15,7 +15,7 @@ import os
 
 __all__ = [
     "DtstError", "Desc", "lib", "make_desc", "dtst_desc_validate", "dtst_desc_workspace_bytes",
-    "dtst_basis_host", "dtst_plan", "dtst_plan_destroy", "dtst_plan_info", "dtst_forward", "dtst_mix",
+    "dtst_basis_host", "dtst_plan", "dtst_plan_destroy", "PLAN_SPLIT_SCHEDULE", "dtst_plan_info", "dtst_forward", "dtst_mix",
     "dtst_inverse", "dtst_forward_adj", "dtst_inverse_adj", "dtst_mix_wgrad", "dtst_block_epilogue",
     "dtst_inverse_block", "dtst_pointwise",
     "dtst_profile_enable",
@@ -25,6 +25,7 @@ __all__ = [
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdtst.so")
 
 DTST_OK = 0
+PLAN_SPLIT_SCHEDULE = 1      # DTST_PLAN_SPLIT_SCHEDULE of include/dtst.h
 STATUS_NAMES = {0: "DTST_OK", 1: "DTST_ERR_INVALID_ARG", 2: "DTST_ERR_UNSUPPORTED",
                 3: "DTST_ERR_OUT_OF_MEMORY", 4: "DTST_ERR_DEVICE"}
 
@@ -66,8 +67,10 @@ def _load():
     sig = {
         "dtst_desc_validate": [ctypes.POINTER(Desc)],
         "dtst_desc_workspace_bytes": [ctypes.POINTER(Desc), ctypes.POINTER(SZ)],
+        "dtst_desc_workspace_bytes_ex": [ctypes.POINTER(Desc), ctypes.c_uint32, ctypes.POINTER(SZ)],
         "dtst_basis_host": [ctypes.POINTER(Desc), I, I, ctypes.POINTER(ctypes.c_float), SZ],
         "dtst_plan": [ctypes.POINTER(Desc), ctypes.POINTER(P)],
+        "dtst_plan_ex": [ctypes.POINTER(Desc), ctypes.c_uint32, ctypes.POINTER(P)],
         "dtst_plan_destroy": [P],
         "dtst_plan_info": [P, ctypes.POINTER(I64), ctypes.POINTER(SZ)],
         "dtst_forward": [P, VP, VP, I, VP, SZ, VP],
@@ -127,9 +130,9 @@ def dtst_desc_validate(desc):
     _check(lib.dtst_desc_validate(ctypes.byref(_desc(desc))))
 
 
-def dtst_desc_workspace_bytes(desc) -> int:
+def dtst_desc_workspace_bytes(desc, flags=0) -> int:
     n = ctypes.c_size_t(0)
-    _check(lib.dtst_desc_workspace_bytes(ctypes.byref(_desc(desc)), ctypes.byref(n)))
+    _check(lib.dtst_desc_workspace_bytes_ex(ctypes.byref(_desc(desc)), int(flags), ctypes.byref(n)))
     return n.value
 
 
@@ -160,9 +163,10 @@ def _stream(stream):
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def dtst_plan(desc):
+def dtst_plan(desc, flags=0):
+    """dtst_plan_ex; flags 0 (default schedule) or PLAN_SPLIT_SCHEDULE."""
     h = ctypes.c_void_p()
-    _check(lib.dtst_plan(ctypes.byref(_desc(desc)), ctypes.byref(h)))
+    _check(lib.dtst_plan_ex(ctypes.byref(_desc(desc)), int(flags), ctypes.byref(h)))
     return h
 
 
@@ -256,10 +260,10 @@ class Plan:
     """Owns one library plan and a torch-allocated workspace; shape and dtype
     checks on the tensors happen here, the arithmetic in the library."""
 
-    def __init__(self, desc, device="cuda"):
+    def __init__(self, desc, device="cuda", flags=0):
         import torch
         self.desc = _desc(desc)
-        self.handle = dtst_plan(self.desc)
+        self.handle = dtst_plan(self.desc, flags)
         self.n_modes, self.ws_bytes = dtst_plan_info(self.handle)
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=device)
         d = self.desc

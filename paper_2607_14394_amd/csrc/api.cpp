@@ -223,6 +223,19 @@ dtst_status run_inverse_chain(const dtst_plan_st* p, int64_t channels, const voi
   return ok();
 }
 
+// Descriptor and plan-flag checks shared by dtst_desc_validate and dtst_plan_ex.
+dtst_status validate_ex(const dtst_desc* d, uint32_t flags) {
+  dtst::Derived dv;
+  std::string err;
+  const dtst_status s = dtst::derive(d, flags, &dv, &err);
+  if (s != DTST_OK) return fail(s, err);
+  if (dv.d.c_out > dtst::kMixMaxCout)
+    return fail(DTST_ERR_UNSUPPORTED, "c_out above " + std::to_string(dtst::kMixMaxCout) + " for the mix kernels");
+  if (dtst::mix_lds_bytes(dv.d.batch, dv.d.c_in, dv.d.c_out) > 160 * 1024)
+    return fail(DTST_ERR_UNSUPPORTED, "batch * channels too large for one workgroup of the mix kernels");
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -240,32 +253,26 @@ const char* dtst_status_string(dtst_status s) {
 
 const char* dtst_last_error(void) { return g_last_error.c_str(); }
 
-dtst_status dtst_desc_validate(const dtst_desc* d) {
-  dtst::Derived dv;
-  std::string err;
-  const dtst_status s = dtst::derive(d, &dv, &err);
-  if (s != DTST_OK) return fail(s, err);
-  if (dv.d.c_out > dtst::kMixMaxCout)
-    return fail(DTST_ERR_UNSUPPORTED, "c_out above " + std::to_string(dtst::kMixMaxCout) + " for the mix kernels");
-  if (dtst::mix_lds_bytes(dv.d.batch, dv.d.c_in, dv.d.c_out) > 160 * 1024)
-    return fail(DTST_ERR_UNSUPPORTED, "batch * channels too large for one workgroup of the mix kernels");
-  return ok();
-}
+dtst_status dtst_desc_validate(const dtst_desc* d) { return validate_ex(d, 0); }
 
-dtst_status dtst_desc_workspace_bytes(const dtst_desc* d, size_t* bytes) {
+dtst_status dtst_desc_workspace_bytes_ex(const dtst_desc* d, uint32_t flags, size_t* bytes) {
   if (!bytes) return fail(DTST_ERR_INVALID_ARG, "bytes is null");
   dtst::Derived dv;
   std::string err;
-  const dtst_status s = dtst::derive(d, &dv, &err);
+  const dtst_status s = dtst::derive(d, flags, &dv, &err);
   if (s != DTST_OK) return fail(s, err);
   *bytes = dv.ws_bytes;
   return ok();
 }
 
+dtst_status dtst_desc_workspace_bytes(const dtst_desc* d, size_t* bytes) {
+  return dtst_desc_workspace_bytes_ex(d, 0, bytes);
+}
+
 dtst_status dtst_basis_host(const dtst_desc* d, int dim, int kind, float* out, size_t count) {
   dtst::Derived dv;
   std::string err;
-  const dtst_status s = dtst::derive(d, &dv, &err);
+  const dtst_status s = dtst::derive(d, 0, &dv, &err);
   if (s != DTST_OK) return fail(s, err);
   if (dim < 0 || dim > 3 || (kind != 0 && kind != 1) || out == nullptr)
     return fail(DTST_ERR_INVALID_ARG, "dim must be 0..3, kind 0 or 1, out non-null");
@@ -275,14 +282,14 @@ dtst_status dtst_basis_host(const dtst_desc* d, int dim, int kind, float* out, s
   return ok();
 }
 
-dtst_status dtst_plan(const dtst_desc* d, dtst_plan_t* out) {
+dtst_status dtst_plan_ex(const dtst_desc* d, uint32_t flags, dtst_plan_t* out) {
   if (!out) return fail(DTST_ERR_INVALID_ARG, "out is null");
-  const dtst_status vs = dtst_desc_validate(d);
+  const dtst_status vs = validate_ex(d, flags);
   if (vs != DTST_OK) return vs;
   dtst_plan_st* p = new (std::nothrow) dtst_plan_st();
   if (!p) return fail(DTST_ERR_OUT_OF_MEMORY, "host allocation failed");
   std::string err;
-  dtst::derive(d, &p->dv, &err);
+  dtst::derive(d, flags, &p->dv, &err);
   std::vector<float> host;
   try {
     dtst::build_images(p->dv, &host);
@@ -321,6 +328,8 @@ dtst_status dtst_plan(const dtst_desc* d, dtst_plan_t* out) {
   *out = p;
   return ok();
 }
+
+dtst_status dtst_plan(const dtst_desc* d, dtst_plan_t* out) { return dtst_plan_ex(d, 0, out); }
 
 dtst_status dtst_plan_destroy(dtst_plan_t p) {
   {

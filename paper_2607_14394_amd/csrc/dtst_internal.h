@@ -96,7 +96,7 @@ struct Derived {
 };
 
 // Host-side validation and derivation (pure C++; no HIP).
-dtst_status derive(const dtst_desc* d, Derived* out, std::string* err);
+dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string* err);
 // Build every image of the blob (fp64 maths, rounded to fp32 once).
 void build_images(const Derived& dv, std::vector<float>* blob);
 // Plain (K x N_loc) complex fp32 basis of one dimension (kind 0: B, 1: conj B).

@@ -10,8 +10,9 @@
 // 2 C_in C_out / (4 (C_in + 2 C_out)) flop per byte (2.7 at C = 16): bound by
 // HBM traffic on x and y, so it runs on the VALU.  Each thread owns four
 // consecutive points of one batch entry (16-byte accesses), reads their C_in
-// input channels once per chunk of 16 output channels, and reads w (and the
-// bias) from LDS (the same entry for every lane).
+// input channels once per chunk of output channels (C_out rounded up to a
+// multiple of 4 when that is at most 16, else chunks of 12 or 16), and reads
+// w (and the bias) from LDS (the same entry for every lane).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>

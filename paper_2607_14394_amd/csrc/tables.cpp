@@ -9,8 +9,6 @@
 // large k*n products (k*n reaches 2.6e5 at N = 512).
 #include <algorithm>
 #include <cmath>
-#include <cstdlib>
-#include <cstring>
 #include <limits>
 
 #include "dtst_internal.h"
@@ -54,7 +52,7 @@ int64_t retained_index(const dtst_desc& d, int dim, int64_t p) {
   return p < k ? p : d.n_global[dim] - 2 * k + p;
 }
 
-dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
+dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string* err) {
   if (!d || !out) {
     *err = "null descriptor";
     return DTST_ERR_INVALID_ARG;
@@ -84,6 +82,10 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
   }
   if (d->batch < 0 || d->c_in < 1 || d->c_out < 1) {
     *err = "need batch >= 0, c_in >= 1, c_out >= 1";
+    return DTST_ERR_INVALID_ARG;
+  }
+  if ((flags & ~uint32_t(DTST_PLAN_SPLIT_SCHEDULE)) != 0) {
+    *err = "unknown plan flag";
     return DTST_ERR_INVALID_ARG;
   }
 
@@ -206,11 +208,10 @@ dtst_status derive(const dtst_desc* d, Derived* out, std::string* err) {
   // ---- fused forward t + z + y ----
   // Taken when the y contraction fits the fused kernel's registers (one
   // 16-column tile of K_z K_t per wave of 16, at most two 16-row k tiles of
-  // K_y per wave) and its LDS.  DTST_SCHEDULE=split in the environment at
-  // plan time keeps the separate t + z and y launches.
+  // K_y per wave) and its LDS.  The plan flag DTST_PLAN_SPLIT_SCHEDULE keeps
+  // the separate t + z and y launches.
   {
-    const char* sched = std::getenv("DTST_SCHEDULE");
-    const bool split = sched != nullptr && std::strcmp(sched, "split") == 0;
+    const bool split = (flags & DTST_PLAN_SPLIT_SCHEDULE) != 0;
     sc.ncy = fold_y ? 2 : 1;
     sc.kyt = fold_y ? dv.ay_f.kth : dv.ay_f.ktiles;
     const int mcols = static_cast<int>(nn_y);

@@ -68,21 +68,34 @@ def test_invalid_descriptors(kw, status):
     assert str(e.value)
 
 
-def test_workspace_bytes(monkeypatch):
+def test_workspace_bytes():
     d = desc(batch=2, c_in=2, c_out=3)
     # complex intermediates of the largest channel count: (.., Nx, Ky, Kz, Kt) between the y and x
     # steps, and (.., Nx, Ny, Kz, Kt) between the t+z and y steps when those are separate launches
     w1 = 2 * 3 * 4 * 10 * 4 * 3 * 8
     w2 = 2 * 3 * 4 * 4 * 4 * 3 * 8
     r = lambda v: (v + 255) // 256 * 256
-    monkeypatch.delenv("DTST_SCHEDULE", raising=False)
     assert D.dtst_desc_workspace_bytes(d) == r(w2)          # y fused into the stream kernels
     assert D.dtst_desc_workspace_bytes(desc(batch=0)) == 0
     # N_t = 6 (not a multiple of 4) keeps the separate launches
     d6 = desc(batch=2, c_in=2, c_out=3, n_global=(12, 10, 8, 6), n_local=(4, 10, 8, 6))
     assert D.dtst_desc_workspace_bytes(d6) == r(2 * 3 * 4 * 10 * 4 * 3 * 8) + r(w2)
-    monkeypatch.setenv("DTST_SCHEDULE", "split")
-    assert D.dtst_desc_workspace_bytes(d) == r(w1) + r(w2)
+    assert D.dtst_desc_workspace_bytes(d, D.PLAN_SPLIT_SCHEDULE) == r(w1) + r(w2)
+    # the library reads no environment: the schedule is a plan option only
+    os.environ["DTST_SCHEDULE"] = "split"
+    try:
+        assert D.dtst_desc_workspace_bytes(d) == r(w2)
+    finally:
+        del os.environ["DTST_SCHEDULE"]
+
+
+def test_unknown_plan_flag_rejected():
+    n = ctypes.c_size_t(0)
+    st = D.lib.dtst_desc_workspace_bytes_ex(ctypes.byref(desc()), 2, ctypes.byref(n))
+    assert st == 1 and b"flag" in D.lib.dtst_last_error()
+    h = ctypes.c_void_p()
+    st = D.lib.dtst_plan_ex(ctypes.byref(desc()), 1 << 31, ctypes.byref(h))
+    assert st == 1 and h.value is None
 
 
 @pytest.mark.parametrize("g", [

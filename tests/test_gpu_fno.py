@@ -20,6 +20,11 @@ CASES = {
     "pencils": ((12, 10, 8, 8), (3, 2, 2), 3, 1, 4, 3, 2, (2, 2)),
     # k_t = 16 of N_t = 32, as the paper's modes (8, 8, 8, 16): the separate t+z and y launches
     "kt16_slabs": ((8, 8, 16, 32), (2, 2, 4), 16, 1, 5, 2, 3, (2, 1)),
+    # the paper's width d_v = 20 (Sec. VI-A) with five fields in and out, on a small grid
+    "dv20_small": ((8, 8, 16, 32), (2, 2, 4), 16, 1, 20, 5, 5, (2, 1)),
+    # the paper's model shape (Sec. VI-A): d_v = 20, modes (8, 8, 8, 16) -- K = 16 of each
+    # spatial dimension and k_t = 16 -- on a 32^3 x 32 grid in 4 x-slabs of 8 (P = 4)
+    "paper_model_32cubed": ((32, 32, 32, 32), (8, 8, 8), 16, 1, 20, 5, 5, (4, 1)),
 }
 
 

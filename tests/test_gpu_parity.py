@@ -65,14 +65,14 @@ FUSED_CASES = ["tiny_baseline", "tiny_slab", "tiny_pencil", "k_above_nloc", "fol
                "cfg1_full", "many_planes", "y_image_global"]
 
 
-def _setup(name):
+def _setup(name, split=False):
     torch = torch_gpu()
     import paper_2607_14394_amd as D
     g = geometry(*CASES[name])
     g.validate()
     say(f"[case {name}] n_global={g.n_global} n_local={g.n_local} offset={g.offset} "
-        f"kmax={g.kmax} kt={g.kt} B={g.batch} Cin={g.c_in} Cout={g.c_out}")
-    plan = D.Plan(desc_of(g))
+        f"kmax={g.kmax} kt={g.kt} B={g.batch} Cin={g.c_in} Cout={g.c_out} split={split}")
+    plan = D.Plan(desc_of(g), flags=D.PLAN_SPLIT_SCHEDULE if split else 0)
     return torch, D, g, plan
 
 
@@ -319,9 +319,12 @@ def test_errors_launch_nothing():
     assert "destroyed" in str(e.value)
 
 
-# (n_local, B, C_in, C_out): 16-byte path with one and two chunks of 16 output
-# channels, the scalar path (point count not a multiple of 4), C_in != C_out.
-EPILOGUE_SHAPES = [((4, 6, 8, 8), 2, 16, 16), ((3, 5, 4, 8), 1, 3, 37), ((3, 5, 7, 3), 2, 5, 2),
+# (n_local, B, C_in, C_out): 16-byte path with one chunk of 16 output channels,
+# chunks of 16 with a ragged last one (37), chunks of 12 (C_out = 20, the FNO's
+# width d_v, and 17 with a ragged last chunk), the scalar path (point count not
+# a multiple of 4) and narrow outputs, C_in != C_out.
+EPILOGUE_SHAPES = [((4, 6, 8, 8), 2, 16, 16), ((3, 5, 4, 8), 1, 3, 37), ((4, 6, 8, 8), 1, 20, 20),
+                   ((3, 5, 4, 8), 2, 7, 17), ((3, 5, 7, 3), 1, 20, 20), ((3, 5, 7, 3), 2, 5, 2),
                    ((2, 2, 2, 2), 1, 1, 1)]
 
 
@@ -394,6 +397,8 @@ INVERSE_BLOCK_CASES = {
     "many_inputs": ((4, 4, 32, 32), (4, 4, 32, 32), (0, 0, 0, 0), (1, 1, 4), 3, 1, 64, 16),
     "kt12": ((4, 4, 16, 32), (4, 4, 16, 32), (0, 0, 0, 0), (1, 2, 4), 12, 1, 2, 3),
     "nt21": ((4, 6, 8, 21), (4, 6, 8, 21), (0, 0, 0, 0), (2, 2, 2), 6, 2, 2, 2),
+    # the FNO's width d_v = 20 (two chunks of 12 output channels)
+    "dv20": ((8, 6, 32, 32), (8, 6, 32, 32), (0, 0, 0, 0), (2, 2, 8), 5, 1, 20, 20),
 }
 
 
@@ -420,14 +425,11 @@ def test_inverse_block(name):
 
 @pytest.mark.parametrize("schedule", ["fused", "split"])
 @pytest.mark.parametrize("name", FUSED_CASES)
-def test_forward_schedules(name, schedule, monkeypatch):
-    """Both forward schedules (one t+z+y launch, or t+z then y) against the
-    oracle; the library's own per-kernel timing names the kernels that ran."""
-    if schedule == "split":
-        monkeypatch.setenv("DTST_SCHEDULE", "split")
-    else:
-        monkeypatch.delenv("DTST_SCHEDULE", raising=False)
-    torch, D, g, plan = _setup(name)
+def test_forward_schedules(name, schedule):
+    """Both forward schedules (one t+z+y launch, or t+z then y, chosen by the
+    plan option) against the oracle; the library's own per-kernel timing
+    names the kernels that ran."""
+    torch, D, g, plan = _setup(name, split=schedule == "split")
     x = rand_real((g.batch, g.c_in) + g.n_local, 111)
     ref = O.forward(x, g)
     out = Guarded(torch, plan.spectral_shape(g.c_in), torch.complex64)
@@ -456,14 +458,11 @@ def test_forward_schedules(name, schedule, monkeypatch):
 
 @pytest.mark.parametrize("schedule", ["fused", "split"])
 @pytest.mark.parametrize("name", FUSED_CASES)
-def test_inverse_schedules(name, schedule, monkeypatch):
-    """Both inverse schedules (y + z + t in one launch, or y then z + t) for
-    the inverse and forward_adj against the oracle, with the kernels that ran."""
-    if schedule == "split":
-        monkeypatch.setenv("DTST_SCHEDULE", "split")
-    else:
-        monkeypatch.delenv("DTST_SCHEDULE", raising=False)
-    torch, D, g, plan = _setup(name)
+def test_inverse_schedules(name, schedule):
+    """Both inverse schedules (y + z + t in one launch, or y then z + t,
+    chosen by the plan option) for the inverse and forward_adj against the
+    oracle, with the kernels that ran."""
+    torch, D, g, plan = _setup(name, split=schedule == "split")
     yh = rand_cplx((g.batch, g.c_out) + g.K, 113)
     out = Guarded(torch, plan.spatial_shape(g.c_out), torch.float32)
     D.dtst_profile_collect()

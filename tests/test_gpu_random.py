@@ -73,24 +73,20 @@ if not CASES:
     pytestmark = [pytest.mark.gpu, pytest.mark.skip(reason="libdtst.so not built")]
 
 
-def _setup(seed, args, split, monkeypatch):
+def _setup(seed, args, split):
     torch = torch_gpu()
     import paper_2607_14394_amd as D
-    if split:
-        monkeypatch.setenv("DTST_SCHEDULE", "split")
-    else:
-        monkeypatch.delenv("DTST_SCHEDULE", raising=False)
     g = geometry(*args)
     say(f"[random seed {seed}{' split' if split else ''}] n_global={g.n_global} n_local={g.n_local} "
         f"offset={g.offset} kmax={g.kmax} kt={g.kt} B={g.batch} Cin={g.c_in} Cout={g.c_out}")
-    return torch, D, g, D.Plan(desc_of(g))
+    return torch, D, g, D.Plan(desc_of(g), flags=D.PLAN_SPLIT_SCHEDULE if split else 0)
 
 
 @pytest.mark.parametrize("idx", range(len(CASES)))
-def test_random_geometry(idx, monkeypatch):
+def test_random_geometry(idx):
     seed, args = CASES[idx]
     # every fourth geometry also forces the separate t+z / y launches
-    torch, D, g, plan = _setup(seed, args, idx % 4 == 3, monkeypatch)
+    torch, D, g, plan = _setup(seed, args, idx % 4 == 3)
     M = plan.n_modes
 
     x = rand_real((g.batch, g.c_in) + g.n_local, seed)

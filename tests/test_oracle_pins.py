@@ -64,6 +64,44 @@ def test_fig5_retained_rows_golden():
     assert O.retained_indices(n, k).tolist() == want
 
 
+def test_mode_index_flattening():
+    """The flattened mode order m = ((ix Ky + iy) Kz + iz) Kt + it (ascending
+    stored index per dimension, Fig. 5; the contiguous S_p ranges of the
+    equal partition of Sec. V-A are ranges of this m): numpy's row-major
+    ravel_multi_index over (2kx, 2ky, 2kz, kt), the reshape of a
+    (B, C, Kx, Ky, Kz, Kt) spectrum to (B, C, M) that the tests and the mix
+    use, and the coefficient stored at m equal to a brute-force direct sum at
+    the stored frequencies of (ix, iy, iz, it)."""
+    g = O.Geometry((12, 10, 14, 8), (5, 10, 14, 8), (3, 0, 0, 0), (3, 2, 4), 3, 1, 1, 1)
+    g.validate()
+    K = g.K
+    M = O.n_modes(g)
+    assert M == int(np.prod(K))
+    ix, iy, iz, it = np.meshgrid(*[np.arange(k) for k in K], indexing="ij")
+    m = O.mode_index(g, ix, iy, iz, it)
+    assert np.array_equal(m, np.ravel_multi_index((ix, iy, iz, it), K))
+    assert np.array_equal(np.sort(m.ravel()), np.arange(M))                  # a bijection onto 0..M-1
+    assert np.array_equal(np.arange(M).reshape(K)[ix, iy, iz, it], m)        # the (B, C, M) reshape
+    # t fastest, then z, y, x: neighbouring stored indices are stride 1, Kt, Kz Kt, Ky Kz Kt apart
+    assert O.mode_index(g, 0, 0, 0, 1) == 1 and O.mode_index(g, 0, 0, 1, 0) == K[3]
+    assert O.mode_index(g, 0, 1, 0, 0) == K[2] * K[3] and O.mode_index(g, 1, 0, 0, 0) == K[1] * K[2] * K[3]
+    # the coefficient at flattened m is the direct sum at the stored frequencies of its indices
+    x = rand_shard(g, 55)
+    flat = O.forward(x, g).reshape(1, 1, M)
+    idx = [O.retained_indices(g.n_global[i], g.kmax[i]) for i in range(3)] + [O.retained_t(g.kt)]
+    rng = np.random.default_rng(56)
+    pts = np.stack(np.meshgrid(*[np.arange(nl) for nl in g.n_local], indexing="ij"), -1).reshape(-1, 4)
+    glob = pts + np.asarray(g.offset)
+    xv = x[0, 0].reshape(-1)
+    for _ in range(12):
+        a = tuple(int(rng.integers(0, k)) for k in K)
+        freq = [int(idx[d][a[d]]) for d in range(4)]
+        ph = sum(freq[d] * glob[:, d] / g.n_global[d] for d in range(4))
+        want = sum(v * cmath.exp(-2j * math.pi * p) for v, p in zip(xv, ph))
+        got = flat[0, 0, O.mode_index(g, *a)]
+        assert abs(got - want) <= 1e-10 * max(1.0, abs(want)), (a, got, want)
+
+
 def _brute_forward(x, g):
     """Eq. (full_dft) over dom(p) with plain complex exponentials."""
     K = g.K
