@@ -311,25 +311,36 @@ def forward_workload(torch, D, synth, cfg, device, block=False):
             return dt, float(layers), (f"fp64 oracle, {layers} whole {what} of this workload ({P} shard forwards "
                                        f"summed, mix over all {M} modes, {P} shard inverses{extra}), inputs in "
                                        f"host memory")
-        nc = 1
+        # one (b, c) slice after another of shard 0 through the forward and
+        # the inverse, each with the mix over a block of modes, until
+        # min_seconds have passed
         ms = 8192
         g, x = shards[0]
-        geo = _geo(O, g, batch=1, c_in=nc, c_out=nc)
-        xs = x[0:1, 0:nc].cpu().numpy()
+        geo = _geo(O, g, batch=1, c_in=1, c_out=1)
         Ws = W[:ms, :, :].cpu().numpy()
         Xs = synth.np_complex_normal((B, ci, ms), 12345)
-        Ys = synth.np_complex_normal((1, nc) + geo.K, 12346)
-        Wbs = Wb[:nc, :nc].cpu().numpy() if block else None
-        t0 = time.perf_counter()
-        O.forward(xs, geo)
-        O.mix(Xs, Ws, 0, ms, c_out=co)
-        ys = O.inverse(Ys, geo)
-        if block:
-            O.block_epilogue(xs, Wbs, ys)
-        dt = time.perf_counter() - t0
-        frac = (2 * nc * _vol(g) * 4 + ms * ci * co * 8) / w.bytes
-        return dt, frac, (f"fp64 oracle: forward and inverse of one (b, c) slice of shard 0 and the mix over "
-                          f"{ms} modes; GB/s scaled by the share of the layer's bytes it covers ({frac:.2e})")
+        Ys = synth.np_complex_normal((1, 1) + geo.K, 12346)
+        slices = []
+        dt = 0.0
+        for s_i in range(B * ci):
+            b, c = divmod(s_i, ci)
+            xs = x[b:b + 1, c:c + 1].cpu().numpy()
+            Wbs = Wb[c:c + 1, c:c + 1].cpu().numpy() if block else None
+            t0 = time.perf_counter()
+            O.forward(xs, geo)
+            O.mix(Xs, Ws, 0, ms, c_out=co)
+            ys = O.inverse(Ys, geo)
+            if block:
+                O.block_epilogue(xs, Wbs, ys)
+            dt += time.perf_counter() - t0
+            slices.append((b, c))
+            if dt >= min_seconds:
+                break
+        n = len(slices)
+        frac = n * (2 * _vol(g) * 4 + ms * ci * co * 8) / w.bytes
+        return dt, frac, (f"fp64 oracle: {n} (b, c) slices of shard 0, each through the forward and the inverse "
+                          f"with the mix over {ms} modes; GB/s scaled by the share of the layer's bytes they "
+                          f"cover ({frac:.2e})")
 
     w.cpu_sample = cpu_sample
     return w
@@ -384,24 +395,30 @@ def backward_workload(torch, D, synth, cfg, device):
         """One (b, c) slice through inverse_adj and forward_adj, and the
         data and weight gradients over a mode range, on the fp64 oracle."""
         import oracle as O
-        nc = 1
         ms = 4096
-        geo = _geo(O, g, batch=1, c_in=nc, c_out=nc)
-        gys = gy[0:1, 0:nc].cpu().numpy()
+        geo = _geo(O, g, batch=1, c_in=1, c_out=1)
         Ws = W[:ms].cpu().numpy()
         Xs = synth.np_complex_normal((B, ci, ms), 12345)
         Gs = synth.np_complex_normal((B, co, ms), 12346)
-        GXs = synth.np_complex_normal((1, nc) + geo.K, 12347)
-        t0 = time.perf_counter()
-        O.inverse_adj(gys, geo)
-        O.mix_data_grad(Gs, Ws, 0, ms)
-        O.mix_wgrad(Xs, Gs, 0, ms)
-        O.forward_adj(GXs, geo)
-        dt = time.perf_counter() - t0
-        frac = (2 * nc * _vol(g) * 4 + 2 * ms * ci * co * 8) / w.bytes
-        return dt, frac, (f"fp64 oracle: inverse_adj and forward_adj of one (b, c) slice and the data and "
-                          f"weight gradients over {ms} modes; GB/s scaled by the share of the step's bytes "
-                          f"it covers ({frac:.2e})")
+        GXs = synth.np_complex_normal((1, 1) + geo.K, 12347)
+        n = 0
+        dt = 0.0
+        for s_i in range(B * co):
+            b, c = divmod(s_i, co)
+            gys = gy[b:b + 1, c:c + 1].cpu().numpy()
+            t0 = time.perf_counter()
+            O.inverse_adj(gys, geo)
+            O.mix_data_grad(Gs, Ws, 0, ms)
+            O.mix_wgrad(Xs, Gs, 0, ms)
+            O.forward_adj(GXs, geo)
+            dt += time.perf_counter() - t0
+            n += 1
+            if dt >= min_seconds:
+                break
+        frac = n * (2 * _vol(g) * 4 + 2 * ms * ci * co * 8) / w.bytes
+        return dt, frac, (f"fp64 oracle: {n} (b, c) slices through inverse_adj and forward_adj, each with the "
+                          f"data and weight gradients over {ms} modes; GB/s scaled by the share of the step's "
+                          f"bytes they cover ({frac:.2e})")
 
     w.cpu_sample = cpu_sample
     return w
@@ -451,20 +468,28 @@ def fno_workload(torch, D, synth, cfg, device):
         fp64 oracle."""
         import numpy as np
         import oracle as O
-        nc, ms = 1, 4096
-        geo = _geo(O, g0, batch=1, c_in=nc, c_out=nc)
-        xs0 = xs[0][0:1, 0:nc].cpu().numpy()
+        ms = 4096
+        geo = _geo(O, g0, batch=1, c_in=1, c_out=1)
         Rs = layers[0][0][:ms]
         Xs = synth.np_complex_normal((B, dv, ms), 12345)
-        Ys = synth.np_complex_normal((1, nc) + geo.K, 12346)
-        t0 = time.perf_counter()
-        O.forward(xs0, geo)
-        O.mix(Xs, Rs, 0, ms, c_out=dv)
-        O.block_epilogue(xs0, np.eye(nc), O.inverse(Ys, geo))
-        dt = time.perf_counter() - t0
-        frac = (2 * nc * V * 4 + ms * dv * dv * 8) / w.bytes
-        return dt, frac, (f"fp64 oracle: one Fourier layer of one (b, c) slice of shard 0 and the mix over {ms} "
-                          f"modes; GB/s scaled by the share of the forward's bytes it covers ({frac:.2e})")
+        Ys = synth.np_complex_normal((1, 1) + geo.K, 12346)
+        n = 0
+        dt = 0.0
+        for it in range(64):
+            c = it % xs[0].shape[1]
+            xs0 = xs[0][0:1, c:c + 1].cpu().numpy()
+            t0 = time.perf_counter()
+            O.forward(xs0, geo)
+            O.mix(Xs, Rs, 0, ms, c_out=dv)
+            O.block_epilogue(xs0, np.eye(1), O.inverse(Ys, geo))
+            dt += time.perf_counter() - t0
+            n += 1
+            if dt >= min_seconds:
+                break
+        frac = n * (2 * V * 4 + ms * dv * dv * 8) / w.bytes
+        return dt, frac, (f"fp64 oracle: {n} channel slices of shard 0, each through one Fourier layer (forward, "
+                          f"inverse, bypass and GELU) with the mix over {ms} modes; GB/s scaled by the share of "
+                          f"the forward's bytes they cover ({frac:.2e})")
 
     w.cpu_sample = cpu_sample
     return w
