@@ -220,6 +220,24 @@ dtst_status dtst_block_epilogue(dtst_plan_t p, const float* x, const float* w_by
 dtst_status dtst_inverse_block(dtst_plan_t p, const void* yhat, const float* x, const float* w_bypass, float* y,
                                void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- no-allocation variant ------------------------------------------------ */
+
+/* For callers that cannot allocate device memory or hand over a workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same computation, arguments and errors as dtst_forward, with
+ * the library's own per-device scratch array of DTST_SCRATCH_BYTES as the
+ * workspace, so the call allocates nothing (no hipMalloc, no allocating
+ * library routine).  Every GPU the library runs on holds its own array from
+ * the time the library is loaded until the process ends.  A plan whose
+ * workspace (dtst_plan_info) exceeds DTST_SCRATCH_BYTES gets
+ * DTST_ERR_UNSUPPORTED and nothing is launched.  Every call on one GPU
+ * shares that GPU's array and the array keeps the last call's contents:
+ * calls that overlap in time on one GPU (other streams, threads or plans)
+ * race and give undefined results, so the caller serialises them.  Nothing
+ * in the array needs clearing: a call reads only entries it wrote before. */
+#define DTST_SCRATCH_BYTES ((size_t)64 << 20)
+dtst_status dtst_forward_noalloc(dtst_plan_t p, const float* x, void* xhat, int accumulate, void* stream);
+
 /* ---- instrumentation ----------------------------------------------------- */
 
 /* Per-kernel device time, for callers that time the path (benchmarks,

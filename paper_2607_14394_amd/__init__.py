@@ -15,17 +15,17 @@ import os
 
 __all__ = [
     "DtstError", "Desc", "lib", "make_desc", "dtst_desc_validate", "dtst_desc_workspace_bytes",
-    "dtst_basis_host", "dtst_plan", "dtst_plan_destroy", "PLAN_SPLIT_SCHEDULE", "dtst_plan_info", "dtst_forward", "dtst_mix",
+    "dtst_basis_host", "dtst_plan", "dtst_plan_destroy", "dtst_plan_info", "dtst_forward", "dtst_mix",
     "dtst_inverse", "dtst_forward_adj", "dtst_inverse_adj", "dtst_mix_wgrad", "dtst_block_epilogue",
-    "dtst_inverse_block", "dtst_pointwise",
-    "dtst_profile_enable",
-    "dtst_profile_collect", "Plan", "LIB_PATH",
+    "dtst_inverse_block", "dtst_pointwise", "dtst_forward_noalloc", "dtst_profile_enable",
+    "dtst_profile_collect", "Plan", "LIB_PATH", "PLAN_SPLIT_SCHEDULE", "SCRATCH_BYTES", "torch_stream",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdtst.so")
 
 DTST_OK = 0
 PLAN_SPLIT_SCHEDULE = 1      # DTST_PLAN_SPLIT_SCHEDULE of include/dtst.h
+SCRATCH_BYTES = 64 << 20     # DTST_SCRATCH_BYTES of include/dtst.h
 STATUS_NAMES = {0: "DTST_OK", 1: "DTST_ERR_INVALID_ARG", 2: "DTST_ERR_UNSUPPORTED",
                 3: "DTST_ERR_OUT_OF_MEMORY", 4: "DTST_ERR_DEVICE"}
 
@@ -82,6 +82,7 @@ def _load():
         "dtst_block_epilogue": [P, VP, VP, VP, VP],
         "dtst_inverse_block": [P, VP, VP, VP, VP, VP, SZ, VP],
         "dtst_pointwise": [VP, VP, VP, VP, I64, I64, I64, I64, I, VP],
+        "dtst_forward_noalloc": [P, VP, VP, I, VP],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -156,11 +157,16 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def torch_stream():
+    """The current torch stream as the integer value of its hipStream_t."""
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
 def _stream(stream):
     if stream is not None:
         return ctypes.c_void_p(int(stream))
-    import torch
-    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    return ctypes.c_void_p(torch_stream())
 
 
 def dtst_plan(desc, flags=0):
@@ -190,6 +196,10 @@ def _wsargs(ws):
 def dtst_forward(plan, x, xhat, accumulate, ws, stream=None):
     p, n = _wsargs(ws)
     _check(lib.dtst_forward(plan, _ptr(x), _ptr(xhat), int(accumulate), p, n, _stream(stream)))
+
+
+def dtst_forward_noalloc(plan, x, xhat, accumulate, stream=None):
+    _check(lib.dtst_forward_noalloc(plan, _ptr(x), _ptr(xhat), int(accumulate), _stream(stream)))
 
 
 def dtst_mix(plan, xhat, w_shard, yhat, m0, m1, op=0, stream=None):

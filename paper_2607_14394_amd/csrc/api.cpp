@@ -321,6 +321,12 @@ dtst_status dtst_plan_ex(const dtst_desc* d, uint32_t flags, dtst_plan_t* out) {
     delete p;
     return fail(DTST_ERR_DEVICE, std::string("kernel setup: ") + hipGetErrorString(static_cast<hipError_t>(pe)));
   }
+  // Device address of this device's scratch array (dtst_forward_noalloc),
+  // looked up once per device while the plan's device is current.  A failed
+  // lookup does not fail the plan: dtst_forward_noalloc repeats it and
+  // reports the error.
+  void* scratch = nullptr;
+  (void)dtst::scratch_address(p->device, &scratch);
   {
     std::lock_guard<std::mutex> lk(g_plans_mu);
     live_plans().insert(p);
@@ -362,6 +368,24 @@ dtst_status dtst_forward(dtst_plan_t p, const float* x, void* xhat, int accumula
   DeviceGuard guard(p->device);
   if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
   return run_forward_chain(p, p->dv.d.c_in, x, xhat, accumulate, workspace, p->blob + p->dv.img.t_fwd, stream);
+}
+
+dtst_status dtst_forward_noalloc(dtst_plan_t p, const float* x, void* xhat, int accumulate, void* stream) {
+  DTST_TRY(check_plan(p));
+  if (p->dv.d.batch == 0) return ok();
+  DTST_TRY(check_ptr(x, "x"));
+  DTST_TRY(check_ptr(xhat, "xhat"));
+  if (accumulate != 0 && accumulate != 1) return fail(DTST_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  if (p->dv.ws_bytes > dtst::kScratchBytes)
+    return fail(DTST_ERR_UNSUPPORTED, "this plan needs a workspace of " + std::to_string(p->dv.ws_bytes) +
+                                          " bytes, above the " + std::to_string(dtst::kScratchBytes) +
+                                          "-byte scratch array of dtst_forward_noalloc; use dtst_forward");
+  DeviceGuard guard(p->device);
+  if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
+  void* scratch = nullptr;  // found at plan creation on this device
+  const int se = dtst::scratch_address(p->device, &scratch);
+  if (se != hipSuccess) return device_status(se, "scratch array lookup");
+  return run_forward_chain(p, p->dv.d.c_in, x, xhat, accumulate, scratch, p->blob + p->dv.img.t_fwd, stream);
 }
 
 dtst_status dtst_inverse_adj(dtst_plan_t p, const float* g_y, void* g_yhat, int accumulate, void* workspace,

@@ -145,4 +145,11 @@ int launch_pointwise(const float* x, const float* w, const float* bias, float* y
 int launch_wgrad(const void* xhat, const void* gy, void* gw, int64_t B, int64_t ci, int64_t co,
                  int64_t M, int64_t m0, int64_t m1, int accumulate, void* stream);
 
+// Bytes of the per-device scratch array that dtst_forward_noalloc uses as its
+// workspace (k_scratch.hip).
+constexpr size_t kScratchBytes = DTST_SCRATCH_BYTES;
+// Device address of `device`'s scratch array, looked up with that device
+// current on the first call and kept; hipSuccess or the HIP error.
+int scratch_address(int device, void** out);
+
 }  // namespace dtst
