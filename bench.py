@@ -170,12 +170,13 @@ def _t_classes(g):
 
 def _z_classes(g):
     """z mode classes of the streaming kernels: 4 when z also splits by
-    k mod 4 (N_z % 4 == 0, even k_max, k_t > 8, at most 16 modes per class),
-    2 when it only folds in halves, else 1; the z MFMA work divides by it."""
+    k mod 4 (N_z % 4 == 0, even k_max, and at most 16 modes per class with
+    k_t > 8 or at most 8 with k_t <= 8), 2 when it only folds in halves, else
+    1; the z MFMA work divides by it."""
     if not _folded(g, 2):
         return 1
     Kz = 2 * g["kmax"][2]
-    if g["n_global"][2] % 4 == 0 and g["kmax"][2] % 2 == 0 and g["kt"] > 8 and Kz <= 64:
+    if g["n_global"][2] % 4 == 0 and g["kmax"][2] % 2 == 0 and Kz <= (64 if g["kt"] > 8 else 32):
         return 4
     return 2
 

@@ -94,6 +94,9 @@ __device__ __forceinline__ void times_i_regs(const v4f (&a)[CT], v4f (&out)[CT])
   for (int ct = 0; ct < CT; ++ct) out[ct] = v4f{-a[ct][2], -a[ct][3], a[ct][0], a[ct][1]};
 }
 
+// The forward's t-contracted values hold Re and Im of k_t 8 lanes apart when
+// CT = 1 (and when t folds); the inverse's z-expanded values of the four-class
+// fold hold them in registers i and i + 2 of one lane (CT = 1, and t folds).
 template <int NCLS, int CT, int TF = 0>
 __device__ __forceinline__ void fold_classes(v4f (&V)[NCLS][CT]) {
   if constexpr (NCLS == 2) {
@@ -105,7 +108,6 @@ __device__ __forceinline__ void fold_classes(v4f (&V)[NCLS][CT]) {
       V[1][ct] = d;
     }
   } else if constexpr (NCLS == 4) {
-    static_assert(CT == 2, "the four-class z fold needs Re and Im in separate column tiles");
     // S0 = (V0 + V2) + (V1 + V3)      S2 = (V0 + V2) - (V1 + V3)
     // S1 = (V0 - V2) - i (V1 - V3)    S3 = (V0 - V2) + i (V1 - V3)
     v4f a[CT], b[CT], c[CT], d[CT], id[CT];
@@ -116,7 +118,7 @@ __device__ __forceinline__ void fold_classes(v4f (&V)[NCLS][CT]) {
       c[ct] = V[0][ct] - V[2][ct];
       d[ct] = V[1][ct] - V[3][ct];
     }
-    if constexpr (TF) times_i_lanes<CT>(d, id);
+    if constexpr (TF || CT == 1) times_i_lanes<CT>(d, id);
     else times_i<CT>(d, id);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
@@ -140,7 +142,6 @@ __device__ __forceinline__ void unfold_classes(v4f (&E)[NCLS][CT]) {
       E[1][ct] = d;
     }
   } else if constexpr (NCLS == 4) {
-    static_assert(CT == 2, "the four-class z fold needs Re and Im in separate column tiles");
     // y0 = (E0 + E2) + (E1 + E3)      y2 = (E0 + E2) - (E1 + E3)
     // y1 = (E0 - E2) + i (E1 - E3)    y3 = (E0 - E2) - i (E1 - E3)
     v4f a[CT], b[CT], c[CT], d[CT], id[CT];
@@ -151,7 +152,7 @@ __device__ __forceinline__ void unfold_classes(v4f (&E)[NCLS][CT]) {
       c[ct] = E[0][ct] - E[2][ct];
       d[ct] = E[1][ct] - E[3][ct];
     }
-    if constexpr (TF) times_i_regs<CT>(d, id);
+    if constexpr (TF || CT == 1) times_i_regs<CT>(d, id);
     else times_i<CT>(d, id);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
@@ -317,8 +318,29 @@ __device__ __forceinline__ void tz_finish(const v4f (&P)[NCLS][MT][CT], const St
           const int p = (16 * mr + 4 * g + i) * NCLS + cl;
           if (kc < a.kt && p < a.kz) st(p * a.kt + kc, re, im);
         }
+  } else if constexpr (CT == 1 && MT == 1) {
+    static_assert(NCLS == 4, "one row tile per class is used by the four-class z fold only");
+    // Register 2j holds (Re B) V and register 2j + 1 (Im B) V of slot
+    // s = 2g + j.  Lanes m < 8 finish class 2cp (k_t = m), lanes m >= 8
+    // class 2cp + 1 (k_t = m - 8) of the same slot, trading values as below;
+    // the two modes 4s + 2cp and 4s + 2cp + 1 are adjacent.
+    const bool hi = m >= KTP;
+    const int kc = hi ? m - KTP : m;
+#pragma unroll
+    for (int cp = 0; cp < NCLS / 2; ++cp)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const float q0 = P[2 * cp][0][0][2 * j], u0 = P[2 * cp][0][0][2 * j + 1];
+        const float q1 = P[2 * cp + 1][0][0][2 * j], u1 = P[2 * cp + 1][0][0][2 * j + 1];
+        const float rq = ror8(hi ? q0 : q1);
+        const float ru = ror8(hi ? u0 : u1);
+        const float re = hi ? rq - u1 : q0 - ru;
+        const float im = hi ? q1 + ru : rq + u0;
+        const int p = (2 * g + j) * NCLS + 2 * cp + (hi ? 1 : 0);
+        if (kc < a.kt && p < a.kz) st(p * a.kt + kc, re, im);
+      }
   } else if constexpr (CT == 1) {
-    static_assert(NCLS <= 2, "the four-class z fold needs CT = 2");
+    static_assert(NCLS <= 2, "the four-class z fold of one column tile uses one row tile per class");
     // Lanes m < 8 finish mode p0 (k_t = m), lanes m >= 8 the next mode
     // p0 + 1 (k_t = m - 8): z class 1 of the same slot when folded, else
     // the next accumulator register.  Each lane pair trades the values the
@@ -418,9 +440,12 @@ __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2*
 // The (K_y x K_z K_t) result of the plane is written once.  The shard is read
 // once and the (N_y x K_z K_t) intermediate never reaches HBM.
 // ---------------------------------------------------------------------------
-// Waves per workgroup and tile buffers per wave of fwd_tzy_kernel.
+// Waves per workgroup and tile buffers per wave of fwd_tzy_kernel (a tile of
+// the four-class z fold is twice as large: three buffers keep two 8 KiB tiles
+// in flight per wave within the registers of two waves per SIMD).
 constexpr int kFusedWaves = 8;
 constexpr int kFusedBufs = 4;
+constexpr int kFusedBufs4 = 3;
 // Staging of the fused kernels' basis images in LDS: entries [0, nimg) of
 // the staged range are the z image, the next ny4 the y image, which sits
 // yshift float4 further on in LDS (after the row exchange).  The copy runs in
@@ -494,7 +519,7 @@ template <int TH, int NCLS, int MODE, int NCY, int KYT, int NW, int NB, int YL>
 __global__ void __launch_bounds__(64 * NW)
 fwd_tzy_kernel(const float* __restrict__ x, float2* __restrict__ out, const float* __restrict__ timg,
                const float4* __restrict__ zimg, const float4* __restrict__ yimg, StreamArgs a, FusedArgs f) {
-  constexpr int CT = 1, MT = 2;
+  constexpr int CT = 1, MT = NCLS == 4 ? 1 : 2;
   constexpr int SPW = 16 / NW;  // slots of a group per wave
   constexpr int MTW = 16 / NW;  // 16-column tiles of the y contraction per wave
   extern __shared__ float4 lds[];
@@ -735,10 +760,16 @@ fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
 // expansion: c = 16ct + m with c < 8CT the Re rows of k_t = c and the rest
 // the Im rows of k_t = c - 8CT; with TF k_t = 2(2(m >> 2) + (m & 1)) + ct
 // and part (m >> 1) & 1.
-template <int CT, int TF>
+// With the four-class z fold of one column tile (CT = 1, NCLS = 4) row m is
+// k_t = 2(m >> 2) + (m & 1), part (m >> 1) & 1 (Re and Im of one k_t in
+// registers i and i + 2 of one lane, as with TF).
+template <int CT, int TF, int NCLS = 1>
 __device__ __forceinline__ void inv_row_kt(int ct, int m, int* kt, bool* is_re) {
   if constexpr (TF) {
     *kt = 2 * (2 * (m >> 2) + (m & 1)) + ct;
+    *is_re = ((m >> 1) & 1) == 0;
+  } else if constexpr (CT == 1 && NCLS == 4) {
+    *kt = 2 * (m >> 2) + (m & 1);
     *is_re = ((m >> 1) & 1) == 0;
   } else {
     const int c = 16 * ct + m;
@@ -748,57 +779,78 @@ __device__ __forceinline__ void inv_row_kt(int ct, int m, int* kt, bool* is_re) 
 }
 
 // Spectrum index (p * K_t + k_t) of the value this lane needs for slot
-// s = 16qh + 4g + i of class cl at the k_t of row m of tile ct, or -1 when
-// the mode is not retained.  A pure function of the lane and the shape, so
-// the validity is recomputed where it is used instead of being kept in
-// registers across the row-ahead load.
-template <int CT, int NCLS, int TF>
+// s = 16qh + 4g + i (MT = 1: s = 2g + i, i < 2) of class cl at the k_t of
+// row m of tile ct, or -1 when the mode is not retained.  A pure function of
+// the lane and the shape, so the validity is recomputed where it is used
+// instead of being kept in registers across the row-ahead load.
+template <int CT, int NCLS, int TF, int MT = 2>
 __device__ __forceinline__ int u_index(const StreamArgs& a, int m, int g, int cl, int ct, int qh, int i, bool* is_re) {
-  const int s = 16 * qh + 4 * g + i;
+  const int s = MT == 1 ? 2 * g + i : 16 * qh + 4 * g + i;
   const int p = s * NCLS + cl;
   int kt;
-  inv_row_kt<CT, TF>(ct, m, &kt, is_re);
+  inv_row_kt<CT, TF, NCLS>(ct, m, &kt, is_re);
   return (p < a.kz && kt < a.kt) ? p * a.kt + kt : -1;
 }
+
+// Spectrum values per lane, class and column tile: 4 per pair of row tiles,
+// 2 with one row tile (MT = 1).
+template <int MT>
+struct USlots {
+  static constexpr int QH = MT == 1 ? 1 : MT / 2;
+  static constexpr int N = MT == 1 ? 2 : 4;
+};
 
 // Spectrum values this lane needs from one row (Re and Im rows read the same
 // value; lanes of modes that are not retained read the row start).
 template <int CT, int MT, int NCLS, int TF = 0>
 __device__ __forceinline__ void load_u(const float2* urow, const StreamArgs& a, int m, int g,
-                                       float2 (&dst)[NCLS][CT][MT / 2][4]) {
+                                       float2 (&dst)[NCLS][CT][USlots<MT>::QH][4]) {
 #pragma unroll
   for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-      for (int qh = 0; qh < MT / 2; ++qh)
+      for (int qh = 0; qh < USlots<MT>::QH; ++qh)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < USlots<MT>::N; ++i) {
           bool is_re;
-          const int idx = u_index<CT, NCLS, TF>(a, m, g, cl, ct, qh, i, &is_re);
+          const int idx = u_index<CT, NCLS, TF, MT>(a, m, g, cl, ct, qh, i, &is_re);
           dst[cl][ct][qh][i] = urow[idx < 0 ? 0 : idx];
         }
 }
 
 // A operand of the z expansion (rows c, K index kz' = 16q + 4g + i):
-// kz' < KCP pairs with Re C_z, kz' >= KCP with Im C_z.
+// kz' < KCP pairs with Re C_z, kz' >= KCP with Im C_z; with MT = 1 K index
+// 4g + i is slot 2g + (i >> 1), Re C_z for even i and Im C_z for odd i.
 template <int CT, int MT, int NCLS, int TF = 0>
-__device__ __forceinline__ void build_a(const float2 (&u)[NCLS][CT][MT / 2][4], const StreamArgs& a, int m, int g,
-                                        float (&A)[NCLS][CT][MT][4]) {
+__device__ __forceinline__ void build_a(const float2 (&u)[NCLS][CT][USlots<MT>::QH][4], const StreamArgs& a, int m,
+                                        int g, float (&A)[NCLS][CT][MT][4]) {
 #pragma unroll
   for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int qh = 0; qh < MT / 2; ++qh)
+    for (int ct = 0; ct < CT; ++ct) {
+      if constexpr (MT == 1) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           bool is_re;
-          const bool ok = u_index<CT, NCLS, TF>(a, m, g, cl, ct, qh, i, &is_re) >= 0;
-          const float2 v = ok ? u[cl][ct][qh][i] : make_float2(0.f, 0.f);
-          A[cl][ct][qh][i] = is_re ? v.x : v.y;
-          A[cl][ct][qh + MT / 2][i] = is_re ? -v.y : v.x;
+          const int j = i >> 1;
+          const bool ok = u_index<CT, NCLS, TF, MT>(a, m, g, cl, ct, 0, j, &is_re) >= 0;
+          const float2 v = ok ? u[cl][ct][0][j] : make_float2(0.f, 0.f);
+          A[cl][ct][0][i] = (i & 1) == 0 ? (is_re ? v.x : v.y) : (is_re ? -v.y : v.x);
         }
+      } else {
+#pragma unroll
+        for (int qh = 0; qh < MT / 2; ++qh)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            bool is_re;
+            const bool ok = u_index<CT, NCLS, TF, MT>(a, m, g, cl, ct, qh, i, &is_re) >= 0;
+            const float2 v = ok ? u[cl][ct][qh][i] : make_float2(0.f, 0.f);
+            A[cl][ct][qh][i] = is_re ? v.x : v.y;
+            A[cl][ct][qh + MT / 2][i] = is_re ? -v.y : v.x;
+          }
+      }
+    }
 }
 
 template <int CT, int TH, int MT, int NCLS, int MODE, int TF = 0>
@@ -827,79 +879,89 @@ __device__ __forceinline__ void inv_row(const float (&A)[NCLS][CT][MT][4], float
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct) W[cl][ct] = mfma(A[cl][ct][q][i], B[cl][q][i], W[cl][ct]);
     unfold_classes<NCLS, CT, TF>(W);
-    v4f Y[NCLS][TH];
+    // The t expansion and the stores run over groups of HG output z classes
+    // (all of them at once, except the four-class fold of one row tile, whose
+    // sixteen-wave inverse keeps two groups of two within its registers).
+    constexpr int HG = (NCLS == 4 && MT == 1) ? 1 : NCLS;
+    const int zl = zt * 16 + m;
+    const bool zok = zl < a.zh;
 #pragma unroll
-    for (int hf = 0; hf < NCLS; ++hf)
+    for (int h0 = 0; h0 < NCLS; h0 += HG) {
+      v4f Y[HG][TH];
 #pragma unroll
-      for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = v4f{0.f, 0.f, 0.f, 0.f};
-    if constexpr (TF) {
-      // Even k_t (tile 0) into Y[.][mt], odd k_t (tile 1) into
-      // Y[.][mt + TH/2], for t < N_t/2; then E + O at t, E - O at t + N_t/2.
+      for (int hh = 0; hh < HG; ++hh)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int hf = 0; hf < NCLS; ++hf)
-#pragma unroll
-          for (int mt = 0; mt < TH / 2; ++mt) {
-            Y[hf][mt] = mfma(ta[mt][0][i], W[hf][0][i], Y[hf][mt]);
-            Y[hf][mt + TH / 2] = mfma(ta[mt][1][i], W[hf][1][i], Y[hf][mt + TH / 2]);
-          }
-#pragma unroll
-      for (int hf = 0; hf < NCLS; ++hf)
-#pragma unroll
-        for (int mt = 0; mt < TH / 2; ++mt) {
-          const v4f e = Y[hf][mt], o = Y[hf][mt + TH / 2];
-          Y[hf][mt] = e + o;
-          Y[hf][mt + TH / 2] = e - o;
-        }
-    } else {
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
+        for (int mt = 0; mt < TH; ++mt) Y[hh][mt] = v4f{0.f, 0.f, 0.f, 0.f};
+      if constexpr (TF) {
+        // Even k_t (tile 0) into Y[.][mt], odd k_t (tile 1) into
+        // Y[.][mt + TH/2], for t < N_t/2; then E + O at t, E - O at t + N_t/2.
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int hf = 0; hf < NCLS; ++hf)
+          for (int hh = 0; hh < HG; ++hh)
 #pragma unroll
-            for (int mt = 0; mt < TH; ++mt) Y[hf][mt] = mfma(ta[mt][ct][i], W[hf][ct][i], Y[hf][mt]);
-    }
-
-    const int zl = zt * 16 + m;
-    const bool zok = zl < a.zh;
-    if (MODE != 0 && TH == 2 && a.nt == 32) {
-      // Rows of exactly 32 floats: lanes m and m^8 trade one 16-byte
-      // chunk (DPP row rotate by 8) so that each store instruction writes
-      // 8 whole 128-byte rows instead of 16 half rows.
-      const bool lo = m < 8;
-      const int za = zt * 16 + (m & 7), zb = za + 8;
-      const int tch = (lo ? 0 : 16) + 4 * g;
+            for (int mt = 0; mt < TH / 2; ++mt) {
+              Y[hh][mt] = mfma(ta[mt][0][i], W[h0 + hh][0][i], Y[hh][mt]);
+              Y[hh][mt + TH / 2] = mfma(ta[mt][1][i], W[h0 + hh][1][i], Y[hh][mt + TH / 2]);
+            }
 #pragma unroll
-      for (int hf = 0; hf < NCLS; ++hf) {
-        float va[4], vb[4];
+        for (int hh = 0; hh < HG; ++hh)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float send = lo ? Y[hf][TH - 1][i] : Y[hf][0][i];
-          const float recv = ror8(send);
-          va[i] = lo ? Y[hf][0][i] : recv;
-          vb[i] = lo ? recv : Y[hf][TH - 1][i];
-        }
-        if (MODE == 2 || za < a.zh) store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
-        if (MODE == 2 || zb < a.zh) store_stream(yrow + int64_t(zb + hf * a.zh) * a.nt + tch, vb[0], vb[1], vb[2], vb[3]);
-      }
-      continue;
-    }
+          for (int mt = 0; mt < TH / 2; ++mt) {
+            const v4f e = Y[hh][mt], o = Y[hh][mt + TH / 2];
+            Y[hh][mt] = e + o;
+            Y[hh][mt + TH / 2] = e - o;
+          }
+      } else {
 #pragma unroll
-    for (int hf = 0; hf < NCLS; ++hf) {
-      float* dst = yrow + int64_t(zl + hf * a.zh) * a.nt;
-#pragma unroll
-      for (int mt = 0; mt < TH; ++mt) {
-        const int t0 = 16 * mt + 4 * g;
-        if (MODE != 0) {
-          if (MODE == 2 || (zok && t0 < a.nt))
-            store_stream(dst + t0, Y[hf][mt][0], Y[hf][mt][1], Y[hf][mt][2], Y[hf][mt][3]);
-        } else {
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            if (zok && t0 + i < a.nt) __builtin_nontemporal_store(Y[hf][mt][i], dst + t0 + i);
+#pragma unroll
+            for (int hh = 0; hh < HG; ++hh)
+#pragma unroll
+              for (int mt = 0; mt < TH; ++mt) Y[hh][mt] = mfma(ta[mt][ct][i], W[h0 + hh][ct][i], Y[hh][mt]);
+      }
+
+      if (MODE != 0 && TH == 2 && a.nt == 32) {
+        // Rows of exactly 32 floats: lanes m and m^8 trade one 16-byte
+        // chunk (DPP row rotate by 8) so that each store instruction writes
+        // 8 whole 128-byte rows instead of 16 half rows.
+        const bool lo = m < 8;
+        const int za = zt * 16 + (m & 7), zb = za + 8;
+        const int tch = (lo ? 0 : 16) + 4 * g;
+#pragma unroll
+        for (int hh = 0; hh < HG; ++hh) {
+          const int hf = h0 + hh;
+          float va[4], vb[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float send = lo ? Y[hh][TH - 1][i] : Y[hh][0][i];
+            const float recv = ror8(send);
+            va[i] = lo ? Y[hh][0][i] : recv;
+            vb[i] = lo ? recv : Y[hh][TH - 1][i];
+          }
+          if (MODE == 2 || za < a.zh)
+            store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
+          if (MODE == 2 || zb < a.zh)
+            store_stream(yrow + int64_t(zb + hf * a.zh) * a.nt + tch, vb[0], vb[1], vb[2], vb[3]);
+        }
+        continue;
+      }
+#pragma unroll
+      for (int hh = 0; hh < HG; ++hh) {
+        float* dst = yrow + int64_t(zl + (h0 + hh) * a.zh) * a.nt;
+#pragma unroll
+        for (int mt = 0; mt < TH; ++mt) {
+          const int t0 = 16 * mt + 4 * g;
+          if (MODE != 0) {
+            if (MODE == 2 || (zok && t0 < a.nt))
+              store_stream(dst + t0, Y[hh][mt][0], Y[hh][mt][1], Y[hh][mt][2], Y[hh][mt][3]);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (zok && t0 + i < a.nt) __builtin_nontemporal_store(Y[hh][mt][i], dst + t0 + i);
+          }
         }
       }
     }
@@ -917,7 +979,7 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
   const int64_t row_len = int64_t(a.nz) * a.nt;
   const int64_t spec_len = int64_t(a.kz) * a.kt;
 
-  float2 un[NCLS][CT][MT / 2][4];
+  float2 un[NCLS][CT][USlots<MT>::QH][4];
   if constexpr (TF) {
     // The t-folded instances run two waves per SIMD, which hide each row's
     // spectrum load; the registers of a row-ahead copy would not fit.
@@ -985,7 +1047,7 @@ template <int TH, int NCLS, int MODE, int NCY, int JQY, int YL>
 __global__ void __launch_bounds__(1024)
 inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float* __restrict__ timg,
                const float4* __restrict__ zimg, const float4* __restrict__ yimg, StreamArgs a, FusedArgs f) {
-  constexpr int CT = 1, MT = 2;
+  constexpr int CT = 1, MT = NCLS == 4 ? 1 : 2;
   extern __shared__ float4 lds[];
   const int nimg = NCLS * a.zt * MT * 64;
   float2* vlds = reinterpret_cast<float2*>(lds + nimg);
@@ -1082,7 +1144,7 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
       if (s < f.slots) {
 #pragma unroll
         for (int h = 0; h < NCY; ++h) {
-          float2 uu[NCLS][CT][MT / 2][4];
+          float2 uu[NCLS][CT][USlots<MT>::QH][4];
           load_u<CT, MT, NCLS>(vlds + (h * 16 + w) * f.mrow, a, m, g, uu);
           float A[NCLS][CT][MT][4];
           build_a<CT, MT, NCLS>(uu, a, m, g, A);
@@ -1126,18 +1188,34 @@ void pick3(int mode, fwd_fn* f, inv_fn* v) {
 
 template <int CT, int TH, int MT, int TF>
 void pick2(int ncls, int mode, fwd_fn* f, inv_fn* v) {
-  if constexpr (CT == 2 && MT == 2) {
+  if constexpr (MT == 1) {
+    // one row tile per class: the four-class fold of one column tile only
     if (ncls == 4) {
-      pick3<CT, TH, MT, 4, TF>(mode, f, v);
-      return;
+      pick3<CT, TH, 1, 4, TF>(mode, f, v);
+    } else {
+      *f = nullptr;
+      *v = nullptr;
     }
+  } else {
+    if constexpr (CT == 2 && MT == 2) {
+      if (ncls == 4) {
+        pick3<CT, TH, MT, 4, TF>(mode, f, v);
+        return;
+      }
+    }
+    if (ncls == 2) pick3<CT, TH, MT, 2, TF>(mode, f, v);
+    else pick3<CT, TH, MT, 1, TF>(mode, f, v);
   }
-  if (ncls == 2) pick3<CT, TH, MT, 2, TF>(mode, f, v);
-  else pick3<CT, TH, MT, 1, TF>(mode, f, v);
 }
 
 template <int CT, int TH, int TF>
 void pick1(int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
+  if constexpr (CT == 1 && !TF) {
+    if (mt == 1) {
+      pick2<CT, TH, 1, TF>(ncls, mode, f, v);
+      return;
+    }
+  }
   if (mt == 2) pick2<CT, TH, 2, TF>(ncls, mode, f, v);
   else if (mt == 4) pick2<CT, TH, 4, TF>(ncls, mode, f, v);
   else pick2<CT, TH, 8, TF>(ncls, mode, f, v);
@@ -1152,9 +1230,10 @@ void pick0(int th, int mt, int ncls, int mode, fwd_fn* f, inv_fn* v) {
 
 template <int TH, int NCLS, int MODE, int YL>
 fused_fn pick_fused4(int ncy, int kyt) {
-  if (ncy == 2) return fwd_tzy_kernel<TH, NCLS, MODE, 2, 1, kFusedWaves, kFusedBufs, YL>;
-  if (kyt == 1) return fwd_tzy_kernel<TH, NCLS, MODE, 1, 1, kFusedWaves, kFusedBufs, YL>;
-  return fwd_tzy_kernel<TH, NCLS, MODE, 1, 2, kFusedWaves, kFusedBufs, YL>;
+  constexpr int NB = NCLS == 4 ? kFusedBufs4 : kFusedBufs;
+  if (ncy == 2) return fwd_tzy_kernel<TH, NCLS, MODE, 2, 1, kFusedWaves, NB, YL>;
+  if (kyt == 1) return fwd_tzy_kernel<TH, NCLS, MODE, 1, 1, kFusedWaves, NB, YL>;
+  return fwd_tzy_kernel<TH, NCLS, MODE, 1, 2, kFusedWaves, NB, YL>;
 }
 
 template <int TH, int NCLS, int MODE>
@@ -1188,17 +1267,24 @@ ifused_fn pick_ifused2(int mode, int ncy, int jqy, int yl) {
 // and the y image in LDS (YL = 1) or read from global memory.
 ifused_fn pick_ifused(const StreamCfg& c) {
   const int mode = mode_of(c), yl = c.fused_y_lds;
-  if (c.th == 1)
+  if (c.th == 1) {
+    if (c.ncls == 4) return pick_ifused2<1, 4>(mode, c.ncy, c.kyt, yl);
     return c.ncls == 2 ? pick_ifused2<1, 2>(mode, c.ncy, c.kyt, yl) : pick_ifused2<1, 1>(mode, c.ncy, c.kyt, yl);
+  }
+  if (c.ncls == 4) return pick_ifused2<2, 4>(mode, c.ncy, c.kyt, yl);
   return c.ncls == 2 ? pick_ifused2<2, 2>(mode, c.ncy, c.kyt, yl) : pick_ifused2<2, 1>(mode, c.ncy, c.kyt, yl);
 }
 
-// Fused t + z + y instances: CT = 1, MT = 2, TH <= 2, NCLS <= 2, 16-byte
-// loads; (NCY, KYT) = (2, 1) folded, (1, 1) or (1, 2) otherwise.
+// Fused t + z + y instances: CT = 1, TH <= 2, 16-byte loads, NCLS <= 2 with
+// MT = 2 or NCLS = 4 with MT = 1; (NCY, KYT) = (2, 1) folded, (1, 1) or
+// (1, 2) otherwise.
 fused_fn pick_fused(const StreamCfg& c) {
   const int mode = mode_of(c), yl = c.fused_y_lds;
-  if (c.th == 1)
+  if (c.th == 1) {
+    if (c.ncls == 4) return pick_fused2<1, 4>(mode, c.ncy, c.kyt, yl);
     return c.ncls == 2 ? pick_fused2<1, 2>(mode, c.ncy, c.kyt, yl) : pick_fused2<1, 1>(mode, c.ncy, c.kyt, yl);
+  }
+  if (c.ncls == 4) return pick_fused2<2, 4>(mode, c.ncy, c.kyt, yl);
   return c.ncls == 2 ? pick_fused2<2, 2>(mode, c.ncy, c.kyt, yl) : pick_fused2<2, 1>(mode, c.ncy, c.kyt, yl);
 }
 

@@ -134,17 +134,20 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
     return DTST_ERR_UNSUPPORTED;
   }
   // z folds when this shard holds the whole even z extent: into 2 classes by
-  // mode parity, or into 4 by k mod 4 when N_z % 4 == 0, the stored position
-  // of a mode has its residue (k even), Re / Im of k_t sit in separate column
-  // tiles (ct == 2, which keeps the factors +-i lane-local) and each class
-  // holds at most 16 modes (one Re and one Im row tile: the four-class
-  // kernels fit their registers only at that size).
+  // mode parity, or into 4 by k mod 4 when N_z % 4 == 0 and the stored
+  // position of a mode has its residue (k even).  The four-class fold takes
+  // either Re / Im of k_t in separate column tiles (ct == 2, the factors +-i
+  // swap tiles) with at most 16 modes per class (one Re and one Im row tile:
+  // the kernels fit their registers only at that size), or one column tile
+  // (ct == 1, the factors +-i trade lanes m and m ^ 8) with at most 8 modes
+  // per class, whose Re and Im rows then share one 16-row tile (mt == 1).
   const bool fold = d->n_local[2] == d->n_global[2] && d->n_global[2] % 2 == 0;
-  const bool fold4 =
-      fold && d->n_global[2] % 4 == 0 && d->kmax[2] % 2 == 0 && sc.ct == 2 && sc.kz <= 4 * 16;
-  sc.ncls = fold4 ? 4 : (fold ? 2 : 1);
+  const bool fold4_base = fold && d->n_global[2] % 4 == 0 && d->kmax[2] % 2 == 0;
+  const bool fold4_ct2 = fold4_base && sc.ct == 2 && sc.kz <= 4 * 16;
+  const bool fold4_ct1 = fold4_base && sc.ct == 1 && sc.kz <= 4 * 8;
+  sc.ncls = (fold4_ct2 || fold4_ct1) ? 4 : (fold ? 2 : 1);
   const int slots = static_cast<int>(ceil_div(sc.kz, sc.ncls));
-  int kcp = static_cast<int>(round_up(slots, 16));
+  int kcp = fold4_ct1 ? 8 : static_cast<int>(round_up(slots, 16));
   if (kcp == 48) kcp = 64;
   if (kcp > 64) {
     *err = "more than 64 retained z modes per parity class is not covered";
@@ -224,7 +227,8 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
     sc.fused_lds_bytes = sc.lds_bytes + size_t(16) * sc.ncy * sc.fused_mrow * 8;
     sc.fused_y_lds = sc.fused_lds_bytes + std::max(yf, yi) <= 160 * 1024 ? 1 : 0;
     if (sc.fused_y_lds) sc.fused_lds_bytes += std::max(yf, yi);
-    sc.fuse_y = (!split && sc.ct == 1 && sc.mt == 2 && sc.th <= 2 && sc.ncls <= 2 && sc.vec && dv.K[1] <= 32 &&
+    sc.fuse_y = (!split && sc.ct == 1 && ((sc.mt == 2 && sc.ncls <= 2) || (sc.mt == 1 && sc.ncls == 4)) &&
+                 sc.th <= 2 && sc.vec && dv.K[1] <= 32 &&
                  mcols <= 256 && sc.kyt <= (fold_y ? 1 : 2) && sc.fused_lds_bytes <= 160 * 1024)
                     ? 1
                     : 0;
@@ -303,6 +307,9 @@ void t_forward_image(const Derived& dv, bool adjoint_of_inverse, float* dst) {
 // staged in LDS): float4 entry ((cl*ZT + zt)*MT + mt)*64 + lane, component
 // i, holds row r = 16mt + m at z = 16zt + 4g + i of class cl; rows [0, KCP)
 // are Re B_z[p][z], rows [KCP, 2KCP) are Im B_z[p][z], p = s*NCLS + cl.
+// With MT = 1 (KCP = 8) row r holds slot s = 2(r >> 2) + ((r >> 1) & 1),
+// Re for even r and Im for odd r, so that the products with Re B_z and Im B_z
+// of one slot land in accumulator registers 2j and 2j + 1 of one lane.
 void z_forward_image(const Derived& dv, float* dst) {
   const StreamCfg& sc = dv.sc;
   const dtst_desc& d = dv.d;
@@ -314,8 +321,8 @@ void z_forward_image(const Derived& dv, float* dst) {
             const int m = lane & 15, g = lane >> 4;
             const int row = 16 * mt + m;
             const int z = 16 * zt + 4 * g + i;
-            const bool is_re = row < sc.kcp;
-            const int s = is_re ? row : row - sc.kcp;
+            const bool is_re = sc.mt == 1 ? (row & 1) == 0 : row < sc.kcp;
+            const int s = sc.mt == 1 ? 2 * (row >> 2) + ((row >> 1) & 1) : (is_re ? row : row - sc.kcp);
             const int p = s * sc.ncls + cl;
             double v = 0.0;
             if (p < sc.kz && z < sc.zh) {
@@ -332,7 +339,10 @@ void z_forward_image(const Derived& dv, float* dst) {
 // c = 16ct + 4g + i: Re C_t[t][kt] for c < 8CT, -Im C_t[t][kt] otherwise,
 // where C_t[t][kt] = scale(kt) conj(B_t[kt][t]).  t-folded (tf), only
 // t < N_t/2 is filled and K index 4g + i of tile ct is
-// k_t = 2(2g + (i & 1)) + ct, Re for i < 2 and Im otherwise.
+// k_t = 2(2g + (i & 1)) + ct, Re for i < 2 and Im otherwise.  With the
+// four-class z fold of one column tile (MT = 1), K index 4g + i is
+// k_t = 2g + (i & 1), Re for i < 2 and Im otherwise (Re and Im of one k_t in
+// registers i and i + 2 of one lane of the z expansion).
 void t_inverse_image(const Derived& dv, bool is_inverse, float* dst) {
   const StreamCfg& sc = dv.sc;
   const dtst_desc& d = dv.d;
@@ -346,8 +356,10 @@ void t_inverse_image(const Derived& dv, bool is_inverse, float* dst) {
           const int m = lane & 15, g = lane >> 4;
           const int t = 16 * mt + m;
           const int c = 16 * ct + 4 * g + i;
-          const bool is_re = sc.tf ? i < 2 : c < ktp;
-          const int kt = sc.tf ? 2 * (2 * g + (i & 1)) + ct : (is_re ? c : c - ktp);
+          const bool reg_pairs = sc.tf || sc.mt == 1;
+          const bool is_re = reg_pairs ? i < 2 : c < ktp;
+          const int kt = sc.tf ? 2 * (2 * g + (i & 1)) + ct
+                               : (sc.mt == 1 ? 2 * g + (i & 1) : (is_re ? c : c - ktp));
           double v = 0.0;
           if (t < tlim && kt < sc.kt) {
             double re, im;
@@ -363,6 +375,8 @@ void t_inverse_image(const Derived& dv, bool is_inverse, float* dst) {
 // staged in LDS): float4 entry ((cl*ZT + zt)*MT + q)*64 + lane, component
 // i, holds row kz' = 16q + 4g + i at z = 16zt + m: Re C_z[z][p] for
 // kz' < KCP and Im C_z[z][p] otherwise, C_z[z][p] = conj(B_z[p][z]).
+// With MT = 1 (KCP = 8) row kz' holds slot s = 2g + (i >> 1), Re for even i
+// and Im for odd i.
 void z_inverse_image(const Derived& dv, float* dst) {
   const StreamCfg& sc = dv.sc;
   const dtst_desc& d = dv.d;
@@ -374,8 +388,8 @@ void z_inverse_image(const Derived& dv, float* dst) {
             const int m = lane & 15, g = lane >> 4;
             const int kzp = 16 * q + 4 * g + i;
             const int z = 16 * zt + m;
-            const bool is_re = kzp < sc.kcp;
-            const int s = is_re ? kzp : kzp - sc.kcp;
+            const bool is_re = sc.mt == 1 ? (i & 1) == 0 : kzp < sc.kcp;
+            const int s = sc.mt == 1 ? 2 * g + (i >> 1) : (is_re ? kzp : kzp - sc.kcp);
             const int p = s * sc.ncls + cl;
             double v = 0.0;
             if (p < sc.kz && z < sc.zh) {
