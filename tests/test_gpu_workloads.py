@@ -83,7 +83,7 @@ def _mix_sampled(torch, D, plan, g, cfg, M, name):
 @pytest.mark.parametrize("cfg", [3, 4])
 def test_layer_full_size(cfg):
     """Forward on whole sampled (b, c) slices, mix / wgrad on sampled modes,
-    inverse and forward_adj on sampled points."""
+    inverse and forward_adj on sampled points and on one whole slice each."""
     torch = torch_gpu()
     import paper_2607_14394_amd as D
     g = synth.geometry(cfg)
@@ -112,6 +112,10 @@ def test_layer_full_size(cfg):
         ref = O.inverse_at_points(np_of(yh[b, c]), go, pts)
         got = np.array([y[(b, c) + p].item() for p in pts])
         check(got, ref, f"inverse b={b} c={c} (sampled points)")
+    # one whole (b, c) slice of the shard against the oracle's inverse
+    b, c = B - 1, co - 2
+    check(np_of(y[b:b + 1, c:c + 1]), O.inverse(np_of(yh[b:b + 1, c:c + 1]), go),
+          f"inverse b={b} c={c} (whole slice)")
     del y
     gx = torch.empty((B, ci) + tuple(g["n_local"]), dtype=torch.float32, device="cuda")
     gxh = yh if ci == co else synth.torch_complex_normal((B, ci) + plan.K, 77, "cuda")
@@ -120,6 +124,8 @@ def test_layer_full_size(cfg):
         ref = O.forward_adj_at_points(np_of(gxh[b, c]), go, pts)
         got = np.array([gx[(b, c) + p].item() for p in pts])
         check(got, ref, f"forward_adj b={b} c={c} (sampled points)")
+        check(np_of(gx[b:b + 1, c:c + 1]), O.forward_adj(np_of(gxh[b:b + 1, c:c + 1]), go),
+              f"forward_adj b={b} c={c} (whole slice)")
     del gx, yh, gxh
     plan.close()
     free(torch)
@@ -188,6 +194,8 @@ def test_decomposition_128cubed(cfg):
             pts = sampled_points(g["n_local"], 32, 29)
             ref = O.inverse_at_points(np_of(yh[0, 5]), geo_of(g), pts)
             check(np.array([y[(0, 5) + q].item() for q in pts]), ref, f"shard {p} inverse vs oracle (points)")
+            check(np_of(y[:, 5:6]), O.inverse(np_of(yh[:, 5:6]), geo_of(g)),
+                  f"shard {p} inverse vs oracle (whole channel)")
         plan.close()
         del y
     pf.close()
@@ -198,7 +206,8 @@ def test_decomposition_128cubed(cfg):
 def test_backward_full_size():
     """Workload 5 (modes 64/64/64/16 on the 64x256x256x32 shard): the
     inverse adjoint on whole sampled slices, the mix data gradient and the
-    weight gradient (34.4 GB each) on sampled modes, forward_adj on points."""
+    weight gradient (34.4 GB each) on sampled modes, forward_adj on points
+    and on a whole slice, and the inverse at these modes on a whole slice."""
     torch = torch_gpu()
     import paper_2607_14394_amd as D
     cfg = 5
@@ -226,6 +235,10 @@ def test_backward_full_size():
     ref = O.forward_adj_at_points(np_of(gxh[1, 7]), go, pts)
     got = np.array([gx[(1, 7) + p].item() for p in pts])
     check(got, ref, "forward_adj b=1 c=7 (sampled points)")
+    # whole (b, c) slices of forward_adj and of the inverse at these modes against the oracle
+    check(np_of(gx[1:2, 7:8]), O.forward_adj(np_of(gxh[1:2, 7:8]), go), "forward_adj b=1 c=7 (whole slice)")
+    plan.inverse(gxh, gx)
+    check(np_of(gx[0:1, 30:31]), O.inverse(np_of(gxh[0:1, 30:31]), go), "inverse b=0 c=30 (whole slice)")
     del gxh, gx
     plan.close()
     free(torch)
