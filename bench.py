@@ -120,10 +120,12 @@ def work(g, channels, m_count=None, acc_share=0.0):
     fy = 0.5 if _folded(g, 1) else 1.0
     fx = 0.5 if _folded(g, 0) else 1.0
     w = {}
+    # the t-folded kernels take the complex z products in three real products instead of four
+    z_prod = 0.75 if _t_classes(g) == 2 else 1.0
     w["stream_fwd_tz"] = dict(
         bytes=rows * (Nz * Nt * 4 + Kz * Kt * 8),
         flops=sf["t"] + sf["z"],
-        mfma_flops=sf["t"] / _t_classes(g) + sf["z"] / _z_classes(g))
+        mfma_flops=sf["t"] / _t_classes(g) + sf["z"] / _z_classes(g) * z_prod)
     w["axis_fwd_y"] = dict(bytes=B * C * Nx * (Ny + Ky) * Kz * Kt * 8, flops=sf["y"], mfma_flops=sf["y"] * fy)
     # t + z + y in one launch: reads the shard once, writes the y-contracted rows
     w["stream_fwd_tzy"] = dict(

@@ -252,7 +252,17 @@ __device__ __forceinline__ void t_part(const float (&xv)[NCLS][TH][4], const boo
 // Contracts z of the t-contracted tile V (z tile zt) into P; P is cleared
 // first when zt == 0.  Accumulator register i of V is the B operand of the
 // step whose K index is z = 16zt + 4g + i.
-template <int CT, int MT, int NCLS>
+//
+// t-folded (TF) tiles take the complex product in three real products
+// instead of four: with B = Br + i Bi (row tiles mr and mr + MT/2 of the
+// image) and V = Vr + i Vi,
+//   k1 = (Br + Bi) Vr,   k2 = Br (Vi - Vr),   k3 = Bi (Vr + Vi),
+//   Re BV = k1 - k3,     Im BV = k1 + k2,
+// accumulated in P[.][mr][0] (k1), P[.][mr][1] (k2) and P[.][mr + MT/2][0]
+// (k3).  The B operands are rearranged first so that lanes m < 8 carry the
+// even k_t = 2m and lanes m >= 8 the odd k_t = 2(m - 8) + 1 (Re and Im then
+// share a lane and the finish needs no exchange).
+template <int CT, int MT, int NCLS, int TF = 0>
 __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* lds, const StreamArgs& a, int zt,
                                        int lane, v4f (&P)[NCLS][MT][CT]) {
   float4 A[NCLS][MT];
@@ -267,6 +277,36 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+  }
+  if constexpr (TF) {
+    static_assert(CT == 2 && MT % 2 == 0, "t-folded tiles: two k_t tiles, Re and Im row tiles");
+    const bool lo = (lane & 15) < 8;
+    v4f G1[NCLS], G2[NCLS], G3[NCLS];
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // tile 0: Re (m < 8) / Im (m >= 8) of even k_t; tile 1: the same of odd k_t
+        const float t0 = V[cl][0][i], t1 = V[cl][1][i];
+        const float x0 = ror8(t0), x1 = ror8(t1);
+        const float vi = lo ? x0 : t1;  // Im V of this lane's k_t
+        const float vr = lo ? t0 : x1;  // Re V of this lane's k_t
+        G1[cl][i] = vr;
+        G2[cl][i] = vi - vr;
+        G3[cl][i] = vr + vi;
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+        for (int mr = 0; mr < MT / 2; ++mr) {
+          const float br = A[cl][mr][i], bi = A[cl][mr + MT / 2][i];
+          P[cl][mr][0] = mfma(br + bi, G1[cl][i], P[cl][mr][0]);
+          P[cl][mr][1] = mfma(br, G2[cl][i], P[cl][mr][1]);
+          P[cl][mr + MT / 2][0] = mfma(bi, G3[cl][i], P[cl][mr + MT / 2][0]);
+        }
+    return;
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -286,7 +326,7 @@ __device__ __forceinline__ void tz_tile(const float (&xv)[NCLS][TH][4], const bo
                                         int zt, int lane, v4f (&P)[NCLS][MT][CT]) {
   v4f V[NCLS][CT];
   t_part<CT, TH, NCLS, MODE, TF>(xv, ok, bt, V);
-  z_part<CT, MT, NCLS>(V, lds, a, zt, lane, P);
+  z_part<CT, MT, NCLS, TF>(V, lds, a, zt, lane, P);
 }
 
 // Combines the real-stacked products of a finished row into complex
@@ -299,8 +339,9 @@ __device__ __forceinline__ void tz_finish(const v4f (&P)[NCLS][MT][CT], const St
                                           Store&& st) {
   constexpr int KTP = 8 * CT;
   if constexpr (TF) {
-    // Lanes m < 8 finish the even k_t = 2m of tile 0, lanes m >= 8 the odd
-    // k_t = 2(m - 8) + 1 of tile 1, trading values as in the CT = 1 case.
+    // Lanes m < 8 hold the even k_t = 2m, lanes m >= 8 the odd
+    // k_t = 2(m - 8) + 1 (three-product form of z_part):
+    // Re = k1 - k3, Im = k1 + k2.
     const bool hi = m >= 8;
     const int kc = 2 * (m & 7) + (hi ? 1 : 0);
 #pragma unroll
@@ -309,14 +350,9 @@ __device__ __forceinline__ void tz_finish(const v4f (&P)[NCLS][MT][CT], const St
       for (int mr = 0; mr < MT / 2; ++mr)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float q0 = P[cl][mr][0][i], u0 = P[cl][mr + MT / 2][0][i];
-          const float q1 = P[cl][mr][1][i], u1 = P[cl][mr + MT / 2][1][i];
-          const float rq = ror8(hi ? q0 : q1);
-          const float ru = ror8(hi ? u0 : u1);
-          const float re = hi ? rq - u1 : q0 - ru;
-          const float im = hi ? q1 + ru : rq + u0;
+          const float k1 = P[cl][mr][0][i], k2 = P[cl][mr][1][i], k3 = P[cl][mr + MT / 2][0][i];
           const int p = (16 * mr + 4 * g + i) * NCLS + cl;
-          if (kc < a.kt && p < a.kz) st(p * a.kt + kc, re, im);
+          if (kc < a.kt && p < a.kz) st(p * a.kt + kc, k1 - k3, k1 + k2);
         }
   } else if constexpr (CT == 1 && MT == 1) {
     static_assert(NCLS == 4, "one row tile per class is used by the four-class z fold only");
@@ -968,6 +1004,164 @@ __device__ __forceinline__ void inv_row(const float (&A)[NCLS][CT][MT][4], float
   }
 }
 
+// t-folded inverse row (CT = 2, N_t = 32 whole) with the three-product
+// complex z expansion.  Row r = 4g + i of the z expansion (the MFMA M index)
+// is k_t = 2(2g + (i & 1)) + (i >> 1): registers 0, 1 hold even k_t and 2, 3
+// odd k_t, which the t fold needs apart.  With U the spectrum and C = Cr + i Ci
+// the z basis (K index: 16 modes per block, slot 16qh + 4g + i),
+//   k1 = sum (Ur + Ui) Cr,   k2 = sum Ur (Ci - Cr),   k3 = sum Ui (Cr + Ci),
+//   Re W = k1 - k3,          Im W = k1 + k2,
+// three MFMAs per K step where the four real products took four; Re W and
+// Im W sit in the same register of the same lane, so the factors +-i of the
+// four-class unfold are swaps of the two arrays.  The t image (A operand of
+// the t expansion) holds, at tile ct and register i, part ct (0: Re, 1: -Im)
+// of C_t at that k_t.
+
+// k_t of row m (the M index) of the t-folded z expansion.
+__device__ __forceinline__ int tfg_kt(int m) { return 2 * (2 * (m >> 2) + (m & 1)) + ((m >> 1) & 1); }
+
+// Spectrum index of (slot 16qh + 4g + i of class cl, k_t of row m), or -1.
+template <int NCLS>
+__device__ __forceinline__ int tfg_index(const StreamArgs& a, int m, int g, int cl, int qh, int i) {
+  const int p = (16 * qh + 4 * g + i) * NCLS + cl;
+  const int kt = tfg_kt(m);
+  return (p < a.kz && kt < a.kt) ? p * a.kt + kt : -1;
+}
+
+template <int MT, int NCLS>
+__device__ __forceinline__ void load_u_tfg(const float2* urow, const StreamArgs& a, int m, int g,
+                                           float2 (&dst)[NCLS][MT / 2][4]) {
+#pragma unroll
+  for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+    for (int qh = 0; qh < MT / 2; ++qh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int idx = tfg_index<NCLS>(a, m, g, cl, qh, i);
+        dst[cl][qh][i] = urow[idx < 0 ? 0 : idx];
+      }
+}
+
+template <int TH, int MT, int NCLS, int MODE>
+__device__ __forceinline__ void inv_row_tfg(const float2 (&u)[NCLS][MT / 2][4], float* __restrict__ yrow,
+                                            const float (&ta)[TH][2][4], const float4* lds, const StreamArgs& a,
+                                            int lane) {
+  static_assert(TH % 2 == 0 && MODE != 0, "t folding needs whole 16-byte t groups");
+  const int m = lane & 15, g = lane >> 4;
+  // A operands of the three products: Ur + Ui, Ur, Ui (zero where the mode
+  // or k_t is not retained)
+  float A1[NCLS][MT / 2][4], A2[NCLS][MT / 2][4], A3[NCLS][MT / 2][4];
+#pragma unroll
+  for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+    for (int qh = 0; qh < MT / 2; ++qh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = tfg_index<NCLS>(a, m, g, cl, qh, i) >= 0;
+        const float ur = ok ? u[cl][qh][i].x : 0.f, ui = ok ? u[cl][qh][i].y : 0.f;
+        A1[cl][qh][i] = ur + ui;
+        A2[cl][qh][i] = ur;
+        A3[cl][qh][i] = ui;
+      }
+  for (int zt = 0; zt < a.zt; ++zt) {
+    v4f Wr[NCLS], Wi[NCLS];
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl) {
+      v4f k1 = v4f{0.f, 0.f, 0.f, 0.f}, k2 = k1, k3 = k1;
+#pragma unroll
+      for (int qh = 0; qh < MT / 2; ++qh) {
+        // z image: block qh holds Re C_z, block qh + MT/2 Im C_z of the same slots
+        const float4 cr = lds[((cl * a.zt + zt) * MT + qh) * 64 + lane];
+        const float4 ci = lds[((cl * a.zt + zt) * MT + qh + MT / 2) * 64 + lane];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          k1 = mfma(A1[cl][qh][i], cr[i], k1);
+          k2 = mfma(A2[cl][qh][i], ci[i] - cr[i], k2);
+          k3 = mfma(A3[cl][qh][i], cr[i] + ci[i], k3);
+        }
+      }
+      Wr[cl] = k1 - k3;
+      Wi[cl] = k1 + k2;
+    }
+    if constexpr (NCLS == 2) {
+      // even modes + odd modes at z, even - odd at z + N_z/2
+      const v4f sr = Wr[0] + Wr[1], dr = Wr[0] - Wr[1];
+      const v4f si = Wi[0] + Wi[1], di = Wi[0] - Wi[1];
+      Wr[0] = sr;
+      Wr[1] = dr;
+      Wi[0] = si;
+      Wi[1] = di;
+    } else if constexpr (NCLS == 4) {
+      // y0 = (E0 + E2) + (E1 + E3)      y2 = (E0 + E2) - (E1 + E3)
+      // y1 = (E0 - E2) + i (E1 - E3)    y3 = (E0 - E2) - i (E1 - E3)
+      const v4f ar = Wr[0] + Wr[2], ai = Wi[0] + Wi[2];
+      const v4f br = Wr[1] + Wr[3], bi = Wi[1] + Wi[3];
+      const v4f cr = Wr[0] - Wr[2], ci = Wi[0] - Wi[2];
+      const v4f dr = Wr[1] - Wr[3], di = Wi[1] - Wi[3];
+      Wr[0] = ar + br;
+      Wi[0] = ai + bi;
+      Wr[2] = ar - br;
+      Wi[2] = ai - bi;
+      Wr[1] = cr - di;  // c + i d
+      Wi[1] = ci + dr;
+      Wr[3] = cr + di;  // c - i d
+      Wi[3] = ci - dr;
+    }
+    const int zl = zt * 16 + m;
+#pragma unroll
+    for (int hf = 0; hf < NCLS; ++hf) {
+      // even k_t (registers 0, 1) into E, odd (2, 3) into O, for t < N_t/2
+      v4f E[TH / 2], O[TH / 2];
+#pragma unroll
+      for (int mt = 0; mt < TH / 2; ++mt) {
+        E[mt] = v4f{0.f, 0.f, 0.f, 0.f};
+        O[mt] = v4f{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int mt = 0; mt < TH / 2; ++mt) {
+          v4f& acc = i < 2 ? E[mt] : O[mt];
+          acc = mfma(ta[mt][0][i], Wr[hf][i], acc);
+          acc = mfma(ta[mt][1][i], Wi[hf][i], acc);
+        }
+      v4f Y[TH];
+#pragma unroll
+      for (int mt = 0; mt < TH / 2; ++mt) {
+        Y[mt] = E[mt] + O[mt];
+        Y[mt + TH / 2] = E[mt] - O[mt];
+      }
+      if (TH == 2 && a.nt == 32) {
+        // lanes m and m^8 trade one 16-byte chunk so that each store writes
+        // 8 whole 128-byte rows
+        const bool lo = m < 8;
+        const int za = zt * 16 + (m & 7), zb = za + 8;
+        const int tch = (lo ? 0 : 16) + 4 * g;
+        float va[4], vb[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float send = lo ? Y[TH - 1][i] : Y[0][i];
+          const float recv = ror8(send);
+          va[i] = lo ? Y[0][i] : recv;
+          vb[i] = lo ? recv : Y[TH - 1][i];
+        }
+        if (MODE == 2 || za < a.zh)
+          store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
+        if (MODE == 2 || zb < a.zh)
+          store_stream(yrow + int64_t(zb + hf * a.zh) * a.nt + tch, vb[0], vb[1], vb[2], vb[3]);
+      } else {
+        float* dst = yrow + int64_t(zl + hf * a.zh) * a.nt;
+#pragma unroll
+        for (int mt = 0; mt < TH; ++mt) {
+          const int t0 = 16 * mt + 4 * g;
+          if (MODE == 2 || (zl < a.zh && t0 < a.nt))
+            store_stream(dst + t0, Y[mt][0], Y[mt][1], Y[mt][2], Y[mt][3]);
+        }
+      }
+    }
+  }
+}
+
 // Each row's spectrum is loaded one row ahead (except in the t-folded
 // instances, see below).
 template <int CT, int TH, int MT, int NCLS, int MODE, int TF>
@@ -979,18 +1173,17 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
   const int64_t row_len = int64_t(a.nz) * a.nt;
   const int64_t spec_len = int64_t(a.kz) * a.kt;
 
-  float2 un[NCLS][CT][USlots<MT>::QH][4];
   if constexpr (TF) {
     // The t-folded instances run two waves per SIMD, which hide each row's
     // spectrum load; the registers of a row-ahead copy would not fit.
     for (int64_t r = wave; r < a.rows; r += wstride) {
-      float A[NCLS][CT][MT][4];
-      load_u<CT, MT, NCLS, TF>(in + r * spec_len, a, m, g, un);
-      build_a<CT, MT, NCLS, TF>(un, a, m, g, A);
-      inv_row<CT, TH, MT, NCLS, MODE, TF>(A, y + r * row_len, ta, lds, a, lane);
+      float2 ut[NCLS][MT / 2][4];
+      load_u_tfg<MT, NCLS>(in + r * spec_len, a, m, g, ut);
+      inv_row_tfg<TH, MT, NCLS, MODE>(ut, y + r * row_len, ta, lds, a, lane);
     }
     return;
   }
+  float2 un[NCLS][CT][USlots<MT>::QH][4];
   load_u<CT, MT, NCLS, TF>(in + wave * spec_len, a, m, g, un);
   for (int64_t r = wave; r < a.rows; r += wstride) {
     float A[NCLS][CT][MT][4];

@@ -339,7 +339,8 @@ void z_forward_image(const Derived& dv, float* dst) {
 // c = 16ct + 4g + i: Re C_t[t][kt] for c < 8CT, -Im C_t[t][kt] otherwise,
 // where C_t[t][kt] = scale(kt) conj(B_t[kt][t]).  t-folded (tf), only
 // t < N_t/2 is filled and K index 4g + i of tile ct is
-// k_t = 2(2g + (i & 1)) + ct, Re for i < 2 and Im otherwise.  With the
+// k_t = 2(2g + (i & 1)) + (i >> 1), Re for ct = 0 and Im for ct = 1 (the
+// rows of the three-product z expansion of the t-folded inverse).  With the
 // four-class z fold of one column tile (MT = 1), K index 4g + i is
 // k_t = 2g + (i & 1), Re for i < 2 and Im otherwise (Re and Im of one k_t in
 // registers i and i + 2 of one lane of the z expansion).
@@ -356,9 +357,9 @@ void t_inverse_image(const Derived& dv, bool is_inverse, float* dst) {
           const int m = lane & 15, g = lane >> 4;
           const int t = 16 * mt + m;
           const int c = 16 * ct + 4 * g + i;
-          const bool reg_pairs = sc.tf || sc.mt == 1;
-          const bool is_re = reg_pairs ? i < 2 : c < ktp;
-          const int kt = sc.tf ? 2 * (2 * g + (i & 1)) + ct
+          // t-folded: tile ct holds part ct (0 Re, 1 -Im) of k_t = 2(2g + (i & 1)) + (i >> 1)
+          const bool is_re = sc.tf ? ct == 0 : (sc.mt == 1 ? i < 2 : c < ktp);
+          const int kt = sc.tf ? 2 * (2 * g + (i & 1)) + (i >> 1)
                                : (sc.mt == 1 ? 2 * g + (i & 1) : (is_re ? c : c - ktp));
           double v = 0.0;
           if (t < tlim && kt < sc.kt) {
