@@ -6,9 +6,12 @@
 // (j = y, k = k_y), forward x with the shard-sum accumulate of Eq.
 // (dtst_reduce) (j = x, k = k_x), and the inverse expansions over x and y
 // with conj(B)^T (Sec. V-A Eq. dtst_inverse, reverse order).  The complex
-// product is done as four real MFMA products with the basis split into
-// (Re, Im) parts and the imaginary input negated once per load, so the
-// epilogue is lane-local.
+// product B X, with the basis split into (Re, Im) parts Br, Bi, takes three
+// real MFMA products instead of four:
+//   k1 = (Br + Bi) Xr,   k2 = Br (Xi - Xr),   k3 = Bi (Xr + Xi),
+//   Re = k1 - k3,        Im = k1 + k2,
+// with Br + Bi formed per basis tile and Xi - Xr, Xr + Xi once per input
+// load; every accumulator is lane-local, and so is the epilogue.
 //
 // Folding (FOLD != 0): when the spatial side of the contraction covers the
 // whole even global extent N, exp(-2 pi i k (n + N/2) / N) = (-1)^k
@@ -149,17 +152,19 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
         }
     };
 
-    // FOLD 2 keeps separate even / odd accumulators (index e).
+    // FOLD 2 keeps separate even / odd accumulators (index e); k1, k2, k3
+    // of the three-product form.
     constexpr int NE = FOLD == 2 ? 2 : 1;
-    v4f accr[NE][KT][NT], acci[NE][KT][NT];
+    v4f acc1[NE][KT][NT], acc2[NE][KT][NT], acc3[NE][KT][NT];
 #pragma unroll
     for (int e = 0; e < NE; ++e)
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-          accr[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
-          acci[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+          acc1[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+          acc2[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+          acc3[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
         }
 
     float2 vn[NC][NS][NT][4];
@@ -217,9 +222,9 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
     };
     load_basis(0);
     for (int q = 0; q < a.JQ; ++q) {
-      // B operands: V[c or fold class][nt][i] as (re, im, -im)
+      // B operands: V[c or fold class][nt][i] as (Xr, Xi - Xr, Xr + Xi)
       constexpr int NV = FOLD == 0 ? 1 : 2;
-      float vr[NV][NT][4], vi[NV][NT][4], nvi[NV][NT][4];
+      float vr[NV][NT][4], vd[NV][NT][4], vs[NV][NT][4];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -236,8 +241,8 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
             }
             if (!o) x = make_float2(0.f, 0.f);
             vr[v][nt][i] = x.x;
-            vi[v][nt][i] = x.y;
-            nvi[v][nt][i] = -x.y;
+            vd[v][nt][i] = x.y - x.x;
+            vs[v][nt][i] = x.x + x.y;
           }
         }
       if (q + 1 < a.JQ) load(q + 1, vn, okn);
@@ -250,25 +255,25 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
           const float4 br = bre[kk][e], bi = bim[kk][e];
           const int v = FOLD == 1 ? (kt >= a.kth ? 1 : 0) : (FOLD == 2 ? e : 0);
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < 4; ++i) {
+            const float r = br[i], im = bi[i], rpi = br[i] + bi[i];
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-              const float r = br[i], im = bi[i];
-              float xr, xi, xni;
+              float xr, xd, xs;
               if (FOLD == 1) {  // uniform select of the fold class of this tile
                 xr = v ? vr[NV - 1][nt][i] : vr[0][nt][i];
-                xi = v ? vi[NV - 1][nt][i] : vi[0][nt][i];
-                xni = v ? nvi[NV - 1][nt][i] : nvi[0][nt][i];
+                xd = v ? vd[NV - 1][nt][i] : vd[0][nt][i];
+                xs = v ? vs[NV - 1][nt][i] : vs[0][nt][i];
               } else {
                 xr = vr[FOLD == 2 ? e : 0][nt][i];
-                xi = vi[FOLD == 2 ? e : 0][nt][i];
-                xni = nvi[FOLD == 2 ? e : 0][nt][i];
+                xd = vd[FOLD == 2 ? e : 0][nt][i];
+                xs = vs[FOLD == 2 ? e : 0][nt][i];
               }
-              accr[e][kk][nt] = mfma(r, xr, accr[e][kk][nt]);
-              acci[e][kk][nt] = mfma(r, xi, acci[e][kk][nt]);
-              accr[e][kk][nt] = mfma(im, xni, accr[e][kk][nt]);
-              acci[e][kk][nt] = mfma(im, xr, acci[e][kk][nt]);
+              acc1[e][kk][nt] = mfma(rpi, xr, acc1[e][kk][nt]);
+              acc2[e][kk][nt] = mfma(r, xd, acc2[e][kk][nt]);
+              acc3[e][kk][nt] = mfma(im, xs, acc3[e][kk][nt]);
             }
+          }
         }
       }
       if (q + 1 < a.JQ) load_basis(q + 1);
@@ -283,12 +288,15 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
         const int n = nw + 16 * nt + m;
         const bool nok = n < a.NN;
         float2* ob = out + b * int64_t(a.KO) * a.NN;
+        // Re = k1 - k3, Im = k1 + k2 of accumulator set e
+        auto re_of = [&](int e, int i) { return acc1[e][kk][nt][i] - acc3[e][kk][nt][i]; };
+        auto im_of = [&](int e, int i) { return acc1[e][kk][nt][i] + acc2[e][kk][nt][i]; };
         if (FOLD == 0) {
           float re[4], im[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            re[i] = accr[0][kk][nt][i];
-            im[i] = acci[0][kk][nt][i];
+            re[i] = re_of(0, i);
+            im[i] = im_of(0, i);
           }
           const int k0 = 16 * kt + 4 * g;
           store_tile(re, im, n, nok, ACC, [&](int i) { return ob + int64_t(k0 + i) * a.NN; },
@@ -298,8 +306,8 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
           float re[4], im[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            re[i] = accr[0][kk][nt][i];
-            im[i] = acci[0][kk][nt][i];
+            re[i] = re_of(0, i);
+            im[i] = im_of(0, i);
           }
           const int c = kt >= a.kth ? 1 : 0;
           const int s0 = 16 * (kt - c * a.kth) + 4 * g;
@@ -313,8 +321,8 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
             float re[4], im[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const float er = accr[0][kk][nt][i], ei = acci[0][kk][nt][i];
-              const float odr = accr[NE - 1][kk][nt][i], odi = acci[NE - 1][kk][nt][i];
+              const float er = re_of(0, i), ei = im_of(0, i);
+              const float odr = re_of(NE - 1, i), odi = im_of(NE - 1, i);
               re[i] = hf == 0 ? er + odr : er - odr;
               im[i] = hf == 0 ? ei + odi : ei - odi;
             }
