@@ -336,6 +336,126 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
   }
 }
 
+// Folded inverse expansion (FOLD 2) whose whole contraction fits in a few K
+// steps (JQ <= 2: at most 32 retained modes per parity class).  Such a
+// launch writes four times what it reads (E + O and E - O over N/2 rows from
+// K/2 modes of each class), so each workgroup loads its input columns once,
+// keeps them in registers and loops over every block of KT output tiles: the
+// stores of one block overlap the products of the next, and no other
+// workgroup re-reads the input.  KT output tiles per block, NT 16-column
+// tiles per wave.
+template <int KT, int NT, int JQ>
+__global__ void __launch_bounds__(256)
+axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float4* __restrict__ img,
+                   AxisArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  const int wave = threadIdx.x >> 6;
+  const int64_t total = a.total;
+  for (int64_t hw = blockIdx.x; hw < total; hw += gridDim.x) {
+    const int64_t base = (hw / gridDim.x) * gridDim.x;
+    const int64_t grid_round = (total - base < int64_t(gridDim.x)) ? total - base : int64_t(gridDim.x);
+    const int64_t L = base + xcd_logical(hw - base, grid_round);
+    const int nbk = static_cast<int>(L % a.nblocks);
+    const int64_t b = L / a.nblocks;
+    const int nw = nbk * (64 * NT) + wave * (16 * NT);
+    const float2* inb = in + b * int64_t(a.J) * a.NN;
+    float2* ob = out + b * int64_t(a.KO) * a.NN;
+    const int64_t spare = m < int64_t(a.J) * a.NN ? m : 0;
+
+    // K index jj = 16q + 4g + i: rows 2jj (even modes, class 0) and 2jj + 1 (odd modes, class 1)
+    float2 x[JQ][2][NT][4];
+#pragma unroll
+    for (int q = 0; q < JQ; ++q)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int jj = 16 * q + 4 * g + i;
+          const int n = nw + 16 * nt + m;
+          const bool ok = jj < a.jh && n < a.NN;
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            int64_t idx = ok ? int64_t(2 * jj + c) * a.NN + n : spare;
+            opaque(idx);
+            const float2 v = inb[idx];
+            x[q][c][nt][i] = ok ? v : make_float2(0.f, 0.f);
+          }
+        }
+
+    for (int kb = 0; kb < a.kblocks; ++kb) {
+      v4f acc1[2][KT][NT], acc2[2][KT][NT], acc3[2][KT][NT];
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int kk = 0; kk < KT; ++kk)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            acc1[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+            acc2[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+            acc3[e][kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+          }
+#pragma unroll
+      for (int q = 0; q < JQ; ++q) {
+        float4 bre[KT][2], bim[KT][2];
+#pragma unroll
+        for (int kk = 0; kk < KT; ++kk) {
+          const int kt = min(kb * KT + kk, a.ktiles - 1);
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            // image entry (((kt * JQ + q) * 2 + class) * 2 + part) * 64 + lane
+            const float4* ip = img + ((int64_t(kt) * a.JQ + q) * 2 + e) * 2 * 64 + lane;
+            bre[kk][e] = ip[0];
+            bim[kk][e] = ip[64];
+          }
+        }
+#pragma unroll
+        for (int kk = 0; kk < KT; ++kk)
+#pragma unroll
+          for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float r = bre[kk][e][i], im = bim[kk][e][i], rpi = r + im;
+#pragma unroll
+              for (int nt = 0; nt < NT; ++nt) {
+                const float2 v = x[q][e][nt][i];
+                acc1[e][kk][nt] = mfma(rpi, v.x, acc1[e][kk][nt]);
+                acc2[e][kk][nt] = mfma(r, v.y - v.x, acc2[e][kk][nt]);
+                acc3[e][kk][nt] = mfma(im, v.x + v.y, acc3[e][kk][nt]);
+              }
+            }
+      }
+      // rows y = 16kt + 4g + i < KO/2: E + O at y, E - O at y + KO/2
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) {
+        const int kt = kb * KT + kk;
+        if (kt >= a.ktiles) continue;
+        const int y0 = 16 * kt + 4 * g;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int n = nw + 16 * nt + m;
+          const bool nok = n < a.NN;
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            float re[4], im[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float er = acc1[0][kk][nt][i] - acc3[0][kk][nt][i];
+              const float ei = acc1[0][kk][nt][i] + acc2[0][kk][nt][i];
+              const float odr = acc1[1][kk][nt][i] - acc3[1][kk][nt][i];
+              const float odi = acc1[1][kk][nt][i] + acc2[1][kk][nt][i];
+              re[i] = hf == 0 ? er + odr : er - odr;
+              im[i] = hf == 0 ? ei + odi : ei - odi;
+            }
+            store_tile(re, im, n, nok, 0, [&](int i) { return ob + int64_t(y0 + i + hf * a.oh) * a.NN; },
+                       [&](int i) { return y0 + i < a.oh; });
+          }
+        }
+      }
+    }
+  }
+}
+
 template <int KT, int FOLD, int ACC>
 void launch_kt(int nt, int grid, hipStream_t s, const float2* pin, float2* pout, const float4* pimg,
                const AxisArgs& a) {
@@ -386,6 +506,26 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
   const float4* pimg = reinterpret_cast<const float4*>(img);
   // Accumulation only happens on forward-direction launches (fold 0 or 1).
   if (c.fold == 2 && a.acc) return hipErrorInvalidValue;
+  if (c.fold == 2 && c.JQ <= 2) {
+    // The whole contraction in registers; every workgroup loops over all k
+    // tiles one at a time (measured fastest at the backward workload's
+    // 64-mode y expansion against blocks of two or four tiles), so the work
+    // items are (b, column block) only.
+    AxisArgs e = a;
+    e.kblocks = c.ktiles;
+    const int ent = nb * ((c.NN + 127) / 128) < 2048 ? 1 : 2;
+    e.nblocks = (c.NN + 64 * ent - 1) / (64 * ent);
+    e.total = nb * e.nblocks;
+    const int g2 = static_cast<int>(e.total < cap ? e.total : cap);
+    if (c.JQ == 1) {
+      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 1>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+    } else {
+      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+    }
+    return hipGetLastError();
+  }
   if (c.fold == 2) launch_fold<2, 0>(kt, nt, grid, s, pin, pout, pimg, a);
   else if (c.fold == 1) a.acc ? launch_fold<1, 1>(kt, nt, grid, s, pin, pout, pimg, a)
                               : launch_fold<1, 0>(kt, nt, grid, s, pin, pout, pimg, a);
