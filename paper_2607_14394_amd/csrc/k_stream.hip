@@ -318,17 +318,6 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
         for (int ct = 0; ct < CT; ++ct) P[cl][mt][ct] = mfma(A[cl][mt][i], V[cl][ct][i], P[cl][mt][ct]);
 }
 
-// Contracts t, then z, of the tile (z tile zt) held in xv into P.  Within the
-// tile the independent accumulator chains are interleaved step by step.
-template <int CT, int TH, int MT, int NCLS, int MODE, int TF = 0>
-__device__ __forceinline__ void tz_tile(const float (&xv)[NCLS][TH][4], const bool (&ok)[NCLS][TH * 4],
-                                        const float (&bt)[TH * 4][CT], const float4* lds, const StreamArgs& a,
-                                        int zt, int lane, v4f (&P)[NCLS][MT][CT]) {
-  v4f V[NCLS][CT];
-  t_part<CT, TH, NCLS, MODE, TF>(xv, ok, bt, V);
-  z_part<CT, MT, NCLS, TF>(V, lds, a, zt, lane, P);
-}
-
 // Combines the real-stacked products of a finished row into complex
 // coefficients and hands each one to st(index p * K_t + k_t, re, im):
 // (Re B) V and (Im B) V sit in row tiles mt and mt + MT/2 of the same lane;
@@ -414,49 +403,66 @@ __device__ __forceinline__ void tz_finish(const v4f (&P)[NCLS][MT][CT], const St
   }
 }
 
-// Every wave walks its (row, z-tile) pairs in order and keeps the next
-// pair's loads in flight while it computes the current one.
+// Every wave walks its (row, z-tile) pairs in order and keeps the next PD
+// pairs' loads in flight while it computes the current one (PD = 2 for the
+// t-folded instances, whose tiles take the fewest products per byte, else
+// 1).  Buffer k holds the tiles k, k + PD, k + 2 PD, ... and is refilled as
+// soon as its tile is contracted; the loop runs whole passes over the PD
+// buffers so that every buffer index is a compile-time constant (no
+// register copies, which would wait for loads still in flight).  Every load
+// is unconditional -- positions past the wave's last tile re-read its last
+// row and are never contracted -- so that the wait for a tile covers that
+// tile's loads only, not the ones issued after it.
 template <int CT, int TH, int MT, int NCLS, int MODE, int TF>
 __device__ __forceinline__ void fwd_tz_body(const float* __restrict__ x, float2* __restrict__ out,
                                             const float (&bt)[TH * 4][CT], const float4* lds,
                                             const StreamArgs& a, int64_t wave, int64_t wstride) {
+  constexpr int PD = TF ? 2 : 1;
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
-  const int64_t n_iter = ((a.rows - 1 - wave) / wstride + 1) * a.zt;
+  const int64_t n_rows = (a.rows - 1 - wave) / wstride + 1;
+  const int64_t n_iter = n_rows * a.zt;
+  const int64_t last_row = wave + (n_rows - 1) * wstride;
 
-  float xn[NCLS][TH][4];
-  bool okn[NCLS][TH * 4];
-  load_tile<TH, NCLS, MODE>(x, a, m, g, wave, 0, xn, okn);
-  int64_t rn = wave;
+  float xb[PD][NCLS][TH][4];
+  bool okb[PD][NCLS][TH * 4];
+  int64_t rp[PD], itp[PD];
+  int ztp[PD];
+  int64_t rn = wave, itn = 0;
   int ztn = 0;
-  v4f P[NCLS][MT][CT];
-
-  for (int64_t it = 0; it < n_iter; ++it) {
-    float xv[NCLS][TH][4];
-    bool ok[NCLS][TH * 4];
-#pragma unroll
-    for (int hf = 0; hf < NCLS; ++hf)
-#pragma unroll
-      for (int h = 0; h < TH; ++h)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          xv[hf][h][j] = xn[hf][h][j];
-          ok[hf][4 * h + j] = okn[hf][4 * h + j];
-        }
-    const int64_t r = rn;
-    const int zt = ztn;
+  auto fetch = [&](int k) __attribute__((always_inline)) {
+    rp[k] = rn;
+    ztp[k] = ztn;
+    itp[k] = itn++;
+    load_tile<TH, NCLS, MODE>(x, a, m, g, rn < last_row ? rn : last_row, ztn, xb[k], okb[k]);
     if (++ztn == a.zt) {
       ztn = 0;
       rn += wstride;
     }
-    if (it + 1 < n_iter) load_tile<TH, NCLS, MODE>(x, a, m, g, rn, ztn, xn, okn);
+  };
+#pragma unroll
+  for (int k = 0; k < PD; ++k) fetch(k);
+  v4f P[NCLS][MT][CT];
 
-    tz_tile<CT, TH, MT, NCLS, MODE, TF>(xv, ok, bt, lds, a, zt, lane, P);
-    if (zt != a.zt - 1) continue;
-
+  auto step = [&](auto kc) __attribute__((always_inline)) {
+    constexpr int k = decltype(kc)::value;
+    const bool live = itp[k] < n_iter;
+    const int64_t r = rp[k];
+    const int zt = ztp[k];
+    v4f V[NCLS][CT];
+    if (live) t_part<CT, TH, NCLS, MODE, TF>(xb[k], okb[k], bt, V);
+    fetch(k);
+    if (!live) return;
+    z_part<CT, MT, NCLS, TF>(V, lds, a, zt, lane, P);
+    if (zt != a.zt - 1) return;
     float2* orow = out + r * int64_t(a.kz) * a.kt;
     tz_finish<CT, MT, NCLS, TF>(P, a, m, g, [&](int idx, float re, float im) { orow[idx] = make_float2(re, im); });
-  }
+  };
+  static_assert(PD == 1 || PD == 2, "one or two tiles in flight");
+  do {
+    step(std::integral_constant<int, 0>{});
+    if constexpr (PD > 1) step(std::integral_constant<int, 1>{});
+  } while (itp[0] < n_iter);
 }
 
 // ---------------------------------------------------------------------------
@@ -1042,27 +1048,15 @@ __device__ __forceinline__ void load_u_tfg(const float2* urow, const StreamArgs&
       }
 }
 
+// The A operands of the three products, Ur + Ui, Ur and Ui, are formed from
+// the lane's spectrum values per z tile (zero where the mode or k_t is not
+// retained), so that u is the only per-row state.
 template <int TH, int MT, int NCLS, int MODE>
 __device__ __forceinline__ void inv_row_tfg(const float2 (&u)[NCLS][MT / 2][4], float* __restrict__ yrow,
                                             const float (&ta)[TH][2][4], const float4* lds, const StreamArgs& a,
                                             int lane) {
   static_assert(TH % 2 == 0 && MODE != 0, "t folding needs whole 16-byte t groups");
   const int m = lane & 15, g = lane >> 4;
-  // A operands of the three products: Ur + Ui, Ur, Ui (zero where the mode
-  // or k_t is not retained)
-  float A1[NCLS][MT / 2][4], A2[NCLS][MT / 2][4], A3[NCLS][MT / 2][4];
-#pragma unroll
-  for (int cl = 0; cl < NCLS; ++cl)
-#pragma unroll
-    for (int qh = 0; qh < MT / 2; ++qh)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool ok = tfg_index<NCLS>(a, m, g, cl, qh, i) >= 0;
-        const float ur = ok ? u[cl][qh][i].x : 0.f, ui = ok ? u[cl][qh][i].y : 0.f;
-        A1[cl][qh][i] = ur + ui;
-        A2[cl][qh][i] = ur;
-        A3[cl][qh][i] = ui;
-      }
   for (int zt = 0; zt < a.zt; ++zt) {
     v4f Wr[NCLS], Wi[NCLS];
 #pragma unroll
@@ -1075,9 +1069,11 @@ __device__ __forceinline__ void inv_row_tfg(const float2 (&u)[NCLS][MT / 2][4], 
         const float4 ci = lds[((cl * a.zt + zt) * MT + qh + MT / 2) * 64 + lane];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          k1 = mfma(A1[cl][qh][i], cr[i], k1);
-          k2 = mfma(A2[cl][qh][i], ci[i] - cr[i], k2);
-          k3 = mfma(A3[cl][qh][i], cr[i] + ci[i], k3);
+          const bool ok = tfg_index<NCLS>(a, m, g, cl, qh, i) >= 0;
+          const float ur = ok ? u[cl][qh][i].x : 0.f, ui = ok ? u[cl][qh][i].y : 0.f;
+          k1 = mfma(ur + ui, cr[i], k1);
+          k2 = mfma(ur, ci[i] - cr[i], k2);
+          k3 = mfma(ui, cr[i] + ci[i], k3);
         }
       }
       Wr[cl] = k1 - k3;
@@ -1174,13 +1170,32 @@ __device__ __forceinline__ void inv_zt_body(const float2* __restrict__ in, float
   const int64_t spec_len = int64_t(a.kz) * a.kt;
 
   if constexpr (TF) {
-    // The t-folded instances run two waves per SIMD, which hide each row's
-    // spectrum load; the registers of a row-ahead copy would not fit.
-    for (int64_t r = wave; r < a.rows; r += wstride) {
-      float2 ut[NCLS][MT / 2][4];
-      load_u_tfg<MT, NCLS>(in + r * spec_len, a, m, g, ut);
-      inv_row_tfg<TH, MT, NCLS, MODE>(ut, y + r * row_len, ta, lds, a, lane);
-    }
+    // Two spectrum buffers: while one row is expanded the next row's values
+    // are in flight in the other; passes of two rows keep the buffer index a
+    // compile-time constant, and the loads are unconditional (past the last
+    // row the wave re-reads its last row, which is not expanded again).
+    const int64_t n_rows = (a.rows - 1 - wave) / wstride + 1;
+    const int64_t last_row = wave + (n_rows - 1) * wstride;
+    float2 ub[2][NCLS][MT / 2][4];
+    int64_t rp[2];
+    int64_t rn = wave;
+    auto fetch = [&](int k) __attribute__((always_inline)) {
+      rp[k] = rn;
+      load_u_tfg<MT, NCLS>(in + (rn < last_row ? rn : last_row) * spec_len, a, m, g, ub[k]);
+      rn += wstride;
+    };
+    fetch(0);
+    fetch(1);
+    auto step = [&](auto kc) __attribute__((always_inline)) {
+      constexpr int k = decltype(kc)::value;
+      const int64_t r = rp[k];
+      if (r <= last_row) inv_row_tfg<TH, MT, NCLS, MODE>(ub[k], y + r * row_len, ta, lds, a, lane);
+      fetch(k);
+    };
+    do {
+      step(std::integral_constant<int, 0>{});
+      step(std::integral_constant<int, 1>{});
+    } while (rp[0] <= last_row);
     return;
   }
   float2 un[NCLS][CT][USlots<MT>::QH][4];
