@@ -152,11 +152,30 @@ def work(g, channels, m_count=None, acc_share=0.0):
     return w
 
 
+def _block_zt_work(g):
+    """The fused inverse z + t expansion and block epilogue: reads the
+    y-expanded spectrum (B, C_out, N_x, N_y, K_z, K_t) and the block input x,
+    writes y once.  Executed flops: the z expansion with z folded in two
+    classes where the shard holds the whole even N_z (three real products per
+    complex one when t folds), the t expansion (halved when t folds), and the
+    bypass (C_out x C_in per point) on the matrix cores."""
+    B, ci, co = g["batch"], g["c_in"], g["c_out"]
+    Nx, Ny, Nz, Nt = g["n_local"]
+    Kz, Kt = 2 * g["kmax"][2], g["kt"]
+    V = _vol(g)
+    sf = stage_flops(g, co)
+    zc = 2 if _folded(g, 2) else 1
+    tc = _t_classes(g)
+    byp = 2 * B * V * ci * co
+    return dict(bytes=B * co * Nx * Ny * Kz * Kt * 8 + B * (ci + co) * V * 4, flops=sf["t"] + sf["z"] + byp,
+                mfma_flops=sf["t"] / tc + sf["z"] / zc * (0.75 if tc == 2 else 1.0) + byp)
+
+
 # Kernel roles whose products run on the matrix cores (the per-dimension
 # contractions); the mix, its gradients and the point-wise layers run on the
 # vector ALUs.
 CONTRACTION_ROLES = ("stream_fwd_tzy", "stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "axis_inv_x", "axis_inv_y",
-                     "stream_inv_zt", "stream_inv_yzt")
+                     "stream_inv_zt", "stream_inv_yzt", "stream_inv_zt_block")
 
 
 def _folded(g, dim):
@@ -274,6 +293,7 @@ def forward_workload(torch, D, synth, cfg, device, block=False):
     B0, ci0, co0, V0 = g0["batch"], g0["c_in"], g0["c_out"], _vol(g0)
     per["block_epilogue"] = dict(bytes=B0 * V0 * (ci0 + 2 * co0) * 4, flops=2 * B0 * V0 * ci0 * co0,
                                  mfma_flops=2 * B0 * V0 * ci0 * co0)
+    per["stream_inv_zt_block"] = _block_zt_work(g0)
     w.work = per
     B, ci, co = g0["batch"], g0["c_in"], g0["c_out"]
     w.bytes = P * B * (ci + co) * _vol(g0) * 4 + M * ci * co * 8   # read x, write y, read W
@@ -455,6 +475,7 @@ def fno_workload(torch, D, synth, cfg, device):
     per["mix"] = _mix_work(g0, M // P, "mix")
     V = _vol(g0)
     per["block_epilogue"] = dict(bytes=B * V * 3 * dv * 4, flops=2 * B * V * dv * dv, mfma_flops=2 * B * V * dv * dv)
+    per["stream_inv_zt_block"] = _block_zt_work(g0)
     # lift (C_in -> d_v) and projection (d_v -> C_out) move and compute the same per point when C_in = C_out
     pw = [B * V * (cin + dv) * 4, B * V * (dv + cout) * 4]
     per["pointwise"] = dict(bytes=sum(pw) / 2, flops=B * V * dv * (cin + cout), mfma_flops=B * V * dv * (cin + cout))

@@ -128,7 +128,11 @@ enum {
    * agrees with the default schedule to rounding (the contraction order of
    * Sec. V-B is the same); the workspace then also holds the (.., N_x, N_y,
    * K_z, K_t) intermediate. */
-  DTST_PLAN_SPLIT_SCHEDULE = 1u
+  DTST_PLAN_SPLIT_SCHEDULE = 1u,
+  /* Run dtst_inverse_block as the inverse followed by a separate epilogue
+   * launch (the form of dtst_inverse + dtst_block_epilogue) instead of the
+   * fused z + t expansion and epilogue kernel.  Same result to rounding. */
+  DTST_PLAN_UNFUSED_BLOCK = 2u
 };
 
 /* dtst_plan with options: `flags` is 0 or a combination of the DTST_PLAN_*
@@ -212,13 +216,30 @@ dtst_status dtst_pointwise(const float* x, const float* w, const float* bias, fl
  * Asynchronous on `stream`, no allocation. */
 dtst_status dtst_block_epilogue(dtst_plan_t p, const float* x, const float* w_bypass, float* y, void* stream);
 
-/* The block's last step in one call: the inverse partial DFT of yhat (as
- * dtst_inverse) followed by the block epilogue (as dtst_block_epilogue),
+/* The block's last step in one call (Algorithm 1, last step; Eq.
+ * dtst_inverse for the spectral part): the inverse partial DFT of yhat
+ * followed by the block epilogue,
  *   y = GELU( w_bypass x + inverse(yhat) ),
- * with the same arrays, layouts, alignment and overlap rules; both steps are
- * enqueued on `stream` one after the other.  No allocation. */
+ * with the arrays, layouts, alignment and overlap rules of dtst_inverse and
+ * dtst_block_epilogue.  Where the plan allows it (N_t^loc a multiple of 4 and
+ * at most 32, C_in and C_out at most 32, at most 32 z modes per fold class,
+ * the per-workgroup buffers within the LDS; see
+ * dtst_plan_block_workspace_bytes) the z and t expansions and the epilogue
+ * run as one kernel that writes y once and reads x once; otherwise, or with
+ * DTST_PLAN_UNFUSED_BLOCK, the inverse and the epilogue are enqueued one
+ * after the other.  The workspace must hold
+ * dtst_plan_block_workspace_bytes(p) bytes (DTST_ERR_INVALID_ARG otherwise);
+ * it is scratch, owned by the caller.  Asynchronous on `stream`, no
+ * allocation. */
 dtst_status dtst_inverse_block(dtst_plan_t p, const void* yhat, const float* x, const float* w_bypass, float* y,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes dtst_inverse_block needs with this plan (at least the
+ * workspace of dtst_plan_info; larger where the layer's own calls fuse the y
+ * expansion and the block kernel reads the y-expanded (B, C_out, N_x, N_y,
+ * K_z, K_t) intermediate), and whether it runs the fused kernel (1) or the
+ * two launches (0).  Either output may be null. */
+dtst_status dtst_plan_block_info(dtst_plan_t p, size_t* workspace_bytes, int* fused);
 
 /* ---- no-allocation variant ------------------------------------------------ */
 

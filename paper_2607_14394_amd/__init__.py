@@ -18,13 +18,15 @@ __all__ = [
     "dtst_basis_host", "dtst_plan", "dtst_plan_destroy", "dtst_plan_info", "dtst_forward", "dtst_mix",
     "dtst_inverse", "dtst_forward_adj", "dtst_inverse_adj", "dtst_mix_wgrad", "dtst_block_epilogue",
     "dtst_inverse_block", "dtst_pointwise", "dtst_forward_noalloc", "dtst_profile_enable",
-    "dtst_profile_collect", "Plan", "LIB_PATH", "PLAN_SPLIT_SCHEDULE", "SCRATCH_BYTES", "torch_stream",
+    "dtst_profile_collect", "dtst_plan_block_info", "Plan", "LIB_PATH", "PLAN_SPLIT_SCHEDULE",
+    "PLAN_UNFUSED_BLOCK", "SCRATCH_BYTES", "torch_stream",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdtst.so")
 
 DTST_OK = 0
 PLAN_SPLIT_SCHEDULE = 1      # DTST_PLAN_SPLIT_SCHEDULE of include/dtst.h
+PLAN_UNFUSED_BLOCK = 2       # DTST_PLAN_UNFUSED_BLOCK of include/dtst.h
 SCRATCH_BYTES = 64 << 20     # DTST_SCRATCH_BYTES of include/dtst.h
 STATUS_NAMES = {0: "DTST_OK", 1: "DTST_ERR_INVALID_ARG", 2: "DTST_ERR_UNSUPPORTED",
                 3: "DTST_ERR_OUT_OF_MEMORY", 4: "DTST_ERR_DEVICE"}
@@ -73,6 +75,7 @@ def _load():
         "dtst_plan_ex": [ctypes.POINTER(Desc), ctypes.c_uint32, ctypes.POINTER(P)],
         "dtst_plan_destroy": [P],
         "dtst_plan_info": [P, ctypes.POINTER(I64), ctypes.POINTER(SZ)],
+        "dtst_plan_block_info": [P, ctypes.POINTER(SZ), ctypes.POINTER(I)],
         "dtst_forward": [P, VP, VP, I, VP, SZ, VP],
         "dtst_mix": [P, VP, VP, VP, I64, I64, I, VP],
         "dtst_inverse": [P, VP, VP, VP, SZ, VP],
@@ -170,7 +173,8 @@ def _stream(stream):
 
 
 def dtst_plan(desc, flags=0):
-    """dtst_plan_ex; flags 0 (default schedule) or PLAN_SPLIT_SCHEDULE."""
+    """dtst_plan_ex; flags 0 or a combination of PLAN_SPLIT_SCHEDULE and
+    PLAN_UNFUSED_BLOCK."""
     h = ctypes.c_void_p()
     _check(lib.dtst_plan_ex(ctypes.byref(_desc(desc)), int(flags), ctypes.byref(h)))
     return h
@@ -185,6 +189,14 @@ def dtst_plan_info(plan):
     ws = ctypes.c_size_t(0)
     _check(lib.dtst_plan_info(plan, ctypes.byref(m), ctypes.byref(ws)))
     return m.value, ws.value
+
+
+def dtst_plan_block_info(plan):
+    """(workspace bytes of dtst_inverse_block, 1 if it runs the fused kernel)."""
+    ws = ctypes.c_size_t(0)
+    fused = ctypes.c_int(0)
+    _check(lib.dtst_plan_block_info(plan, ctypes.byref(ws), ctypes.byref(fused)))
+    return ws.value, fused.value
 
 
 def _wsargs(ws):
@@ -276,6 +288,9 @@ class Plan:
         self.handle = dtst_plan(self.desc, flags)
         self.n_modes, self.ws_bytes = dtst_plan_info(self.handle)
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=device)
+        self.block_ws_bytes, self.block_fused = dtst_plan_block_info(self.handle)
+        self.ws_block = None   # allocated by the first inverse_block when larger than ws
+        self.device = device
         d = self.desc
         self.K = (2 * d.kmax[0], 2 * d.kmax[1], 2 * d.kmax[2], d.kt)
         self.n_local = tuple(d.n_local)
@@ -354,7 +369,12 @@ class Plan:
         self._need(x, self.spatial_shape(self.desc.c_in), torch.float32, "x")
         self._need(w_bypass, (self.desc.c_out, self.desc.c_in), torch.float32, "w_bypass")
         self._need(y, self.spatial_shape(self.desc.c_out), torch.float32, "y")
-        dtst_inverse_block(self.handle, yhat, x, w_bypass, y, self.ws, stream)
+        ws = self.ws
+        if self.block_ws_bytes > self.ws_bytes:
+            if self.ws_block is None:
+                self.ws_block = torch.empty(self.block_ws_bytes, dtype=torch.uint8, device=self.device)
+            ws = self.ws_block
+        dtst_inverse_block(self.handle, yhat, x, w_bypass, y, ws, stream)
 
     def block_epilogue(self, x, w_bypass, y, stream=None):
         """y <- GELU(w_bypass x + y) in place (the block's bypass and activation)."""

@@ -98,10 +98,10 @@ dtst_status check_ws(const dtst_plan_st* p, const void* ws, size_t ws_bytes) {
 
 // ---- per-kernel event timing (dtst_profile_enable / dtst_profile_collect) ----
 enum KernelRole { K_FWD_TZ, K_AXIS_FWD_Y, K_AXIS_FWD_X, K_AXIS_INV_X, K_AXIS_INV_Y, K_INV_ZT, K_MIX, K_MIX_H,
-                  K_WGRAD, K_BLOCK, K_FWD_TZY, K_INV_YZT, K_POINTWISE, K_COUNT };
+                  K_WGRAD, K_BLOCK, K_FWD_TZY, K_INV_YZT, K_POINTWISE, K_INV_ZT_BLOCK, K_COUNT };
 const char* const kRoleNames[K_COUNT] = {"stream_fwd_tz", "axis_fwd_y", "axis_fwd_x", "axis_inv_x", "axis_inv_y",
                                          "stream_inv_zt", "mix", "mix_h", "wgrad", "block_epilogue",
-                                         "stream_fwd_tzy", "stream_inv_yzt", "pointwise"};
+                                         "stream_fwd_tzy", "stream_inv_yzt", "pointwise", "stream_inv_zt_block"};
 
 struct Profiler {
   std::mutex mu;
@@ -315,7 +315,9 @@ dtst_status dtst_plan_ex(const dtst_desc* d, uint32_t flags, dtst_plan_t* out) {
     delete p;
     return fail(DTST_ERR_DEVICE, std::string("hipMemcpy of the basis tables: ") + hipGetErrorString(e));
   }
-  const int pe = dtst::prepare_stream(&p->dv.sc);
+  int pe = dtst::prepare_stream(&p->dv.sc);
+  if (pe == hipSuccess && p->dv.blk)
+    pe = dtst::prepare_block_zt(p->dv.sb, p->dv.d.c_in, p->dv.d.c_out, &p->dv.grid_blk);
   if (pe != hipSuccess) {
     (void)hipFree(p->blob);
     delete p;
@@ -546,11 +548,41 @@ dtst_status dtst_inverse_block(dtst_plan_t p, const void* yhat, const float* x, 
   if (dv.d.batch == 0) return ok();
   DTST_TRY(check_ptr(yhat, "yhat"));
   DTST_TRY(check_block(p, x, w_bypass, y));
-  DTST_TRY(check_ws(p, workspace, workspace_bytes));
+  if (workspace_bytes < dv.blk_ws_bytes)
+    return fail(DTST_ERR_INVALID_ARG, "workspace too small: need " + std::to_string(dv.blk_ws_bytes) +
+                                          " bytes, got " + std::to_string(workspace_bytes));
+  if (dv.blk_ws_bytes > 0) DTST_TRY(check_ptr(workspace, "workspace"));
   DeviceGuard guard(p->device);
   if (guard.err != hipSuccess) return device_status(guard.err, "hipSetDevice");
-  DTST_TRY(run_inverse_chain(p, dv.d.c_out, yhat, y, workspace, p->blob + dv.img.t_inv, stream));
-  return run_block_epilogue(p, x, w_bypass, y, stream);
+  if (!dv.blk) {
+    DTST_TRY(run_inverse_chain(p, dv.d.c_out, yhat, y, workspace, p->blob + dv.img.t_inv, stream));
+    return run_block_epilogue(p, x, w_bypass, y, stream);
+  }
+  // x expansion into W2, y expansion into W1, then z + t with the epilogue
+  const int64_t B = dv.d.batch, co = dv.d.c_out;
+  char* w1 = static_cast<char*>(workspace);
+  char* w2 = w1 + dv.blk_w1_bytes;
+  int e = timed(K_AXIS_INV_X, stream, [&] {
+    return dtst::launch_axis(dv.ax_i, B * co, yhat, w2, p->blob + dv.img.x_inv, 0, stream);
+  });
+  if (e != hipSuccess) return device_status(e, "x expansion launch");
+  const int64_t planes = B * co * dv.d.n_local[0];
+  e = timed(K_AXIS_INV_Y, stream,
+            [&] { return dtst::launch_axis(dv.ay_i, planes, w2, w1, p->blob + dv.img.y_inv, 0, stream); });
+  if (e != hipSuccess) return device_status(e, "y expansion launch");
+  e = timed(K_INV_ZT_BLOCK, stream, [&] {
+    return dtst::launch_inv_zt_block(dv.sb, dv.grid_blk, w1, x, w_bypass, y, B,
+                                     dv.d.n_local[0] * dv.d.n_local[1], dv.d.c_in, co, p->blob + dv.img.t_blk,
+                                     p->blob + dv.img.z_blk, stream);
+  });
+  return device_status(e, "z+t expansion and block epilogue launch");
+}
+
+dtst_status dtst_plan_block_info(dtst_plan_t p, size_t* workspace_bytes, int* fused) {
+  DTST_TRY(check_plan(p));
+  if (workspace_bytes) *workspace_bytes = p->dv.blk_ws_bytes;
+  if (fused) *fused = p->dv.blk;
+  return ok();
 }
 
 dtst_status dtst_profile_enable(int on) {

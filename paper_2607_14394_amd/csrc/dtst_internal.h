@@ -81,6 +81,7 @@ struct Images {
   size_t t_inv = 0, t_inv_adjoint_of_forward = 0;  // streaming inverse, A operand
   size_t z_inv = 0;                                // streaming inverse, LDS image
   size_t y_fwd = 0, x_fwd = 0, y_inv = 0, x_inv = 0;  // axis images
+  size_t z_blk = 0, t_blk = 0;                         // fused inverse + block epilogue
   size_t total = 0;
 };
 
@@ -93,6 +94,14 @@ struct Derived {
   size_t ws_bytes = 0;
   size_t w1_bytes = 0;  // workspace offset of W2 (0 with the fused y: no W1)
   Images img;
+  // Fused inverse + block epilogue (inv_zt_block_kernel): its z + t
+  // configuration (z folded into at most 2 classes), whether dtst_inverse_block
+  // uses it, the workspace it needs (W1 then W2), and its resident grid (set
+  // at plan creation on the plan's device).
+  StreamCfg sb;
+  int blk = 0;
+  size_t blk_ws_bytes = 0, blk_w1_bytes = 0;
+  int grid_blk = 0;
 };
 
 // Host-side validation and derivation (pure C++; no HIP).
@@ -125,6 +134,16 @@ int launch_inv_yzt(const StreamCfg& c, const AxisCfg& ay, const void* in, float*
                    const float* timg, const float* zimg, const float* yimg, void* stream);
 int launch_inv_zt(const StreamCfg& c, const void* in, float* y, int64_t rows,
                   const float* timg, const float* zimg, void* stream);
+// Fused inverse z + t expansion and block epilogue (k_block_zt.hip):
+//   y[b,o,.] = GELU(w x[b,.,.] + zt-expansion of in[b,o,.]) over the
+// batch * nxy (b, x, y) rows; in is the y-expanded spectrum
+// (B, C_out, N_x, N_y, K_z, K_t), c its z + t configuration (Derived::sb).
+size_t block_zt_lds_bytes(const StreamCfg& c, int64_t co);
+bool block_zt_supported(const StreamCfg& c, int64_t ci, int64_t co);
+int prepare_block_zt(const StreamCfg& c, int64_t ci, int64_t co, int* grid);
+int launch_inv_zt_block(const StreamCfg& c, int grid_resident, const void* in, const float* x, const float* w,
+                        float* y, int64_t batch, int64_t nxy, int64_t ci, int64_t co, const float* timg,
+                        const float* zimg, void* stream);
 int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const float* img,
                 int accumulate, void* stream);
 // LDS bytes of one workgroup of the mix kernels (mix, mix_h and wgrad alike).

@@ -1,0 +1,555 @@
+// Inverse z + t expansion fused with the block epilogue (Sec. V "Block
+// Structure"; Algorithm 1, its first and last step):
+//
+//   y[b,o,n] = GELU( sum_i w[o,i] x[b,i,n] + Re sum_{kz,kt} C_t C_z V[b,o,kz,kt] ),
+//
+// where V is the y-expanded spectrum (B, C_out, N_x, N_y, K_z, K_t) of the
+// inverse chain and C_z, C_t the z and t expansion bases (half-spectrum
+// weights and 1/prod N folded into C_t).  The separate epilogue kernel reads
+// y back and writes it again; here every output value is written once and
+// the layer input x is read once.
+//
+// A workgroup of kBlkWaves waves owns one (b, x, y) row at a time
+// (persistent over rows) and produces every output channel of it, one chunk
+// at a time: a chunk is the 16 z rows of one z tile of one fold class (all
+// N_t of them), so a z tile of a folded row is two chunks.
+//   phase 1: wave w expands the chunk for the channels o = w, w + kBlkWaves,
+//            ... from the row's spectrum (staged in LDS for every channel at
+//            the row start): the z expansion and class unfold once per z
+//            tile (kept in registers for the tile's second chunk), the t
+//            expansion of the chunk's class; the values go to one of two LDS
+//            buffers as [o][z row][t];
+//   phase 2: wave w takes one 64-point group of the chunk and forms
+//            y[o][p] = GELU(Ys[o][p] + sum_i w[o,i] x[i][p]) on the matrix
+//            cores: M = output channel (16 per tile), N = point, K = input
+//            channel, the accumulators starting from the expanded values read
+//            back from LDS.  Lane (g, m) holds points 4m..4m+3 of the group
+//            (N tile j = point 4m + j), so the x loads and the output stores
+//            are 16-byte accesses of 16 consecutive lanes over 256 bytes of
+//            one channel.  x is loaded NCLS chunks ahead.
+// With two buffers, phase 1 of the next chunk writes the buffer phase 2 of
+// the previous chunk has finished reading: one barrier per chunk.
+// MFMA 16x16x4 fp32 lane layout (lane l, m = l & 15, g = l >> 4):
+//   A operand A[m][g], B operand B[g][m], accumulator register i: C[4g+i][m].
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "dtst_internal.h"
+
+namespace dtst {
+namespace {
+
+#include "stream_ops.h"
+
+// A chunk has 16 z rows of at most 32 t: at most 8 groups of 64 points, one
+// per wave.
+constexpr int kBlkWaves = 8;
+
+// GELU(v) = v Phi(v), Phi(v) = (1 + erf(v / sqrt 2)) / 2, with erf from the
+// rational-exponential approximation of Abramowitz & Stegun, Handbook of
+// Mathematical Functions, formula 7.1.26 (absolute error below 1.5e-7 for
+// x >= 0; erf is odd): erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5))))
+// exp(-x^2), t = 1 / (1 + p x).  Branch-free: q = (1 - erf(|v| / sqrt 2)) / 2
+// is Phi(-|v|), and Phi(v) = 1 - q for v >= 0, q otherwise.
+__device__ __forceinline__ float gelu_as(float v) {
+  const float x = fabsf(v) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+  float poly = fmaf(t, 1.061405429f, -1.453152027f);
+  poly = fmaf(t, poly, 1.421413741f);
+  poly = fmaf(t, poly, -0.284496736f);
+  poly = fmaf(t, poly, 0.254829592f);
+  const float e = __builtin_amdgcn_exp2f(-1.44269504088896341f * x * x);
+  const float q = 0.5f * (poly * t) * e;
+  return v * (v >= 0.f ? 1.0f - q : q);
+}
+
+struct BlockArgs {
+  int64_t rows;  // B * N_x * N_y
+  int64_t xy;    // N_x * N_y
+  int ci, co;
+  int groups;    // 64-point groups per chunk: N_t / 4
+  int ostride;   // LDS floats per output channel of a buffer: 16 * N_t
+};
+
+// Float offset of (z row zr, t) in a channel of an LDS value buffer.  With
+// N_t = 32 the 16-byte t chunk index is XORed with bits 1..3 of the z row, so
+// that the 16 z rows one MFMA tile writes (one row per lane) spread over the
+// banks instead of two rows of 128 bytes sharing them.
+__device__ __forceinline__ int yoff(int zr, int t, int nt) {
+  return nt == 32 ? zr * 32 + (t ^ (((zr >> 1) & 7) << 2)) : zr * nt + t;
+}
+
+// z expansion and class unfold of one z tile for one channel's row (the
+// t-expansion operands of the tile's chunks), unfolded t.
+template <int CT, int MT, int NCLS>
+__device__ __forceinline__ void zexp_plain(const float2* urow, const StreamArgs& a, const float4 (&Bz)[NCLS][MT],
+                                           int m, int g, v4f (&W)[NCLS][CT]) {
+  float2 un[NCLS][CT][USlots<MT>::QH][4];
+  load_u<CT, MT, NCLS>(urow, a, m, g, un);
+  float A[NCLS][CT][MT][4];
+  build_a<CT, MT, NCLS>(un, a, m, g, A);
+#pragma unroll
+  for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) W[cl][ct] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int q = 0; q < MT; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) W[cl][ct] = mfma(A[cl][ct][q][i], Bz[cl][q][i], W[cl][ct]);
+  unfold_classes<NCLS, CT>(W);
+}
+
+// t expansion of one class of a z tile (unfolded t) into yb[z row][t].
+template <int CT, int TH>
+__device__ __forceinline__ void texp_plain(const v4f (&W)[CT], const float (&ta)[TH][CT][4], float* yb, int nt,
+                                           int m, int g) {
+  v4f Y[TH];
+#pragma unroll
+  for (int mt = 0; mt < TH; ++mt) Y[mt] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int mt = 0; mt < TH; ++mt) Y[mt] = mfma(ta[mt][ct][i], W[ct][i], Y[mt]);
+#pragma unroll
+  for (int mt = 0; mt < TH; ++mt) {
+    const int t0 = 16 * mt + 4 * g;
+    if (t0 < nt) *reinterpret_cast<v4f*>(yb + yoff(m, t0, nt)) = Y[mt];
+  }
+}
+
+// t folded (CT = 2, N_t = 32 whole): the three-product z expansion of
+// inv_row_tfg for one z tile and the class unfold; Re and Im of the
+// expanded values in separate arrays.
+template <int MT, int NCLS>
+__device__ __forceinline__ void zexp_tfg(const float2* urow, const StreamArgs& a, const float4* lz, int zt, int m,
+                                         int g, int lane, v4f (&Wr)[NCLS], v4f (&Wi)[NCLS]) {
+  float2 u[NCLS][MT / 2][4];
+  load_u_tfg<MT, NCLS>(urow, a, m, g, u);
+#pragma unroll
+  for (int cl = 0; cl < NCLS; ++cl) {
+    v4f k1 = v4f{0.f, 0.f, 0.f, 0.f}, k2 = k1, k3 = k1;
+#pragma unroll
+    for (int qh = 0; qh < MT / 2; ++qh) {
+      const float4 cr = lz[((cl * a.zt + zt) * MT + qh) * 64 + lane];
+      const float4 ci = lz[((cl * a.zt + zt) * MT + qh + MT / 2) * 64 + lane];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = tfg_index<NCLS>(a, m, g, cl, qh, i) >= 0;
+        const float ur = ok ? u[cl][qh][i].x : 0.f, ui = ok ? u[cl][qh][i].y : 0.f;
+        k1 = mfma(ur + ui, cr[i], k1);
+        k2 = mfma(ur, ci[i] - cr[i], k2);
+        k3 = mfma(ui, cr[i] + ci[i], k3);
+      }
+    }
+    Wr[cl] = k1 - k3;
+    Wi[cl] = k1 + k2;
+  }
+  if constexpr (NCLS == 2) {
+    const v4f sr = Wr[0] + Wr[1], dr = Wr[0] - Wr[1];
+    const v4f si = Wi[0] + Wi[1], di = Wi[0] - Wi[1];
+    Wr[0] = sr;
+    Wr[1] = dr;
+    Wi[0] = si;
+    Wi[1] = di;
+  }
+}
+
+// Even / odd k_t t expansion of one class (E + O at t, E - O at t + 16).
+template <int TH>
+__device__ __forceinline__ void texp_tfg(const v4f& Wr, const v4f& Wi, const float (&ta)[TH][2][4], float* yb, int m,
+                                         int g) {
+  v4f E[TH / 2], O[TH / 2];
+#pragma unroll
+  for (int mt = 0; mt < TH / 2; ++mt) {
+    E[mt] = v4f{0.f, 0.f, 0.f, 0.f};
+    O[mt] = v4f{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int mt = 0; mt < TH / 2; ++mt) {
+      v4f& acc = i < 2 ? E[mt] : O[mt];
+      acc = mfma(ta[mt][0][i], Wr[i], acc);
+      acc = mfma(ta[mt][1][i], Wi[i], acc);
+    }
+#pragma unroll
+  for (int mt = 0; mt < TH / 2; ++mt) {
+    const int t0 = 16 * mt + 4 * g;
+    *reinterpret_cast<v4f*>(yb + yoff(m, t0, 32)) = E[mt] + O[mt];
+    *reinterpret_cast<v4f*>(yb + yoff(m, t0 + 16, 32)) = E[mt] - O[mt];
+  }
+}
+
+// KI: K steps of 4 input channels (C_in <= 4 KI); OT: tiles of 16 output
+// channels (C_out <= 16 OT); SPF: float4 of the row's spectrum per thread
+// (C_out K_z K_t <= 2 * 64 kBlkWaves SPF); XD: chunks of x loaded ahead.
+//
+// The loop is software-pipelined: step c runs phase 2 of chunk c - 1 and
+// phase 1 of chunk c (they use different LDS buffers, so the wave's matrix
+// products of one overlap the vector work and the memory traffic of the
+// other), then one barrier.  Steps come in passes of four so that the
+// buffer, the fold class of phase 1 and the x buffer are compile-time indices.
+template <int CT, int TH, int MT, int NCLS, int TF, int KI, int OT, int SPF, int XD>
+__global__ void __launch_bounds__(64 * kBlkWaves)
+inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, const float* __restrict__ wb,
+                    float* __restrict__ y, const float* __restrict__ timg, const float4* __restrict__ zimg,
+                    StreamArgs a, BlockArgs ba) {
+  constexpr int NW = kBlkWaves;
+  // output channels per wave in phase 1 (the class bounds C_in and C_out by 4 KI)
+  constexpr int KC = (4 * KI + NW - 1) / NW;
+  static_assert(!TF || (CT == 2 && TH == 2), "t folding needs two k_t tiles and N_t = 32");
+  static_assert(XD == 1 || XD == 2 || XD == 4, "x one, two or four chunks ahead");
+  // LDS: the z image, the row's spectrum of every output channel, two
+  // buffers of a chunk's expanded values [o][z row][t].
+  extern __shared__ float4 lds[];
+  const int nimg = NCLS * a.zt * MT * 64;
+  const int spec_len = a.kz * a.kt;
+  const int n4 = ba.co * spec_len / 2;  // float4 of the row's spectrum
+  float2* sbuf = reinterpret_cast<float2*>(lds + nimg);
+  float* ybuf = reinterpret_cast<float*>(lds + nimg + n4);
+  const int bufsz = ba.co * ba.ostride;  // floats per buffer
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int m = lane & 15, g = lane >> 4;
+  const int w = tid >> 6;
+  if (blockIdx.x >= ba.rows) return;  // the host never launches more workgroups than rows
+
+  for (int i = tid; i < nimg; i += blockDim.x) lds[i] = zimg[i];
+
+  // A operand of the t expansion (rows t = 16mt + m); with TF only mt < TH/2.
+  float ta[TH][CT][4];
+#pragma unroll
+  for (int mt = 0; mt < TH; ++mt)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        ta[mt][ct][i] = (TF && mt >= TH / 2) ? 0.f : timg[((mt * CT + ct) * 4 + i) * 64 + lane];
+  // A operands of the bypass: w[o = 16ot + m][i = 4s + g], zero outside.
+  float wa[OT][KI];
+#pragma unroll
+  for (int ot = 0; ot < OT; ++ot)
+#pragma unroll
+    for (int s = 0; s < KI; ++s) {
+      const int o = 16 * ot + m, i = 4 * s + g;
+      wa[ot][s] = (o < ba.co && i < ba.ci) ? wb[o * ba.ci + i] : 0.f;
+    }
+
+  const int64_t row_len = int64_t(a.nz) * a.nt;
+  const int nt = a.nt;
+  const int cpr = a.zt * NCLS;  // chunks per row
+
+  // Chunk position: row, z tile, class; chunks of a row run z tile by z tile.
+  struct Cur {
+    int64_t row;
+    int zt, hf;
+  };
+  auto next = [&](Cur c) {
+    if (++c.hf == NCLS) {
+      c.hf = 0;
+      if (++c.zt == a.zt) {
+        c.zt = 0;
+        c.row += gridDim.x;
+      }
+    }
+    return c;
+  };
+
+  // This wave's 64-point group of a chunk: offset of the lane's 4 points
+  // within the (N_z x N_t) row, LDS offset within a channel of the buffer,
+  // and whether the points exist (a wave past the chunk's groups, or a z row
+  // past a ragged last z tile).
+  struct Grp {
+    int64_t off;
+    int loff;
+    bool ok;
+  };
+  auto group = [&](const Cur& c) {
+    Grp q;
+    const int po = w * 64 + 4 * m;
+    const int zr = po / nt, t = po - zr * nt;
+    const int zl = c.zt * 16 + zr;
+    const bool gok = w < ba.groups;
+    q.ok = gok && zl < a.zh;
+    q.off = q.ok ? int64_t(zl + c.hf * a.zh) * nt + t : 0;
+    q.loff = gok ? yoff(zr, t, nt) : 0;
+    return q;
+  };
+
+  // x of this wave's group, XD chunks ahead (unconditional loads: lanes of
+  // missing points read the row start, input channels past C_in read the
+  // last one; both are multiplied by zero weights or not stored).
+  float4 xv[XD][KI];
+  auto load_x = [&](int k, const Cur& c) __attribute__((always_inline)) {
+    const int64_t rr = c.row < ba.rows ? c.row : ba.rows - 1;
+    const int64_t b = rr / ba.xy, rxy = rr - b * ba.xy;
+    const Grp q = group(c);
+#pragma unroll
+    for (int s = 0; s < KI; ++s) {
+      const int i = 4 * s + g < ba.ci ? 4 * s + g : ba.ci - 1;
+      xv[k][s] = *reinterpret_cast<const float4*>(x + ((b * ba.ci + i) * ba.xy + rxy) * row_len + q.off);
+    }
+  };
+  // The spectrum of row r (every output channel) into the LDS buffer: the
+  // loads go out first and the LDS stores follow the caller's other work.
+  auto spec_load = [&](int64_t r, v4f (&sp)[SPF]) __attribute__((always_inline)) {
+    const int64_t rr = r < ba.rows ? r : ba.rows - 1;
+    const int64_t b = rr / ba.xy, rxy = rr - b * ba.xy;
+#pragma unroll
+    for (int k = 0; k < SPF; ++k) {
+      const int e4 = min(tid + 64 * NW * k, n4 - 1);
+      const int o = (2 * e4) / spec_len, j = 2 * e4 - o * spec_len;
+      sp[k] = *reinterpret_cast<const v4f*>(in + ((b * ba.co + o) * ba.xy + rxy) * spec_len + j);
+    }
+  };
+  auto spec_store = [&](const v4f (&sp)[SPF]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < SPF; ++k) {
+      const int e4 = tid + 64 * NW * k;
+      if (e4 < n4) reinterpret_cast<v4f*>(sbuf)[e4] = sp[k];
+    }
+  };
+
+  // z expansions of this wave's channels, kept for the z tile's chunks
+  v4f Wz[KC][NCLS][CT];              // unfolded t
+  v4f Wzr[KC][NCLS], Wzi[KC][NCLS];  // t folded
+
+  // Phase 1 of chunk c into buffer PAR (its class HF is c.hf).
+  auto phase1 = [&](auto parc, auto hfc, const Cur& c) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(parc)::value, HF = decltype(hfc)::value;
+    float* yb = ybuf + PAR * bufsz;
+    if constexpr (TF) {
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int o = w + NW * k;
+        if (o < ba.co) {
+          if (HF == 0) zexp_tfg<MT, NCLS>(sbuf + o * spec_len, a, lds, c.zt, m, g, lane, Wzr[k], Wzi[k]);
+          texp_tfg<TH>(Wzr[k][HF], Wzi[k][HF], ta, yb + o * ba.ostride, m, g);
+        }
+      }
+    } else {
+      if (HF == 0) {
+        float4 Bz[NCLS][MT];
+#pragma unroll
+        for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+          for (int q = 0; q < MT; ++q) Bz[cl][q] = lds[((cl * a.zt + c.zt) * MT + q) * 64 + lane];
+#pragma unroll
+        for (int k = 0; k < KC; ++k) {
+          const int o = w + NW * k;
+          if (o < ba.co) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[k]);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int o = w + NW * k;
+        if (o < ba.co) texp_plain<CT, TH>(Wz[k][HF], ta, yb + o * ba.ostride, nt, m, g);
+      }
+    }
+  };
+
+  // Phase 2 of chunk c from buffer PAR with x buffer XB.
+  auto phase2 = [&](auto parc, auto xbc, const Cur& c) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(parc)::value, XB = decltype(xbc)::value;
+    const float* yb = ybuf + PAR * bufsz;
+    const Grp q = group(c);
+    v4f C[OT][4];
+#pragma unroll
+    for (int ot = 0; ot < OT; ++ot)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = 16 * ot + 4 * g + r;
+        const float4 v = *reinterpret_cast<const float4*>(yb + (o < ba.co ? o : ba.co - 1) * ba.ostride + q.loff);
+        C[ot][0][r] = v.x;
+        C[ot][1][r] = v.y;
+        C[ot][2][r] = v.z;
+        C[ot][3][r] = v.w;
+      }
+#pragma unroll
+    for (int s = 0; s < KI; ++s) {
+      const bool iok = 4 * s + g < ba.ci;
+      const float4 xs = xv[XB][s];
+      const float b0 = iok ? xs.x : 0.f, b1 = iok ? xs.y : 0.f, b2 = iok ? xs.z : 0.f, b3 = iok ? xs.w : 0.f;
+#pragma unroll
+      for (int ot = 0; ot < OT; ++ot) {
+        C[ot][0] = mfma(wa[ot][s], b0, C[ot][0]);
+        C[ot][1] = mfma(wa[ot][s], b1, C[ot][1]);
+        C[ot][2] = mfma(wa[ot][s], b2, C[ot][2]);
+        C[ot][3] = mfma(wa[ot][s], b3, C[ot][3]);
+      }
+    }
+    const int64_t b = c.row / ba.xy, rxy = c.row - b * ba.xy;
+#pragma unroll
+    for (int ot = 0; ot < OT; ++ot)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = 16 * ot + 4 * g + r;
+        if (q.ok && o < ba.co) {
+          float* dst = y + ((b * ba.co + o) * ba.xy + rxy) * row_len + q.off;
+          // ordinary (cached) stores: measured faster here than streaming ones
+          *reinterpret_cast<v4f*>(dst) =
+              v4f{gelu_as(C[ot][0][r]), gelu_as(C[ot][1][r]), gelu_as(C[ot][2][r]), gelu_as(C[ot][3][r])};
+        }
+      }
+  };
+
+  // One pipeline step: phase 2 of chunk c2 (the previous one, when it
+  // exists), the x of the chunk XD - 1 further on into phase 2's x buffer,
+  // phase 1 of chunk c1 (when it exists), one barrier.  The x loads are
+  // unconditional (past the end they re-read the last row), so that no
+  // register holding a load in flight is merged with another value.  The
+  // step whose phase 1 is a row's last chunk then moves the next row's
+  // spectrum into LDS (the row's last reader of it is the phase 1 of its last
+  // z tile's first chunk).
+  Cur c1 = Cur{static_cast<int64_t>(blockIdx.x), 0, 0};  // phase 1
+  Cur c2 = c1;                                             // phase 2 (valid from step 1 on)
+  Cur cx = c1;                                             // next x to load
+  auto step = [&](auto sc, bool has2) __attribute__((always_inline)) {
+    constexpr int S4 = decltype(sc)::value;     // step index mod 4
+    constexpr int PAR = S4 & 1;                 // buffer of phase 1; phase 2 reads 1 - PAR
+    constexpr int HF = NCLS == 2 ? PAR : 0;     // chunks alternate classes when z folds
+    constexpr int XB = (S4 + 3) % XD;           // x buffer of phase 2's chunk (step - 1)
+    const bool has1 = c1.row < ba.rows;
+    auto body = [&]() __attribute__((always_inline)) {
+      if (has2) phase2(std::integral_constant<int, 1 - PAR>{}, std::integral_constant<int, XB>{}, c2);
+      load_x(XB, cx);
+      cx = next(cx);
+      if (has1) phase1(std::integral_constant<int, PAR>{}, std::integral_constant<int, HF>{}, c1);
+    };
+    // (c1.hf == HF by construction: with z folded, only odd steps end a row)
+    if (has1 && HF == NCLS - 1 && c1.zt == a.zt - 1) {
+      // the spectrum loads go out before the step's work, the LDS stores after it
+      v4f sp[SPF];
+      spec_load(c1.row + gridDim.x, sp);
+      body();
+      if constexpr (NCLS == 1) __syncthreads();  // this phase 1 read the spectrum buffer
+      spec_store(sp);
+    } else {
+      body();
+    }
+    __syncthreads();
+    c2 = c1;
+    c1 = next(c1);
+  };
+
+  // prologue: the first row's spectrum, the x of the first XD - 1 chunks
+  {
+    v4f sp[SPF];
+    spec_load(c1.row, sp);
+    spec_store(sp);
+  }
+#pragma unroll
+  for (int k = 0; k < XD - 1; ++k) {
+    load_x(k, cx);
+    cx = next(cx);
+  }
+  __syncthreads();
+  step(std::integral_constant<int, 0>{}, false);
+  // every pass runs four steps; the only exit is at the end of a pass
+  do {
+    step(std::integral_constant<int, 1>{}, c2.row < ba.rows);
+    step(std::integral_constant<int, 2>{}, c2.row < ba.rows);
+    step(std::integral_constant<int, 3>{}, c2.row < ba.rows);
+    step(std::integral_constant<int, 0>{}, c2.row < ba.rows);
+  } while (c2.row < ba.rows);
+}
+
+typedef void (*blk_fn)(const float2*, const float*, const float*, float*, const float*, const float4*, StreamArgs,
+                       BlockArgs);
+
+template <int CT, int TH, int MT, int NCLS, int TF>
+blk_fn pick_kio(int kio) {
+  if (kio == 0) return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 4, 1, 4, 2>;
+  if (kio == 1) return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 5, 2, 5, 1>;
+  return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 8, 2, 8, 1>;
+}
+
+// float4 of a row's spectrum per thread for each (KI, OT) class.
+constexpr int kSpf[3] = {4, 5, 8};
+
+template <int CT, int TH, int TF>
+blk_fn pick_mn(int mt, int ncls, int kio) {
+  if (mt == 2) return ncls == 2 ? pick_kio<CT, TH, 2, 2, TF>(kio) : pick_kio<CT, TH, 2, 1, TF>(kio);
+  return ncls == 2 ? pick_kio<CT, TH, 4, 2, TF>(kio) : pick_kio<CT, TH, 4, 1, TF>(kio);
+}
+
+// (KI, OT) class of a channel count: 0 up to 16, 1 up to 20, 2 up to 32.
+int kio_of(int64_t ci, int64_t co) {
+  const int64_t c = ci > co ? ci : co;
+  return c <= 16 ? 0 : (c <= 20 ? 1 : 2);
+}
+
+blk_fn pick_blk(const StreamCfg& c, int kio) {
+  if (c.tf) return pick_mn<2, 2, 1>(c.mt, c.ncls, kio);
+  if (c.ct == 1) return c.th == 1 ? pick_mn<1, 1, 0>(c.mt, c.ncls, kio) : pick_mn<1, 2, 0>(c.mt, c.ncls, kio);
+  return c.th == 1 ? pick_mn<2, 1, 0>(c.mt, c.ncls, kio) : pick_mn<2, 2, 0>(c.mt, c.ncls, kio);
+}
+
+}  // namespace
+
+size_t block_zt_lds_bytes(const StreamCfg& c, int64_t co) {
+  return size_t(c.ncls) * c.zt * c.mt * 64 * 16 + size_t(co) * c.kz * c.kt * 8 +
+         2 * size_t(co) * 16 * c.nt * sizeof(float);
+}
+
+bool block_zt_supported(const StreamCfg& c, int64_t ci, int64_t co) {
+  if (!(c.vec && c.th <= 2 && c.ncls <= 2 && (c.mt == 2 || c.mt == 4) && (!c.tf || (c.ct == 2 && c.th == 2)) &&
+        ci <= 32 && co <= 32 && (c.kz * c.kt) % 2 == 0))
+    return false;
+  const int64_t n4 = co * c.kz * c.kt / 2;
+  return n4 <= int64_t(64) * kBlkWaves * kSpf[kio_of(ci, co)] && block_zt_lds_bytes(c, co) <= 160 * 1024;
+}
+
+int prepare_block_zt(const StreamCfg& c, int64_t ci, int64_t co, int* grid) {
+  const void* fn = reinterpret_cast<const void*>(pick_blk(c, kio_of(ci, co)));
+  const size_t lds = block_zt_lds_bytes(c, co);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  int dev = 0, cus = 0, per_cu = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64 * kBlkWaves, lds)) != hipSuccess) return e;
+  if (per_cu <= 0) return hipErrorInvalidConfiguration;
+  *grid = cus * per_cu;
+  return hipSuccess;
+}
+
+int launch_inv_zt_block(const StreamCfg& c, int grid_resident, const void* in, const float* x, const float* w,
+                        float* y, int64_t batch, int64_t nxy, int64_t ci, int64_t co, const float* timg,
+                        const float* zimg, void* stream) {
+  const int64_t rows = batch * nxy;
+  if (rows <= 0) return hipSuccess;
+  if (!block_zt_supported(c, ci, co) || grid_resident <= 0) return hipErrorInvalidConfiguration;
+  StreamArgs a;
+  a.rows = rows;
+  a.nt = c.nt;
+  a.nz = c.nz;
+  a.kt = c.kt;
+  a.kz = c.kz;
+  a.zh = c.zh;
+  a.zt = c.zt;
+  a.vec = c.vec;
+  a.full = 0;
+  BlockArgs ba;
+  ba.rows = rows;
+  ba.xy = nxy;
+  ba.ci = static_cast<int>(ci);
+  ba.co = static_cast<int>(co);
+  ba.groups = c.nt / 4;
+  ba.ostride = 16 * c.nt;
+  if (ba.groups > kBlkWaves) return hipErrorInvalidConfiguration;
+  const int64_t grid = rows < grid_resident ? rows : grid_resident;
+  hipLaunchKernelGGL(pick_blk(c, kio_of(ci, co)), dim3(static_cast<unsigned>(grid)), dim3(64 * kBlkWaves),
+                     block_zt_lds_bytes(c, co), static_cast<hipStream_t>(stream), static_cast<const float2*>(in), x,
+                     w, y, timg, reinterpret_cast<const float4*>(zimg), a, ba);
+  return hipGetLastError();
+}
+
+}  // namespace dtst

@@ -84,7 +84,7 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
     *err = "need batch >= 0, c_in >= 1, c_out >= 1";
     return DTST_ERR_INVALID_ARG;
   }
-  if ((flags & ~uint32_t(DTST_PLAN_SPLIT_SCHEDULE)) != 0) {
+  if ((flags & ~uint32_t(DTST_PLAN_SPLIT_SCHEDULE | DTST_PLAN_UNFUSED_BLOCK)) != 0) {
     *err = "unknown plan flag";
     return DTST_ERR_INVALID_ARG;
   }
@@ -236,6 +236,30 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   dv.w1_bytes = sc.fuse_y ? 0 : w1;
   dv.ws_bytes = dv.w1_bytes + w2;
 
+  // ---- fused inverse z + t expansion and block epilogue ----
+  // The same z + t expansion as the split inverse, with z folded into at
+  // most two classes (a chunk of the kernel is one z tile of every class),
+  // fed by the separate y expansion: dtst_inverse_block's workspace holds W1
+  // then W2 even where the layer's own calls fuse y.  The plan flag
+  // DTST_PLAN_UNFUSED_BLOCK keeps the inverse and the epilogue separate.
+  {
+    StreamCfg sb = sc;
+    sb.ncls = fold ? 2 : 1;
+    sb.kcp = static_cast<int>(round_up(ceil_div(sc.kz, sb.ncls), 16));
+    sb.mt = sb.kcp / 8;
+    sb.zh = sb.nz / sb.ncls;
+    sb.zt = static_cast<int>(ceil_div(sb.zh, 16));
+    sb.lds_bytes = size_t(sb.ncls) * sb.zt * sb.mt * 64 * 16;
+    sb.fuse_y = 0;
+    dv.sb = sb;
+    dv.blk = ((flags & DTST_PLAN_UNFUSED_BLOCK) == 0 && sb.kcp <= 32 &&
+              block_zt_supported(sb, d->c_in, d->c_out))
+                 ? 1
+                 : 0;
+    dv.blk_w1_bytes = dv.blk ? w1 : dv.w1_bytes;
+    dv.blk_ws_bytes = dv.blk ? w1 + w2 : dv.ws_bytes;
+  }
+
 
   // ---- image offsets (floats, 256-byte aligned) ----
   Images& im = dv.img;
@@ -258,6 +282,8 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   im.x_fwd = take(axis_img(dv.ax_f));
   im.y_inv = take(axis_img(dv.ay_i));
   im.x_inv = take(axis_img(dv.ax_i));
+  im.z_blk = take(size_t(dv.sb.ncls) * dv.sb.zt * dv.sb.mt * 64 * 4);
+  im.t_blk = take(t_img);
   im.total = off;
 
   *out = dv;
@@ -467,6 +493,12 @@ void build_images(const Derived& dv, std::vector<float>* blob) {
   axis_image(dv, dv.ax_f, 0, false, b + dv.img.x_fwd);
   axis_image(dv, dv.ay_i, 1, true, b + dv.img.y_inv);
   axis_image(dv, dv.ax_i, 0, true, b + dv.img.x_inv);
+  // the fused inverse + block epilogue's z and t images: those of the
+  // inverse for its own z configuration
+  Derived db = dv;
+  db.sc = dv.sb;
+  z_inverse_image(db, b + dv.img.z_blk);
+  t_inverse_image(db, true, b + dv.img.t_blk);
 }
 
 void plain_basis(const dtst_desc& d, int dim, int kind, float* out) {

@@ -91,8 +91,11 @@ def test_workspace_bytes():
 
 def test_unknown_plan_flag_rejected():
     n = ctypes.c_size_t(0)
-    st = D.lib.dtst_desc_workspace_bytes_ex(ctypes.byref(desc()), 2, ctypes.byref(n))
+    st = D.lib.dtst_desc_workspace_bytes_ex(ctypes.byref(desc()), 4, ctypes.byref(n))
     assert st == 1 and b"flag" in D.lib.dtst_last_error()
+    # the two documented flags, alone and together, are accepted
+    for flags in (D.PLAN_SPLIT_SCHEDULE, D.PLAN_UNFUSED_BLOCK, D.PLAN_SPLIT_SCHEDULE | D.PLAN_UNFUSED_BLOCK):
+        assert D.lib.dtst_desc_workspace_bytes_ex(ctypes.byref(desc()), flags, ctypes.byref(n)) == 0
     h = ctypes.c_void_p()
     st = D.lib.dtst_plan_ex(ctypes.byref(desc()), 1 << 31, ctypes.byref(h))
     assert st == 1 and h.value is None

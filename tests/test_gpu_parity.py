@@ -389,29 +389,49 @@ def test_block_epilogue_rejects_overlap():
     plan.close()
 
 
-# (n_global, n_local, offset, kmax, kt, B, C_in, C_out): folded and sharded z,
-# many input channels, both k_t column layouts, scalar t.
+# (n_global, n_local, offset, kmax, kt, B, C_in, C_out), and whether the
+# fused z + t expansion and epilogue kernel covers the shape: folded and
+# sharded z, many input channels, both k_t column layouts, scalar t, the
+# FNO's width d_v = 20; for the fused kernel every instance form: one and two
+# k_t tiles (t folded or not), one and two t tiles, 16 and 32 z slots per
+# class, one and two z classes, each channel class (<= 16, <= 20, <= 32),
+# ragged z tiles and t extents that are not a multiple of 16.
 INVERSE_BLOCK_CASES = {
-    "fold": ((8, 6, 32, 32), (8, 6, 32, 32), (0, 0, 0, 0), (2, 2, 8), 5, 2, 3, 6),
-    "z_shard": ((8, 6, 64, 16), (8, 6, 32, 16), (0, 0, 16, 0), (2, 2, 4), 4, 1, 20, 16),
-    "many_inputs": ((4, 4, 32, 32), (4, 4, 32, 32), (0, 0, 0, 0), (1, 1, 4), 3, 1, 64, 16),
-    "kt12": ((4, 4, 16, 32), (4, 4, 16, 32), (0, 0, 0, 0), (1, 2, 4), 12, 1, 2, 3),
-    "nt21": ((4, 6, 8, 21), (4, 6, 8, 21), (0, 0, 0, 0), (2, 2, 2), 6, 2, 2, 2),
-    # the FNO's width d_v = 20 (two chunks of 12 output channels)
-    "dv20": ((8, 6, 32, 32), (8, 6, 32, 32), (0, 0, 0, 0), (2, 2, 8), 5, 1, 20, 20),
+    "fold": (((8, 6, 32, 32), (8, 6, 32, 32), (0, 0, 0, 0), (2, 2, 8), 5, 2, 3, 6), True),
+    "z_shard": (((8, 6, 64, 16), (8, 6, 32, 16), (0, 0, 16, 0), (2, 2, 4), 4, 1, 20, 16), True),
+    "many_inputs": (((4, 4, 32, 32), (4, 4, 32, 32), (0, 0, 0, 0), (1, 1, 4), 3, 1, 64, 16), False),
+    "kt12": (((4, 4, 16, 32), (4, 4, 16, 32), (0, 0, 0, 0), (1, 2, 4), 12, 1, 2, 3), True),
+    "nt21": (((4, 6, 8, 21), (4, 6, 8, 21), (0, 0, 0, 0), (2, 2, 2), 6, 2, 2, 2), False),
+    "dv20": (((8, 6, 32, 32), (8, 6, 32, 32), (0, 0, 0, 0), (2, 2, 8), 5, 1, 20, 20), True),
+    "dv20_tfold": (((8, 8, 32, 32), (8, 8, 32, 32), (0, 0, 0, 0), (4, 4, 8), 16, 1, 20, 20), True),
+    "mt4_fold": (((4, 4, 64, 16), (4, 4, 64, 16), (0, 0, 0, 0), (1, 2, 24), 3, 1, 5, 7), True),
+    "mt4_z_shard": (((4, 4, 64, 16), (4, 4, 48, 16), (0, 0, 8, 0), (1, 2, 12), 3, 2, 4, 3), True),
+    "ct2_th1": (((4, 6, 16, 16), (4, 6, 16, 16), (0, 0, 0, 0), (2, 2, 4), 9, 1, 3, 5), True),
+    "ct2_t_shard": (((4, 4, 16, 64), (4, 4, 16, 32), (0, 0, 0, 32), (1, 1, 4), 12, 1, 6, 4), True),
+    "c32": (((4, 4, 32, 16), (4, 4, 32, 16), (0, 0, 0, 0), (1, 1, 4), 3, 1, 32, 24), True),
+    "ragged_z": (((4, 4, 40, 8), (4, 4, 40, 8), (0, 0, 0, 0), (1, 1, 6), 2, 1, 4, 4), True),
+    "nt12_ragged": (((4, 4, 24, 12), (4, 4, 24, 12), (0, 0, 0, 0), (2, 2, 5), 4, 1, 3, 2), True),
+    "nt20": (((4, 6, 32, 20), (4, 6, 32, 20), (0, 0, 0, 0), (2, 2, 6), 7, 1, 5, 5), True),
+    "batch3": (((4, 6, 32, 32), (2, 6, 32, 32), (2, 0, 0, 0), (2, 2, 8), 6, 3, 5, 9), True),
 }
 
 
+@pytest.mark.parametrize("unfused", [False, True], ids=["default", "unfused"])
 @pytest.mark.parametrize("name", list(INVERSE_BLOCK_CASES))
-def test_inverse_block(name):
+def test_inverse_block(name, unfused):
     """y = GELU(W x + inverse(yhat)) in one call against the oracle's
-    inverse followed by its block epilogue."""
+    inverse followed by its block epilogue: the fused z + t expansion and
+    epilogue kernel where the plan covers the shape, and the two launches of
+    a plan made with PLAN_UNFUSED_BLOCK."""
     torch = torch_gpu()
     import paper_2607_14394_amd as D
-    g = geometry(*INVERSE_BLOCK_CASES[name])
-    say(f"[inverse block {name}] n_global={g.n_global} n_local={g.n_local} kmax={g.kmax} kt={g.kt} "
-        f"B={g.batch} Cin={g.c_in} Cout={g.c_out}")
-    plan = D.Plan(desc_of(g))
+    spec, fusable = INVERSE_BLOCK_CASES[name]
+    g = geometry(*spec)
+    say(f"[inverse block {name} unfused={unfused}] n_global={g.n_global} n_local={g.n_local} kmax={g.kmax} "
+        f"kt={g.kt} B={g.batch} Cin={g.c_in} Cout={g.c_out}")
+    plan = D.Plan(desc_of(g), flags=D.PLAN_UNFUSED_BLOCK if unfused else 0)
+    assert plan.block_fused == (fusable and not unfused)
+    assert plan.block_ws_bytes >= plan.ws_bytes
     yh = rand_cplx((g.batch, g.c_out) + g.K, 140)
     x = rand_real((g.batch, g.c_in) + g.n_local, 141)
     wb = (rand_real((g.c_out, g.c_in), 142) / np.sqrt(g.c_in)).astype(np.float32)
@@ -420,6 +440,27 @@ def test_inverse_block(name):
     torch.cuda.synchronize()
     check(np_of(Y.t), O.block_epilogue(x, wb, O.inverse(yh, g)), "inverse + block epilogue")
     assert Y.guards_intact()
+    plan.close()
+
+
+def test_inverse_block_workspace_too_small():
+    """A workspace below dtst_plan_block_info's size is rejected before any
+    launch (the fused kernel also needs the y-expanded intermediate)."""
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    g = geometry(*INVERSE_BLOCK_CASES["fold"][0])
+    plan = D.Plan(desc_of(g))
+    assert plan.block_fused == 1 and plan.block_ws_bytes > plan.ws_bytes
+    yh = torch.zeros(plan.spectral_shape(g.c_out), dtype=torch.complex64, device="cuda")
+    x = torch.zeros(plan.spatial_shape(g.c_in), dtype=torch.float32, device="cuda")
+    wb = torch.zeros((g.c_out, g.c_in), dtype=torch.float32, device="cuda")
+    y = torch.full(plan.spatial_shape(g.c_out), 3.0, dtype=torch.float32, device="cuda")
+    small = torch.empty(plan.block_ws_bytes - 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(D.DtstError) as e:
+        D.dtst_inverse_block(plan.handle, yh, x, wb, y, small)
+    assert e.value.status == 1
+    torch.cuda.synchronize()
+    assert bool((y == 3.0).all().item())
     plan.close()
 
 
