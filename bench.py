@@ -117,8 +117,8 @@ def work(g, channels, m_count=None, acc_share=0.0):
     M = Kx * Ky * Kz * Kt
     rows = B * C * Nx * Ny
     sf = stage_flops(g, C)
-    fy = 0.5 if _folded(g, 1) else 1.0
-    fx = 0.5 if _folded(g, 0) else 1.0
+    fy = 1.0 / _axis_classes(g, 1)
+    fx = 1.0 / _axis_classes(g, 0)
     w = {}
     # the t-folded kernels take the complex z products in three real products instead of four
     z_prod = 0.75 if _t_classes(g) == 2 else 1.0
@@ -181,6 +181,17 @@ CONTRACTION_ROLES = ("stream_fwd_tzy", "stream_fwd_tz", "axis_fwd_y", "axis_fwd_
 def _folded(g, dim):
     """The library folds a dimension whose whole even extent is local."""
     return g["n_local"][dim] == g["n_global"][dim] and g["n_global"][dim] % 2 == 0
+
+
+def _axis_classes(g, dim):
+    """Mode classes of the separate x / y contractions: 4 when the whole
+    extent is local with N % 4 == 0 and the K = 2 k_max retained modes fill
+    whole 16-mode tiles per class (K % 64 == 0, K <= 128), 2 when the
+    dimension only folds in halves, else 1; their MFMA work divides by it."""
+    if not _folded(g, dim):
+        return 1
+    K = 2 * g["kmax"][dim]
+    return 4 if g["n_global"][dim] % 4 == 0 and K % 64 == 0 and K <= 128 else 2
 
 
 def _t_classes(g):

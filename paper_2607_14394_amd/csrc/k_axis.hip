@@ -22,6 +22,16 @@
 // n + N/2.  Either way the MFMA work halves.  The parity of a retained mode
 // equals the parity of its position p, because N is even.
 //
+// Four-class folding (FOLD 3 forward, FOLD 4 inverse): with N % 4 == 0 and
+// an even k_max, k mod 4 equals the position p mod 4 of a retained mode, and
+// exp(-2 pi i k (n + q N/4) / N) = (-i)^{k q} exp(-2 pi i k n / N).  Class c
+// = p mod 4 then takes a quarter-length contraction over n < N/4: the
+// forward feeds class c with S_c[n] = sum_q (-i)^{c q} in[n + q N/4] (from
+// the sums and differences of the rows n, n + N/2 and n + N/4, n + 3N/4),
+// and the inverse forms the class sums E_c over n < N/4 and writes
+// sum_c i^{c q} E_c at n + q N/4.  The MFMA work is a quarter of the direct
+// contraction's; used when every class fills whole 16-mode tiles.
+//
 // Work split: a 256-thread workgroup owns one b, 64*NT consecutive n (16*NT
 // per wave) and a block of up to KT 16-row tiles of k.  Every lane streams
 // in[b][j][n] for its n with 8-byte loads (16 lanes cover 128 contiguous
@@ -56,8 +66,9 @@ __device__ __forceinline__ float swap_adjacent(float v) {
 struct AxisArgs {
   int64_t nb, total;
   int J, KO, NN, JQ, ktiles, kth, kblocks, nblocks, acc;
-  int jh;  // FOLD 1: J/2 (contracted half); FOLD 2: J/2 (modes per class)
-  int oh;  // FOLD 2: KO/2 (output half)
+  int jh;  // FOLD 1: J/2 (contracted half); FOLD 2: J/2 (modes per class);
+           // FOLD 3: J/4 (contracted quarter); FOLD 4: J/4 (modes per class)
+  int oh;  // FOLD 2: KO/2 (output half); FOLD 4: KO/4 (output quarter)
 };
 
 // Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
@@ -107,8 +118,10 @@ template <int KT, int NT, int FOLD, int ACC>
 __global__ void __launch_bounds__(256)
 axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float4* __restrict__ img,
             AxisArgs a) {
-  constexpr int NC = FOLD == 2 ? 2 : 1;  // input classes loaded per K step
-  constexpr int NS = FOLD == 1 ? 2 : 1;  // input rows combined per K index
+  constexpr int NC = FOLD == 2 ? 2 : 1;                        // input classes loaded per K step
+  constexpr int NS = FOLD == 1 ? 2 : (FOLD == 3 ? 4 : 1);      // input rows combined per K index
+  static_assert(FOLD != 3 || KT == 4, "four-class tiles: one k tile per class");
+  static_assert(FOLD != 4, "four-class inverse runs in axis_expand_kernel");
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
   const int wave = threadIdx.x >> 6;
@@ -130,6 +143,7 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
 
     // K index jj = 16q + 4g + i.  FOLD 0: row jj.  FOLD 1: rows jj and
     // jj + J/2.  FOLD 2: rows 2jj (even modes) and 2jj + 1 (odd modes).
+    // FOLD 3: rows jj + s J/4, s = 0..3.
     auto load = [&](int q, float2 (&dst)[NC][NS][NT][4], bool (&ok)[NT][4]) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
@@ -144,7 +158,7 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
           for (int c = 0; c < NC; ++c)
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-              const int row = FOLD == 0 ? jj : (FOLD == 1 ? jj + s * a.jh : 2 * jj + c);
+              const int row = FOLD == 0 ? jj : (FOLD == 2 ? 2 * jj + c : jj + s * a.jh);
               int64_t idx = v_ok ? int64_t(row) * a.NN + n : spare;
               opaque(idx);
               dst[c][s][nt][i] = inb[idx];
@@ -174,12 +188,15 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
     // Accumulating launches (forward x, the shard sum): fetch the values the
     // output holds now right behind the first input loads, so that read is not
     // a second round trip after the MFMAs.  Output row of tile kt, row i:
-    // FOLD 0: 16kt + 4g + i; FOLD 1: mode 2s + c of class c = (kt >= kth).
+    // FOLD 0: 16kt + 4g + i; FOLD 1: mode 2s + c of class c = (kt >= kth),
+    // s = 16 (kt - c kth) + 4g + i; FOLD 3: mode 4s + c of class c = kt mod 4,
+    // s = 16 (kt / 4) + 4g + i.
     auto out_row = [&](int kt, int i) {
       if (FOLD == 1) {
         const int c = kt >= a.kth ? 1 : 0;
         return 2 * (16 * (kt - c * a.kth) + 4 * g + i) + c;
       }
+      if (FOLD == 3) return 4 * (16 * (kt >> 2) + 4 * g + i) + (kt & 3);
       return 16 * kt + 4 * g + i;
     };
     float4 pre[ACC ? KT : 1][ACC ? NT : 1][2];
@@ -221,7 +238,44 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
       }
     };
     load_basis(0);
-    for (int q = 0; q < a.JQ; ++q) {
+    for (int q = 0; q < a.JQ && FOLD == 3; ++q) {
+      // class inputs S_c of the four rows n + s J/4 (zero outside the tile):
+      // e = x0 + x2, f = x1 + x3, u = x0 - x2, d = x1 - x3;
+      // S_0 = e + f, S_2 = e - f, S_1 = u - i d, S_3 = u + i d
+      float2 sc[4][NT][4];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float2 x0 = vn[0][0][nt][i], x1 = vn[0][1 % NS][nt][i];
+          const float2 x2 = vn[0][2 % NS][nt][i], x3 = vn[0][3 % NS][nt][i];
+          const float er = x0.x + x2.x, ei = x0.y + x2.y, fr = x1.x + x3.x, fi = x1.y + x3.y;
+          const float ur = x0.x - x2.x, ui = x0.y - x2.y, dr = x1.x - x3.x, di = x1.y - x3.y;
+          const bool o = okn[nt][i];
+          sc[0][nt][i] = o ? make_float2(er + fr, ei + fi) : make_float2(0.f, 0.f);
+          sc[1][nt][i] = o ? make_float2(ur + di, ui - dr) : make_float2(0.f, 0.f);
+          sc[2][nt][i] = o ? make_float2(er - fr, ei - fi) : make_float2(0.f, 0.f);
+          sc[3][nt][i] = o ? make_float2(ur - di, ui + dr) : make_float2(0.f, 0.f);
+        }
+      if (q + 1 < a.JQ) load(q + 1, vn, okn);
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) {  // tile kk holds class kk
+        const float4 br = bre[kk][0], bi = bim[kk][0];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float r = br[i], im = bi[i], rpi = br[i] + bi[i];
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const float2 x = sc[kk & 3][nt][i];
+            acc1[0][kk][nt] = mfma(rpi, x.x, acc1[0][kk][nt]);
+            acc2[0][kk][nt] = mfma(r, x.y - x.x, acc2[0][kk][nt]);
+            acc3[0][kk][nt] = mfma(im, x.x + x.y, acc3[0][kk][nt]);
+          }
+        }
+      }
+      if (q + 1 < a.JQ) load_basis(q + 1);
+    }
+    for (int q = 0; q < a.JQ && FOLD != 3; ++q) {
       // B operands: V[c or fold class][nt][i] as (Xr, Xi - Xr, Xr + Xi)
       constexpr int NV = FOLD == 0 ? 1 : 2;
       float vr[NV][NT][4], vd[NV][NT][4], vs[NV][NT][4];
@@ -301,6 +355,18 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
           const int k0 = 16 * kt + 4 * g;
           store_tile(re, im, n, nok, ACC, [&](int i) { return ob + int64_t(k0 + i) * a.NN; },
                      [&](int i) { return k0 + i < a.KO; }, ACC ? pre[ACC ? kk : 0][ACC ? nt : 0] : nullptr);
+        } else if (FOLD == 3) {
+          // tile kt holds class c = kt mod 4, slots s = 16 (kt / 4) + 4g + i, mode p = 4s + c
+          float re[4], im[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            re[i] = re_of(0, i);
+            im[i] = im_of(0, i);
+          }
+          const int c = kt & 3;
+          const int s0 = 16 * (kt >> 2) + 4 * g;
+          store_tile(re, im, n, nok, ACC, [&](int i) { return ob + int64_t(4 * (s0 + i) + c) * a.NN; },
+                     [&](int i) { return 4 * (s0 + i) + c < a.KO; }, ACC ? pre[ACC ? kk : 0][ACC ? nt : 0] : nullptr);
         } else if (FOLD == 1) {
           // tile kt holds class c = kt >= kth, slots s = 16 (kt - c kth) + 4g + i, mode p = 2s + c
           float re[4], im[4];
@@ -336,15 +402,15 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
   }
 }
 
-// Folded inverse expansion (FOLD 2) whose whole contraction fits in a few K
-// steps (JQ <= 2: at most 32 retained modes per parity class).  Such a
-// launch writes four times what it reads (E + O and E - O over N/2 rows from
-// K/2 modes of each class), so each workgroup loads its input columns once,
-// keeps them in registers and loops over every block of KT output tiles: the
-// stores of one block overlap the products of the next, and no other
-// workgroup re-reads the input.  KT output tiles per block, NT 16-column
-// tiles per wave.
-template <int KT, int NT, int JQ>
+// Folded inverse expansion (FOLD 2 with NCL = 2 classes, FOLD 4 with NCL =
+// 4) whose whole contraction fits in a few K steps (JQ <= 2: at most 32
+// retained modes per class).  Such a launch writes several times what it
+// reads (N rows from K modes), so each workgroup loads its input columns
+// once, keeps them in registers and loops over every block of KT output
+// tiles: the stores of one block overlap the products of the next, and no
+// other workgroup re-reads the input.  KT output tiles per block (one 16-row
+// tile of the N/NCL rows of a class sum), NT 16-column tiles per wave.
+template <int KT, int NT, int JQ, int NCL>
 __global__ void __launch_bounds__(256)
 axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float4* __restrict__ img,
                    AxisArgs a) {
@@ -363,8 +429,8 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
     float2* ob = out + b * int64_t(a.KO) * a.NN;
     const int64_t spare = m < int64_t(a.J) * a.NN ? m : 0;
 
-    // K index jj = 16q + 4g + i: rows 2jj (even modes, class 0) and 2jj + 1 (odd modes, class 1)
-    float2 x[JQ][2][NT][4];
+    // K index jj = 16q + 4g + i: row NCL jj + c (mode of class c)
+    float2 x[JQ][NCL][NT][4];
 #pragma unroll
     for (int q = 0; q < JQ; ++q)
 #pragma unroll
@@ -375,8 +441,8 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
           const int n = nw + 16 * nt + m;
           const bool ok = jj < a.jh && n < a.NN;
 #pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            int64_t idx = ok ? int64_t(2 * jj + c) * a.NN + n : spare;
+          for (int c = 0; c < NCL; ++c) {
+            int64_t idx = ok ? int64_t(NCL * jj + c) * a.NN + n : spare;
             opaque(idx);
             const float2 v = inb[idx];
             x[q][c][nt][i] = ok ? v : make_float2(0.f, 0.f);
@@ -384,9 +450,9 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
         }
 
     for (int kb = 0; kb < a.kblocks; ++kb) {
-      v4f acc1[2][KT][NT], acc2[2][KT][NT], acc3[2][KT][NT];
+      v4f acc1[NCL][KT][NT], acc2[NCL][KT][NT], acc3[NCL][KT][NT];
 #pragma unroll
-      for (int e = 0; e < 2; ++e)
+      for (int e = 0; e < NCL; ++e)
 #pragma unroll
         for (int kk = 0; kk < KT; ++kk)
 #pragma unroll
@@ -397,14 +463,14 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
           }
 #pragma unroll
       for (int q = 0; q < JQ; ++q) {
-        float4 bre[KT][2], bim[KT][2];
+        float4 bre[KT][NCL], bim[KT][NCL];
 #pragma unroll
         for (int kk = 0; kk < KT; ++kk) {
           const int kt = min(kb * KT + kk, a.ktiles - 1);
 #pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            // image entry (((kt * JQ + q) * 2 + class) * 2 + part) * 64 + lane
-            const float4* ip = img + ((int64_t(kt) * a.JQ + q) * 2 + e) * 2 * 64 + lane;
+          for (int e = 0; e < NCL; ++e) {
+            // image entry (((kt * JQ + q) * NCL + class) * 2 + part) * 64 + lane
+            const float4* ip = img + ((int64_t(kt) * a.JQ + q) * NCL + e) * 2 * 64 + lane;
             bre[kk][e] = ip[0];
             bim[kk][e] = ip[64];
           }
@@ -412,7 +478,7 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
 #pragma unroll
         for (int kk = 0; kk < KT; ++kk)
 #pragma unroll
-          for (int e = 0; e < 2; ++e)
+          for (int e = 0; e < NCL; ++e)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const float r = bre[kk][e][i], im = bim[kk][e][i], rpi = r + im;
@@ -425,7 +491,10 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
               }
             }
       }
-      // rows y = 16kt + 4g + i < KO/2: E + O at y, E - O at y + KO/2
+      // rows y = 16kt + 4g + i < KO/NCL of the class sums E_c (Re = k1 - k3,
+      // Im = k1 + k2).  NCL 2: E_0 + E_1 at y, E_0 - E_1 at y + KO/2.  NCL 4:
+      // with P = E_0 + E_2, Q = E_0 - E_2, R = E_1 + E_3, T = E_1 - E_3, the
+      // rows y + h KO/4 get P + R, Q + i T, P - R, Q - i T (h = 0..3).
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk) {
         const int kt = kb * KT + kk;
@@ -435,17 +504,30 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
         for (int nt = 0; nt < NT; ++nt) {
           const int n = nw + 16 * nt + m;
           const bool nok = n < a.NN;
+          auto er = [&](int e, int i) { return acc1[e][kk][nt][i] - acc3[e][kk][nt][i]; };
+          auto ei = [&](int e, int i) { return acc1[e][kk][nt][i] + acc2[e][kk][nt][i]; };
 #pragma unroll
-          for (int hf = 0; hf < 2; ++hf) {
+          for (int hf = 0; hf < NCL; ++hf) {
             float re[4], im[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const float er = acc1[0][kk][nt][i] - acc3[0][kk][nt][i];
-              const float ei = acc1[0][kk][nt][i] + acc2[0][kk][nt][i];
-              const float odr = acc1[1][kk][nt][i] - acc3[1][kk][nt][i];
-              const float odi = acc1[1][kk][nt][i] + acc2[1][kk][nt][i];
-              re[i] = hf == 0 ? er + odr : er - odr;
-              im[i] = hf == 0 ? ei + odi : ei - odi;
+              if (NCL == 2) {
+                re[i] = hf == 0 ? er(0, i) + er(NCL - 1, i) : er(0, i) - er(NCL - 1, i);
+                im[i] = hf == 0 ? ei(0, i) + ei(NCL - 1, i) : ei(0, i) - ei(NCL - 1, i);
+              } else {
+                const int c2 = 2 % NCL, c3 = 3 % NCL;
+                if (hf == 0 || hf == 2) {
+                  const float pr = er(0, i) + er(c2, i), pi = ei(0, i) + ei(c2, i);
+                  const float rr = er(1, i) + er(c3, i), ri = ei(1, i) + ei(c3, i);
+                  re[i] = hf == 0 ? pr + rr : pr - rr;
+                  im[i] = hf == 0 ? pi + ri : pi - ri;
+                } else {
+                  const float qr = er(0, i) - er(c2, i), qi = ei(0, i) - ei(c2, i);
+                  const float tr = er(1, i) - er(c3, i), ti = ei(1, i) - ei(c3, i);
+                  re[i] = hf == 1 ? qr - ti : qr + ti;
+                  im[i] = hf == 1 ? qi + tr : qi - tr;
+                }
+              }
             }
             store_tile(re, im, n, nok, 0, [&](int i) { return ob + int64_t(y0 + i + hf * a.oh) * a.NN; },
                        [&](int i) { return y0 + i < a.oh; });
@@ -486,8 +568,9 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
   a.JQ = c.JQ;
   a.ktiles = c.ktiles;
   a.kth = c.kth;
-  a.jh = c.J / 2;
-  a.oh = c.KO / 2;
+  const int ncls = (c.fold == 3 || c.fold == 4) ? 4 : 2;
+  a.jh = c.J / ncls;
+  a.oh = c.KO / ncls;
   a.acc = accumulate ? 1 : 0;
   // FOLD 2 keeps two accumulator sets; cap its k block at 2 tiles.
   const int kmax = c.fold == 2 ? 2 : 4;
@@ -504,8 +587,37 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
   const float2* pin = static_cast<const float2*>(in);
   float2* pout = static_cast<float2*>(out);
   const float4* pimg = reinterpret_cast<const float4*>(img);
-  // Accumulation only happens on forward-direction launches (fold 0 or 1).
-  if (c.fold == 2 && a.acc) return hipErrorInvalidValue;
+  // Accumulation only happens on forward-direction launches (fold 0, 1, 3).
+  if ((c.fold == 2 || c.fold == 4) && a.acc) return hipErrorInvalidValue;
+  if (c.fold == 3) {
+    // one k tile per class in every block (KT = 4), one 16-column tile per
+    // wave (the four class inputs and twelve accumulator tiles of NT = 2
+    // would not fit the registers of two waves per SIMD)
+    if (c.ktiles % 4 != 0) return hipErrorInvalidValue;
+    AxisArgs f = a;
+    f.kblocks = c.ktiles / 4;
+    f.nblocks = (c.NN + 63) / 64;
+    f.total = nb * f.kblocks * f.nblocks;
+    const int g3 = static_cast<int>(f.total < cap ? f.total : cap);
+    if (f.acc) hipLaunchKernelGGL((axis_kernel<4, 1, 3, 1>), dim3(g3), dim3(256), 0, s, pin, pout, pimg, f);
+    else hipLaunchKernelGGL((axis_kernel<4, 1, 3, 0>), dim3(g3), dim3(256), 0, s, pin, pout, pimg, f);
+    return hipGetLastError();
+  }
+  if (c.fold == 4) {
+    // the four class sums of one output tile per block, the contraction in
+    // one or two K steps (at most 32 modes per class), one 16-column tile per
+    // wave (two would hold twice the inputs and accumulators: one wave per
+    // SIMD)
+    if (c.JQ > 2) return hipErrorInvalidValue;
+    AxisArgs e = a;
+    e.kblocks = c.ktiles;
+    e.nblocks = (c.NN + 63) / 64;
+    e.total = nb * e.nblocks;
+    const int g4 = static_cast<int>(e.total < cap ? e.total : cap);
+    if (c.JQ == 1) hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1, 4>), dim3(g4), dim3(256), 0, s, pin, pout, pimg, e);
+    else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 4>), dim3(g4), dim3(256), 0, s, pin, pout, pimg, e);
+    return hipGetLastError();
+  }
   if (c.fold == 2 && c.JQ <= 2) {
     // The whole contraction in registers; every workgroup loops over all k
     // tiles one at a time (measured fastest at the backward workload's
@@ -518,11 +630,11 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
     e.total = nb * e.nblocks;
     const int g2 = static_cast<int>(e.total < cap ? e.total : cap);
     if (c.JQ == 1) {
-      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 1>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
-      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 1, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
     } else {
-      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
-      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 2, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
     }
     return hipGetLastError();
   }

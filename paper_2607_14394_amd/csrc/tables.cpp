@@ -37,6 +37,10 @@ inline double half_weight(int64_t nt, int64_t kt) {
   return 2.0;
 }
 
+// Classes stacked in an inverse axis image entry (fold 2: parity, fold 4:
+// k mod 4); the forward images hold one class per k tile.
+inline int axis_image_classes(const AxisCfg& a) { return a.fold == 2 ? 2 : (a.fold == 4 ? 4 : 1); }
+
 bool mul_ok(int64_t a, int64_t b, int64_t* out) {
   if (a < 0 || b < 0) return false;
   if (a != 0 && b > std::numeric_limits<int64_t>::max() / a) return false;
@@ -181,6 +185,13 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
     } else if (fold == 2) {
       a.JQ = static_cast<int>(ceil_div(J / 2, 16));
       a.ktiles = static_cast<int>(ceil_div(KO / 2, 16));
+    } else if (fold == 3) {
+      a.JQ = static_cast<int>(ceil_div(J / 4, 16));
+      a.kth = static_cast<int>(ceil_div(KO / 4, 16));
+      a.ktiles = 4 * a.kth;
+    } else if (fold == 4) {
+      a.JQ = static_cast<int>(ceil_div(J / 4, 16));
+      a.ktiles = static_cast<int>(ceil_div(KO / 4, 16));
     } else {
       a.JQ = static_cast<int>(ceil_div(J, 16));
       a.ktiles = static_cast<int>(ceil_div(KO, 16));
@@ -236,6 +247,26 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   dv.w1_bytes = sc.fuse_y ? 0 : w1;
   dv.ws_bytes = dv.w1_bytes + w2;
 
+  // Separate x and y launches fold in four classes (k mod 4, which is the
+  // position mod 4 when N % 4 == 0 and k_max is even) when every class fills
+  // whole 16-mode tiles (K % 64 == 0) and the inverse's class sums take at
+  // most two K steps (K <= 128): a quarter of the direct MFMA work instead of
+  // a half.
+  {
+    auto four = [&](int dim) {
+      const int64_t n = d->n_global[dim], k = dv.K[dim];
+      return d->n_local[dim] == n && n % 4 == 0 && k % 64 == 0 && k <= 128;
+    };
+    if (four(1) && !sc.fuse_y) {
+      dv.ay_f = axis(static_cast<int>(d->n_local[1]), static_cast<int>(dv.K[1]), nn_y, 3);
+      dv.ay_i = axis(static_cast<int>(dv.K[1]), static_cast<int>(d->n_local[1]), nn_y, 4);
+    }
+    if (four(0)) {
+      dv.ax_f = axis(static_cast<int>(d->n_local[0]), static_cast<int>(dv.K[0]), nn_x, 3);
+      dv.ax_i = axis(static_cast<int>(dv.K[0]), static_cast<int>(d->n_local[0]), nn_x, 4);
+    }
+  }
+
   // ---- fused inverse z + t expansion and block epilogue ----
   // The same z + t expansion as the split inverse, with z folded into at
   // most two classes (a chunk of the kernel is one z tile of every class),
@@ -277,7 +308,7 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   im.t_inv = take(t_img);
   im.t_inv_adjoint_of_forward = take(t_img);
   im.z_inv = take(z_img);
-  auto axis_img = [](const AxisCfg& a) { return size_t(a.ktiles) * a.JQ * (a.fold == 2 ? 2 : 1) * 2 * 64 * 4; };
+  auto axis_img = [](const AxisCfg& a) { return size_t(a.ktiles) * a.JQ * axis_image_classes(a) * 2 * 64 * 4; };
   im.y_fwd = take(axis_img(dv.ay_f));
   im.x_fwd = take(axis_img(dv.ax_f));
   im.y_inv = take(axis_img(dv.ay_i));
@@ -436,10 +467,14 @@ void z_inverse_image(const Derived& dv, float* dst) {
 //           mode p = 2 (16 (kt - c kth) + m) + c, column j = 16q + 4g + i < J/2.
 //   fold 2: entry (((kt*JQ + q)*2 + c)*2 + part)*64 + lane = basis[y][p],
 //           y = 16kt + m < KO/2, mode p = 2 (16q + 4g + i) + c.
+//   fold 3: fold 0's entry layout; tile kt holds class c = kt mod 4, mode
+//           p = 4 (16 (kt / 4) + m) + c, column j = 16q + 4g + i < J/4.
+//   fold 4: entry (((kt*JQ + q)*4 + c)*2 + part)*64 + lane = basis[y][p],
+//           y = 16kt + m < KO/4, mode p = 4 (16q + 4g + i) + c.
 // forward: basis[k][j] = B_dim[k][j]; inverse: basis[y][p] = conj(B_dim[p][y]).
 void axis_image(const Derived& dv, const AxisCfg& a, int dim, bool inverse, float* dst) {
   const dtst_desc& d = dv.d;
-  const int ncls = a.fold == 2 ? 2 : 1;
+  const int ncls = axis_image_classes(a);
   for (int kt = 0; kt < a.ktiles; ++kt)
     for (int q = 0; q < a.JQ; ++q)
       for (int c = 0; c < ncls; ++c)
@@ -458,6 +493,14 @@ void axis_image(const Derived& dv, const AxisCfg& a, int dim, bool inverse, floa
                 k = 16 * kt + m;
                 j = 2 * (16 * q + 4 * g + i) + c;
                 ok = k < a.KO / 2 && j < a.J;
+              } else if (a.fold == 3) {
+                k = 4 * (16 * (kt >> 2) + m) + (kt & 3);
+                j = 16 * q + 4 * g + i;
+                ok = k < a.KO && j < a.J / 4;
+              } else if (a.fold == 4) {
+                k = 16 * kt + m;
+                j = 4 * (16 * q + 4 * g + i) + c;
+                ok = k < a.KO / 4 && j < a.J;
               } else {
                 k = 16 * kt + m;
                 j = 16 * q + 4 * g + i;

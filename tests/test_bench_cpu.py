@@ -113,6 +113,15 @@ def test_work_uses_stage_flops_and_folds():
     assert w["axis_fwd_x"]["mfma_flops"] == sf["x"] * 0.75
     zc = bench._z_classes(g)
     assert w["stream_fwd_tzy"]["mfma_flops"] == sf["t"] + sf["z"] / zc + sf["y"] / 2
+    # the backward workload keeps K_y = 64 of the whole N_y = 256: y folds in four classes
+    import synth
+    g5 = synth.geometry(5)
+    assert bench._axis_classes(g5, 1) == 4 and bench._axis_classes(g5, 0) == 1
+    sf5 = bench.stage_flops(g5, 32)
+    w5 = bench.work(g5, 32)
+    assert w5["axis_fwd_y"]["mfma_flops"] == sf5["y"] / 4 * 0.75 == w5["axis_inv_y"]["mfma_flops"]
+    # K = 32 per dimension (workload 3) would leave half-empty tiles: two classes only
+    assert bench._axis_classes(g, 1) == 2
     # the accumulating x contraction also reads the spectrum back
     wa = bench.work(g, 32, acc_share=1.0)
     spec = g["batch"] * 32 * 32 * 32 * 32 * 8 * 8

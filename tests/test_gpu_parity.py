@@ -49,6 +49,11 @@ CASES = {
     "tfold_z_shard_mt8": ((4, 6, 96, 32), (4, 6, 40, 32), (0, 0, 24, 0), (1, 2, 20), 16, 1, 1, 2),
     "tfold_mt4_slab": ((8, 6, 90, 32), (4, 6, 90, 32), (4, 0, 0, 0), (2, 2, 20), 16, 2, 1, 1),
     "t_shard_nt32_kt16": ((4, 4, 16, 64), (4, 4, 16, 32), (0, 0, 0, 32), (1, 2, 4), 16, 1, 2, 2),
+    # four-class x and y folds of the separate axis launches (whole N % 4 == 0, K % 64 == 0):
+    # x and y both folded (x forward accumulating into the spectrum), then a ragged quarter
+    # (N_y / 4 = 50) with two k tiles per class and two K steps of the inverse class sums
+    "axis_four_class": ((64, 128, 8, 8), (64, 128, 8, 8), (0, 0, 0, 0), (32, 32, 2), 3, 1, 2, 2),
+    "axis_four_class_ragged": ((8, 200, 8, 8), (4, 200, 8, 8), (4, 0, 0, 0), (2, 64, 2), 3, 2, 1, 2),
     # more (b, c, x) planes than the fused t+z+y kernel has resident workgroups
     "many_planes": ((48, 8, 16, 8), (48, 8, 16, 8), (0, 0, 0, 0), (4, 2, 4), 3, 2, 4, 3),
     # N_y = N_z = 512: the fused kernels' y basis images do not fit next to the z image and the
