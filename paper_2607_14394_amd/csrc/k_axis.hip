@@ -410,14 +410,20 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
 // tiles: the stores of one block overlap the products of the next, and no
 // other workgroup re-reads the input.  KT output tiles per block (one 16-row
 // tile of the N/NCL rows of a class sum), NT 16-column tiles per wave.
-template <int KT, int NT, int JQ, int NCL>
+// LI: the basis image is copied to LDS once per workgroup, right behind the
+// first input loads.  Global loads and stores share a wave's memory counter,
+// so image reads from global memory inside the loop would wait for the
+// previous block's stores to complete; LDS reads do not.
+template <int KT, int NT, int JQ, int NCL, int LI>
 __global__ void __launch_bounds__(256)
 axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float4* __restrict__ img,
                    AxisArgs a) {
+  extern __shared__ float4 simg[];
   const int lane = threadIdx.x & 63;
   const int m = lane & 15, g = lane >> 4;
   const int wave = threadIdx.x >> 6;
   const int64_t total = a.total;
+  bool staged = false;
   for (int64_t hw = blockIdx.x; hw < total; hw += gridDim.x) {
     const int64_t base = (hw / gridDim.x) * gridDim.x;
     const int64_t grid_round = (total - base < int64_t(gridDim.x)) ? total - base : int64_t(gridDim.x);
@@ -448,6 +454,12 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
             x[q][c][nt][i] = ok ? v : make_float2(0.f, 0.f);
           }
         }
+    if (LI && !staged) {
+      const int n4 = a.ktiles * JQ * NCL * 2 * 64;
+      for (int e = threadIdx.x; e < n4; e += 256) simg[e] = img[e];
+      __syncthreads();
+      staged = true;
+    }
 
     for (int kb = 0; kb < a.kblocks; ++kb) {
       v4f acc1[NCL][KT][NT], acc2[NCL][KT][NT], acc3[NCL][KT][NT];
@@ -470,9 +482,9 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
 #pragma unroll
           for (int e = 0; e < NCL; ++e) {
             // image entry (((kt * JQ + q) * NCL + class) * 2 + part) * 64 + lane
-            const float4* ip = img + ((int64_t(kt) * a.JQ + q) * NCL + e) * 2 * 64 + lane;
-            bre[kk][e] = ip[0];
-            bim[kk][e] = ip[64];
+            const int ie = ((kt * JQ + q) * NCL + e) * 2 * 64 + lane;
+            bre[kk][e] = LI ? simg[ie] : img[ie];
+            bim[kk][e] = LI ? simg[ie + 64] : img[ie + 64];
           }
         }
 #pragma unroll
@@ -536,6 +548,14 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
       }
     }
   }
+}
+
+// LDS bytes of an expand kernel's staged basis image (ncl classes per
+// entry), or 0 when the image is larger than 32 KiB and is read from global
+// memory instead (two workgroups of the expand kernels share a CU).
+size_t expand_lds_bytes(const AxisCfg& c, int ncl) {
+  const size_t b = size_t(c.ktiles) * c.JQ * ncl * 2 * 64 * sizeof(float4);
+  return b <= 32 * 1024 ? b : 0;
 }
 
 template <int KT, int FOLD, int ACC>
@@ -614,8 +634,14 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
     e.nblocks = (c.NN + 63) / 64;
     e.total = nb * e.nblocks;
     const int g4 = static_cast<int>(e.total < cap ? e.total : cap);
-    if (c.JQ == 1) hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1, 4>), dim3(g4), dim3(256), 0, s, pin, pout, pimg, e);
-    else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 4>), dim3(g4), dim3(256), 0, s, pin, pout, pimg, e);
+    const size_t lds = expand_lds_bytes(c, 4);
+    if (lds > 0) {
+      if (c.JQ == 1) hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1, 4, 1>), dim3(g4), dim3(256), lds, s, pin, pout, pimg, e);
+      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 4, 1>), dim3(g4), dim3(256), lds, s, pin, pout, pimg, e);
+    } else {
+      if (c.JQ == 1) hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1, 4, 0>), dim3(g4), dim3(256), 0, s, pin, pout, pimg, e);
+      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 4, 0>), dim3(g4), dim3(256), 0, s, pin, pout, pimg, e);
+    }
     return hipGetLastError();
   }
   if (c.fold == 2 && c.JQ <= 2) {
@@ -629,12 +655,21 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
     e.nblocks = (c.NN + 64 * ent - 1) / (64 * ent);
     e.total = nb * e.nblocks;
     const int g2 = static_cast<int>(e.total < cap ? e.total : cap);
-    if (c.JQ == 1) {
-      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 1, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
-      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+    const size_t lds = expand_lds_bytes(c, 2);
+    if (lds > 0) {
+      if (c.JQ == 1) {
+        if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 1, 2, 1>), dim3(g2), dim3(256), lds, s, pin, pout, pimg, e);
+        else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1, 2, 1>), dim3(g2), dim3(256), lds, s, pin, pout, pimg, e);
+      } else {
+        if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 2, 2, 1>), dim3(g2), dim3(256), lds, s, pin, pout, pimg, e);
+        else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 2, 1>), dim3(g2), dim3(256), lds, s, pin, pout, pimg, e);
+      }
+    } else if (c.JQ == 1) {
+      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 1, 2, 0>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 1, 2, 0>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
     } else {
-      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 2, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
-      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 2>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      if (ent == 2) hipLaunchKernelGGL((axis_expand_kernel<1, 2, 2, 2, 0>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
+      else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 2, 0>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
     }
     return hipGetLastError();
   }

@@ -45,6 +45,7 @@ struct MixArgs {
 };
 
 typedef float v2f __attribute__((ext_vector_type(2)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 // Spectrum entries of one batch chunk processed together.
 constexpr int BCH = 2;
@@ -312,8 +313,11 @@ mix_h_kernel(const float2* __restrict__ gy, const float2* __restrict__ w, float2
 // and streams the rows out with non-temporal stores (g_w is written once and
 // not read back here, except for the accumulate read-modify-write).  With
 // almost no reads to overlap, this keeps the stores flowing while the next
-// block's spectra arrive.
-template <int LPR, int OPL>
+// block's spectra arrive.  W = 2: every lane holds the column pairs
+// o = 2 (lr + LPR s) + {0, 1} and writes them with one 16-byte store (half
+// the store instructions of W = 1 for the same bytes; needs an even C_out
+// and a 16-byte aligned g_w).
+template <int LPR, int OPL, int W>
 __global__ void __launch_bounds__(256)
 wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2* __restrict__ gw, MixArgs a) {
   constexpr int R = Rows<OPL>::value;
@@ -321,6 +325,7 @@ wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2
   extern __shared__ float2 sm[];
   const int nx = a.B * a.ci * (MPB + 1), ng = a.B * a.co * (MPB + 1);
   const int lr = threadIdx.x % LPR, mm = threadIdx.x / LPR;
+  auto col = [&](int s, int w) { return W * (lr + LPR * s) + w; };
   int64_t k0, k1;
   span(a.nblk, &k0, &k1);
   float2 prex[PRE], preg[PRE];
@@ -337,8 +342,28 @@ wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2
     const int64_t mbase = a.m0 + lm0;
     const bool active = mm < nm;
     float2* gm = gw + (lm0 + (active ? mm : 0)) * int64_t(a.ci) * a.co;
-    float2 acc[R][OPL];
-    if (a.acc) load_rows<OPL, R>(acc, gm, 0, a.ci, a.co, lr, LPR, active);
+    // rows i0 .. i0 + R - 1 of this mode's (ci x co) block of g_w (the
+    // accumulate read; rows or columns outside read its first element and
+    // are never used)
+    auto load_acc = [&](float2 (&v)[R][OPL][W], int i0) {
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int s = 0; s < OPL; ++s) {
+          const int i = i0 + r, o = col(s, 0);
+          const bool ok = active && i < a.ci && o < a.co;
+          const float2* src = gm + (ok ? int64_t(i) * a.co + o : 0);
+          if (W == 2) {
+            const float4 t = *reinterpret_cast<const float4*>(src);
+            v[r][s][0] = make_float2(t.x, t.y);
+            v[r][s][W - 1] = make_float2(t.z, t.w);
+          } else {
+            v[r][s][0] = *src;
+          }
+        }
+    };
+    float2 acc[R][OPL][W];
+    if (a.acc) load_acc(acc, 0);
     put<MPB>(sx, prex, x, a.B * a.ci, a.M, mbase, nm);
     put<MPB>(sg, preg, gy, a.B * a.co, a.M, mbase, nm);
     if (k + 1 < k1) {
@@ -350,22 +375,27 @@ wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2
     if (!active) continue;
     for (int i0 = 0; i0 < a.ci; i0 += R) {
       if (a.acc) {
-        if (i0 > 0) load_rows<OPL, R>(acc, gm, i0, a.ci, a.co, lr, LPR, true);
+        if (i0 > 0) load_acc(acc, i0);
       } else {
 #pragma unroll
         for (int r = 0; r < R; ++r)
 #pragma unroll
-          for (int s = 0; s < OPL; ++s) acc[r][s] = make_float2(0.f, 0.f);
+          for (int s = 0; s < OPL; ++s)
+#pragma unroll
+            for (int w = 0; w < W; ++w) acc[r][s][w] = make_float2(0.f, 0.f);
       }
       for (int b0 = 0; b0 < a.B; b0 += BCH) {
-        float2 gv[BCH][OPL];
+        float2 gv[BCH][OPL][W];
 #pragma unroll
         for (int q = 0; q < BCH; ++q)
 #pragma unroll
-          for (int s = 0; s < OPL; ++s) {
-            const int o = lr + LPR * s;
-            gv[q][s] = (b0 + q < a.B && o < a.co) ? sg[sidx<MPB>((b0 + q) * a.co + o, mm)] : make_float2(0.f, 0.f);
-          }
+          for (int s = 0; s < OPL; ++s)
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+              const int o = col(s, w);
+              gv[q][s][w] =
+                  (b0 + q < a.B && o < a.co) ? sg[sidx<MPB>((b0 + q) * a.co + o, mm)] : make_float2(0.f, 0.f);
+            }
 #pragma unroll
         for (int r = 0; r < R; ++r) {
           if (i0 + r >= a.ci) continue;
@@ -374,11 +404,13 @@ wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2
             if (b0 + q >= a.B) continue;
             const float2 xv = sx[sidx<MPB>((b0 + q) * a.ci + i0 + r, mm)];
 #pragma unroll
-            for (int s = 0; s < OPL; ++s) {
-              const float2 p = cjmul(xv, gv[q][s]);
-              acc[r][s].x += p.x;
-              acc[r][s].y += p.y;
-            }
+            for (int s = 0; s < OPL; ++s)
+#pragma unroll
+              for (int w = 0; w < W; ++w) {
+                const float2 p = cjmul(xv, gv[q][s][w]);
+                acc[r][s][w].x += p.x;
+                acc[r][s][w].y += p.y;
+              }
           }
         }
       }
@@ -388,10 +420,14 @@ wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2
         if (i >= a.ci) continue;
 #pragma unroll
         for (int s = 0; s < OPL; ++s) {
-          const int o = lr + LPR * s;
+          const int o = col(s, 0);
           if (o >= a.co) continue;
-          __builtin_nontemporal_store(v2f{acc[r][s].x, acc[r][s].y},
-                                      reinterpret_cast<v2f*>(gm + int64_t(i) * a.co + o));
+          if (W == 2)
+            __builtin_nontemporal_store(v4f{acc[r][s][0].x, acc[r][s][0].y, acc[r][s][W - 1].x, acc[r][s][W - 1].y},
+                                        reinterpret_cast<v4f*>(gm + int64_t(i) * a.co + o));
+          else
+            __builtin_nontemporal_store(v2f{acc[r][s][0].x, acc[r][s][0].y},
+                                        reinterpret_cast<v2f*>(gm + int64_t(i) * a.co + o));
         }
       }
     }
@@ -409,7 +445,10 @@ int opl_of(int64_t co) {
   return o <= 1 ? 1 : (o <= 2 ? 2 : (o <= 4 ? 4 : 8));
 }
 
-MixArgs make_args(int64_t B, int64_t ci, int64_t co, int64_t M, int64_t m0, int64_t m1, int acc) {
+// cols: the columns one lane group spans per row slot (C_out, or C_out / 2
+// for wgrad's column pairs).
+MixArgs make_args(int64_t B, int64_t ci, int64_t co, int64_t M, int64_t m0, int64_t m1, int acc,
+                  int64_t cols = 0) {
   MixArgs a;
   a.M = M;
   a.m0 = m0;
@@ -417,7 +456,7 @@ MixArgs make_args(int64_t B, int64_t ci, int64_t co, int64_t M, int64_t m0, int6
   a.B = static_cast<int>(B);
   a.ci = static_cast<int>(ci);
   a.co = static_cast<int>(co);
-  a.lpr = lanes_per_row(co);
+  a.lpr = lanes_per_row(cols > 0 ? cols : co);
   a.mpb = 256 / a.lpr;
   a.acc = acc;
   a.nblk = (a.count + a.mpb - 1) / a.mpb;
@@ -453,9 +492,10 @@ int64_t resident_workgroups(mix_fn f, size_t lds) {
   return n;
 }
 
-// LDS of one mode block's spectra.
-size_t block_lds(int64_t B, int64_t ci, int64_t co) {
-  const size_t mpb = size_t(256 / lanes_per_row(co));
+// LDS of one mode block's spectra (mode blocks of 256 / lanes_per_row(cols)
+// modes; cols = C_out unless given).
+size_t block_lds(int64_t B, int64_t ci, int64_t co, int64_t cols = 0) {
+  const size_t mpb = size_t(256 / lanes_per_row(cols > 0 ? cols : co));
   return sizeof(float2) * size_t(B) * size_t(ci + co) * (mpb + 1);
 }
 
@@ -481,8 +521,9 @@ int launch(mix_fn f, size_t lds, bool persistent, const float2* p0, const float2
 
 }  // namespace
 
-// Largest LDS of a mix workgroup: wgrad's double-buffered spectra of one
-// mode block (mix and mix_h use half of it).
+// LDS a mix workgroup needs: wgrad's double-buffered spectra of one mode
+// block (mix and mix_h use half of it; wgrad's column-pair form, taken only
+// where it fits, twice as many modes).
 size_t mix_lds_bytes(int64_t B, int64_t ci, int64_t co) { return 2 * block_lds(B, ci, co); }
 
 namespace {
@@ -512,7 +553,11 @@ struct MixHK {
 };
 template <int L, int O>
 struct WgradK {
-  static constexpr mix_fn fn = wgrad_kernel<L, O>;
+  static constexpr mix_fn fn = wgrad_kernel<L, O, 1>;
+};
+template <int L, int O>
+struct WgradK2 {
+  static constexpr mix_fn fn = wgrad_kernel<L, O, 2>;
 };
 
 }  // namespace
@@ -536,6 +581,14 @@ int launch_mix_h(const void* gy, const void* w, void* gx, int64_t B, int64_t ci,
 int launch_wgrad(const void* xhat, const void* gy, void* gw, int64_t B, int64_t ci, int64_t co, int64_t M,
                  int64_t m0, int64_t m1, int accumulate, void* stream) {
   if (B <= 0 || m1 <= m0) return hipSuccess;
+  // column pairs (16-byte stores) for an even C_out of at least 4 when g_w
+  // is 16-byte aligned and the doubled mode block still fits the LDS
+  const size_t lds2 = 2 * block_lds(B, ci, co, co / 2);
+  if (co % 2 == 0 && co >= 4 && (reinterpret_cast<uintptr_t>(gw) & 15) == 0 && lds2 <= 160 * 1024) {
+    const MixArgs a = make_args(B, ci, co, M, m0, m1, accumulate ? 1 : 0, co / 2);
+    return launch(pick<WgradK2>(co / 2), lds2, true, static_cast<const float2*>(xhat),
+                  static_cast<const float2*>(gy), static_cast<float2*>(gw), a, stream);
+  }
   const MixArgs a = make_args(B, ci, co, M, m0, m1, accumulate ? 1 : 0);
   return launch(pick<WgradK>(co), mix_lds_bytes(B, ci, co), true, static_cast<const float2*>(xhat),
                 static_cast<const float2*>(gy), static_cast<float2*>(gw), a, stream);
