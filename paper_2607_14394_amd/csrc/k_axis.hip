@@ -42,6 +42,9 @@
 // (16 bytes) and each store instruction covers whole 128-byte lines.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+#include <vector>
+
 #include "dtst_internal.h"
 
 namespace dtst {
@@ -402,6 +405,218 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
   }
 }
 
+// Persistent, software-pipelined form of the forward-direction contraction
+// (FOLD 0, 1 or 3, no accumulate) for launches whose basis image fits in
+// LDS.  A grid of resident workgroups walks its work items (b, k block,
+// column block) in order; every wave runs one flat sequence of (item, K
+// step) positions and keeps the input rows of the next PD positions in
+// flight, across item boundaries, so the first steps of an item are loaded
+// while the previous item is still being contracted and written (a work
+// item of a short contraction, J = 64 for instance, is only four K steps:
+// one workgroup per item would expose the input latency at every item
+// start).  The image is copied to LDS once per workgroup; its reads then
+// never wait behind input loads or output stores (global loads and stores
+// share one memory counter per wave, LDS reads do not).  Buffer k holds
+// positions k, k + PD, ...; the loop runs whole passes over the buffers so
+// every buffer index is a compile-time constant.  Loads past the last
+// position re-read the last item's rows and are never used.
+template <int KT, int NT, int FOLD>
+__global__ void __launch_bounds__(256)
+axis_pipe_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float4* __restrict__ img,
+                 AxisArgs a) {
+  static_assert(FOLD == 0 || FOLD == 1 || FOLD == 3, "forward-direction folds only");
+  static_assert(FOLD != 3 || KT == 4, "four-class tiles: one k tile per class");
+  constexpr int NS = FOLD == 1 ? 2 : (FOLD == 3 ? 4 : 1);  // input rows combined per K index
+  constexpr int PD = 2;
+  extern __shared__ float4 simg[];
+  const int lane = threadIdx.x & 63;
+  const int m = lane & 15, g = lane >> 4;
+  const int wave = threadIdx.x >> 6;
+  const int64_t G = gridDim.x;
+  const int64_t n_it = a.total > int64_t(blockIdx.x) ? (a.total - 1 - blockIdx.x) / G + 1 : 0;
+  if (n_it == 0) return;
+  const int lim = FOLD == 0 ? a.J : a.jh;
+  const int64_t spare = m < int64_t(a.J) * a.NN ? m : 0;
+
+  // work item `it` of this workgroup -> (b, k block, first column of this
+  // wave); items of one round of the grid are spread over the XCDs in
+  // contiguous logical ranges (as in axis_kernel)
+  struct Item {
+    int64_t b;
+    int kb, nw;
+  };
+  // (32-bit index arithmetic: the launcher takes this kernel only for fewer
+  // than 2^31 work items)
+  auto item_of = [&](int64_t it) {
+    const uint32_t g32 = static_cast<uint32_t>(G), tot = static_cast<uint32_t>(a.total);
+    const uint32_t base = static_cast<uint32_t>(it) * g32;
+    const uint32_t grid_round = tot - base < g32 ? tot - base : g32;
+    const uint32_t per = grid_round / 8, bid = blockIdx.x;
+    const uint32_t L = base + (bid >= per * 8 ? bid : (bid % 8) * per + bid / 8);
+    const uint32_t nbl = static_cast<uint32_t>(a.nblocks), kbl = static_cast<uint32_t>(a.kblocks);
+    Item r;
+    const uint32_t rest = L / nbl;
+    const int nbk = static_cast<int>(L - rest * nbl);
+    const uint32_t b = rest / kbl;
+    r.kb = static_cast<int>(rest - b * kbl);
+    r.b = b;
+    r.nw = nbk * (64 * NT) + wave * (16 * NT);
+    return r;
+  };
+
+  float2 vb[PD][NS][NT][4];
+  bool okb[PD][NT][4];
+  // load position (item, step) and its item
+  int64_t it_l = 0;
+  int q_l = 0;
+  Item t_l = item_of(0);
+  auto load = [&](auto kc) __attribute__((always_inline)) {
+    constexpr int k = decltype(kc)::value;
+    const float2* inb = in + t_l.b * int64_t(a.J) * a.NN;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int jj = 16 * q_l + 4 * g + i;
+        const int n = t_l.nw + 16 * nt + m;
+        const bool v_ok = jj < lim && n < a.NN;
+        okb[k][nt][i] = v_ok;
+#pragma unroll
+        for (int sr = 0; sr < NS; ++sr) {
+          int64_t idx = v_ok ? int64_t(jj + sr * (FOLD == 0 ? 0 : a.jh)) * a.NN + n : spare;
+          opaque(idx);
+          vb[k][sr][nt][i] = inb[idx];
+        }
+      }
+    if (++q_l == a.JQ) {
+      q_l = 0;
+      if (it_l + 1 < n_it) t_l = item_of(++it_l);
+    }
+  };
+  load(std::integral_constant<int, 0>{});
+  load(std::integral_constant<int, 1>{});
+  {
+    const int n4 = a.ktiles * a.JQ * 2 * 64;
+    for (int e = threadIdx.x; e < n4; e += 256) simg[e] = img[e];
+  }
+  __syncthreads();
+
+  v4f acc1[KT][NT], acc2[KT][NT], acc3[KT][NT];
+  auto clear = [&]() {
+#pragma unroll
+    for (int kk = 0; kk < KT; ++kk)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        acc1[kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+        acc2[kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+        acc3[kk][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+      }
+  };
+  clear();
+
+  // compute position
+  int64_t it_c = 0;
+  int q_c = 0;
+  Item t_c = item_of(0);
+
+  auto step = [&](auto kc) __attribute__((always_inline)) {
+    constexpr int k = decltype(kc)::value;
+    const bool live = it_c < n_it;
+    // class inputs of this position: V[v][nt][i] (v = fold class of a tile;
+    // FOLD 3: S_c as in axis_kernel, zero outside the tile)
+    constexpr int NV = FOLD == 0 ? 1 : (FOLD == 1 ? 2 : 4);
+    float2 xv[NV][NT][4];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool o = okb[k][nt][i];
+        const float2 x0 = vb[k][0][nt][i];
+        if (FOLD == 0) {
+          xv[0][nt][i] = o ? x0 : make_float2(0.f, 0.f);
+        } else if (FOLD == 1) {
+          const float2 x1 = vb[k][NS - 1][nt][i];
+          xv[0][nt][i] = o ? make_float2(x0.x + x1.x, x0.y + x1.y) : make_float2(0.f, 0.f);
+          xv[NV - 1][nt][i] = o ? make_float2(x0.x - x1.x, x0.y - x1.y) : make_float2(0.f, 0.f);
+        } else {
+          const float2 x1 = vb[k][1 % NS][nt][i], x2 = vb[k][2 % NS][nt][i], x3 = vb[k][3 % NS][nt][i];
+          const float er = x0.x + x2.x, ei = x0.y + x2.y, fr = x1.x + x3.x, fi = x1.y + x3.y;
+          const float ur = x0.x - x2.x, ui = x0.y - x2.y, dr = x1.x - x3.x, di = x1.y - x3.y;
+          xv[0][nt][i] = o ? make_float2(er + fr, ei + fi) : make_float2(0.f, 0.f);
+          xv[1 % NV][nt][i] = o ? make_float2(ur + di, ui - dr) : make_float2(0.f, 0.f);
+          xv[2 % NV][nt][i] = o ? make_float2(er - fr, ei - fi) : make_float2(0.f, 0.f);
+          xv[3 % NV][nt][i] = o ? make_float2(ur - di, ui + dr) : make_float2(0.f, 0.f);
+        }
+      }
+    load(kc);
+    if (!live) return;
+    float4 br[KT], bi[KT];
+#pragma unroll
+    for (int kk = 0; kk < KT; ++kk) {
+      const int kt = min(t_c.kb * KT + kk, a.ktiles - 1);
+      const int ie = (kt * a.JQ + q_c) * 2 * 64 + lane;
+      br[kk] = simg[ie];
+      bi[kk] = simg[ie + 64];
+    }
+    // i outermost: consecutive products into one accumulator are 3 KT NT
+    // instructions apart
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int kk = 0; kk < KT; ++kk) {
+        const int kt = min(t_c.kb * KT + kk, a.ktiles - 1);
+        // fold class of tile kt: FOLD 1 (kt >= kth), FOLD 3 (kt mod 4 = kk)
+        const int v = FOLD == 1 ? (kt >= a.kth ? 1 : 0) : (FOLD == 3 ? (kk & 3) : 0);
+        const float r = br[kk][i], im = bi[kk][i], rpi = r + im;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          float2 x;
+          if (FOLD == 1) x = v ? xv[NV - 1][nt][i] : xv[0][nt][i];  // uniform select
+          else x = xv[FOLD == 3 ? (kk & 3) % NV : 0][nt][i];
+          acc1[kk][nt] = mfma(rpi, x.x, acc1[kk][nt]);
+          acc2[kk][nt] = mfma(r, x.y - x.x, acc2[kk][nt]);
+          acc3[kk][nt] = mfma(im, x.x + x.y, acc3[kk][nt]);
+        }
+      }
+    if (++q_c < a.JQ) return;
+    // item finished: Re = k1 - k3, Im = k1 + k2 of every tile, rows as in axis_kernel
+    float2* ob = out + t_c.b * int64_t(a.KO) * a.NN;
+#pragma unroll
+    for (int kk = 0; kk < KT; ++kk) {
+      const int kt = t_c.kb * KT + kk;
+      if (kt >= a.ktiles) continue;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int n = t_c.nw + 16 * nt + m;
+        float re[4], im[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          re[i] = acc1[kk][nt][i] - acc3[kk][nt][i];
+          im[i] = acc1[kk][nt][i] + acc2[kk][nt][i];
+        }
+        auto row = [&](int i) {
+          if (FOLD == 1) {
+            const int c = kt >= a.kth ? 1 : 0;
+            return 2 * (16 * (kt - c * a.kth) + 4 * g + i) + c;
+          }
+          if (FOLD == 3) return 4 * (16 * (kt >> 2) + 4 * g + i) + (kt & 3);
+          return 16 * kt + 4 * g + i;
+        };
+        store_tile(re, im, n, n < a.NN, 0, [&](int i) { return ob + int64_t(row(i)) * a.NN; },
+                   [&](int i) { return row(i) < a.KO; });
+      }
+    }
+    clear();
+    q_c = 0;
+    if (++it_c < n_it) t_c = item_of(it_c);
+  };
+  static_assert(PD == 2, "two positions in flight");
+  do {
+    step(std::integral_constant<int, 0>{});
+    step(std::integral_constant<int, 1>{});
+  } while (it_c < n_it);
+}
+
 // Folded inverse expansion (FOLD 2 with NCL = 2 classes, FOLD 4 with NCL =
 // 4) whose whole contraction fits in a few K steps (JQ <= 2: at most 32
 // retained modes per class).  Such a launch writes several times what it
@@ -558,6 +773,72 @@ size_t expand_lds_bytes(const AxisCfg& c, int ncl) {
   return b <= 32 * 1024 ? b : 0;
 }
 
+typedef void (*axis_fn)(const float2*, const float2*, float2*, const float4*, AxisArgs);
+
+// Workgroups of kernel f with `lds` bytes of dynamic LDS the current device
+// holds at once (cached per kernel, LDS size and device).
+int64_t resident(const void* f, size_t lds) {
+  struct Entry {
+    const void* f;
+    size_t lds;
+    int dev;
+    int64_t n;
+  };
+  static std::mutex mu;
+  static std::vector<Entry> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    for (const Entry& e : cache)
+      if (e.f == f && e.lds == lds && e.dev == dev) return e.n;
+  }
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, f, 256, lds) != hipSuccess) return 0;
+  const int64_t n = int64_t(cus) * (per_cu > 0 ? per_cu : 1);
+  std::lock_guard<std::mutex> lock(mu);
+  cache.push_back(Entry{f, lds, dev, n});
+  return n;
+}
+
+// The persistent pipelined kernel for (KT, NT, FOLD).
+template <int FOLD>
+const void* pipe_fn(int kt, int nt) {
+  if (FOLD == 3) return reinterpret_cast<const void*>(axis_pipe_kernel<4, 1, 3>);
+  if (kt == 1) return nt == 2 ? reinterpret_cast<const void*>(axis_pipe_kernel<1, 2, FOLD == 3 ? 0 : FOLD>)
+                              : reinterpret_cast<const void*>(axis_pipe_kernel<1, 1, FOLD == 3 ? 0 : FOLD>);
+  if (kt == 2) return nt == 2 ? reinterpret_cast<const void*>(axis_pipe_kernel<2, 2, FOLD == 3 ? 0 : FOLD>)
+                              : reinterpret_cast<const void*>(axis_pipe_kernel<2, 1, FOLD == 3 ? 0 : FOLD>);
+  return nt == 2 ? reinterpret_cast<const void*>(axis_pipe_kernel<4, 2, FOLD == 3 ? 0 : FOLD>)
+                 : reinterpret_cast<const void*>(axis_pipe_kernel<4, 1, FOLD == 3 ? 0 : FOLD>);
+}
+
+// Launches the pipelined kernel when its image fits 64 KiB of LDS; returns
+// false (nothing launched) otherwise.
+bool launch_pipe(int fold, int kt, int nt, const AxisCfg& c, AxisArgs a, hipStream_t s, const float2* pin,
+                 float2* pout, const float4* pimg, hipError_t* err) {
+  const size_t lds = size_t(c.ktiles) * c.JQ * 2 * 64 * sizeof(float4);
+  if (lds > 64 * 1024 || a.nb * a.kblocks * ((c.NN + 63) / 64) >= (int64_t(1) << 31)) return false;
+  // four k tiles keep twelve accumulator tiles per column tile: one column
+  // tile per wave (two would leave one wave per SIMD)
+  if (kt == 4) nt = 1;
+  if (nt == 1) {
+    a.nblocks = (c.NN + 63) / 64;
+    a.total = a.nb * a.kblocks * a.nblocks;
+  }
+  const void* f = fold == 0 ? pipe_fn<0>(kt, nt) : (fold == 1 ? pipe_fn<1>(kt, nt) : pipe_fn<3>(kt, nt));
+  const int64_t res = resident(f, lds);
+  if (res <= 0) {
+    *err = hipErrorInvalidConfiguration;
+    return true;
+  }
+  const int grid = static_cast<int>(a.total < res ? a.total : res);
+  void* args[] = {&pin, &pout, &pimg, &a};
+  *err = hipLaunchKernel(f, dim3(grid), dim3(256), args, lds, s);
+  return true;
+}
+
 template <int KT, int FOLD, int ACC>
 void launch_kt(int nt, int grid, hipStream_t s, const float2* pin, float2* pout, const float4* pimg,
                const AxisArgs& a) {
@@ -619,6 +900,8 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
     f.nblocks = (c.NN + 63) / 64;
     f.total = nb * f.kblocks * f.nblocks;
     const int g3 = static_cast<int>(f.total < cap ? f.total : cap);
+    hipError_t perr = hipSuccess;
+    if (!f.acc && launch_pipe(3, 4, 1, c, f, s, pin, pout, pimg, &perr)) return perr;
     if (f.acc) hipLaunchKernelGGL((axis_kernel<4, 1, 3, 1>), dim3(g3), dim3(256), 0, s, pin, pout, pimg, f);
     else hipLaunchKernelGGL((axis_kernel<4, 1, 3, 0>), dim3(g3), dim3(256), 0, s, pin, pout, pimg, f);
     return hipGetLastError();
@@ -672,6 +955,10 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
       else hipLaunchKernelGGL((axis_expand_kernel<1, 1, 2, 2, 0>), dim3(g2), dim3(256), 0, s, pin, pout, pimg, e);
     }
     return hipGetLastError();
+  }
+  if (c.fold != 2 && !a.acc) {
+    hipError_t perr = hipSuccess;
+    if (launch_pipe(c.fold, kt, nt, c, a, s, pin, pout, pimg, &perr)) return perr;
   }
   if (c.fold == 2) launch_fold<2, 0>(kt, nt, grid, s, pin, pout, pimg, a);
   else if (c.fold == 1) a.acc ? launch_fold<1, 1>(kt, nt, grid, s, pin, pout, pimg, a)
