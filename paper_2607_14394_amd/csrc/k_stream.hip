@@ -146,7 +146,6 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
   }
   if constexpr (TF) {
     static_assert(CT == 2 && MT % 2 == 0, "t-folded tiles: two k_t tiles, Re and Im row tiles");
-    const bool lo = (lane & 15) < 8;
     v4f G1[NCLS], G2[NCLS], G3[NCLS];
 #pragma unroll
     for (int cl = 0; cl < NCLS; ++cl)
@@ -154,9 +153,11 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
       for (int i = 0; i < 4; ++i) {
         // tile 0: Re (m < 8) / Im (m >= 8) of even k_t; tile 1: the same of odd k_t
         const float t0 = V[cl][0][i], t1 = V[cl][1][i];
-        const float x0 = ror8(t0), x1 = ror8(t1);
-        const float vi = lo ? x0 : t1;  // Im V of this lane's k_t
-        const float vr = lo ? t0 : x1;  // Re V of this lane's k_t
+        // Im V of this lane's k_t: lanes m < 8 take lane m + 8 of tile 0
+        // (DPP banks 0, 1), lanes m >= 8 keep tile 1; Re V: lanes m >= 8 take
+        // lane m - 8 of tile 1 (banks 2, 3), lanes m < 8 keep tile 0
+        const float vi = ror8_into<0x3>(t1, t0);
+        const float vr = ror8_into<0xC>(t0, t1);
         G1[cl][i] = vr;
         G2[cl][i] = vi - vr;
         G3[cl][i] = vr + vi;
@@ -748,10 +749,10 @@ __device__ __forceinline__ void inv_row(const float (&A)[NCLS][CT][MT][4], float
           float va[4], vb[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float send = lo ? Y[hh][TH - 1][i] : Y[hh][0][i];
-            const float recv = ror8(send);
-            va[i] = lo ? Y[hh][0][i] : recv;
-            vb[i] = lo ? recv : Y[hh][TH - 1][i];
+            // lanes m >= 8 take the first tile of lane m - 8, lanes m < 8
+            // the second tile of lane m + 8 (bank-masked DPP moves)
+            va[i] = ror8_into<0xC>(Y[hh][0][i], Y[hh][TH - 1][i]);
+            vb[i] = ror8_into<0x3>(Y[hh][TH - 1][i], Y[hh][0][i]);
           }
           if (MODE == 2 || za < a.zh)
             store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);
@@ -869,10 +870,8 @@ __device__ __forceinline__ void inv_row_tfg(const float2 (&u)[NCLS][MT / 2][4], 
         float va[4], vb[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float send = lo ? Y[TH - 1][i] : Y[0][i];
-          const float recv = ror8(send);
-          va[i] = lo ? Y[0][i] : recv;
-          vb[i] = lo ? recv : Y[TH - 1][i];
+          va[i] = ror8_into<0xC>(Y[0][i], Y[TH - 1][i]);
+          vb[i] = ror8_into<0x3>(Y[TH - 1][i], Y[0][i]);
         }
         if (MODE == 2 || za < a.zh)
           store_stream(yrow + int64_t(za + hf * a.zh) * a.nt + tch, va[0], va[1], va[2], va[3]);

@@ -28,6 +28,14 @@ __device__ __forceinline__ float ror8(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xf, 0xf, false));
 }
 
+// ror8 of src written only to the lanes of the DPP banks in BANKS (bank b =
+// lanes 4b..4b+3 of every row of 16); the other lanes return old.
+template <int BANKS>
+__device__ __forceinline__ float ror8_into(float old, float src) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(src), 0x128, 0xf, BANKS, false));
+}
+
 // ---------------------------------------------------------------------------
 // z folding.  With z undistributed and N = N_z divisible by NCLS,
 // B[k, z + jN/NCLS] = w^(kj) B[k, z] with w = -1 (NCLS = 2) or -i (NCLS = 4),
