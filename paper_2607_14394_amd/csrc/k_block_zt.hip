@@ -132,20 +132,21 @@ __device__ __forceinline__ void zexp_tfg(const float2* urow, const StreamArgs& a
                                          int g, int lane, v4f (&Wr)[NCLS], v4f (&Wi)[NCLS]) {
   float2 u[NCLS][MT / 2][4];
   load_u_tfg<MT, NCLS>(urow, a, m, g, u);
+  constexpr int MTI = 3 * MT / 2;  // image blocks per (class, z tile): Cr, Ci - Cr, Cr + Ci
 #pragma unroll
   for (int cl = 0; cl < NCLS; ++cl) {
     v4f k1 = v4f{0.f, 0.f, 0.f, 0.f}, k2 = k1, k3 = k1;
 #pragma unroll
     for (int qh = 0; qh < MT / 2; ++qh) {
-      const float4 cr = lz[((cl * a.zt + zt) * MT + qh) * 64 + lane];
-      const float4 ci = lz[((cl * a.zt + zt) * MT + qh + MT / 2) * 64 + lane];
+      const float4* zb = lz + ((cl * a.zt + zt) * MTI + qh) * 64 + lane;
+      const float4 cr = zb[0], dm = zb[(MT / 2) * 64], sp = zb[MT * 64];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool ok = tfg_index<NCLS>(a, m, g, cl, qh, i) >= 0;
         const float ur = ok ? u[cl][qh][i].x : 0.f, ui = ok ? u[cl][qh][i].y : 0.f;
         k1 = mfma(ur + ui, cr[i], k1);
-        k2 = mfma(ur, ci[i] - cr[i], k2);
-        k3 = mfma(ui, cr[i] + ci[i], k3);
+        k2 = mfma(ur, dm[i], k2);
+        k3 = mfma(ui, sp[i], k3);
       }
     }
     Wr[cl] = k1 - k3;
@@ -209,7 +210,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   // LDS: the z image, the row's spectrum of every output channel, two
   // buffers of a chunk's expanded values [o][z row][t].
   extern __shared__ float4 lds[];
-  const int nimg = NCLS * a.zt * MT * 64;
+  const int nimg = NCLS * a.zt * (TF ? 3 * MT / 2 : MT) * 64;  // z image blocks per (class, z tile)
   const int spec_len = a.kz * a.kt;
   const int n4 = ba.co * spec_len / 2;  // float4 of the row's spectrum
   float2* sbuf = reinterpret_cast<float2*>(lds + nimg);
@@ -495,7 +496,7 @@ blk_fn pick_blk(const StreamCfg& c, int kio) {
 }  // namespace
 
 size_t block_zt_lds_bytes(const StreamCfg& c, int64_t co) {
-  return size_t(c.ncls) * c.zt * c.mt * 64 * 16 + size_t(co) * c.kz * c.kt * 8 +
+  return size_t(c.ncls) * c.zt * (c.tf ? 3 * c.mt / 2 : c.mt) * 64 * 16 + size_t(co) * c.kz * c.kt * 8 +
          2 * size_t(co) * 16 * c.nt * sizeof(float);
 }
 

@@ -131,11 +131,12 @@ __device__ __forceinline__ void t_part(const float (&xv)[NCLS][TH][4], const boo
 template <int CT, int MT, int NCLS, int TF = 0>
 __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* lds, const StreamArgs& a, int zt,
                                        int lane, v4f (&P)[NCLS][MT][CT]) {
+  constexpr int MTS = TF ? 3 * MT / 2 : MT;  // image blocks per (class, z tile)
   float4 A[NCLS][MT];
 #pragma unroll
   for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) A[cl][mt] = lds[((cl * a.zt + zt) * MT + mt) * 64 + lane];
+    for (int mt = 0; mt < MT; ++mt) A[cl][mt] = lds[((cl * a.zt + zt) * MTS + mt) * 64 + lane];
   if (zt == 0) {
 #pragma unroll
     for (int cl = 0; cl < NCLS; ++cl)
@@ -146,6 +147,13 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
   }
   if constexpr (TF) {
     static_assert(CT == 2 && MT % 2 == 0, "t-folded tiles: two k_t tiles, Re and Im row tiles");
+    // image blocks per (class, z tile): Re, Im and Re + Im row tiles
+    constexpr int MTI = 3 * MT / 2;
+    float4 Bs[NCLS][MT / 2];
+#pragma unroll
+    for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+      for (int mr = 0; mr < MT / 2; ++mr) Bs[cl][mr] = lds[((cl * a.zt + zt) * MTI + MT + mr) * 64 + lane];
     v4f G1[NCLS], G2[NCLS], G3[NCLS];
 #pragma unroll
     for (int cl = 0; cl < NCLS; ++cl)
@@ -169,7 +177,7 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
 #pragma unroll
         for (int mr = 0; mr < MT / 2; ++mr) {
           const float br = A[cl][mr][i], bi = A[cl][mr + MT / 2][i];
-          P[cl][mr][0] = mfma(br + bi, G1[cl][i], P[cl][mr][0]);
+          P[cl][mr][0] = mfma(Bs[cl][mr][i], G1[cl][i], P[cl][mr][0]);
           P[cl][mr][1] = mfma(br, G2[cl][i], P[cl][mr][1]);
           P[cl][mr + MT / 2][0] = mfma(bi, G3[cl][i], P[cl][mr + MT / 2][0]);
         }
@@ -634,7 +642,7 @@ __global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH, TF)
 fwd_tz_kernel(const float* __restrict__ x, float2* __restrict__ out,
               const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
   extern __shared__ float4 lds[];
-  const int nimg = NCLS * a.zt * MT * 64;
+  const int nimg = NCLS * a.zt * (TF ? 3 * MT / 2 : MT) * 64;  // image blocks per (class, z tile)
   for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
   __syncthreads();
 
@@ -791,6 +799,21 @@ __device__ __forceinline__ void inv_row_tfg(const float2 (&u)[NCLS][MT / 2][4], 
                                             int lane) {
   static_assert(TH % 2 == 0 && MODE != 0, "t folding needs whole 16-byte t groups");
   const int m = lane & 15, g = lane >> 4;
+  constexpr int MTI = 3 * MT / 2;  // image blocks per (class, z tile)
+  // the row's A operands Ur + Ui, Ur, Ui (zero where the mode or k_t is not
+  // retained), formed once for every z tile
+  float us[NCLS][MT / 2][4], ur[NCLS][MT / 2][4], ui[NCLS][MT / 2][4];
+#pragma unroll
+  for (int cl = 0; cl < NCLS; ++cl)
+#pragma unroll
+    for (int qh = 0; qh < MT / 2; ++qh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = tfg_index<NCLS>(a, m, g, cl, qh, i) >= 0;
+        ur[cl][qh][i] = ok ? u[cl][qh][i].x : 0.f;
+        ui[cl][qh][i] = ok ? u[cl][qh][i].y : 0.f;
+        us[cl][qh][i] = ur[cl][qh][i] + ui[cl][qh][i];
+      }
   for (int zt = 0; zt < a.zt; ++zt) {
     v4f Wr[NCLS], Wi[NCLS];
 #pragma unroll
@@ -798,16 +821,14 @@ __device__ __forceinline__ void inv_row_tfg(const float2 (&u)[NCLS][MT / 2][4], 
       v4f k1 = v4f{0.f, 0.f, 0.f, 0.f}, k2 = k1, k3 = k1;
 #pragma unroll
       for (int qh = 0; qh < MT / 2; ++qh) {
-        // z image: block qh holds Re C_z, block qh + MT/2 Im C_z of the same slots
-        const float4 cr = lds[((cl * a.zt + zt) * MT + qh) * 64 + lane];
-        const float4 ci = lds[((cl * a.zt + zt) * MT + qh + MT / 2) * 64 + lane];
+        // z image blocks of these K entries: Cr, Ci - Cr, Cr + Ci (C_z = Cr + i Ci)
+        const float4* zb = lds + ((cl * a.zt + zt) * MTI + qh) * 64 + lane;
+        const float4 cr = zb[0], dm = zb[(MT / 2) * 64], sp = zb[MT * 64];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const bool ok = tfg_index<NCLS>(a, m, g, cl, qh, i) >= 0;
-          const float ur = ok ? u[cl][qh][i].x : 0.f, ui = ok ? u[cl][qh][i].y : 0.f;
-          k1 = mfma(ur + ui, cr[i], k1);
-          k2 = mfma(ur, ci[i] - cr[i], k2);
-          k3 = mfma(ui, cr[i] + ci[i], k3);
+          k1 = mfma(us[cl][qh][i], cr[i], k1);
+          k2 = mfma(ur[cl][qh][i], dm[i], k2);
+          k3 = mfma(ui[cl][qh][i], sp[i], k3);
         }
       }
       Wr[cl] = k1 - k3;
@@ -945,7 +966,7 @@ __global__ void __launch_bounds__(256) DTST_STREAM_WAVES(CT, MT, NCLS, TH, TF)
 inv_zt_kernel(const float2* __restrict__ in, float* __restrict__ y,
               const float* __restrict__ timg, const float4* __restrict__ zimg, StreamArgs a) {
   extern __shared__ float4 lds[];
-  const int nimg = NCLS * a.zt * MT * 64;
+  const int nimg = NCLS * a.zt * (TF ? 3 * MT / 2 : MT) * 64;  // image blocks per (class, z tile)
   for (int i = threadIdx.x; i < nimg; i += blockDim.x) lds[i] = zimg[i];
   __syncthreads();
 

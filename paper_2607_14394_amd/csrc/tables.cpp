@@ -41,6 +41,11 @@ inline double half_weight(int64_t nt, int64_t kt) {
 // k mod 4); the forward images hold one class per k tile.
 inline int axis_image_classes(const AxisCfg& a) { return a.fold == 2 ? 2 : (a.fold == 4 ? 4 : 1); }
 
+// z image blocks of 16 rows (forward) or 16 K entries (inverse) per (class,
+// z tile): mt, plus mt / 2 when t folds (the three-product form's third
+// operand, see z_forward_image and z_inverse_image).
+inline int z_blocks(const StreamCfg& s) { return s.tf ? 3 * s.mt / 2 : s.mt; }
+
 bool mul_ok(int64_t a, int64_t b, int64_t* out) {
   if (a < 0 || b < 0) return false;
   if (a != 0 && b > std::numeric_limits<int64_t>::max() / a) return false;
@@ -165,7 +170,7 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   // t folds (even k_t from x(t) + x(t + N_t/2), odd k_t from the difference)
   // in the split kernels when the shard holds the whole t extent of 32.
   sc.tf = (sc.ct == 2 && sc.th == 2 && sc.nt == 32 && d->n_local[3] == d->n_global[3]) ? 1 : 0;
-  sc.lds_bytes = size_t(sc.ncls) * sc.zt * sc.mt * 64 * 16;
+  sc.lds_bytes = size_t(sc.ncls) * sc.zt * z_blocks(sc) * 64 * 16;
   if (sc.lds_bytes > 160 * 1024) {
     *err = "z basis image exceeds the 160 KiB LDS of a workgroup";
     return DTST_ERR_UNSUPPORTED;
@@ -280,7 +285,7 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
     sb.mt = sb.kcp / 8;
     sb.zh = sb.nz / sb.ncls;
     sb.zt = static_cast<int>(ceil_div(sb.zh, 16));
-    sb.lds_bytes = size_t(sb.ncls) * sb.zt * sb.mt * 64 * 16;
+    sb.lds_bytes = size_t(sb.ncls) * sb.zt * z_blocks(sb) * 64 * 16;
     sb.fuse_y = 0;
     dv.sb = sb;
     dv.blk = ((flags & DTST_PLAN_UNFUSED_BLOCK) == 0 && sb.kcp <= 32 &&
@@ -301,7 +306,7 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
     return o;
   };
   const size_t t_img = size_t(sc.th) * 4 * sc.ct * 64;
-  const size_t z_img = size_t(sc.ncls) * sc.zt * sc.mt * 64 * 4;
+  const size_t z_img = size_t(sc.ncls) * sc.zt * z_blocks(sc) * 64 * 4;
   im.t_fwd = take(t_img);
   im.t_fwd_adjoint_of_inverse = take(t_img);
   im.z_fwd = take(z_img);
@@ -313,7 +318,7 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   im.x_fwd = take(axis_img(dv.ax_f));
   im.y_inv = take(axis_img(dv.ay_i));
   im.x_inv = take(axis_img(dv.ax_i));
-  im.z_blk = take(size_t(dv.sb.ncls) * dv.sb.zt * dv.sb.mt * 64 * 4);
+  im.z_blk = take(size_t(dv.sb.ncls) * dv.sb.zt * z_blocks(dv.sb) * 64 * 4);
   im.t_blk = take(t_img);
   im.total = off;
 
@@ -367,15 +372,21 @@ void t_forward_image(const Derived& dv, bool adjoint_of_inverse, float* dst) {
 // With MT = 1 (KCP = 8) row r holds slot s = 2(r >> 2) + ((r >> 1) & 1),
 // Re for even r and Im for odd r, so that the products with Re B_z and Im B_z
 // of one slot land in accumulator registers 2j and 2j + 1 of one lane.
+// With t folded, blocks mt + mt' of the 3 mt / 2 blocks, mt' >= mt, hold
+// Re B + Im B of the rows of block mt' - mt (the first factor of the
+// three-product form).
 void z_forward_image(const Derived& dv, float* dst) {
   const StreamCfg& sc = dv.sc;
   const dtst_desc& d = dv.d;
+  const int nb = z_blocks(sc);
   for (int cl = 0; cl < sc.ncls; ++cl)
     for (int zt = 0; zt < sc.zt; ++zt)
-      for (int mt = 0; mt < sc.mt; ++mt)
+      for (int mb = 0; mb < nb; ++mb)
         for (int lane = 0; lane < 64; ++lane)
           for (int i = 0; i < 4; ++i) {
             const int m = lane & 15, g = lane >> 4;
+            const bool sum = mb >= sc.mt;  // t folded only
+            const int mt = sum ? mb - sc.mt : mb;
             const int row = 16 * mt + m;
             const int z = 16 * zt + 4 * g + i;
             const bool is_re = sc.mt == 1 ? (row & 1) == 0 : row < sc.kcp;
@@ -385,9 +396,9 @@ void z_forward_image(const Derived& dv, float* dst) {
             if (p < sc.kz && z < sc.zh) {
               double re, im;
               bval(d, 2, p, z, &re, &im);
-              v = is_re ? re : im;
+              v = sum ? re + im : (is_re ? re : im);
             }
-            dst[((((size_t)cl * sc.zt + zt) * sc.mt + mt) * 64 + lane) * 4 + i] = static_cast<float>(v);
+            dst[((((size_t)cl * sc.zt + zt) * nb + mb) * 64 + lane) * 4 + i] = static_cast<float>(v);
           }
 }
 
@@ -435,17 +446,34 @@ void t_inverse_image(const Derived& dv, bool is_inverse, float* dst) {
 // kz' < KCP and Im C_z[z][p] otherwise, C_z[z][p] = conj(B_z[p][z]).
 // With MT = 1 (KCP = 8) row kz' holds slot s = 2g + (i >> 1), Re for even i
 // and Im for odd i.
+// With t folded, the blocks hold the three-product operands of C_z = Cr +
+// i Ci (Cr = Re B, Ci = -Im B): blocks qh < mt / 2 Cr, the next mt / 2
+// blocks Ci - Cr, the last mt / 2 Cr + Ci, each for the K entries of block qh.
 void z_inverse_image(const Derived& dv, float* dst) {
   const StreamCfg& sc = dv.sc;
   const dtst_desc& d = dv.d;
+  const int nb = z_blocks(sc);
   for (int cl = 0; cl < sc.ncls; ++cl)
     for (int zt = 0; zt < sc.zt; ++zt)
-      for (int q = 0; q < sc.mt; ++q)
+      for (int q = 0; q < nb; ++q)
         for (int lane = 0; lane < 64; ++lane)
           for (int i = 0; i < 4; ++i) {
             const int m = lane & 15, g = lane >> 4;
-            const int kzp = 16 * q + 4 * g + i;
             const int z = 16 * zt + m;
+            if (sc.tf) {
+              const int half = sc.mt / 2, kind = q / half, qh = q % half;
+              const int p = (16 * qh + 4 * g + i) * sc.ncls + cl;
+              double v = 0.0;
+              if (p < sc.kz && z < sc.zh) {
+                double re, im;
+                bval(d, 2, p, z, &re, &im);
+                const double cr = re, ci = -im;
+                v = kind == 0 ? cr : (kind == 1 ? ci - cr : cr + ci);
+              }
+              dst[((((size_t)cl * sc.zt + zt) * nb + q) * 64 + lane) * 4 + i] = static_cast<float>(v);
+              continue;
+            }
+            const int kzp = 16 * q + 4 * g + i;
             const bool is_re = sc.mt == 1 ? (i & 1) == 0 : kzp < sc.kcp;
             const int s = sc.mt == 1 ? 2 * g + (i >> 1) : (is_re ? kzp : kzp - sc.kcp);
             const int p = s * sc.ncls + cl;
@@ -455,7 +483,7 @@ void z_inverse_image(const Derived& dv, float* dst) {
               bval(d, 2, p, z, &re, &im);
               v = is_re ? re : -im;
             }
-            dst[((((size_t)cl * sc.zt + zt) * sc.mt + q) * 64 + lane) * 4 + i] = static_cast<float>(v);
+            dst[((((size_t)cl * sc.zt + zt) * nb + q) * 64 + lane) * 4 + i] = static_cast<float>(v);
           }
 }
 
