@@ -120,14 +120,15 @@ __device__ __forceinline__ void t_part(const float (&xv)[NCLS][TH][4], const boo
 // step whose K index is z = 16zt + 4g + i.
 //
 // t-folded (TF) tiles take the complex product in three real products
-// instead of four: with B = Br + i Bi (row tiles mr and mr + MT/2 of the
-// image) and V = Vr + i Vi,
-//   k1 = (Br + Bi) Vr,   k2 = Br (Vi - Vr),   k3 = Bi (Vr + Vi),
+// instead of four: with B = Br + i Bi and V = Vr + i Vi,
+//   k1 = Br (Vr + Vi),   k2 = (Bi - Br) Vr,   k3 = (Br + Bi) Vi,
 //   Re BV = k1 - k3,     Im BV = k1 + k2,
-// accumulated in P[.][mr][0] (k1), P[.][mr][1] (k2) and P[.][mr + MT/2][0]
-// (k3).  The B operands are rearranged first so that lanes m < 8 carry the
-// even k_t = 2m and lanes m >= 8 the odd k_t = 2(m - 8) + 1 (Re and Im then
-// share a lane and the finish needs no exchange).
+// the three basis factors read from the image (blocks mr, mr + MT/2 and
+// mr + MT of a class and z tile), accumulated in P[.][mr][0] (k1),
+// P[.][mr][1] (k2) and P[.][mr + MT/2][0] (k3).  The B operands are
+// rearranged first so that lanes m < 8 carry the even k_t = 2m and lanes
+// m >= 8 the odd k_t = 2(m - 8) + 1 (Re and Im then share a lane and the
+// finish needs no exchange).
 template <int CT, int MT, int NCLS, int TF = 0>
 __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* lds, const StreamArgs& a, int zt,
                                        int lane, v4f (&P)[NCLS][MT][CT]) {
@@ -147,7 +148,7 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
   }
   if constexpr (TF) {
     static_assert(CT == 2 && MT % 2 == 0, "t-folded tiles: two k_t tiles, Re and Im row tiles");
-    // image blocks per (class, z tile): Re, Im and Re + Im row tiles
+    // image blocks per (class, z tile): Br, Bi - Br and Br + Bi row tiles
     constexpr int MTI = 3 * MT / 2;
     float4 Bs[NCLS][MT / 2];
 #pragma unroll
@@ -166,9 +167,9 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
         // lane m - 8 of tile 1 (banks 2, 3), lanes m < 8 keep tile 0
         const float vi = ror8_into<0x3>(t1, t0);
         const float vr = ror8_into<0xC>(t0, t1);
-        G1[cl][i] = vr;
-        G2[cl][i] = vi - vr;
-        G3[cl][i] = vr + vi;
+        G1[cl][i] = vr + vi;
+        G2[cl][i] = vr;
+        G3[cl][i] = vi;
       }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -176,10 +177,10 @@ __device__ __forceinline__ void z_part(const v4f (&V)[NCLS][CT], const float4* l
       for (int cl = 0; cl < NCLS; ++cl)
 #pragma unroll
         for (int mr = 0; mr < MT / 2; ++mr) {
-          const float br = A[cl][mr][i], bi = A[cl][mr + MT / 2][i];
-          P[cl][mr][0] = mfma(Bs[cl][mr][i], G1[cl][i], P[cl][mr][0]);
-          P[cl][mr][1] = mfma(br, G2[cl][i], P[cl][mr][1]);
-          P[cl][mr + MT / 2][0] = mfma(bi, G3[cl][i], P[cl][mr + MT / 2][0]);
+          // A[.][mr] = Br, A[.][mr + MT/2] = Bi - Br, Bs = Br + Bi
+          P[cl][mr][0] = mfma(A[cl][mr][i], G1[cl][i], P[cl][mr][0]);
+          P[cl][mr][1] = mfma(A[cl][mr + MT / 2][i], G2[cl][i], P[cl][mr][1]);
+          P[cl][mr + MT / 2][0] = mfma(Bs[cl][mr][i], G3[cl][i], P[cl][mr + MT / 2][0]);
         }
     return;
   }

@@ -372,9 +372,9 @@ void t_forward_image(const Derived& dv, bool adjoint_of_inverse, float* dst) {
 // With MT = 1 (KCP = 8) row r holds slot s = 2(r >> 2) + ((r >> 1) & 1),
 // Re for even r and Im for odd r, so that the products with Re B_z and Im B_z
 // of one slot land in accumulator registers 2j and 2j + 1 of one lane.
-// With t folded, blocks mt + mt' of the 3 mt / 2 blocks, mt' >= mt, hold
-// Re B + Im B of the rows of block mt' - mt (the first factor of the
-// three-product form).
+// With t folded, the blocks hold the three-product operands of B = Br +
+// i Bi: blocks mr < mt / 2 Br, the next mt / 2 blocks Bi - Br, the last
+// mt / 2 Br + Bi, each for the rows (slots) of block mr.
 void z_forward_image(const Derived& dv, float* dst) {
   const StreamCfg& sc = dv.sc;
   const dtst_desc& d = dv.d;
@@ -385,18 +385,26 @@ void z_forward_image(const Derived& dv, float* dst) {
         for (int lane = 0; lane < 64; ++lane)
           for (int i = 0; i < 4; ++i) {
             const int m = lane & 15, g = lane >> 4;
-            const bool sum = mb >= sc.mt;  // t folded only
-            const int mt = sum ? mb - sc.mt : mb;
-            const int row = 16 * mt + m;
             const int z = 16 * zt + 4 * g + i;
-            const bool is_re = sc.mt == 1 ? (row & 1) == 0 : row < sc.kcp;
-            const int s = sc.mt == 1 ? 2 * (row >> 2) + ((row >> 1) & 1) : (is_re ? row : row - sc.kcp);
-            const int p = s * sc.ncls + cl;
             double v = 0.0;
-            if (p < sc.kz && z < sc.zh) {
-              double re, im;
-              bval(d, 2, p, z, &re, &im);
-              v = sum ? re + im : (is_re ? re : im);
+            if (sc.tf) {
+              const int half = sc.mt / 2, kind = mb / half, mr = mb % half;
+              const int p = (16 * mr + m) * sc.ncls + cl;
+              if (p < sc.kz && z < sc.zh) {
+                double re, im;
+                bval(d, 2, p, z, &re, &im);
+                v = kind == 0 ? re : (kind == 1 ? im - re : re + im);
+              }
+            } else {
+              const int row = 16 * mb + m;
+              const bool is_re = sc.mt == 1 ? (row & 1) == 0 : row < sc.kcp;
+              const int s = sc.mt == 1 ? 2 * (row >> 2) + ((row >> 1) & 1) : (is_re ? row : row - sc.kcp);
+              const int p = s * sc.ncls + cl;
+              if (p < sc.kz && z < sc.zh) {
+                double re, im;
+                bval(d, 2, p, z, &re, &im);
+                v = is_re ? re : im;
+              }
             }
             dst[((((size_t)cl * sc.zt + zt) * nb + mb) * 64 + lane) * 4 + i] = static_cast<float>(v);
           }
