@@ -247,10 +247,21 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   const int nt = a.nt;
   const int cpr = a.zt * NCLS;  // chunks per row
 
+  // Channel stride of x and y (floats).
+  const int64_t cs = ba.xy * row_len;
+
   // Chunk position: row, z tile, class; chunks of a row run z tile by z tile.
+  // xb, yb: float offsets of channel 0 of the row (b, x, y) in x and y (rows
+  // past the end use the last row, whose x the loads past the end re-read).
   struct Cur {
-    int64_t row;
+    int64_t row, xb, yb;
     int zt, hf;
+  };
+  auto at_row = [&](Cur& c) {
+    const int64_t rr = c.row < ba.rows ? c.row : ba.rows - 1;
+    const int64_t b = rr / ba.xy, rxy = rr - b * ba.xy;
+    c.xb = b * ba.ci * cs + rxy * row_len;
+    c.yb = b * ba.co * cs + rxy * row_len;
   };
   auto next = [&](Cur c) {
     if (++c.hf == NCLS) {
@@ -258,6 +269,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
       if (++c.zt == a.zt) {
         c.zt = 0;
         c.row += gridDim.x;
+        at_row(c);
       }
     }
     return c;
@@ -268,34 +280,37 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   // and whether the points exist (a wave past the chunk's groups, or a z row
   // past a ragged last z tile).
   struct Grp {
-    int64_t off;
+    int off;
     int loff;
     bool ok;
   };
+  const int gpo = w * 64 + 4 * m;
+  const int gzr = gpo / nt, gt = gpo - gzr * nt;  // z row and t of the lane's points in a chunk
+  const bool gok = w < ba.groups;
+  const int gloff = gok ? yoff(gzr, gt, nt) : 0;
   auto group = [&](const Cur& c) {
     Grp q;
-    const int po = w * 64 + 4 * m;
-    const int zr = po / nt, t = po - zr * nt;
-    const int zl = c.zt * 16 + zr;
-    const bool gok = w < ba.groups;
+    const int zl = c.zt * 16 + gzr;
     q.ok = gok && zl < a.zh;
-    q.off = q.ok ? int64_t(zl + c.hf * a.zh) * nt + t : 0;
-    q.loff = gok ? yoff(zr, t, nt) : 0;
+    q.off = q.ok ? (zl + c.hf * a.zh) * nt + gt : 0;
+    q.loff = gloff;
     return q;
   };
+  // per-lane channel offsets: input channel 4s + g of x, output channel
+  // 16ot + 4g + r of y (the rest is uniform)
+  const int64_t gcs_x = g * cs, gcs_y = 4 * g * cs;
 
   // x of this wave's group, XD chunks ahead (unconditional loads: lanes of
   // missing points read the row start, input channels past C_in read the
   // last one; both are multiplied by zero weights or not stored).
   float4 xv[XD][KI];
   auto load_x = [&](int k, const Cur& c) __attribute__((always_inline)) {
-    const int64_t rr = c.row < ba.rows ? c.row : ba.rows - 1;
-    const int64_t b = rr / ba.xy, rxy = rr - b * ba.xy;
     const Grp q = group(c);
+    const float* xr = x + c.xb + q.off;
 #pragma unroll
     for (int s = 0; s < KI; ++s) {
-      const int i = 4 * s + g < ba.ci ? 4 * s + g : ba.ci - 1;
-      xv[k][s] = *reinterpret_cast<const float4*>(x + ((b * ba.ci + i) * ba.xy + rxy) * row_len + q.off);
+      const int64_t co = 4 * s + g < ba.ci ? 4 * s * cs + gcs_x : (ba.ci - 1) * cs;
+      xv[k][s] = *reinterpret_cast<const float4*>(xr + co);
     }
   };
   // The spectrum of row r (every output channel) into the LDS buffer: the
@@ -386,14 +401,14 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
         C[ot][3] = mfma(wa[ot][s], b3, C[ot][3]);
       }
     }
-    const int64_t b = c.row / ba.xy, rxy = c.row - b * ba.xy;
+    float* yr = y + c.yb + gcs_y + q.off;
 #pragma unroll
     for (int ot = 0; ot < OT; ++ot)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int o = 16 * ot + 4 * g + r;
         if (q.ok && o < ba.co) {
-          float* dst = y + ((b * ba.co + o) * ba.xy + rxy) * row_len + q.off;
+          float* dst = yr + (16 * ot + r) * cs;
           // ordinary (cached) stores: measured faster here than streaming ones
           *reinterpret_cast<v4f*>(dst) =
               v4f{gelu_as(C[ot][0][r]), gelu_as(C[ot][1][r]), gelu_as(C[ot][2][r]), gelu_as(C[ot][3][r])};
@@ -409,7 +424,8 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   // step whose phase 1 is a row's last chunk then moves the next row's
   // spectrum into LDS (the row's last reader of it is the phase 1 of its last
   // z tile's first chunk).
-  Cur c1 = Cur{static_cast<int64_t>(blockIdx.x), 0, 0};  // phase 1
+  Cur c1 = Cur{static_cast<int64_t>(blockIdx.x), 0, 0, 0, 0};  // phase 1
+  at_row(c1);
   Cur c2 = c1;                                             // phase 2 (valid from step 1 on)
   Cur cx = c1;                                             // next x to load
   auto step = [&](auto sc, bool has2) __attribute__((always_inline)) {
