@@ -448,6 +448,41 @@ def test_inverse_block(name, unfused):
     plan.close()
 
 
+@pytest.mark.parametrize("name", ["fold", "dv20_tfold"])
+def test_inverse_block_gelu_range(name):
+    """The fused kernel's GELU over a wide range of arguments: a zero
+    spectrum and W = I give y = GELU(x) exactly, with x swept over
+    [-40, 40] (both tails, where the exponential underflows, and the region
+    around zero).  The kernel's erf approximation is within 1.5e-7 of erf
+    (Abramowitz & Stegun 7.1.26), i.e. Phi within 7.5e-8; the fp32 evaluation
+    of q = Phi(-|x|) <= 1/2 (reciprocal, exponential, five FMAs, about ten
+    roundings) adds at most 1e-6 relative to q; so |y - GELU(x)| <=
+    (7.5e-8 + 5e-7) |x| plus one rounding of the result."""
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    spec, fusable = INVERSE_BLOCK_CASES[name]
+    n_global, n_local, off, kmax, kt, B, _, _ = spec
+    g = geometry(n_global, n_local, off, kmax, kt, B, 4, 4)
+    say(f"[inverse block gelu range {name}] n_local={g.n_local} kt={g.kt}")
+    plan = D.Plan(desc_of(g))
+    assert plan.block_fused == 1
+    yh = np.zeros((g.batch, g.c_out) + g.K, dtype=np.complex64)
+    n = int(np.prod((g.batch, g.c_in) + g.n_local))
+    v = np.linspace(-40.0, 40.0, n)
+    v[: n // 2] = np.sign(v[: n // 2]) * np.abs(v[: n // 2]) ** 3 / 1600.0  # dense around zero too
+    x = np.random.default_rng(143).permutation(v).astype(np.float32).reshape((g.batch, g.c_in) + g.n_local)
+    wb = np.eye(g.c_out, g.c_in, dtype=np.float32)
+    Y = Guarded(torch, plan.spatial_shape(g.c_out), torch.float32)
+    plan.inverse_block(dev(torch, yh), dev(torch, x), dev(torch, wb), Y.t)
+    torch.cuda.synchronize()
+    ref = O.gelu(x.astype(np.float64))
+    err = np.abs(np_of(Y.t).astype(np.float64) - ref)
+    tol = 5.75e-7 * np.abs(x) + 6e-8 * np.abs(ref) + 1e-30
+    assert np.all(err <= tol), float(np.max(err / tol))
+    assert Y.guards_intact()
+    plan.close()
+
+
 def test_inverse_block_workspace_too_small():
     """A workspace below dtst_plan_block_info's size is rejected before any
     launch (the fused kernel also needs the y-expanded intermediate)."""
