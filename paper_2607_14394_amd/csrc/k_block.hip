@@ -12,7 +12,9 @@
 // consecutive points of one batch entry (16-byte accesses), reads their C_in
 // input channels once per chunk of output channels (C_out rounded up to a
 // multiple of 4 when that is at most 16, else chunks of 12 or 16), and reads
-// w (and the bias) from LDS (the same entry for every lane).
+// w (and the bias) from LDS (the same entry for every lane).  GELU is the
+// branch-free Abramowitz & Stegun 7.1.26 form of gelu_as.h (the library
+// erff took about three times as many vector instructions).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -23,9 +25,7 @@ namespace dtst {
 namespace {
 
 
-__device__ __forceinline__ float gelu(float v) {
-  return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
-}
+#include "gelu_as.h"
 
 // ADDY: the accumulators start from y (block epilogue), else from the bias
 // (zero without one).  ACT: 1 applies GELU, 0 none.  OC: output channels per
@@ -98,7 +98,7 @@ pointwise_kernel(const float* __restrict__ x, const float* __restrict__ w, const
         float* yp = yb + int64_t(o0 + oo) * V;
         float r[P];
 #pragma unroll
-        for (int p = 0; p < P; ++p) r[p] = ACT ? gelu(acc[oo][p]) : acc[oo][p];
+        for (int p = 0; p < P; ++p) r[p] = ACT ? gelu_as(acc[oo][p]) : acc[oo][p];
         if constexpr (VEC) {
           *reinterpret_cast<float4*>(yp) = make_float4(r[0], r[1], r[2], r[3]);
         } else {
@@ -143,11 +143,13 @@ int launch_pw(const float* x, const float* w, const float* bias, float* y, int64
   // fewer unused outputs (a single wider pass held more registers and fewer
   // waves, and measured slower at C_out = 20).
   const int64_t waste12 = (co + 11) / 12 * 12 - co, waste16 = (co + 15) / 16 * 16 - co;
-  switch (co <= 16 ? (co + 3) / 4 : (waste12 < waste16 ? 3 : 4)) {
+  const int pick = co <= 16 ? int((co + 3) / 4) : (waste12 < waste16 ? 3 : 4);
+  switch (pick) {
     case 1: return launch_pw_oc<ADDY, ACT, 4>(x, w, bias, y, B, ci, co, V, stream);
     case 2: return launch_pw_oc<ADDY, ACT, 8>(x, w, bias, y, B, ci, co, V, stream);
     case 3: return launch_pw_oc<ADDY, ACT, 12>(x, w, bias, y, B, ci, co, V, stream);
-    default: return launch_pw_oc<ADDY, ACT, 16>(x, w, bias, y, B, ci, co, V, stream);
+    case 4: return launch_pw_oc<ADDY, ACT, 16>(x, w, bias, y, B, ci, co, V, stream);
+    default: return launch_pw_oc<ADDY, ACT, 32>(x, w, bias, y, B, ci, co, V, stream);
   }
 }
 
