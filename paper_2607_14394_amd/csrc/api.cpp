@@ -316,8 +316,13 @@ dtst_status dtst_plan_ex(const dtst_desc* d, uint32_t flags, dtst_plan_t* out) {
     return fail(DTST_ERR_DEVICE, std::string("hipMemcpy of the basis tables: ") + hipGetErrorString(e));
   }
   int pe = dtst::prepare_stream(&p->dv.sc);
-  if (pe == hipSuccess && p->dv.blk)
-    pe = dtst::prepare_block_zt(p->dv.sb, p->dv.d.c_in, p->dv.d.c_out, &p->dv.grid_blk);
+  if (pe == hipSuccess && p->dv.blk &&
+      dtst::prepare_block_zt(p->dv.sb, p->dv.d.c_in, p->dv.d.c_out, &p->dv.grid_blk) != hipSuccess) {
+    // the device does not take the fused block kernel at this size: the
+    // plan keeps the two launches (dtst_plan_block_info reports it)
+    (void)hipGetLastError();
+    p->dv.blk = 0;
+  }
   if (pe != hipSuccess) {
     (void)hipFree(p->blob);
     delete p;

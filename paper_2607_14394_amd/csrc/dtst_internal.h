@@ -138,7 +138,7 @@ int launch_inv_zt(const StreamCfg& c, const void* in, float* y, int64_t rows,
 //   y[b,o,.] = GELU(w x[b,.,.] + zt-expansion of in[b,o,.]) over the
 // batch * nxy (b, x, y) rows; in is the y-expanded spectrum
 // (B, C_out, N_x, N_y, K_z, K_t), c its z + t configuration (Derived::sb).
-size_t block_zt_lds_bytes(const StreamCfg& c, int64_t co);
+size_t block_zt_lds_bytes(const StreamCfg& c, int64_t ci, int64_t co);
 bool block_zt_supported(const StreamCfg& c, int64_t ci, int64_t co);
 int prepare_block_zt(const StreamCfg& c, int64_t ci, int64_t co, int* grid);
 int launch_inv_zt_block(const StreamCfg& c, int grid_resident, const void* in, const float* x, const float* w,

@@ -173,22 +173,31 @@ __device__ __forceinline__ void texp_tfg(const v4f& Wr, const v4f& Wi, const flo
 }
 
 // KI: K steps of 4 input channels (C_in <= 4 KI); OT: tiles of 16 output
-// channels (C_out <= 16 OT); SPF: float4 of the row's spectrum per thread
-// (C_out K_z K_t <= 2 * 64 kBlkWaves SPF); XD: chunks of x loaded ahead.
+// channels per pass (C_out <= 16 OT OH); SPF: float4 of the row's spectrum
+// per thread (C_out K_z K_t <= 2 * 64 kBlkWaves SPF); XD: chunks of x loaded
+// ahead; OH: passes over the output channels per chunk.  With OH = 2 (C_out
+// up to 32) a pipeline unit is one half of a chunk's output channels (16 of
+// them), so the LDS buffers hold 16 channels: the two halves of a chunk run
+// in consecutive steps on the same x, which is loaded a chunk (two steps)
+// ahead into the buffer the previous chunk has released.
 //
 // The loop is software-pipelined: step c runs phase 2 of chunk c - 1 and
 // phase 1 of chunk c (they use different LDS buffers, so the wave's matrix
 // products of one overlap the vector work and the memory traffic of the
 // other), then one barrier.  Steps come in passes of four so that the
 // buffer, the fold class of phase 1 and the x buffer are compile-time indices.
-template <int CT, int TH, int MT, int NCLS, int TF, int KI, int OT, int SPF, int XD>
+template <int CT, int TH, int MT, int NCLS, int TF, int KI, int OT, int SPF, int XD, int OH>
 __global__ void __launch_bounds__(64 * kBlkWaves)
 inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, const float* __restrict__ wb,
                     float* __restrict__ y, const float* __restrict__ timg, const float4* __restrict__ zimg,
                     StreamArgs a, BlockArgs ba) {
   constexpr int NW = kBlkWaves;
-  // output channels per wave in phase 1 (the class bounds C_in and C_out by 4 KI)
+  // output channels per wave in phase 1 (the class bounds C_in and C_out by 4 KI),
+  // KCH of them per pass over the output channels
   constexpr int KC = (4 * KI + NW - 1) / NW;
+  constexpr int KCH = KC / OH;
+  static_assert(OH == 1 || (OH == 2 && OT == 1 && XD == 2 && 16 % NW == 0 && KCH * NW == 16),
+                "output halves of 16 channels, x two chunks in flight");
   static_assert(!TF || (CT == 2 && TH == 2), "t folding needs two k_t tiles and N_t = 32");
   static_assert(XD == 1 || XD == 2 || XD == 4, "x one, two or four chunks ahead");
   // LDS: the z image, the row's spectrum of every output channel, two
@@ -199,7 +208,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   const int n4 = ba.co * spec_len / 2;  // float4 of the row's spectrum
   float2* sbuf = reinterpret_cast<float2*>(lds + nimg);
   float* ybuf = reinterpret_cast<float*>(lds + nimg + n4);
-  const int bufsz = ba.co * ba.ostride;  // floats per buffer
+  const int bufsz = (OH == 1 ? ba.co : 16) * ba.ostride;  // floats per buffer
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int m = lane & 15, g = lane >> 4;
@@ -217,10 +226,11 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         ta[mt][ct][i] = (TF && mt >= TH / 2) ? 0.f : timg[((mt * CT + ct) * 4 + i) * 64 + lane];
-  // A operands of the bypass: w[o = 16ot + m][i = 4s + g], zero outside.
-  float wa[OT][KI];
+  // A operands of the bypass: w[o = 16ot + m][i = 4s + g], zero outside
+  // (row tiles of every pass).
+  float wa[OH * OT][KI];
 #pragma unroll
-  for (int ot = 0; ot < OT; ++ot)
+  for (int ot = 0; ot < OH * OT; ++ot)
 #pragma unroll
     for (int s = 0; s < KI; ++s) {
       const int o = 16 * ot + m, i = 4 * s + g;
@@ -239,7 +249,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   // past the end use the last row, whose x the loads past the end re-read).
   struct Cur {
     int64_t row, xb, yb;
-    int zt, hf;
+    int zt, hf, oh;
   };
   auto at_row = [&](Cur& c) {
     const int64_t rr = c.row < ba.rows ? c.row : ba.rows - 1;
@@ -247,7 +257,9 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     c.xb = b * ba.ci * cs + rxy * row_len;
     c.yb = b * ba.co * cs + rxy * row_len;
   };
-  auto next = [&](Cur c) {
+  // next chunk (output pass 0) and next unit (output pass, then chunk)
+  auto next_chunk = [&](Cur c) {
+    c.oh = 0;
     if (++c.hf == NCLS) {
       c.hf = 0;
       if (++c.zt == a.zt) {
@@ -257,6 +269,10 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
       }
     }
     return c;
+  };
+  auto next = [&](Cur c) {
+    if (++c.oh < OH) return c;
+    return next_chunk(c);
   };
 
   // This wave's 64-point group of a chunk: offset of the lane's 4 points
@@ -321,17 +337,19 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   v4f Wz[KC][NCLS][CT];              // unfolded t
   v4f Wzr[KC][NCLS], Wzi[KC][NCLS];  // t folded
 
-  // Phase 1 of chunk c into buffer PAR (its class HF is c.hf).
-  auto phase1 = [&](auto parc, auto hfc, const Cur& c) __attribute__((always_inline)) {
-    constexpr int PAR = decltype(parc)::value, HF = decltype(hfc)::value;
+  // Phase 1 of unit c (chunk class HF, output pass OHI) into buffer PAR:
+  // this wave's channels o = 16 OHI + w + NW k of the pass (o = w + NW k
+  // with one pass), at buffer channel o - 16 OHI.
+  auto phase1 = [&](auto parc, auto hfc, auto ohc, const Cur& c) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(parc)::value, HF = decltype(hfc)::value, OHI = decltype(ohc)::value;
     float* yb = ybuf + PAR * bufsz;
     if constexpr (TF) {
 #pragma unroll
-      for (int k = 0; k < KC; ++k) {
-        const int o = w + NW * k;
+      for (int k = 0; k < KCH; ++k) {
+        const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
         if (o < ba.co) {
-          if (HF == 0) zexp_tfg<MT, NCLS>(sbuf + o * spec_len, a, lds, c.zt, m, g, lane, Wzr[k], Wzi[k]);
-          texp_tfg<TH>(Wzr[k][HF], Wzi[k][HF], ta, yb + o * ba.ostride, m, g);
+          if (HF == 0) zexp_tfg<MT, NCLS>(sbuf + o * spec_len, a, lds, c.zt, m, g, lane, Wzr[kk], Wzi[kk]);
+          texp_tfg<TH>(Wzr[kk][HF], Wzi[kk][HF], ta, yb + ol * ba.ostride, m, g);
         }
       }
     } else {
@@ -342,22 +360,23 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
           for (int q = 0; q < MT; ++q) Bz[cl][q] = lds[((cl * a.zt + c.zt) * MT + q) * 64 + lane];
 #pragma unroll
-        for (int k = 0; k < KC; ++k) {
-          const int o = w + NW * k;
-          if (o < ba.co) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[k]);
+        for (int k = 0; k < KCH; ++k) {
+          const int kk = OHI * KCH + k, o = 16 * OHI + w + NW * k;
+          if (o < ba.co) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[kk]);
         }
       }
 #pragma unroll
-      for (int k = 0; k < KC; ++k) {
-        const int o = w + NW * k;
-        if (o < ba.co) texp_plain<CT, TH>(Wz[k][HF], ta, yb + o * ba.ostride, nt, m, g);
+      for (int k = 0; k < KCH; ++k) {
+        const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
+        if (o < ba.co) texp_plain<CT, TH>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
       }
     }
   };
 
-  // Phase 2 of chunk c from buffer PAR with x buffer XB.
-  auto phase2 = [&](auto parc, auto xbc, const Cur& c) __attribute__((always_inline)) {
-    constexpr int PAR = decltype(parc)::value, XB = decltype(xbc)::value;
+  // Phase 2 of unit c (output pass OHI: channels 16 (OHI OT + ot) + 4g + r,
+  // buffer channel 16 ot + 4g + r) from buffer PAR with x buffer XB.
+  auto phase2 = [&](auto parc, auto xbc, auto ohc, const Cur& c) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(parc)::value, XB = decltype(xbc)::value, OHI = decltype(ohc)::value;
     const float* yb = ybuf + PAR * bufsz;
     const Grp q = group(c);
     v4f C[OT][4];
@@ -365,8 +384,8 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     for (int ot = 0; ot < OT; ++ot)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int o = 16 * ot + 4 * g + r;
-        const float4 v = *reinterpret_cast<const float4*>(yb + (o < ba.co ? o : ba.co - 1) * ba.ostride + q.loff);
+        const int ol = 16 * ot + 4 * g + r, o = 16 * OHI * OT + ol;
+        const float4 v = *reinterpret_cast<const float4*>(yb + (o < ba.co ? ol : 0) * ba.ostride + q.loff);
         C[ot][0][r] = v.x;
         C[ot][1][r] = v.y;
         C[ot][2][r] = v.z;
@@ -379,10 +398,11 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
       const float b0 = iok ? xs.x : 0.f, b1 = iok ? xs.y : 0.f, b2 = iok ? xs.z : 0.f, b3 = iok ? xs.w : 0.f;
 #pragma unroll
       for (int ot = 0; ot < OT; ++ot) {
-        C[ot][0] = mfma(wa[ot][s], b0, C[ot][0]);
-        C[ot][1] = mfma(wa[ot][s], b1, C[ot][1]);
-        C[ot][2] = mfma(wa[ot][s], b2, C[ot][2]);
-        C[ot][3] = mfma(wa[ot][s], b3, C[ot][3]);
+        const float wv = wa[OHI * OT + ot][s];
+        C[ot][0] = mfma(wv, b0, C[ot][0]);
+        C[ot][1] = mfma(wv, b1, C[ot][1]);
+        C[ot][2] = mfma(wv, b2, C[ot][2]);
+        C[ot][3] = mfma(wv, b3, C[ot][3]);
       }
     }
     float* yr = y + c.yb + gcs_y + q.off;
@@ -390,9 +410,9 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     for (int ot = 0; ot < OT; ++ot)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int o = 16 * ot + 4 * g + r;
+        const int o = 16 * (OHI * OT + ot) + 4 * g + r;
         if (q.ok && o < ba.co) {
-          float* dst = yr + (16 * ot + r) * cs;
+          float* dst = yr + (16 * (OHI * OT + ot) + r) * cs;
           // ordinary (cached) stores: measured faster here than streaming ones
           *reinterpret_cast<v4f*>(dst) =
               v4f{gelu_as(C[ot][0][r]), gelu_as(C[ot][1][r]), gelu_as(C[ot][2][r]), gelu_as(C[ot][3][r])};
@@ -408,29 +428,46 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   // step whose phase 1 is a row's last chunk then moves the next row's
   // spectrum into LDS (the row's last reader of it is the phase 1 of its last
   // z tile's first chunk).
-  Cur c1 = Cur{static_cast<int64_t>(blockIdx.x), 0, 0, 0, 0};  // phase 1
+  Cur c1 = Cur{static_cast<int64_t>(blockIdx.x), 0, 0, 0, 0, 0};  // phase 1
   at_row(c1);
   Cur c2 = c1;                                             // phase 2 (valid from step 1 on)
   Cur cx = c1;                                             // next x to load
   auto step = [&](auto sc, bool has2) __attribute__((always_inline)) {
     constexpr int S4 = decltype(sc)::value;     // step index mod 4
     constexpr int PAR = S4 & 1;                 // buffer of phase 1; phase 2 reads 1 - PAR
-    constexpr int HF = NCLS == 2 ? PAR : 0;     // chunks alternate classes when z folds
-    constexpr int XB = (S4 + 3) % XD;           // x buffer of phase 2's chunk (step - 1)
+    // output pass of phase 1's unit and of phase 2's (the previous) unit
+    constexpr int OH1 = OH == 2 ? (S4 & 1) : 0, OH2 = OH == 2 ? 1 - OH1 : 0;
+    // class of phase 1's chunk: chunks alternate classes when z folds
+    constexpr int HF = NCLS == 2 ? (OH == 2 ? (S4 >> 1) & 1 : PAR) : 0;
+    // x buffer of phase 2's chunk: the previous step's chunk with one pass;
+    // with two passes unit u - 1 belongs to chunk (u - 1) / 2 (buffers by
+    // chunk parity: 1, 0, 0, 1 for S4 = 0..3), and the odd steps (phase 2
+    // on a chunk's first pass) load the next chunk into the other buffer,
+    // which the previous chunk released at the step before
+    constexpr int XB = OH == 2 ? ((S4 == 0 || S4 == 3) ? 1 : 0) : (S4 + 3) % XD;
+    constexpr int XL = OH == 2 ? 1 - XB : XB;
+    constexpr bool LOADS = OH == 1 || (S4 & 1) == 1;
     const bool has1 = c1.row < ba.rows;
     auto body = [&]() __attribute__((always_inline)) {
-      if (has2) phase2(std::integral_constant<int, 1 - PAR>{}, std::integral_constant<int, XB>{}, c2);
-      load_x(XB, cx);
-      cx = next(cx);
-      if (has1) phase1(std::integral_constant<int, PAR>{}, std::integral_constant<int, HF>{}, c1);
+      if (has2)
+        phase2(std::integral_constant<int, 1 - PAR>{}, std::integral_constant<int, XB>{},
+               std::integral_constant<int, OH2>{}, c2);
+      if constexpr (LOADS) {
+        load_x(XL, cx);
+        cx = next_chunk(cx);
+      }
+      if (has1)
+        phase1(std::integral_constant<int, PAR>{}, std::integral_constant<int, HF>{},
+               std::integral_constant<int, OH1>{}, c1);
     };
-    // (c1.hf == HF by construction: with z folded, only odd steps end a row)
-    if (has1 && HF == NCLS - 1 && c1.zt == a.zt - 1) {
+    // (c1.hf == HF and c1.oh == OH1 by construction: only the steps whose
+    // unit is the last class and pass of a chunk can end a row)
+    if (has1 && HF == NCLS - 1 && OH1 == OH - 1 && c1.zt == a.zt - 1) {
       // the spectrum loads go out before the step's work, the LDS stores after it
       v4f sp[SPF];
       spec_load(c1.row + gridDim.x, sp);
       body();
-      if constexpr (NCLS == 1) __syncthreads();  // this phase 1 read the spectrum buffer
+      if constexpr (NCLS == 1) __syncthreads();  // this phase 1 read the spectrum buffer (z expansion)
       spec_store(sp);
     } else {
       body();
@@ -449,7 +486,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
   for (int k = 0; k < XD - 1; ++k) {
     load_x(k, cx);
-    cx = next(cx);
+    cx = next_chunk(cx);
   }
   __syncthreads();
   step(std::integral_constant<int, 0>{}, false);
@@ -467,9 +504,9 @@ typedef void (*blk_fn)(const float2*, const float*, const float*, float*, const 
 
 template <int CT, int TH, int MT, int NCLS, int TF>
 blk_fn pick_kio(int kio) {
-  if (kio == 0) return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 4, 1, 4, 2>;
-  if (kio == 1) return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 5, 2, 5, 1>;
-  return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 8, 2, 8, 1>;
+  if (kio == 0) return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 4, 1, 4, 2, 1>;
+  if (kio == 1) return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 5, 2, 5, 1, 1>;
+  return inv_zt_block_kernel<CT, TH, MT, NCLS, TF, 8, 1, 8, 2, 2>;
 }
 
 // float4 of a row's spectrum per thread for each (KI, OT) class.
@@ -495,9 +532,11 @@ blk_fn pick_blk(const StreamCfg& c, int kio) {
 
 }  // namespace
 
-size_t block_zt_lds_bytes(const StreamCfg& c, int64_t co) {
+size_t block_zt_lds_bytes(const StreamCfg& c, int64_t ci, int64_t co) {
+  // chunk buffers of 16 channels where the instance makes two output passes
+  const int64_t cb = kio_of(ci, co) == 2 ? 16 : co;
   return size_t(c.ncls) * c.zt * (c.tf ? 3 * c.mt / 2 : c.mt) * 64 * 16 + size_t(co) * c.kz * c.kt * 8 +
-         2 * size_t(co) * 16 * c.nt * sizeof(float);
+         2 * size_t(cb) * 16 * c.nt * sizeof(float);
 }
 
 bool block_zt_supported(const StreamCfg& c, int64_t ci, int64_t co) {
@@ -505,12 +544,12 @@ bool block_zt_supported(const StreamCfg& c, int64_t ci, int64_t co) {
         ci <= 32 && co <= 32 && (c.kz * c.kt) % 2 == 0))
     return false;
   const int64_t n4 = co * c.kz * c.kt / 2;
-  return n4 <= int64_t(64) * kBlkWaves * kSpf[kio_of(ci, co)] && block_zt_lds_bytes(c, co) <= 160 * 1024;
+  return n4 <= int64_t(64) * kBlkWaves * kSpf[kio_of(ci, co)] && block_zt_lds_bytes(c, ci, co) <= 160 * 1024;
 }
 
 int prepare_block_zt(const StreamCfg& c, int64_t ci, int64_t co, int* grid) {
   const void* fn = reinterpret_cast<const void*>(pick_blk(c, kio_of(ci, co)));
-  const size_t lds = block_zt_lds_bytes(c, co);
+  const size_t lds = block_zt_lds_bytes(c, ci, co);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
   if (e != hipSuccess) return e;
   int dev = 0, cus = 0, per_cu = 0;
@@ -548,7 +587,7 @@ int launch_inv_zt_block(const StreamCfg& c, int grid_resident, const void* in, c
   if (ba.groups > kBlkWaves) return hipErrorInvalidConfiguration;
   const int64_t grid = rows < grid_resident ? rows : grid_resident;
   hipLaunchKernelGGL(pick_blk(c, kio_of(ci, co)), dim3(static_cast<unsigned>(grid)), dim3(64 * kBlkWaves),
-                     block_zt_lds_bytes(c, co), static_cast<hipStream_t>(stream), static_cast<const float2*>(in), x,
+                     block_zt_lds_bytes(c, ci, co), static_cast<hipStream_t>(stream), static_cast<const float2*>(in), x,
                      w, y, timg, reinterpret_cast<const float4*>(zimg), a, ba);
   return hipGetLastError();
 }

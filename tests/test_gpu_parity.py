@@ -414,6 +414,9 @@ INVERSE_BLOCK_CASES = {
     "ct2_th1": (((4, 6, 16, 16), (4, 6, 16, 16), (0, 0, 0, 0), (2, 2, 4), 9, 1, 3, 5), True),
     "ct2_t_shard": (((4, 4, 16, 64), (4, 4, 16, 32), (0, 0, 0, 32), (1, 1, 4), 12, 1, 6, 4), True),
     "c32": (((4, 4, 32, 16), (4, 4, 32, 16), (0, 0, 0, 0), (1, 1, 4), 3, 1, 32, 24), True),
+    # more than 20 channels: two passes of 16 output channels per chunk (t folded, one z class)
+    "c28_tfold": (((8, 4, 32, 32), (8, 4, 32, 32), (0, 0, 0, 0), (2, 2, 8), 16, 1, 20, 28), True),
+    "c32_z_shard": (((4, 4, 64, 16), (4, 4, 32, 16), (0, 0, 16, 0), (1, 1, 4), 3, 2, 32, 32), True),
     "ragged_z": (((4, 4, 40, 8), (4, 4, 40, 8), (0, 0, 0, 0), (1, 1, 6), 2, 1, 4, 4), True),
     "nt12_ragged": (((4, 4, 24, 12), (4, 4, 24, 12), (0, 0, 0, 0), (2, 2, 5), 4, 1, 3, 2), True),
     "nt20": (((4, 6, 32, 20), (4, 6, 32, 20), (0, 0, 0, 0), (2, 2, 6), 7, 1, 5, 5), True),
