@@ -156,7 +156,7 @@ def _block_zt_work(g):
     """The fused inverse z + t expansion and block epilogue: reads the
     y-expanded spectrum (B, C_out, N_x, N_y, K_z, K_t) and the block input x,
     writes y once.  Executed flops: the z expansion with z folded in two
-    classes where the shard holds the whole even N_z (three real products per
+    classes where that saves padded slots (three real products per
     complex one when t folds), the t expansion (halved when t folds), and the
     bypass (C_out x C_in per point) on the matrix cores."""
     B, ci, co = g["batch"], g["c_in"], g["c_out"]
@@ -164,7 +164,7 @@ def _block_zt_work(g):
     Kz, Kt = 2 * g["kmax"][2], g["kt"]
     V = _vol(g)
     sf = stage_flops(g, co)
-    zc = 2 if _folded(g, 2) else 1
+    zc = _block_z_classes(g)
     tc = _t_classes(g)
     byp = 2 * B * V * ci * co
     return dict(bytes=B * co * Nx * Ny * Kz * Kt * 8 + B * (ci + co) * V * 4, flops=sf["t"] + sf["z"] + byp,
@@ -203,16 +203,39 @@ def _t_classes(g):
 
 
 def _z_classes(g):
-    """z mode classes of the streaming kernels: 4 when z also splits by
-    k mod 4 (N_z % 4 == 0, even k_max, and at most 16 modes per class with
-    k_t > 8 or at most 8 with k_t <= 8), 2 when it only folds in halves, else
-    1; the z MFMA work divides by it."""
+    """z mode classes of the streaming kernels.  z folds only where the shard
+    holds the whole even N_z; the class count is the one with the fewest
+    padded slots per class (the z products per row are those slots x N_z for
+    any count), the smaller one on a tie: 4 (k mod 4: N_z % 4 == 0, even
+    k_max, and at most 16 modes per class with k_t > 8 or 8 with k_t <= 8),
+    2 (parity) or 1.  The z MFMA work divides by it."""
     if not _folded(g, 2):
         return 1
     Kz = 2 * g["kmax"][2]
-    if g["n_global"][2] % 4 == 0 and g["kmax"][2] % 2 == 0 and Kz <= (64 if g["kt"] > 8 else 32):
-        return 4
-    return 2
+    ct = 2 if g["kt"] > 8 else 1
+
+    def padded(n):
+        if n == 4 and ct == 1:
+            return 8
+        k = -(-(-(-Kz // n)) // 16) * 16
+        return 64 if k == 48 else k
+
+    n = 1
+    if padded(2) < padded(n):
+        n = 2
+    four = g["n_global"][2] % 4 == 0 and g["kmax"][2] % 2 == 0 and Kz <= (64 if ct == 2 else 32)
+    if four and padded(4) < padded(n):
+        n = 4
+    return n
+
+
+def _block_z_classes(g):
+    """z classes of the fused inverse + block epilogue kernel: 2 where z folds
+    and the parity classes pad to fewer slots than one class, else 1."""
+    if not _folded(g, 2):
+        return 1
+    Kz = 2 * g["kmax"][2]
+    return 2 if -(-(-(-Kz // 2)) // 16) < -(-Kz // 16) else 1
 
 
 def _sha(path):

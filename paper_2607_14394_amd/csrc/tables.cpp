@@ -150,14 +150,23 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   // the kernels fit their registers only at that size), or one column tile
   // (ct == 1, the factors +-i trade lanes m and m ^ 8) with at most 8 modes
   // per class, whose Re and Im rows then share one 16-row tile (mt == 1).
+  // The z products per row are (padded slots per class) x N_z whatever the
+  // class count, so the count taken is the one with the fewest padded slots
+  // per class, and of those the smallest (fewer class sums and differences):
+  // with at most 16 modes every count pads to one 16-row tile.
   const bool fold = d->n_local[2] == d->n_global[2] && d->n_global[2] % 2 == 0;
   const bool fold4_base = fold && d->n_global[2] % 4 == 0 && d->kmax[2] % 2 == 0;
   const bool fold4_ct2 = fold4_base && sc.ct == 2 && sc.kz <= 4 * 16;
   const bool fold4_ct1 = fold4_base && sc.ct == 1 && sc.kz <= 4 * 8;
-  sc.ncls = (fold4_ct2 || fold4_ct1) ? 4 : (fold ? 2 : 1);
-  const int slots = static_cast<int>(ceil_div(sc.kz, sc.ncls));
-  int kcp = fold4_ct1 ? 8 : static_cast<int>(round_up(slots, 16));
-  if (kcp == 48) kcp = 64;
+  auto padded = [&](int n) {
+    if (n == 4 && sc.ct == 1) return 8;
+    int k = static_cast<int>(round_up(ceil_div(sc.kz, n), 16));
+    return k == 48 ? 64 : k;
+  };
+  sc.ncls = 1;
+  if (fold && padded(2) < padded(sc.ncls)) sc.ncls = 2;
+  if ((fold4_ct2 || fold4_ct1) && padded(4) < padded(sc.ncls)) sc.ncls = 4;
+  int kcp = padded(sc.ncls);
   if (kcp > 64) {
     *err = "more than 64 retained z modes per parity class is not covered";
     return DTST_ERR_UNSUPPORTED;
@@ -280,7 +289,7 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   // DTST_PLAN_UNFUSED_BLOCK keeps the inverse and the epilogue separate.
   {
     StreamCfg sb = sc;
-    sb.ncls = fold ? 2 : 1;
+    sb.ncls = fold && round_up(ceil_div(sc.kz, 2), 16) < round_up(sc.kz, 16) ? 2 : 1;
     sb.kcp = static_cast<int>(round_up(ceil_div(sc.kz, sb.ncls), 16));
     sb.mt = sb.kcp / 8;
     sb.zh = sb.nz / sb.ncls;

@@ -40,6 +40,10 @@ CASES = {
     "radix4_ragged": ((6, 8, 40, 24), (6, 8, 40, 24), (0, 0, 0, 0), (2, 3, 6), 10, 2, 2, 3),
     "radix4_scalar_t": ((4, 6, 24, 21), (4, 6, 24, 21), (0, 0, 0, 0), (1, 2, 4), 11, 1, 1, 2),
     "radix4_full_tiles": ((4, 4, 64, 32), (4, 4, 64, 32), (0, 0, 0, 0), (2, 2, 32), 16, 1, 2, 2),
+    # (with at most 16 z modes every class count pads to one tile, so the kernels take one class;
+    # 17-64 modes keep four): ragged quarter N_z / 4 = 22 with masked 16-byte t, and scalar t
+    "radix4_kz40_ragged": ((4, 6, 88, 24), (4, 6, 88, 24), (0, 0, 0, 0), (1, 2, 20), 10, 1, 2, 2),
+    "radix4_kz36_scalar_t": ((4, 4, 72, 21), (4, 4, 72, 21), (0, 0, 0, 0), (1, 1, 18), 11, 1, 1, 2),
     # odd k_max(z) with N_z % 4 == 0 and k_t > 8 keeps the two-class fold
     "fold2_odd_kz_kt9": ((4, 4, 24, 16), (4, 4, 24, 16), (0, 0, 0, 0), (1, 1, 5), 9, 1, 2, 1),
     # t fold (k_t > 8, whole N_t = 32): two z classes with a ragged z tile and an odd k_t count,
