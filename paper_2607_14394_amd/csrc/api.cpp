@@ -573,7 +573,7 @@ dtst_status dtst_inverse_block(dtst_plan_t p, const void* yhat, const float* x, 
   if (e != hipSuccess) return device_status(e, "x expansion launch");
   const int64_t planes = B * co * dv.d.n_local[0];
   e = timed(K_AXIS_INV_Y, stream,
-            [&] { return dtst::launch_axis(dv.ay_i, planes, w2, w1, p->blob + dv.img.y_inv, 0, stream); });
+            [&] { return dtst::launch_axis(dv.ay_b, planes, w2, w1, p->blob + dv.img.y_blk, 0, stream); });
   if (e != hipSuccess) return device_status(e, "y expansion launch");
   e = timed(K_INV_ZT_BLOCK, stream, [&] {
     return dtst::launch_inv_zt_block(dv.sb, dv.grid_blk, w1, x, w_bypass, y, B,

@@ -72,6 +72,10 @@ struct AxisCfg {
   int JQ = 0;      // 16-wide K steps
   int ktiles = 0;  // 16-row k tiles
   int kth = 0;     // fold 1: k tiles per parity class
+  // parts per image entry: 3 for the axis kernels (Br, Bi - Br, Br + Bi, the
+  // factors of their three-product form), 2 (Re, Im) for the y images of the
+  // fused stream kernels
+  int parts = 3;
 };
 
 // Float offsets of each kernel-ready image inside the plan's device blob.
@@ -82,6 +86,7 @@ struct Images {
   size_t z_inv = 0;                                // streaming inverse, LDS image
   size_t y_fwd = 0, x_fwd = 0, y_inv = 0, x_inv = 0;  // axis images
   size_t z_blk = 0, t_blk = 0;                         // fused inverse + block epilogue
+  size_t y_blk = 0;  // y expansion of dtst_inverse_block (y_inv unless the plan fuses y)
   size_t total = 0;
 };
 
@@ -91,6 +96,7 @@ struct Derived {
   int64_t M = 0;
   StreamCfg sc;
   AxisCfg ay_f, ax_f, ax_i, ay_i;  // per-channel shapes; nb is per (b, c) below
+  AxisCfg ay_b;                    // the inverse y of dtst_inverse_block's separate y launch
   size_t ws_bytes = 0;
   size_t w1_bytes = 0;  // workspace offset of W2 (0 with the fused y: no W1)
   Images img;

@@ -8,10 +8,15 @@
 // with conj(B)^T (Sec. V-A Eq. dtst_inverse, reverse order).  The complex
 // product B X, with the basis split into (Re, Im) parts Br, Bi, takes three
 // real MFMA products instead of four:
-//   k1 = (Br + Bi) Xr,   k2 = Br (Xi - Xr),   k3 = Bi (Xr + Xi),
+//   k1 = Br (Xr + Xi),   k2 = (Bi - Br) Xr,   k3 = (Br + Bi) Xi,
 //   Re = k1 - k3,        Im = k1 + k2,
-// with Br + Bi formed per basis tile and Xi - Xr, Xr + Xi once per input
-// load; every accumulator is lane-local, and so is the epilogue.
+// with the three basis factors stored in the image (parts 0, 1, 2 of an
+// entry) and Xr + Xi formed once per input value; every accumulator is
+// lane-local, and so is the epilogue.  The expand kernel (below), which keeps
+// its inputs for a whole work item, takes the mirror form k1 = (Br + Bi) Xr,
+// k2 = Br (Xi - Xr), k3 = Bi (Xr + Xi) on a two-part image (Re, Im): its
+// image is staged per workgroup, where a third part costs more than one
+// add per basis value.
 //
 // Folding (FOLD != 0): when the spatial side of the contraction covers the
 // whole even global extent N, exp(-2 pi i k (n + N/2) / N) = (-1)^k
@@ -226,7 +231,7 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
     // the previous step, after the input rows of step q + 1 went out, so that
     // waiting for them (the memory counter retires loads in order) never
     // waits for that input prefetch.
-    float4 bre[KT][NE], bim[KT][NE];
+    float4 b0[KT][NE], b1[KT][NE], b2[KT][NE];
     auto load_basis = [&](int q) {
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk) {
@@ -234,9 +239,10 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
           // image: FOLD 2 -> [kt][q][class][part], else [kt][q][part]
-          const float4* ip = img + ((int64_t(kt) * a.JQ + q) * NE + e) * 2 * 64 + lane;
-          bre[kk][e] = ip[0];
-          bim[kk][e] = ip[64];
+          const float4* ip = img + ((int64_t(kt) * a.JQ + q) * NE + e) * 3 * 64 + lane;
+          b0[kk][e] = ip[0];
+          b1[kk][e] = ip[64];
+          b2[kk][e] = ip[128];
         }
       }
     };
@@ -263,25 +269,23 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
       if (q + 1 < a.JQ) load(q + 1, vn, okn);
 #pragma unroll
       for (int kk = 0; kk < KT; ++kk) {  // tile kk holds class kk
-        const float4 br = bre[kk][0], bi = bim[kk][0];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float r = br[i], im = bi[i], rpi = br[i] + bi[i];
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) {
             const float2 x = sc[kk & 3][nt][i];
-            acc1[0][kk][nt] = mfma(rpi, x.x, acc1[0][kk][nt]);
-            acc2[0][kk][nt] = mfma(r, x.y - x.x, acc2[0][kk][nt]);
-            acc3[0][kk][nt] = mfma(im, x.x + x.y, acc3[0][kk][nt]);
+            acc1[0][kk][nt] = mfma(b0[kk][0][i], x.x + x.y, acc1[0][kk][nt]);
+            acc2[0][kk][nt] = mfma(b1[kk][0][i], x.x, acc2[0][kk][nt]);
+            acc3[0][kk][nt] = mfma(b2[kk][0][i], x.y, acc3[0][kk][nt]);
           }
         }
       }
       if (q + 1 < a.JQ) load_basis(q + 1);
     }
     for (int q = 0; q < a.JQ && FOLD != 3; ++q) {
-      // B operands: V[c or fold class][nt][i] as (Xr, Xi - Xr, Xr + Xi)
+      // B operands: V[c or fold class][nt][i] as (Xr + Xi, Xr, Xi)
       constexpr int NV = FOLD == 0 ? 1 : 2;
-      float vr[NV][NT][4], vd[NV][NT][4], vs[NV][NT][4];
+      float vr[NV][NT][4], vi[NV][NT][4], vs[NV][NT][4];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -298,7 +302,7 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
             }
             if (!o) x = make_float2(0.f, 0.f);
             vr[v][nt][i] = x.x;
-            vd[v][nt][i] = x.y - x.x;
+            vi[v][nt][i] = x.y;
             vs[v][nt][i] = x.x + x.y;
           }
         }
@@ -309,26 +313,24 @@ axis_kernel(const float2* __restrict__ in, float2* __restrict__ out, const float
         const int kt = min(kb * KT + kk, a.ktiles - 1);
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
-          const float4 br = bre[kk][e], bi = bim[kk][e];
           const int v = FOLD == 1 ? (kt >= a.kth ? 1 : 0) : (FOLD == 2 ? e : 0);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float r = br[i], im = bi[i], rpi = br[i] + bi[i];
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-              float xr, xd, xs;
+              float xr, xi, xs;
               if (FOLD == 1) {  // uniform select of the fold class of this tile
                 xr = v ? vr[NV - 1][nt][i] : vr[0][nt][i];
-                xd = v ? vd[NV - 1][nt][i] : vd[0][nt][i];
+                xi = v ? vi[NV - 1][nt][i] : vi[0][nt][i];
                 xs = v ? vs[NV - 1][nt][i] : vs[0][nt][i];
               } else {
                 xr = vr[FOLD == 2 ? e : 0][nt][i];
-                xd = vd[FOLD == 2 ? e : 0][nt][i];
+                xi = vi[FOLD == 2 ? e : 0][nt][i];
                 xs = vs[FOLD == 2 ? e : 0][nt][i];
               }
-              acc1[e][kk][nt] = mfma(rpi, xr, acc1[e][kk][nt]);
-              acc2[e][kk][nt] = mfma(r, xd, acc2[e][kk][nt]);
-              acc3[e][kk][nt] = mfma(im, xs, acc3[e][kk][nt]);
+              acc1[e][kk][nt] = mfma(b0[kk][e][i], xs, acc1[e][kk][nt]);
+              acc2[e][kk][nt] = mfma(b1[kk][e][i], xr, acc2[e][kk][nt]);
+              acc3[e][kk][nt] = mfma(b2[kk][e][i], xi, acc3[e][kk][nt]);
             }
           }
         }
@@ -496,7 +498,7 @@ axis_pipe_kernel(const float2* __restrict__ in, float2* __restrict__ out, const 
   load(std::integral_constant<int, 0>{});
   load(std::integral_constant<int, 1>{});
   {
-    const int n4 = a.ktiles * a.JQ * 2 * 64;
+    const int n4 = a.ktiles * a.JQ * 3 * 64;
     for (int e = threadIdx.x; e < n4; e += 256) simg[e] = img[e];
   }
   __syncthreads();
@@ -550,13 +552,14 @@ axis_pipe_kernel(const float2* __restrict__ in, float2* __restrict__ out, const 
       }
     load(kc);
     if (!live) return;
-    float4 br[KT], bi[KT];
+    float4 b0[KT], b1[KT], b2[KT];
 #pragma unroll
     for (int kk = 0; kk < KT; ++kk) {
       const int kt = min(t_c.kb * KT + kk, a.ktiles - 1);
-      const int ie = (kt * a.JQ + q_c) * 2 * 64 + lane;
-      br[kk] = simg[ie];
-      bi[kk] = simg[ie + 64];
+      const int ie = (kt * a.JQ + q_c) * 3 * 64 + lane;
+      b0[kk] = simg[ie];
+      b1[kk] = simg[ie + 64];
+      b2[kk] = simg[ie + 128];
     }
     // i outermost: consecutive products into one accumulator are 3 KT NT
     // instructions apart
@@ -567,15 +570,14 @@ axis_pipe_kernel(const float2* __restrict__ in, float2* __restrict__ out, const 
         const int kt = min(t_c.kb * KT + kk, a.ktiles - 1);
         // fold class of tile kt: FOLD 1 (kt >= kth), FOLD 3 (kt mod 4 = kk)
         const int v = FOLD == 1 ? (kt >= a.kth ? 1 : 0) : (FOLD == 3 ? (kk & 3) : 0);
-        const float r = br[kk][i], im = bi[kk][i], rpi = r + im;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           float2 x;
           if (FOLD == 1) x = v ? xv[NV - 1][nt][i] : xv[0][nt][i];  // uniform select
           else x = xv[FOLD == 3 ? (kk & 3) % NV : 0][nt][i];
-          acc1[kk][nt] = mfma(rpi, x.x, acc1[kk][nt]);
-          acc2[kk][nt] = mfma(r, x.y - x.x, acc2[kk][nt]);
-          acc3[kk][nt] = mfma(im, x.x + x.y, acc3[kk][nt]);
+          acc1[kk][nt] = mfma(b0[kk][i], x.x + x.y, acc1[kk][nt]);
+          acc2[kk][nt] = mfma(b1[kk][i], x.x, acc2[kk][nt]);
+          acc3[kk][nt] = mfma(b2[kk][i], x.y, acc3[kk][nt]);
         }
       }
     if (++q_c < a.JQ) return;
@@ -650,7 +652,9 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
     float2* ob = out + b * int64_t(a.KO) * a.NN;
     const int64_t spare = m < int64_t(a.J) * a.NN ? m : 0;
 
-    // K index jj = 16q + 4g + i: row NCL jj + c (mode of class c)
+    // K index jj = 16q + 4g + i: row NCL jj + c (mode of class c); the B
+    // operands of the three products, Xr, Xi - Xr and Xr + Xi, are formed
+    // once per work item (every output tile reuses them)
     float2 x[JQ][NCL][NT][4];
 #pragma unroll
     for (int q = 0; q < JQ; ++q)
@@ -675,6 +679,20 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
       __syncthreads();
       staged = true;
     }
+    float xr[JQ][NCL][NT][4], xd[JQ][NCL][NT][4], xs[JQ][NCL][NT][4];
+#pragma unroll
+    for (int q = 0; q < JQ; ++q)
+#pragma unroll
+      for (int c = 0; c < NCL; ++c)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float2 v = x[q][c][nt][i];
+            xr[q][c][nt][i] = v.x;
+            xd[q][c][nt][i] = v.y - v.x;
+            xs[q][c][nt][i] = v.x + v.y;
+          }
 
     for (int kb = 0; kb < a.kblocks; ++kb) {
       v4f acc1[NCL][KT][NT], acc2[NCL][KT][NT], acc3[NCL][KT][NT];
@@ -711,10 +729,9 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
               const float r = bre[kk][e][i], im = bim[kk][e][i], rpi = r + im;
 #pragma unroll
               for (int nt = 0; nt < NT; ++nt) {
-                const float2 v = x[q][e][nt][i];
-                acc1[e][kk][nt] = mfma(rpi, v.x, acc1[e][kk][nt]);
-                acc2[e][kk][nt] = mfma(r, v.y - v.x, acc2[e][kk][nt]);
-                acc3[e][kk][nt] = mfma(im, v.x + v.y, acc3[e][kk][nt]);
+                acc1[e][kk][nt] = mfma(rpi, xr[q][e][nt][i], acc1[e][kk][nt]);
+                acc2[e][kk][nt] = mfma(r, xd[q][e][nt][i], acc2[e][kk][nt]);
+                acc3[e][kk][nt] = mfma(im, xs[q][e][nt][i], acc3[e][kk][nt]);
               }
             }
       }
@@ -766,8 +783,9 @@ axis_expand_kernel(const float2* __restrict__ in, float2* __restrict__ out, cons
 }
 
 // LDS bytes of an expand kernel's staged basis image (ncl classes per
-// entry), or 0 when the image is larger than 32 KiB and is read from global
-// memory instead (two workgroups of the expand kernels share a CU).
+// entry, two parts), or 0 when the image is larger than 32 KiB and is read
+// from global memory instead (two workgroups of the expand kernels share a
+// CU, and each one stages the image for its single work item).
 size_t expand_lds_bytes(const AxisCfg& c, int ncl) {
   const size_t b = size_t(c.ktiles) * c.JQ * ncl * 2 * 64 * sizeof(float4);
   return b <= 32 * 1024 ? b : 0;
@@ -818,7 +836,7 @@ const void* pipe_fn(int kt, int nt) {
 // false (nothing launched) otherwise.
 bool launch_pipe(int fold, int kt, int nt, const AxisCfg& c, AxisArgs a, hipStream_t s, const float2* pin,
                  float2* pout, const float4* pimg, hipError_t* err) {
-  const size_t lds = size_t(c.ktiles) * c.JQ * 2 * 64 * sizeof(float4);
+  const size_t lds = size_t(c.ktiles) * c.JQ * 3 * 64 * sizeof(float4);
   if (lds > 64 * 1024 || a.nb * a.kblocks * ((c.NN + 63) / 64) >= (int64_t(1) << 31)) return false;
   // four k tiles keep twelve accumulator tiles per column tile: one column
   // tile per wave (two would leave one wave per SIMD)
@@ -890,6 +908,10 @@ int launch_axis(const AxisCfg& c, int64_t nb, const void* in, void* out, const f
   const float4* pimg = reinterpret_cast<const float4*>(img);
   // Accumulation only happens on forward-direction launches (fold 0, 1, 3).
   if ((c.fold == 2 || c.fold == 4) && a.acc) return hipErrorInvalidValue;
+  // image parts the kernel taking this launch reads: (Re, Im) for the expand
+  // kernel, (Br, Bi - Br, Br + Bi) for the others
+  const bool expand = (c.fold == 2 || c.fold == 4) && c.JQ <= 2;
+  if (c.parts != (expand ? 2 : 3)) return hipErrorInvalidValue;
   if (c.fold == 3) {
     // one k tile per class in every block (KT = 4), one 16-column tile per
     // wave (the four class inputs and twelve accumulator tiles of NT = 2

@@ -281,6 +281,18 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
     }
   }
 
+  // Two-part (Re, Im) images: the inverse expansions of the expand kernel
+  // (fold 2 or 4 within two K steps) and the y images the fused stream
+  // kernels read; dtst_inverse_block expands y with the axis kernels even
+  // where the plan fuses y into the stream kernels.
+  auto expand_parts = [](AxisCfg& a) {
+    if ((a.fold == 2 || a.fold == 4) && a.JQ <= 2) a.parts = 2;
+  };
+  expand_parts(dv.ax_i);
+  expand_parts(dv.ay_i);
+  dv.ay_b = dv.ay_i;
+  if (sc.fuse_y) dv.ay_f.parts = dv.ay_i.parts = 2;
+
   // ---- fused inverse z + t expansion and block epilogue ----
   // The same z + t expansion as the split inverse, with z folded into at
   // most two classes (a chunk of the kernel is one z tile of every class),
@@ -322,11 +334,14 @@ dtst_status derive(const dtst_desc* d, uint32_t flags, Derived* out, std::string
   im.t_inv = take(t_img);
   im.t_inv_adjoint_of_forward = take(t_img);
   im.z_inv = take(z_img);
-  auto axis_img = [](const AxisCfg& a) { return size_t(a.ktiles) * a.JQ * axis_image_classes(a) * 2 * 64 * 4; };
+  auto axis_img = [](const AxisCfg& a) {
+    return size_t(a.ktiles) * a.JQ * axis_image_classes(a) * a.parts * 64 * 4;
+  };
   im.y_fwd = take(axis_img(dv.ay_f));
   im.x_fwd = take(axis_img(dv.ax_f));
   im.y_inv = take(axis_img(dv.ay_i));
   im.x_inv = take(axis_img(dv.ax_i));
+  im.y_blk = sc.fuse_y ? take(axis_img(dv.ay_b)) : im.y_inv;
   im.z_blk = take(size_t(dv.sb.ncls) * dv.sb.zt * z_blocks(dv.sb) * 64 * 4);
   im.t_blk = take(t_img);
   im.total = off;
@@ -505,7 +520,10 @@ void z_inverse_image(const Derived& dv, float* dst) {
 }
 
 // Axis image, float4 entries indexed by lane (m = lane & 15, g = lane >> 4)
-// and component i; part 0 holds Re, part 1 Im.
+// and component i.  With 3 parts (the axis kernels) part 0 holds Br, part 1
+// Bi - Br, part 2 Br + Bi of the basis value Br + i Bi; with 2 parts (the y
+// images of the fused stream kernels) part 0 Re, part 1 Im.  Entry layouts
+// below with 2 parts; 3 parts stride the same way.
 //   fold 0: entry ((kt*JQ + q)*2 + part)*64 + lane = basis[k][j],
 //           k = 16kt + m, j = 16q + 4g + i.
 //   fold 1: same entry layout; tile kt holds parity class c = (kt >= kth),
@@ -523,7 +541,7 @@ void axis_image(const Derived& dv, const AxisCfg& a, int dim, bool inverse, floa
   for (int kt = 0; kt < a.ktiles; ++kt)
     for (int q = 0; q < a.JQ; ++q)
       for (int c = 0; c < ncls; ++c)
-        for (int part = 0; part < 2; ++part)
+        for (int part = 0; part < a.parts; ++part)
           for (int lane = 0; lane < 64; ++lane)
             for (int i = 0; i < 4; ++i) {
               const int m = lane & 15, g = lane >> 4;
@@ -560,9 +578,11 @@ void axis_image(const Derived& dv, const AxisCfg& a, int dim, bool inverse, floa
                 } else {
                   bval(d, dim, k, j, &re, &im);
                 }
-                v = part == 0 ? re : im;
+                if (a.parts == 3) v = part == 0 ? re : (part == 1 ? im - re : re + im);
+                else v = part == 0 ? re : im;
               }
-              dst[(((((size_t)kt * a.JQ + q) * ncls + c) * 2 + part) * 64 + lane) * 4 + i] = static_cast<float>(v);
+              dst[(((((size_t)kt * a.JQ + q) * ncls + c) * a.parts + part) * 64 + lane) * 4 + i] =
+                  static_cast<float>(v);
             }
 }
 
@@ -581,6 +601,7 @@ void build_images(const Derived& dv, std::vector<float>* blob) {
   axis_image(dv, dv.ax_f, 0, false, b + dv.img.x_fwd);
   axis_image(dv, dv.ay_i, 1, true, b + dv.img.y_inv);
   axis_image(dv, dv.ax_i, 0, true, b + dv.img.x_inv);
+  if (dv.img.y_blk != dv.img.y_inv) axis_image(dv, dv.ay_b, 1, true, b + dv.img.y_blk);
   // the fused inverse + block epilogue's z and t images: those of the
   // inverse for its own z configuration
   Derived db = dv;
