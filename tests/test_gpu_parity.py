@@ -334,7 +334,9 @@ def test_errors_launch_nothing():
 # a multiple of 4) and narrow outputs, C_in != C_out.
 EPILOGUE_SHAPES = [((4, 6, 8, 8), 2, 16, 16), ((3, 5, 4, 8), 1, 3, 37), ((4, 6, 8, 8), 1, 20, 20),
                    ((3, 5, 4, 8), 2, 7, 17), ((3, 5, 7, 3), 1, 20, 20), ((3, 5, 7, 3), 2, 5, 2),
-                   ((2, 2, 2, 2), 1, 1, 1)]
+                   ((2, 2, 2, 2), 1, 1, 1),
+                   # one pass over the input channels for 24 < C_out <= 32
+                   ((3, 5, 4, 8), 1, 32, 32), ((4, 6, 8, 8), 2, 9, 25)]
 
 
 @pytest.mark.parametrize("shape", EPILOGUE_SHAPES, ids=lambda s: "nl%s_B%d_ci%d_co%d" % (
