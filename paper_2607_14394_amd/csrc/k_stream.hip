@@ -1059,6 +1059,24 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
   for (int mt = 0; mt < TH; ++mt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) ta[mt][0][i] = timg[(mt * 4 + i) * 64 + lane];
+  // y image from global memory (YL = 0): the entries of group gq are held in
+  // registers, and those of the next group are loaded right after the
+  // group's y expansion, before its row stores: read at the group start they
+  // would wait for the previous group's stores (one memory counter per wave)
+  float4 yb[YL ? 1 : JQY][YL ? 1 : NCY][2];
+  auto load_y = [&](int gq) __attribute__((always_inline)) {
+    if constexpr (!YL) {
+#pragma unroll
+      for (int q = 0; q < JQY; ++q)
+#pragma unroll
+        for (int cl = 0; cl < NCY; ++cl) {
+          const int e = ((gq * JQY + q) * NCY + cl) * 2 * 64 + lane;
+          yb[q][cl][0] = yimg[e];
+          yb[q][cl][1] = yimg[e + 64];
+        }
+    }
+  };
+  load_y(0);
   stage_end(lds, stl);
   __syncthreads();
 
@@ -1078,8 +1096,8 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
           for (int cl = 0; cl < NCY; ++cl) {
             // image entry (((tile * JQ + q) * NCY + class) * 2 + part) * 64 + lane
             const int e = ((gq * JQY + q) * NCY + cl) * 2 * 64 + lane;
-            const float4 br = YL ? ylds[e] : yimg[e];
-            const float4 bi = YL ? ylds[e + 64] : yimg[e + 64];
+            const float4 br = YL ? ylds[e] : yb[YL ? 0 : q][YL ? 0 : cl][0];
+            const float4 bi = YL ? ylds[e + 64] : yb[YL ? 0 : q][YL ? 0 : cl][1];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const float2 v = u_ok(cl, q, i) ? u[cl][q][i] : make_float2(0.f, 0.f);
@@ -1101,6 +1119,7 @@ inv_yzt_kernel(const float2* __restrict__ in, float* __restrict__ y, const float
           }
         }
       }
+      load_y(gq + 1 < f.jq ? gq + 1 : gq);
       __syncthreads();
       const int s = 16 * gq + w;
       if (s < f.slots) {
