@@ -172,6 +172,18 @@ __device__ __forceinline__ void texp_tfg(const v4f& Wr, const v4f& Wi, const flo
   }
 }
 
+// Row g of the result is row 0 (lanes 0..15) of r_g: three gfx950 lane
+// swaps (rows of 16 lanes; v_permlane16_swap trades the odd rows of its
+// first operand with the even rows of its second, v_permlane32_swap the
+// upper half of its first with the lower half of its second).
+__device__ __forceinline__ float gather_rows(float r0, float r1, float r2, float r3) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(r0), __float_as_uint(r1), false, false);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(r2), __float_as_uint(r3), false, false);
+  // a[0]: rows r0.0, r1.0, r0.2, r1.2; b[0]: rows r2.0, r3.0, r2.2, r3.2
+  const auto c = __builtin_amdgcn_permlane32_swap(a[0], b[0], false, false);
+  return __uint_as_float(c[0]);
+}
+
 // KI: K steps of 4 input channels (C_in <= 4 KI); OT: tiles of 16 output
 // channels per pass (C_out <= 16 OT OH); SPF: float4 of the row's spectrum
 // per thread (C_out K_z K_t <= 2 * 64 kBlkWaves SPF); XD: chunks of x loaded
@@ -407,17 +419,35 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     }
     float* yr = y + c.yb + gcs_y + q.off;
 #pragma unroll
-    for (int ot = 0; ot < OT; ++ot)
+    for (int ot = 0; ot < OT; ++ot) {
+      const int o0 = 16 * (OHI * OT + ot);  // first output channel of the tile
+      if (ba.co - o0 <= 4) {
+        // At most 4 channels (C_out = 20 of the paper's width, say): only the
+        // lanes g = 0 hold outputs.  Lane (m, g) takes point 4m + g of lane
+        // (m, 0) for each of the 4 channels, so that every lane evaluates 4
+        // GELUs instead of the 16 of a full tile; each store then covers the
+        // group's 64 points of one channel (256 bytes).
+        if (ba.co > o0) {
+          float* yc = y + c.yb + int64_t(o0) * cs + q.off + g;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float v = gather_rows(C[ot][0][r], C[ot][1][r], C[ot][2][r], C[ot][3][r]);
+            if (q.ok && o0 + r < ba.co) yc[r * cs] = gelu_as(v);
+          }
+        }
+        continue;
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int o = 16 * (OHI * OT + ot) + 4 * g + r;
+        const int o = o0 + 4 * g + r;
         if (q.ok && o < ba.co) {
-          float* dst = yr + (16 * (OHI * OT + ot) + r) * cs;
+          float* dst = yr + (o0 + r) * cs;
           // ordinary (cached) stores: measured faster here than streaming ones
           *reinterpret_cast<v4f*>(dst) =
               v4f{gelu_as(C[ot][0][r]), gelu_as(C[ot][1][r]), gelu_as(C[ot][2][r]), gelu_as(C[ot][3][r])};
         }
       }
+    }
   };
 
   // One pipeline step: phase 2 of chunk c2 (the previous one, when it

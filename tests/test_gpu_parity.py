@@ -427,6 +427,9 @@ INVERSE_BLOCK_CASES = {
     "nt12_ragged": (((4, 4, 24, 12), (4, 4, 24, 12), (0, 0, 0, 0), (2, 2, 5), 4, 1, 3, 2), True),
     "nt20": (((4, 6, 32, 20), (4, 6, 32, 20), (0, 0, 0, 0), (2, 2, 6), 7, 1, 5, 5), True),
     "batch3": (((4, 6, 32, 32), (2, 6, 32, 32), (2, 0, 0, 0), (2, 2, 8), 6, 3, 5, 9), True),
+    # a last tile of 1 or 2 output channels (one pass of two tiles; second pass of two)
+    "c17": (((4, 6, 32, 32), (4, 6, 32, 32), (0, 0, 0, 0), (2, 2, 8), 5, 1, 17, 17), True),
+    "c25_18": (((4, 4, 32, 16), (4, 4, 32, 16), (0, 0, 0, 0), (1, 1, 4), 3, 1, 25, 18), True),
 }
 
 
