@@ -352,14 +352,15 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   // Phase 1 of unit c (chunk class HF, output pass OHI) into buffer PAR:
   // this wave's channels o = 16 OHI + w + NW k of the pass (o = w + NW k
   // with one pass), at buffer channel o - 16 OHI.
-  auto phase1 = [&](auto parc, auto hfc, auto ohc, const Cur& c) __attribute__((always_inline)) {
+  auto phase1 = [&](auto parc, auto hfc, auto ohc, auto fastc, const Cur& c) __attribute__((always_inline)) {
     constexpr int PAR = decltype(parc)::value, HF = decltype(hfc)::value, OHI = decltype(ohc)::value;
+    constexpr bool FAST = decltype(fastc)::value;
     float* yb = ybuf + PAR * bufsz;
     if constexpr (TF) {
 #pragma unroll
       for (int k = 0; k < KCH; ++k) {
         const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
-        if (o < ba.co) {
+        if (FAST || o < ba.co) {
           if (HF == 0) zexp_tfg<MT, NCLS>(sbuf + o * spec_len, a, lds, c.zt, m, g, lane, Wzr[kk], Wzi[kk]);
           texp_tfg<TH>(Wzr[kk][HF], Wzi[kk][HF], ta, yb + ol * ba.ostride, m, g);
         }
@@ -374,30 +375,33 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
         for (int k = 0; k < KCH; ++k) {
           const int kk = OHI * KCH + k, o = 16 * OHI + w + NW * k;
-          if (o < ba.co) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[kk]);
+          if (FAST || o < ba.co) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[kk]);
         }
       }
 #pragma unroll
       for (int k = 0; k < KCH; ++k) {
         const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
-        if (o < ba.co) texp_plain<CT, TH>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
+        if (FAST || o < ba.co) texp_plain<CT, TH>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
       }
     }
   };
 
   // Phase 2 of unit c (output pass OHI: channels 16 (OHI OT + ot) + 4g + r,
   // buffer channel 16 ot + 4g + r) from buffer PAR with x buffer XB.
-  auto phase2 = [&](auto parc, auto xbc, auto ohc, const Cur& c) __attribute__((always_inline)) {
+  // The matrix part of phase 2: the expanded values from LDS plus the
+  // bypass products, into C.
+  auto phase2_mma = [&](auto parc, auto xbc, auto ohc, auto fastc, const Cur& c, v4f (&C)[OT][4])
+                        __attribute__((always_inline)) {
     constexpr int PAR = decltype(parc)::value, XB = decltype(xbc)::value, OHI = decltype(ohc)::value;
+    constexpr bool FAST = decltype(fastc)::value;
     const float* yb = ybuf + PAR * bufsz;
     const Grp q = group(c);
-    v4f C[OT][4];
 #pragma unroll
     for (int ot = 0; ot < OT; ++ot)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int ol = 16 * ot + 4 * g + r, o = 16 * OHI * OT + ol;
-        const float4 v = *reinterpret_cast<const float4*>(yb + (o < ba.co ? ol : 0) * ba.ostride + q.loff);
+        const float4 v = *reinterpret_cast<const float4*>(yb + (FAST || o < ba.co ? ol : 0) * ba.ostride + q.loff);
         C[ot][0][r] = v.x;
         C[ot][1][r] = v.y;
         C[ot][2][r] = v.z;
@@ -405,7 +409,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
       }
 #pragma unroll
     for (int s = 0; s < KI; ++s) {
-      const bool iok = 4 * s + g < ba.ci;
+      const bool iok = FAST || 4 * s + g < ba.ci;
       const float4 xs = xv[XB][s];
       const float b0 = iok ? xs.x : 0.f, b1 = iok ? xs.y : 0.f, b2 = iok ? xs.z : 0.f, b3 = iok ? xs.w : 0.f;
 #pragma unroll
@@ -417,6 +421,24 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
         C[ot][3] = mfma(wv, b3, C[ot][3]);
       }
     }
+  };
+  // The vector part with every tile full and every point present: GELU and
+  // unconditional stores.
+  auto phase2_store_full = [&](auto ohc, const Cur& c, const v4f (&C)[OT][4]) __attribute__((always_inline)) {
+    constexpr int OHI = decltype(ohc)::value;
+    float* yr = y + c.yb + gcs_y + group(c).off;
+#pragma unroll
+    for (int ot = 0; ot < OT; ++ot)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        *reinterpret_cast<v4f*>(yr + (16 * (OHI * OT + ot) + r) * cs) =
+            v4f{gelu_as(C[ot][0][r]), gelu_as(C[ot][1][r]), gelu_as(C[ot][2][r]), gelu_as(C[ot][3][r])};
+  };
+  auto phase2 = [&](auto parc, auto xbc, auto ohc, const Cur& c) __attribute__((always_inline)) {
+    constexpr int OHI = decltype(ohc)::value;
+    const Grp q = group(c);
+    v4f C[OT][4];
+    phase2_mma(parc, xbc, ohc, std::integral_constant<bool, false>{}, c, C);
     float* yr = y + c.yb + gcs_y + q.off;
 #pragma unroll
     for (int ot = 0; ot < OT; ++ot) {
@@ -462,7 +484,8 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   at_row(c1);
   Cur c2 = c1;                                             // phase 2 (valid from step 1 on)
   Cur cx = c1;                                             // next x to load
-  auto step = [&](auto sc, bool has2) __attribute__((always_inline)) {
+  auto step = [&](auto sc, auto fastc, bool has2) __attribute__((always_inline)) {
+    constexpr bool FAST = decltype(fastc)::value;
     constexpr int S4 = decltype(sc)::value;     // step index mod 4
     constexpr int PAR = S4 & 1;                 // buffer of phase 1; phase 2 reads 1 - PAR
     // output pass of phase 1's unit and of phase 2's (the previous) unit
@@ -477,18 +500,32 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     constexpr int XB = OH == 2 ? ((S4 == 0 || S4 == 3) ? 1 : 0) : (S4 + 3) % XD;
     constexpr int XL = OH == 2 ? 1 - XB : XB;
     constexpr bool LOADS = OH == 1 || (S4 & 1) == 1;
-    const bool has1 = c1.row < ba.rows;
+    const bool has1 = FAST || c1.row < ba.rows;
     auto body = [&]() __attribute__((always_inline)) {
-      if (has2)
-        phase2(std::integral_constant<int, 1 - PAR>{}, std::integral_constant<int, XB>{},
-               std::integral_constant<int, OH2>{}, c2);
-      if constexpr (LOADS) {
-        load_x(XL, cx);
-        cx = next_chunk(cx);
+      using P1 = std::integral_constant<int, PAR>;
+      using P2 = std::integral_constant<int, 1 - PAR>;
+      if constexpr (FAST) {
+        // Both phases unconditional: the step is one basic block (no
+        // per-channel or per-store branches), which the compiler schedules
+        // as a whole.  (Taking the two phases in opposite orders on the two
+        // waves of a SIMD was measured slower: C held across phase 1 spills.)
+        v4f C[OT][4];
+        phase2_mma(P2{}, std::integral_constant<int, XB>{}, std::integral_constant<int, OH2>{}, fastc, c2, C);
+        if constexpr (LOADS) {
+          load_x(XL, cx);
+          cx = next_chunk(cx);
+        }
+        phase2_store_full(std::integral_constant<int, OH2>{}, c2, C);
+        phase1(P1{}, std::integral_constant<int, HF>{}, std::integral_constant<int, OH1>{}, fastc, c1);
+      } else {
+        if (has2)
+          phase2(P2{}, std::integral_constant<int, XB>{}, std::integral_constant<int, OH2>{}, c2);
+        if constexpr (LOADS) {
+          load_x(XL, cx);
+          cx = next_chunk(cx);
+        }
+        if (has1) phase1(P1{}, std::integral_constant<int, HF>{}, std::integral_constant<int, OH1>{}, fastc, c1);
       }
-      if (has1)
-        phase1(std::integral_constant<int, PAR>{}, std::integral_constant<int, HF>{},
-               std::integral_constant<int, OH1>{}, c1);
     };
     // (c1.hf == HF and c1.oh == OH1 by construction: only the steps whose
     // unit is the last class and pass of a chunk can end a row)
@@ -519,13 +556,34 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     cx = next_chunk(cx);
   }
   __syncthreads();
-  step(std::integral_constant<int, 0>{}, false);
+  using Gen = std::integral_constant<bool, false>;
+  using Fast = std::integral_constant<bool, true>;
+  step(std::integral_constant<int, 0>{}, Gen{}, false);
+  // Passes whose four units all exist run the unconditional steps when every
+  // tile is full (C_out = 16 OT OH output channels, C_in = 4 KI input
+  // channels) and every chunk complete (N_t = 4 NW, whole z tiles).
+  // (The (KI, OT, OH) classes whose full channel counts differ, C_in up to
+  // 20 with two output tiles, never take them and do not compile them.)
+  constexpr bool kFull = 16 * OT * OH == 4 * KI;
+  const bool full = kFull && ba.co == 16 * OT * OH && ba.ci == 4 * KI && nt == 4 * NW && a.zh % 16 == 0;
+  const int64_t units = ((ba.rows - 1 - blockIdx.x) / gridDim.x + 1) * cpr * OH;  // this workgroup's units
+  int64_t u1 = 1;  // unit of c1
   // every pass runs four steps; the only exit is at the end of a pass
   do {
-    step(std::integral_constant<int, 1>{}, c2.row < ba.rows);
-    step(std::integral_constant<int, 2>{}, c2.row < ba.rows);
-    step(std::integral_constant<int, 3>{}, c2.row < ba.rows);
-    step(std::integral_constant<int, 0>{}, c2.row < ba.rows);
+    if (full && u1 + 3 < units) {
+      if constexpr (kFull) {
+        step(std::integral_constant<int, 1>{}, Fast{}, true);
+        step(std::integral_constant<int, 2>{}, Fast{}, true);
+        step(std::integral_constant<int, 3>{}, Fast{}, true);
+        step(std::integral_constant<int, 0>{}, Fast{}, true);
+      }
+    } else {
+      step(std::integral_constant<int, 1>{}, Gen{}, c2.row < ba.rows);
+      step(std::integral_constant<int, 2>{}, Gen{}, c2.row < ba.rows);
+      step(std::integral_constant<int, 3>{}, Gen{}, c2.row < ba.rows);
+      step(std::integral_constant<int, 0>{}, Gen{}, c2.row < ba.rows);
+    }
+    u1 += 4;
   } while (c2.row < ba.rows);
 }
 

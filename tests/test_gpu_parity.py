@@ -430,6 +430,10 @@ INVERSE_BLOCK_CASES = {
     # a last tile of 1 or 2 output channels (one pass of two tiles; second pass of two)
     "c17": (((4, 6, 32, 32), (4, 6, 32, 32), (0, 0, 0, 0), (2, 2, 8), 5, 1, 17, 17), True),
     "c25_18": (((4, 4, 32, 16), (4, 4, 32, 16), (0, 0, 0, 0), (1, 1, 4), 3, 1, 25, 18), True),
+    # whole tiles (C_in = C_out = 16 or 32, N_t = 32) over 1024 rows: several rows per
+    # workgroup, so that the unconditional passes run between the first and last steps
+    "full_c16": (((16, 64, 64, 32), (16, 64, 64, 32), (0, 0, 0, 0), (2, 4, 8), 5, 1, 16, 16), True),
+    "full_c32": (((16, 64, 32, 32), (16, 64, 32, 32), (0, 0, 0, 0), (2, 4, 8), 6, 1, 32, 32), True),
 }
 
 
