@@ -212,6 +212,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
                 "output halves of 16 channels, x two chunks in flight");
   static_assert(!TF || (CT == 2 && TH == 2), "t folding needs two k_t tiles and N_t = 32");
   static_assert(XD == 1 || XD == 2 || XD == 4, "x one, two or four chunks ahead");
+  static_assert(OT == 1 || OT == 2, "one or two output tiles per pass");
   // LDS: the z image, the row's spectrum of every output channel, two
   // buffers of a chunk's expanded values [o][z row][t].
   extern __shared__ float4 lds[];
@@ -360,7 +361,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
       for (int k = 0; k < KCH; ++k) {
         const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
-        if (FAST || o < ba.co) {
+        if ((FAST && 16 * OHI + NW * (k + 1) <= 4 * KI) || o < ba.co) {
           if (HF == 0) zexp_tfg<MT, NCLS>(sbuf + o * spec_len, a, lds, c.zt, m, g, lane, Wzr[kk], Wzi[kk]);
           texp_tfg<TH>(Wzr[kk][HF], Wzi[kk][HF], ta, yb + ol * ba.ostride, m, g);
         }
@@ -375,13 +376,13 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
         for (int k = 0; k < KCH; ++k) {
           const int kk = OHI * KCH + k, o = 16 * OHI + w + NW * k;
-          if (FAST || o < ba.co) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[kk]);
+          if ((FAST && 16 * OHI + NW * (k + 1) <= 4 * KI) || o < ba.co) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[kk]);
         }
       }
 #pragma unroll
       for (int k = 0; k < KCH; ++k) {
         const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
-        if (FAST || o < ba.co) texp_plain<CT, TH>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
+        if ((FAST && 16 * OHI + NW * (k + 1) <= 4 * KI) || o < ba.co) texp_plain<CT, TH>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
       }
     }
   };
@@ -401,7 +402,8 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int ol = 16 * ot + 4 * g + r, o = 16 * OHI * OT + ol;
-        const float4 v = *reinterpret_cast<const float4*>(yb + (FAST || o < ba.co ? ol : 0) * ba.ostride + q.loff);
+        const bool whole = FAST && 16 * (OHI * OT + ot) + 16 <= 4 * KI;  // tile known to be full
+        const float4 v = *reinterpret_cast<const float4*>(yb + (whole || o < ba.co ? ol : 0) * ba.ostride + q.loff);
         C[ot][0][r] = v.x;
         C[ot][1][r] = v.y;
         C[ot][2][r] = v.z;
@@ -422,17 +424,29 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
       }
     }
   };
-  // The vector part with every tile full and every point present: GELU and
-  // unconditional stores.
+  // The vector part with C_out = 4 KI and every point present: GELU and
+  // unconditional stores (a last tile of 4 channels gathered across rows).
   auto phase2_store_full = [&](auto ohc, const Cur& c, const v4f (&C)[OT][4]) __attribute__((always_inline)) {
     constexpr int OHI = decltype(ohc)::value;
-    float* yr = y + c.yb + gcs_y + group(c).off;
+    const int off = group(c).off;
+    float* yr = y + c.yb + gcs_y + off;
+    auto tile = [&](auto otc) __attribute__((always_inline)) {
+      constexpr int ot = decltype(otc)::value, o0 = 16 * (OHI * OT + ot);
+      if constexpr (o0 + 16 <= 4 * KI) {
 #pragma unroll
-    for (int ot = 0; ot < OT; ++ot)
+        for (int r = 0; r < 4; ++r)
+          *reinterpret_cast<v4f*>(yr + (o0 + r) * cs) =
+              v4f{gelu_as(C[ot][0][r]), gelu_as(C[ot][1][r]), gelu_as(C[ot][2][r]), gelu_as(C[ot][3][r])};
+      } else {
+        static_assert(o0 + 4 == 4 * KI, "a partial tile of the unconditional passes has 4 channels");
+        float* yc = y + c.yb + int64_t(o0) * cs + off + g;
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        *reinterpret_cast<v4f*>(yr + (16 * (OHI * OT + ot) + r) * cs) =
-            v4f{gelu_as(C[ot][0][r]), gelu_as(C[ot][1][r]), gelu_as(C[ot][2][r]), gelu_as(C[ot][3][r])};
+        for (int r = 0; r < 4; ++r)
+          yc[r * cs] = gelu_as(gather_rows(C[ot][0][r], C[ot][1][r], C[ot][2][r], C[ot][3][r]));
+      }
+    };
+    tile(std::integral_constant<int, 0>{});
+    if constexpr (OT > 1) tile(std::integral_constant<int, 1>{});
   };
   auto phase2 = [&](auto parc, auto xbc, auto ohc, const Cur& c) __attribute__((always_inline)) {
     constexpr int OHI = decltype(ohc)::value;
@@ -559,13 +573,12 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   using Gen = std::integral_constant<bool, false>;
   using Fast = std::integral_constant<bool, true>;
   step(std::integral_constant<int, 0>{}, Gen{}, false);
-  // Passes whose four units all exist run the unconditional steps when every
-  // tile is full (C_out = 16 OT OH output channels, C_in = 4 KI input
-  // channels) and every chunk complete (N_t = 4 NW, whole z tiles).
-  // (The (KI, OT, OH) classes whose full channel counts differ, C_in up to
-  // 20 with two output tiles, never take them and do not compile them.)
-  constexpr bool kFull = 16 * OT * OH == 4 * KI;
-  const bool full = kFull && ba.co == 16 * OT * OH && ba.ci == 4 * KI && nt == 4 * NW && a.zh % 16 == 0;
+  // Passes whose four units all exist run the unconditional steps when the
+  // channel counts fill the class (C_in = C_out = 4 KI: 16, 20 or 32, the
+  // last tile of 20 with 4 channels) and every chunk is complete (N_t = 4 NW,
+  // whole z tiles).
+  constexpr bool kFull = 16 * OT * OH == 4 * KI || (OH == 1 && 16 * (OT - 1) + 4 == 4 * KI);
+  const bool full = kFull && ba.co == 4 * KI && ba.ci == 4 * KI && nt == 4 * NW && a.zh % 16 == 0;
   const int64_t units = ((ba.rows - 1 - blockIdx.x) / gridDim.x + 1) * cpr * OH;  // this workgroup's units
   int64_t u1 = 1;  // unit of c1
   // every pass runs four steps; the only exit is at the end of a pass

@@ -434,6 +434,8 @@ INVERSE_BLOCK_CASES = {
     # workgroup, so that the unconditional passes run between the first and last steps
     "full_c16": (((16, 64, 64, 32), (16, 64, 64, 32), (0, 0, 0, 0), (2, 4, 8), 5, 1, 16, 16), True),
     "full_c32": (((16, 64, 32, 32), (16, 64, 32, 32), (0, 0, 0, 0), (2, 4, 8), 6, 1, 32, 32), True),
+    "full_c20": (((16, 64, 64, 32), (16, 64, 64, 32), (0, 0, 0, 0), (2, 4, 8), 5, 1, 20, 20), True),
+    "full_c20_tfold": (((16, 64, 32, 32), (16, 64, 32, 32), (0, 0, 0, 0), (4, 4, 8), 16, 1, 20, 20), True),
 }
 
 
