@@ -62,6 +62,9 @@ def parse():
     ap.add_argument("--fno", action="store_true",
                     help="time the whole FNO forward (lift, 4 Fourier layers, projection) on workload 7, the "
                          "paper's model shape (d_v 20, modes (8, 8, 8, 16)) on 128^3 x 32 in 4 x-slabs")
+    ap.add_argument("--unfused-block", action="store_true",
+                    help="with --block or --fno: plans made with PLAN_UNFUSED_BLOCK, so that every block "
+                         "epilogue runs as the inverse followed by the separate epilogue kernel (for comparison)")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph after the warm-up and replay it in the timed "
                          "region (the same kernels; removes the host's per-launch cost)")
@@ -276,7 +279,7 @@ def _mix_work(g, m_count, kind):
                 mfma_flops=8 * B * m_count * ci * co)
 
 
-def forward_workload(torch, D, synth, cfg, device, block=False):
+def forward_workload(torch, D, synth, cfg, device, block=False, flags=0):
     """Forward partial DFT + mix + inverse over every shard of the workload.
     Workload 2 runs its 8 slabs one after another: the forwards accumulate
     into one spectrum, the mix runs over the 8 mode ranges in turn, and every
@@ -296,7 +299,7 @@ def forward_workload(torch, D, synth, cfg, device, block=False):
         g = synth.geometry(cfg)
         shards.append((g, synth.torch_input(cfg, g, device)))
     g0 = shards[0][0]
-    plans = [D.Plan(g, device) for g, _ in shards]
+    plans = [D.Plan(g, device, flags) for g, _ in shards]
     M = plans[0].n_modes
     W = synth.torch_weights(M, g0["c_in"], g0["c_out"], synth.seed_of(cfg, "weights"), device)
     xhat = torch.empty(plans[0].spectral_shape(g0["c_in"]), dtype=torch.complex64, device=device)
@@ -483,7 +486,7 @@ def backward_workload(torch, D, synth, cfg, device):
     return w
 
 
-def fno_workload(torch, D, synth, cfg, device):
+def fno_workload(torch, D, synth, cfg, device, flags=0):
     """FNO forward (lift, Fourier layers as Algorithm 1, projection) over
     every shard of the workload, run one after another on this GPU."""
     from paper_2607_14394_amd.fno import FNO
@@ -497,7 +500,7 @@ def fno_workload(torch, D, synth, cfg, device):
     lift, layers, proj = synth.fno_params_np(M, dv, cin, cout, L, 1000 * cfg)
     t = lambda a: torch.from_numpy(a).to(device)
     fno = FNO(shards, (t(lift[0]), t(lift[1])), [(t(r), t(wb)) for r, wb in layers], (t(proj[0]), t(proj[1])),
-              device)
+              device, flags)
     xs = [synth.torch_normal(tuple(fno.input_shape(p)), synth.seed_of(cfg, "input") + p, device)
           for p in range(len(shards))]
     outs = [torch.empty(fno.output_shape(p), dtype=torch.float32, device=device) for p in range(len(shards))]
@@ -628,6 +631,12 @@ def main():
         print("bench.py measures one GPU only: every shard of the decomposition runs one after "
               "another on a single MI355X (no collectives); run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    if args.fno and args.block:
+        print("--fno already includes every block's bypass and GELU", file=sys.stderr)
+        sys.exit(2)
+    if args.unfused_block and not (args.block or args.fno):
+        print("--unfused-block applies to --block and --fno", file=sys.stderr)
+        sys.exit(2)
 
     import torch
 
@@ -647,9 +656,6 @@ def main():
 
     device = "cuda"
     cfg = 7 if args.fno else args.workload
-    if args.fno and args.block:
-        print("--fno already includes every block's bypass and GELU", file=sys.stderr)
-        sys.exit(2)
     if args.hbm_warmup_gb > 0:
         # Set-up only, outside every timed region: the stream kernels run up to
         # 13% slower on the first large buffers a fresh process places in HBM;
@@ -669,11 +675,12 @@ def main():
     if cfg == 7 and not args.fno:
         print("workload 7 is the FNO forward: run it with --fno", file=sys.stderr)
         sys.exit(2)
+    flags = D.PLAN_UNFUSED_BLOCK if args.unfused_block else 0
     if args.fno:
-        w = fno_workload(torch, D, synth, cfg, device)
+        w = fno_workload(torch, D, synth, cfg, device, flags)
     else:
         w = (backward_workload(torch, D, synth, cfg, device) if cfg == 5
-             else forward_workload(torch, D, synth, cfg, device, block=args.block))
+             else forward_workload(torch, D, synth, cfg, device, block=args.block, flags=flags))
     log(f"warmup {args.warmup} steps")
 
     # ---- warmup ----

@@ -19,11 +19,13 @@ class FNO:
     """descs: one spectral-layer descriptor per shard (same global grid,
     modes and batch; c_in = c_out = d_v).  lift = (w (d_v, C_in), b (d_v,)),
     layers = [(R (M, d_v, d_v) complex64, W (d_v, d_v) float32), ...],
-    proj = (w (C_out, d_v), b (C_out,)); all device tensors, used as given."""
+    proj = (w (C_out, d_v), b (C_out,)); all device tensors, used as given.
+    flags: plan flags of every shard's plan (PLAN_UNFUSED_BLOCK runs each
+    block epilogue as the inverse followed by the separate epilogue)."""
 
-    def __init__(self, descs, lift, layers, proj, device="cuda"):
+    def __init__(self, descs, lift, layers, proj, device="cuda", flags=0):
         import torch
-        self.plans = [Plan(d, device) for d in descs]
+        self.plans = [Plan(d, device, flags) for d in descs]
         p0 = self.plans[0]
         d = p0.desc
         self.dv = d.c_in

@@ -29,6 +29,14 @@ def test_more_than_one_gpu_exits_with_a_message():
     assert r.stdout == ""
 
 
+def test_unfused_block_needs_a_block_workload():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--unfused-block"],
+                       capture_output=True, text=True, timeout=300, cwd=ROOT)
+    assert r.returncode == 2
+    assert "--unfused-block applies to --block and --fno" in r.stderr
+    assert r.stdout == ""
+
+
 def test_counters_resolve_for_the_default_workload():
     import bench
     with open(os.path.join(ROOT, "profiles", "hbm_counters.json")) as f:
