@@ -357,11 +357,15 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     constexpr int PAR = decltype(parc)::value, HF = decltype(hfc)::value, OHI = decltype(ohc)::value;
     constexpr bool FAST = decltype(fastc)::value;
     float* yb = ybuf + PAR * bufsz;
+    // (Channel o, slot k of this wave, exists; in the unconditional passes,
+    // C_out = 4 KI, this is known at compile time for the slots whose
+    // channels all lie below 4 KI.)
+#define DTST_BLK_HAS(k, o) ((FAST && 16 * OHI + NW * ((k) + 1) <= 4 * KI) || (o) < ba.co)
     if constexpr (TF) {
 #pragma unroll
       for (int k = 0; k < KCH; ++k) {
         const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
-        if ((FAST && 16 * OHI + NW * (k + 1) <= 4 * KI) || o < ba.co) {
+        if (DTST_BLK_HAS(k, o)) {
           if (HF == 0) zexp_tfg<MT, NCLS>(sbuf + o * spec_len, a, lds, c.zt, m, g, lane, Wzr[kk], Wzi[kk]);
           texp_tfg<TH>(Wzr[kk][HF], Wzi[kk][HF], ta, yb + ol * ba.ostride, m, g);
         }
@@ -376,21 +380,23 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
         for (int k = 0; k < KCH; ++k) {
           const int kk = OHI * KCH + k, o = 16 * OHI + w + NW * k;
-          if ((FAST && 16 * OHI + NW * (k + 1) <= 4 * KI) || o < ba.co) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[kk]);
+          if (DTST_BLK_HAS(k, o)) zexp_plain<CT, MT, NCLS>(sbuf + o * spec_len, a, Bz, m, g, Wz[kk]);
         }
       }
 #pragma unroll
       for (int k = 0; k < KCH; ++k) {
         const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
-        if ((FAST && 16 * OHI + NW * (k + 1) <= 4 * KI) || o < ba.co) texp_plain<CT, TH>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
+        if (DTST_BLK_HAS(k, o)) texp_plain<CT, TH>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
       }
     }
   };
 
+#undef DTST_BLK_HAS
+
   // Phase 2 of unit c (output pass OHI: channels 16 (OHI OT + ot) + 4g + r,
-  // buffer channel 16 ot + 4g + r) from buffer PAR with x buffer XB.
-  // The matrix part of phase 2: the expanded values from LDS plus the
-  // bypass products, into C.
+  // buffer channel 16 ot + 4g + r) from buffer PAR with x buffer XB, in two
+  // parts.  The matrix part: the expanded values from LDS plus the bypass
+  // products, into C.
   auto phase2_mma = [&](auto parc, auto xbc, auto ohc, auto fastc, const Cur& c, v4f (&C)[OT][4])
                         __attribute__((always_inline)) {
     constexpr int PAR = decltype(parc)::value, XB = decltype(xbc)::value, OHI = decltype(ohc)::value;
@@ -424,8 +430,9 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
       }
     }
   };
-  // The vector part with C_out = 4 KI and every point present: GELU and
-  // unconditional stores (a last tile of 4 channels gathered across rows).
+  // The vector part in the unconditional passes (C_out = 4 KI, every point
+  // present): GELU and stores without conditions (a last tile of 4 channels
+  // gathered across rows).
   auto phase2_store_full = [&](auto ohc, const Cur& c, const v4f (&C)[OT][4]) __attribute__((always_inline)) {
     constexpr int OHI = decltype(ohc)::value;
     const int off = group(c).off;
@@ -448,6 +455,8 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     tile(std::integral_constant<int, 0>{});
     if constexpr (OT > 1) tile(std::integral_constant<int, 1>{});
   };
+  // The whole of phase 2 with every condition (ragged tiles, missing points
+  // and channels).
   auto phase2 = [&](auto parc, auto xbc, auto ohc, const Cur& c) __attribute__((always_inline)) {
     constexpr int OHI = decltype(ohc)::value;
     const Grp q = group(c);
