@@ -660,3 +660,54 @@ def test_graph_capture_replays(name):
         assert np.array_equal(got, eager), f"replay {r} differs from the eager step"
     check(eager, O.inverse(O.mix(O.forward(np_of(x), g), np_of(W), 0, M).reshape(plan.spectral_shape(g.c_out)), g),
           "eager step vs oracle")
+
+
+@pytest.mark.parametrize("name", ["fold", "full_c16"])
+def test_graph_capture_replays_block(name):
+    """The block of Algorithm 1 (forward, mix, fused inverse + bypass + GELU)
+    captured in a HIP graph: the fused block kernel records no memset and
+    allocates nothing, so every replay (with eager work and synchronisation
+    between them) equals the eager step bit for bit, and the eager step
+    matches the oracle."""
+    torch = torch_gpu()
+    import paper_2607_14394_amd as D
+    spec, fusable = INVERSE_BLOCK_CASES[name]
+    g = geometry(*spec)
+    say(f"[graph block {name}] n_local={g.n_local} kmax={g.kmax} kt={g.kt} Cin={g.c_in} Cout={g.c_out}")
+    plan = D.Plan(desc_of(g))
+    assert plan.block_fused == fusable
+    M = plan.n_modes
+    x = dev(torch, rand_real((g.batch, g.c_in) + g.n_local, 150))
+    W = dev(torch, rand_cplx((M, g.c_in, g.c_out), 151, var=1.0 / (g.c_in * g.c_out)))
+    wb = dev(torch, (rand_real((g.c_out, g.c_in), 152) / np.sqrt(g.c_in)).astype(np.float32))
+    xhat = torch.empty(plan.spectral_shape(g.c_in), dtype=torch.complex64, device="cuda")
+    yhat = torch.empty(plan.spectral_shape(g.c_out), dtype=torch.complex64, device="cuda")
+    y = torch.empty(plan.spatial_shape(g.c_out), dtype=torch.float32, device="cuda")
+
+    def step():
+        plan.forward(x, xhat)
+        plan.mix(xhat, W, yhat, 0, M, op=0)
+        plan.inverse_block(yhat, x, wb, y)
+
+    step()
+    torch.cuda.synchronize()
+    eager = np_of(y).copy()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        step()
+    for r in range(3):
+        y.fill_(-3.0)
+        xhat.fill_(0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(np_of(y), eager), f"replay {r} differs from the eager step"
+    yh = O.mix(O.forward(np_of(x), g), np_of(W), 0, M).reshape(plan.spectral_shape(g.c_out))
+    check(eager, O.block_epilogue(np_of(x), np_of(wb), O.inverse(yh, g)), "eager block vs oracle")
+    plan.close()
