@@ -184,6 +184,19 @@ __device__ __forceinline__ float gather_rows(float r0, float r1, float r2, float
   return __uint_as_float(c[0]);
 }
 
+// Sum over the four 16-lane rows of r_g, left in row g (a reduce-scatter of
+// the 4 x 4 (row, register) values of each lane position): two
+// v_permlane32_swap pairs and one v_permlane16_swap pair with their sums.
+__device__ __forceinline__ float sum_rows_to_row(float r0, float r1, float r2, float r3) {
+  const auto p02 = __builtin_amdgcn_permlane32_swap(__float_as_uint(r0), __float_as_uint(r2), false, false);
+  const auto p13 = __builtin_amdgcn_permlane32_swap(__float_as_uint(r1), __float_as_uint(r3), false, false);
+  // lanes 0..31: r0 of rows (0 + 2, 1 + 3); lanes 32..63: r2 of rows (0 + 2, 1 + 3); likewise r1, r3
+  const float s02 = __uint_as_float(p02[0]) + __uint_as_float(p02[1]);
+  const float s13 = __uint_as_float(p13[0]) + __uint_as_float(p13[1]);
+  const auto q = __builtin_amdgcn_permlane16_swap(__float_as_uint(s02), __float_as_uint(s13), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
 // KI: K steps of 4 input channels (C_in <= 4 KI); OT: tiles of 16 output
 // channels per pass (C_out <= 16 OT OH); SPF: float4 of the row's spectrum
 // per thread (C_out K_z K_t <= 2 * 64 kBlkWaves SPF); XD: chunks of x loaded
@@ -249,6 +262,22 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
       const int o = 16 * ot + m, i = 4 * s + g;
       wa[ot][s] = (o < ba.co && i < ba.ci) ? wb[o * ba.ci + i] : 0.f;
     }
+  // A class whose full channel count leaves a last tile of 4 channels (C =
+  // 20) takes that tile, in its unconditional passes, on the 4 x 4 x 1
+  // sixteen-block products (block b = lanes 4b..4b+3: A from lane 4b + i, B
+  // from lane 4b + j, D[i][j] in register i of lane 4b + j): A of lane
+  // (m, g) is w[o4 + m % 4][4s + g], B its own x of channel 4s + g at point
+  // 4m + jj, so register i of lane (m, g) sums the channels 4s + g of output
+  // channel o4 + i at point 4m + jj, and a sum over the four rows completes
+  // it.  A quarter of the matrix work of a 16-row tile with 12 empty rows.
+  constexpr bool kPart4 = OH == 1 && OT > 1 && 16 * (OT - 1) + 4 == 4 * KI;
+  constexpr int o4 = 16 * (OT - 1);
+  float wp[kPart4 ? KI : 1];
+#pragma unroll
+  for (int s = 0; s < (kPart4 ? KI : 1); ++s) {
+    const int o = o4 + (m & 3), i = 4 * s + g;
+    wp[s] = (kPart4 && o < ba.co && i < ba.ci) ? wb[o * ba.ci + i] : 0.f;
+  }
 
   const int64_t row_len = int64_t(a.nz) * a.nt;
   const int nt = a.nt;
@@ -404,7 +433,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
     const float* yb = ybuf + PAR * bufsz;
     const Grp q = group(c);
 #pragma unroll
-    for (int ot = 0; ot < OT; ++ot)
+    for (int ot = 0; ot < OT - (FAST && kPart4 ? 1 : 0); ++ot)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int ol = 16 * ot + 4 * g + r, o = 16 * OHI * OT + ol;
@@ -415,27 +444,43 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
         C[ot][2][r] = v.z;
         C[ot][3][r] = v.w;
       }
+    // the 4-channel tile of the unconditional passes (see wp): C[OT - 1][jj]
+    // holds its row-partial sums at point 4m + jj, from zero (the expanded
+    // values are added after the row sum)
+    constexpr bool P4 = FAST && kPart4;
+    if constexpr (P4) {
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) C[OT - 1][jj] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
     for (int s = 0; s < KI; ++s) {
       const bool iok = FAST || 4 * s + g < ba.ci;
       const float4 xs = xv[XB][s];
       const float b0 = iok ? xs.x : 0.f, b1 = iok ? xs.y : 0.f, b2 = iok ? xs.z : 0.f, b3 = iok ? xs.w : 0.f;
 #pragma unroll
-      for (int ot = 0; ot < OT; ++ot) {
+      for (int ot = 0; ot < OT - (P4 ? 1 : 0); ++ot) {
         const float wv = wa[OHI * OT + ot][s];
         C[ot][0] = mfma(wv, b0, C[ot][0]);
         C[ot][1] = mfma(wv, b1, C[ot][1]);
         C[ot][2] = mfma(wv, b2, C[ot][2]);
         C[ot][3] = mfma(wv, b3, C[ot][3]);
       }
+      if constexpr (P4) {
+        C[OT - 1][0] = __builtin_amdgcn_mfma_f32_4x4x1f32(wp[s], b0, C[OT - 1][0], 0, 0, 0);
+        C[OT - 1][1] = __builtin_amdgcn_mfma_f32_4x4x1f32(wp[s], b1, C[OT - 1][1], 0, 0, 0);
+        C[OT - 1][2] = __builtin_amdgcn_mfma_f32_4x4x1f32(wp[s], b2, C[OT - 1][2], 0, 0, 0);
+        C[OT - 1][3] = __builtin_amdgcn_mfma_f32_4x4x1f32(wp[s], b3, C[OT - 1][3], 0, 0, 0);
+      }
     }
   };
   // The vector part in the unconditional passes (C_out = 4 KI, every point
   // present): GELU and stores without conditions (a last tile of 4 channels
   // gathered across rows).
-  auto phase2_store_full = [&](auto ohc, const Cur& c, const v4f (&C)[OT][4]) __attribute__((always_inline)) {
-    constexpr int OHI = decltype(ohc)::value;
-    const int off = group(c).off;
+  auto phase2_store_full = [&](auto parc, auto ohc, const Cur& c, const v4f (&C)[OT][4])
+                               __attribute__((always_inline)) {
+    constexpr int PAR = decltype(parc)::value, OHI = decltype(ohc)::value;
+    const Grp q = group(c);
+    const int off = q.off;
     float* yr = y + c.yb + gcs_y + off;
     auto tile = [&](auto otc) __attribute__((always_inline)) {
       constexpr int ot = decltype(otc)::value, o0 = 16 * (OHI * OT + ot);
@@ -444,6 +489,17 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
         for (int r = 0; r < 4; ++r)
           *reinterpret_cast<v4f*>(yr + (o0 + r) * cs) =
               v4f{gelu_as(C[ot][0][r]), gelu_as(C[ot][1][r]), gelu_as(C[ot][2][r]), gelu_as(C[ot][3][r])};
+      } else if constexpr (kPart4) {
+        static_assert(o0 == o4 && o0 + 4 == 4 * KI, "the 4-channel tile is the last one");
+        // row g: output channel o0 + g at the lane's points 4m..4m+3, plus the
+        // expanded values of that channel
+        const float4 e = *reinterpret_cast<const float4*>(ybuf + PAR * bufsz + (16 * ot + g) * ba.ostride + q.loff);
+        const float e4[4] = {e.x, e.y, e.z, e.w};
+        float v[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          v[jj] = gelu_as(sum_rows_to_row(C[ot][jj][0], C[ot][jj][1], C[ot][jj][2], C[ot][jj][3]) + e4[jj]);
+        *reinterpret_cast<v4f*>(y + c.yb + int64_t(o0 + g) * cs + off) = v4f{v[0], v[1], v[2], v[3]};
       } else {
         static_assert(o0 + 4 == 4 * KI, "a partial tile of the unconditional passes has 4 channels");
         float* yc = y + c.yb + int64_t(o0) * cs + off + g;
@@ -538,7 +594,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
           load_x(XL, cx);
           cx = next_chunk(cx);
         }
-        phase2_store_full(std::integral_constant<int, OH2>{}, c2, C);
+        phase2_store_full(P2{}, std::integral_constant<int, OH2>{}, c2, C);
         phase1(P1{}, std::integral_constant<int, HF>{}, std::integral_constant<int, OH1>{}, fastc, c1);
       } else {
         if (has2)
