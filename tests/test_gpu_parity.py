@@ -438,6 +438,7 @@ INVERSE_BLOCK_CASES = {
     "full_c20_tfold": (((16, 64, 32, 32), (16, 64, 32, 32), (0, 0, 0, 0), (4, 4, 8), 16, 1, 20, 20), True),
     # 992 rows: workgroups own 3 or 4 rows, so their counts of unconditional passes differ
     "full_c16_ragged_rows": (((16, 62, 64, 32), (16, 62, 64, 32), (0, 0, 0, 0), (2, 4, 8), 5, 1, 16, 16), True),
+    "full_c20_tfold_ragged_rows": (((16, 62, 32, 32), (16, 62, 32, 32), (0, 0, 0, 0), (4, 4, 8), 16, 1, 20, 20), True),
 }
 
 
