@@ -367,12 +367,12 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
       sp[k] = *reinterpret_cast<const v4f*>(in + ((b * ba.co + o) * ba.xy + rxy) * spec_len + j);
     }
   };
+  // (lanes past the end loaded entry n4 - 1 and store that same value to
+  // it: no per-lane condition, which the compiler would keep as a scalar
+  // lane mask for every k across the whole loop)
   auto spec_store = [&](const v4f (&sp)[SPF]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int k = 0; k < SPF; ++k) {
-      const int e4 = tid + 64 * NW * k;
-      if (e4 < n4) reinterpret_cast<v4f*>(sbuf)[e4] = sp[k];
-    }
+    for (int k = 0; k < SPF; ++k) reinterpret_cast<v4f*>(sbuf)[min(tid + 64 * NW * k, n4 - 1)] = sp[k];
   };
 
   // z expansions of this wave's channels, kept for the z tile's chunks
@@ -646,23 +646,29 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   const bool full = kFull && ba.co == 4 * KI && ba.ci == 4 * KI && nt == 4 * NW && a.zh % 16 == 0;
   const int64_t units = ((ba.rows - 1 - blockIdx.x) / gridDim.x + 1) * cpr * OH;  // this workgroup's units
   int64_t u1 = 1;  // unit of c1
-  // every pass runs four steps; the only exit is at the end of a pass
-  do {
-    if (full && u1 + 3 < units) {
-      if constexpr (kFull) {
+  // Every pass runs four steps; the only exits are at the end of a pass.
+  // The unconditional passes come first (they are contiguous), in a loop of
+  // their own, so that the loop-invariant values of the other steps (lane
+  // masks of their conditions, among others) are not held across them.
+  if constexpr (kFull) {
+    if (full) {
+      while (u1 + 3 < units) {
         step(std::integral_constant<int, 1>{}, Fast{}, true);
         step(std::integral_constant<int, 2>{}, Fast{}, true);
         step(std::integral_constant<int, 3>{}, Fast{}, true);
         step(std::integral_constant<int, 0>{}, Fast{}, true);
+        u1 += 4;
       }
-    } else {
-      step(std::integral_constant<int, 1>{}, Gen{}, c2.row < ba.rows);
-      step(std::integral_constant<int, 2>{}, Gen{}, c2.row < ba.rows);
-      step(std::integral_constant<int, 3>{}, Gen{}, c2.row < ba.rows);
-      step(std::integral_constant<int, 0>{}, Gen{}, c2.row < ba.rows);
     }
-    u1 += 4;
-  } while (c2.row < ba.rows);
+  }
+  // (c2 holds a unit that exists after step 0 and after any unconditional
+  // pass, so this loop runs at least once)
+  while (c2.row < ba.rows) {
+    step(std::integral_constant<int, 1>{}, Gen{}, c2.row < ba.rows);
+    step(std::integral_constant<int, 2>{}, Gen{}, c2.row < ba.rows);
+    step(std::integral_constant<int, 3>{}, Gen{}, c2.row < ba.rows);
+    step(std::integral_constant<int, 0>{}, Gen{}, c2.row < ba.rows);
+  }
 }
 
 typedef void (*blk_fn)(const float2*, const float*, const float*, float*, const float*, const float4*, StreamArgs,
