@@ -89,7 +89,7 @@ __device__ __forceinline__ void zexp_plain(const float2* urow, const StreamArgs&
 }
 
 // t expansion of one class of a z tile (unfolded t) into yb[z row][t].
-template <int CT, int TH>
+template <int CT, int TH, bool WHOLE_T = false>
 __device__ __forceinline__ void texp_plain(const v4f (&W)[CT], const float (&ta)[TH][CT][4], float* yb, int nt,
                                            int m, int g) {
   v4f Y[TH];
@@ -104,7 +104,7 @@ __device__ __forceinline__ void texp_plain(const v4f (&W)[CT], const float (&ta)
 #pragma unroll
   for (int mt = 0; mt < TH; ++mt) {
     const int t0 = 16 * mt + 4 * g;
-    if (t0 < nt) *reinterpret_cast<v4f*>(yb + yoff(m, t0, nt)) = Y[mt];
+    if (WHOLE_T || t0 < nt) *reinterpret_cast<v4f*>(yb + yoff(m, t0, nt)) = Y[mt];
   }
 }
 
@@ -346,12 +346,14 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   // missing points read the row start, input channels past C_in read the
   // last one; both are multiplied by zero weights or not stored).
   float4 xv[XD][KI];
-  auto load_x = [&](int k, const Cur& c) __attribute__((always_inline)) {
+  // (FAST: C_in = 4 KI, every input channel exists)
+  auto load_x = [&](int k, const Cur& c, auto fastc) __attribute__((always_inline)) {
+    constexpr bool FAST = decltype(fastc)::value;
     const Grp q = group(c);
     const float* xr = x + c.xb + q.off;
 #pragma unroll
     for (int s = 0; s < KI; ++s) {
-      const int64_t co = 4 * s + g < ba.ci ? 4 * s * cs + gcs_x : (ba.ci - 1) * cs;
+      const int64_t co = (FAST || 4 * s + g < ba.ci) ? 4 * s * cs + gcs_x : (ba.ci - 1) * cs;
       xv[k][s] = *reinterpret_cast<const float4*>(xr + co);
     }
   };
@@ -415,7 +417,8 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
 #pragma unroll
       for (int k = 0; k < KCH; ++k) {
         const int kk = OHI * KCH + k, ol = w + NW * k, o = 16 * OHI + ol;
-        if (DTST_BLK_HAS(k, o)) texp_plain<CT, TH>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
+        // (FAST: N_t = 16 TH, every t row exists)
+        if (DTST_BLK_HAS(k, o)) texp_plain<CT, TH, FAST>(Wz[kk][HF], ta, yb + ol * ba.ostride, nt, m, g);
       }
     }
   };
@@ -591,7 +594,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
         v4f C[OT][4];
         phase2_mma(P2{}, std::integral_constant<int, XB>{}, std::integral_constant<int, OH2>{}, fastc, c2, C);
         if constexpr (LOADS) {
-          load_x(XL, cx);
+          load_x(XL, cx, fastc);
           cx = next_chunk(cx);
         }
         phase2_store_full(P2{}, std::integral_constant<int, OH2>{}, c2, C);
@@ -600,7 +603,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
         if (has2)
           phase2(P2{}, std::integral_constant<int, XB>{}, std::integral_constant<int, OH2>{}, c2);
         if constexpr (LOADS) {
-          load_x(XL, cx);
+          load_x(XL, cx, fastc);
           cx = next_chunk(cx);
         }
         if (has1) phase1(P1{}, std::integral_constant<int, HF>{}, std::integral_constant<int, OH1>{}, fastc, c1);
@@ -631,7 +634,7 @@ inv_zt_block_kernel(const float2* __restrict__ in, const float* __restrict__ x, 
   }
 #pragma unroll
   for (int k = 0; k < XD - 1; ++k) {
-    load_x(k, cx);
+    load_x(k, cx, std::integral_constant<bool, false>{});
     cx = next_chunk(cx);
   }
   __syncthreads();
