@@ -317,7 +317,7 @@ mix_h_kernel(const float2* __restrict__ gy, const float2* __restrict__ w, float2
 // o = 2 (lr + LPR s) + {0, 1} and writes them with one 16-byte store (half
 // the store instructions of W = 1 for the same bytes; needs an even C_out
 // and a 16-byte aligned g_w).
-template <int LPR, int OPL, int W>
+template <int LPR, int OPL, int W, int ACC>
 __global__ void __launch_bounds__(256)
 wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2* __restrict__ gw, MixArgs a) {
   constexpr int R = Rows<OPL>::value;
@@ -363,7 +363,7 @@ wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2
         }
     };
     float2 acc[R][OPL][W];
-    if (a.acc) load_acc(acc, 0);
+    if constexpr (ACC) load_acc(acc, 0);
     put<MPB>(sx, prex, x, a.B * a.ci, a.M, mbase, nm);
     put<MPB>(sg, preg, gy, a.B * a.co, a.M, mbase, nm);
     if (k + 1 < k1) {
@@ -374,7 +374,7 @@ wgrad_kernel(const float2* __restrict__ x, const float2* __restrict__ gy, float2
     __syncthreads();
     if (!active) continue;
     for (int i0 = 0; i0 < a.ci; i0 += R) {
-      if (a.acc) {
+      if constexpr (ACC) {
         if (i0 > 0) load_acc(acc, i0);
       } else {
 #pragma unroll
@@ -551,13 +551,23 @@ template <int L, int O>
 struct MixHK {
   static constexpr mix_fn fn = mix_h_kernel<L, O>;
 };
+// (accumulating and overwriting instances apart: the accumulate read and its
+// conditions are not compiled into the overwriting kernel)
 template <int L, int O>
 struct WgradK {
-  static constexpr mix_fn fn = wgrad_kernel<L, O, 1>;
+  static constexpr mix_fn fn = wgrad_kernel<L, O, 1, 0>;
 };
 template <int L, int O>
 struct WgradK2 {
-  static constexpr mix_fn fn = wgrad_kernel<L, O, 2>;
+  static constexpr mix_fn fn = wgrad_kernel<L, O, 2, 0>;
+};
+template <int L, int O>
+struct WgradKA {
+  static constexpr mix_fn fn = wgrad_kernel<L, O, 1, 1>;
+};
+template <int L, int O>
+struct WgradK2A {
+  static constexpr mix_fn fn = wgrad_kernel<L, O, 2, 1>;
 };
 
 }  // namespace
@@ -586,11 +596,13 @@ int launch_wgrad(const void* xhat, const void* gy, void* gw, int64_t B, int64_t 
   const size_t lds2 = 2 * block_lds(B, ci, co, co / 2);
   if (co % 2 == 0 && co >= 4 && (reinterpret_cast<uintptr_t>(gw) & 15) == 0 && lds2 <= 160 * 1024) {
     const MixArgs a = make_args(B, ci, co, M, m0, m1, accumulate ? 1 : 0, co / 2);
-    return launch(pick<WgradK2>(co / 2), lds2, true, static_cast<const float2*>(xhat),
+    return launch(accumulate ? pick<WgradK2A>(co / 2) : pick<WgradK2>(co / 2), lds2, true,
+                  static_cast<const float2*>(xhat),
                   static_cast<const float2*>(gy), static_cast<float2*>(gw), a, stream);
   }
   const MixArgs a = make_args(B, ci, co, M, m0, m1, accumulate ? 1 : 0);
-  return launch(pick<WgradK>(co), mix_lds_bytes(B, ci, co), true, static_cast<const float2*>(xhat),
+  return launch(accumulate ? pick<WgradKA>(co) : pick<WgradK>(co), mix_lds_bytes(B, ci, co), true,
+                static_cast<const float2*>(xhat),
                 static_cast<const float2*>(gy), static_cast<float2*>(gw), a, stream);
 }
 
